@@ -1,0 +1,138 @@
+/*
+ * flex.h -- C ABI of the MI355X (gfx950) random-Fourier-feature linear
+ * attention library (Flexformer, arXiv 2606.27748).
+ *
+ * Notation follows the paper.  For one (batch b, head h) slice:
+ *   X in {Q, K}: N x d rows, V: N x dv rows, m frequencies per matrix, d' = 2m.
+ *   Stationary variant (Flexformer_s, Sec. 3.2 first paragraph; feature map
+ *   Eq.(phi_n) of Sec. 3.1):
+ *       phi(x) = s e(x) [cos(W x) ; sin(W x)],           s = sigma / sqrt(m)
+ *   Nonstationary variant (Flexformer_n, Sec. 3.2, Eq.(phi_non)), with
+ *   W'1 = (W1 + W2)/2 and W'2 = (W1 - W2)/2:
+ *       phi(x) = s e(x) [cos(W'1 x) cos(W'2 x) ; sin(W'1 x) cos(W'2 x)],
+ *                                                       s = sigma / (2 sqrt(m))
+ *   Norm factor (Sec. 3.2, learnable scale exp(tau)): e(x) = exp(||x||^2 / exp(tau_h)).
+ *   Attention, Eq.(linear att) of Sec. 2.2:
+ *       O_i = phi(Q_i)^T S / phi(Q_i)^T z,  S = sum_j phi(K_j) V_j^T,  z = sum_j phi(K_j)
+ *   with the sums over all j (non-causal) or over j <= i (causal; the paper's
+ *   autoregressive language model, Sec. 4.2, read with an inclusive mask).
+ *   den_i = phi(Q_i)^T z (per row) is returned for the backward pass.  No clamp
+ *   or epsilon is applied: den_i = 0 yields inf/NaN exactly as the definition.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers owned by the caller; the library never
+ *     allocates, frees or synchronizes.  Work is enqueued on `stream` (a
+ *     hipStream_t; NULL = the default stream) and runs asynchronously.
+ *   - Layouts are contiguous row-major: Q, K [B,H,N,d]; V, O, dO [B,H,N,dv];
+ *     den [B,H,N]; W1, W2 [H,m,d] fp32 (one frequency matrix per head, as in the
+ *     paper's parameter analysis, Appendix B); tau [H] fp32; Phi [B,H,N,2m] with
+ *     features ordered [cos block | sin block] as printed in Eq.(phi_n)/(phi_non).
+ *   - Pointers must be 16-byte aligned.
+ *   - The workspace `ws` is caller-owned device memory of at least
+ *     flex_workspace_size() bytes for the same descriptor and pass; its contents
+ *     on entry do not matter.
+ *   - All arguments are validated before any device work is enqueued.  An
+ *     invalid descriptor, a required NULL pointer, a W2 / variant mismatch or a
+ *     too-small workspace returns an error code with no device work.  A failed
+ *     kernel launch returns FLEX_ERR_HIP.  No C++ exception crosses the ABI.
+ *   - Results are deterministic (bitwise identical from run to run).
+ *   - Supported shapes: N >= 1 (a ragged last chunk is masked); d = dv in
+ *     {32, 64, 128}; m in {64, 128, 256} with the combinations
+ *     (d, m) = (32, 64), (64, 64), (64, 128), (128, 256); chunk = 64.
+ *     Others return FLEX_ERR_UNSUPPORTED.
+ *   - io_dtype FLEX_F32 computes every contraction in fp32 (MFMA f32);
+ *     FLEX_BF16 reads bf16 inputs, projects with a two-term bf16 split of the
+ *     frequencies and contracts bf16 features with fp32 accumulation.
+ */
+#ifndef FLEX_H
+#define FLEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FLEX_ABI_VERSION 1
+
+typedef enum {
+  FLEX_OK = 0,
+  FLEX_ERR_INVALID_ARG = 1,  /* NULL descriptor / pointer, bad sizes or enums   */
+  FLEX_ERR_UNSUPPORTED = 2,  /* valid but not implemented (shape, dtype)        */
+  FLEX_ERR_WORKSPACE = 3,    /* workspace NULL or smaller than required         */
+  FLEX_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed      */
+} flex_status;
+
+typedef enum { FLEX_F32 = 0, FLEX_BF16 = 1 } flex_dtype;
+typedef enum { FLEX_STATIONARY = 0, FLEX_NONSTATIONARY = 1 } flex_variant;
+typedef enum { FLEX_PASS_FEATURE_MAP = 0, FLEX_PASS_FWD = 1, FLEX_PASS_BWD = 2 } flex_pass;
+
+typedef struct {
+  int32_t B, H, N;      /* batch, heads, sequence length                           */
+  int32_t d, dv;        /* head dimension of Q/K and of V (dv must equal d)         */
+  int32_t m;            /* frequencies per matrix (the paper's n); d' = 2m          */
+  int32_t variant;      /* flex_variant                                             */
+  int32_t causal;       /* 0: all j; 1: j <= i                                      */
+  int32_t chunk;        /* causal chunk length; 0 selects 64; only 64 is supported  */
+  int32_t segments;     /* sequence segments per (b,h); 0 selects a heuristic       */
+  int32_t io_dtype;     /* flex_dtype of Q, K, V, O, dO and Phi                     */
+  int32_t grad_dtype;   /* flex_dtype of dQ, dK, dV; only FLEX_F32 is supported     */
+  float sigma;          /* square root of the total spectral measure; 1 by default  */
+} flex_desc;
+
+/* ABI version of the loaded library (FLEX_ABI_VERSION). */
+int32_t flex_abi_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* flex_status_string(int32_t status);
+
+/* Bytes of workspace needed by `pass` (flex_pass) for this descriptor.
+ * Writes *bytes and returns FLEX_OK, or an error code for an invalid or
+ * unsupported descriptor (then *bytes is 0). */
+int32_t flex_workspace_size(const flex_desc* desc, int32_t pass, size_t* bytes);
+
+/* Feature map phi~(X) of Eq.(phi_n) (stationary) or Eq.(phi_non) (nonstationary)
+ * times the norm factor exp(||x||^2/exp(tau)).
+ *   X   [B,H,N,d]   io_dtype, input rows
+ *   W1  [H,m,d]     fp32, frequencies (omega, or omega_1 for the nonstationary variant)
+ *   W2  [H,m,d]     fp32, omega_2; must be NULL for the stationary variant
+ *   tau [H]         fp32, log of the norm-factor scale
+ *   Phi [B,H,N,2m]  io_dtype output, [cos | sin] feature blocks
+ * `causal` and `dv` are ignored. */
+int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1,
+                         const float* W2, const float* tau, void* Phi,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* Forward attention, Eq.(linear att), non-causal or causal.
+ *   Q, K [B,H,N,d], V [B,H,N,dv]   io_dtype
+ *   W1, W2, tau                    as for flex_feature_map
+ *   O    [B,H,N,dv]  io_dtype output
+ *   den  [B,H,N]     fp32 output phi(Q_i)^T z_i, or NULL if not wanted
+ * φ(Q) and φ(K) are formed on chip and never written to memory. */
+int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K,
+                         const void* V, const float* W1, const float* W2,
+                         const float* tau, void* O, float* den,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of flex_linattn_fwd for an upstream gradient dO (the paper gives no
+ * backward; it is the derivative of the forward above).
+ *   Q, K, V, W1, W2, tau  the forward inputs
+ *   O, den               the forward outputs (den must not be NULL)
+ *   dO   [B,H,N,dv]       io_dtype, gradient of the loss with respect to O
+ *   dQ, dK [B,H,N,d], dV [B,H,N,dv]   grad_dtype outputs (overwritten)
+ *   dW1 [H,m,d] fp32 output (overwritten); dW2 [H,m,d] fp32 output, required for
+ *   the nonstationary variant and NULL for the stationary one
+ *   dtau [H] fp32 output or NULL (overwritten when given) */
+int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K,
+                         const void* V, const float* W1, const float* W2,
+                         const float* tau, const void* O, const float* den,
+                         const void* dO, void* dQ, void* dK, void* dV,
+                         float* dW1, float* dW2, float* dtau,
+                         void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLEX_H */

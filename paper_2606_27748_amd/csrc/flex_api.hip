@@ -1,0 +1,209 @@
+// C ABI of the RFF linear attention library: argument validation, workspace
+// sizing, segment selection and dispatch to the gfx950 kernels.
+#include "../../include/flex.h"
+#include "flex_kernels.hpp"
+
+#include <math.h>
+#include <string.h>
+
+using namespace flex;
+
+namespace {
+
+constexpr int kChunk = 64;
+constexpr int kCUs = 256;
+
+bool shape_supported(const flex_desc* d) {
+  if (d->dv != d->d) return false;
+  if (d->grad_dtype != FLEX_F32) return false;
+  if (d->chunk != 0 && d->chunk != kChunk) return false;
+  const bool bf = d->io_dtype == FLEX_BF16;
+  if (d->d == 32 && d->m == 64) return true;
+  if (d->d == 64 && d->m == 64) return true;
+  if (d->d == 64 && d->m == 128) return bf;
+  if (d->d == 128 && d->m == 256) return bf;
+  return false;
+}
+
+// 0 = ok, else a flex_status
+int32_t check_desc(const flex_desc* d) {
+  if (!d) return FLEX_ERR_INVALID_ARG;
+  if (d->B <= 0 || d->H <= 0 || d->N <= 0 || d->d <= 0 || d->dv <= 0 || d->m <= 0)
+    return FLEX_ERR_INVALID_ARG;
+  if (d->variant != FLEX_STATIONARY && d->variant != FLEX_NONSTATIONARY) return FLEX_ERR_INVALID_ARG;
+  if (d->causal != 0 && d->causal != 1) return FLEX_ERR_INVALID_ARG;
+  if (d->io_dtype != FLEX_F32 && d->io_dtype != FLEX_BF16) return FLEX_ERR_INVALID_ARG;
+  if (d->grad_dtype != FLEX_F32 && d->grad_dtype != FLEX_BF16) return FLEX_ERR_INVALID_ARG;
+  if (d->chunk < 0 || d->segments < 0) return FLEX_ERR_INVALID_ARG;
+  if (!(d->sigma > 0.0f) || !isfinite(d->sigma)) return FLEX_ERR_INVALID_ARG;
+  // element counts must fit the 32-bit token and 64-bit element indexing used on device
+  const long long bhn = (long long)d->B * d->H * d->N;
+  if (bhn > (1LL << 40) || (long long)d->B * d->H > (1LL << 30)) return FLEX_ERR_INVALID_ARG;
+  if (!shape_supported(d)) return FLEX_ERR_UNSUPPORTED;
+  return FLEX_OK;
+}
+
+KernelShape kshape(const flex_desc* d) {
+  KernelShape k;
+  k.bf16 = d->io_dtype == FLEX_BF16;
+  k.nonstationary = d->variant == FLEX_NONSTATIONARY;
+  k.causal = d->causal != 0;
+  k.d = d->d;
+  k.m = d->m;
+  return k;
+}
+
+int nchunks_of(const flex_desc* d) { return (d->N + kChunk - 1) / kChunk; }
+
+// Segments per (b,h): enough workgroups to cover the 256 CUs in whole rounds
+// while keeping the per-segment state traffic small.
+int pick_segments(const flex_desc* d) {
+  const int nc = nchunks_of(d);
+  if (d->segments > 0) return d->segments < nc ? d->segments : nc;
+  const long long bh = (long long)d->B * d->H;
+  int best = 1;
+  double best_cost = 1e30;
+  for (int p = 1; p <= nc && p <= 64; ++p) {
+    const int cps = (nc + p - 1) / p;
+    const int used = (nc + cps - 1) / cps;  // segments that hold chunks
+    if (used != p) continue;
+    const long long wgs = bh * p;
+    const long long rounds = (wgs + kCUs - 1) / kCUs;
+    // sweep chunks per CU + pre-pass (about a third of a sweep chunk) + state hand-off
+    const double cost = rounds * (double)cps * (p > 1 || !d->causal ? 1.35 : 1.0) + 0.5 * p * bh / kCUs;
+    if (cost < best_cost - 1e-9) { best_cost = cost; best = p; }
+  }
+  return best;
+}
+
+float s_const_of(const flex_desc* d) {
+  const double s = d->variant == FLEX_STATIONARY ? d->sigma / sqrt((double)d->m)
+                                                 : d->sigma / (2.0 * sqrt((double)d->m));
+  return (float)s;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t ws_bytes_of(const flex_desc* d, int pass) {
+  const KernelShape ks = kshape(d);
+  const size_t bh = (size_t)d->B * d->H;
+  const size_t P = (size_t)pick_segments(d);
+  if (pass == FLEX_PASS_FEATURE_MAP) return 0;
+  if (pass == FLEX_PASS_FWD) return align256(bh * P * fwd_state_floats(ks) * sizeof(float));
+  // backward: key-side and query-side states, frequency-gradient and dtau partials
+  return 2 * align256(bh * P * bwd_state_floats(ks) * sizeof(float)) +
+         align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t flex_abi_version(void) { return FLEX_ABI_VERSION; }
+
+const char* flex_status_string(int32_t s) {
+  switch (s) {
+    case FLEX_OK: return "ok";
+    case FLEX_ERR_INVALID_ARG: return "invalid argument";
+    case FLEX_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case FLEX_ERR_WORKSPACE: return "workspace missing or too small";
+    case FLEX_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int32_t flex_workspace_size(const flex_desc* desc, int32_t pass, size_t* bytes) {
+  if (bytes) *bytes = 0;
+  if (!bytes) return FLEX_ERR_INVALID_ARG;
+  if (pass < FLEX_PASS_FEATURE_MAP || pass > FLEX_PASS_BWD) return FLEX_ERR_INVALID_ARG;
+  const int32_t st = check_desc(desc);
+  if (st != FLEX_OK) return st;
+  *bytes = ws_bytes_of(desc, pass);
+  return FLEX_OK;
+}
+
+int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1, const float* W2,
+                         const float* tau, void* Phi, void* ws, size_t ws_bytes, void* stream) {
+  (void)ws; (void)ws_bytes;
+  const int32_t st = check_desc(desc);
+  if (st != FLEX_OK) return st;
+  if (!X || !W1 || !tau || !Phi) return FLEX_ERR_INVALID_ARG;
+  if ((desc->variant == FLEX_NONSTATIONARY) != (W2 != nullptr)) return FLEX_ERR_INVALID_ARG;
+  if (!aligned16(X) || !aligned16(W1) || (W2 && !aligned16(W2)) || !aligned16(Phi))
+    return FLEX_ERR_INVALID_ARG;
+  FwdArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Q = X; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = Phi;
+  a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
+  a.nchunks = nchunks_of(desc); a.segments = 1; a.chunks_per_seg = a.nchunks;
+  a.s_const = s_const_of(desc);
+  const hipError_t e = launch_fwd(a, kshape(desc), true, (hipStream_t)stream);
+  return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
+}
+
+int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, const void* V,
+                         const float* W1, const float* W2, const float* tau, void* O, float* den,
+                         void* ws, size_t ws_bytes, void* stream) {
+  const int32_t st = check_desc(desc);
+  if (st != FLEX_OK) return st;
+  if (!Q || !K || !V || !W1 || !tau || !O) return FLEX_ERR_INVALID_ARG;
+  if ((desc->variant == FLEX_NONSTATIONARY) != (W2 != nullptr)) return FLEX_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(W1) || (W2 && !aligned16(W2)) ||
+      !aligned16(O) || (den && !aligned16(den)))
+    return FLEX_ERR_INVALID_ARG;
+  const size_t need = ws_bytes_of(desc, FLEX_PASS_FWD);
+  if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
+  FwdArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Q = Q; a.K = K; a.V = V; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = O; a.den = den;
+  a.state = static_cast<float*>(ws);
+  a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
+  a.nchunks = nchunks_of(desc);
+  a.segments = pick_segments(desc);
+  a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
+  a.s_const = s_const_of(desc);
+  const hipError_t e = launch_fwd(a, kshape(desc), false, (hipStream_t)stream);
+  return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
+}
+
+int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, const void* V,
+                         const float* W1, const float* W2, const float* tau, const void* O,
+                         const float* den, const void* dO, void* dQ, void* dK, void* dV, float* dW1,
+                         float* dW2, float* dtau, void* ws, size_t ws_bytes, void* stream) {
+  const int32_t st = check_desc(desc);
+  if (st != FLEX_OK) return st;
+  const bool ns = desc->variant == FLEX_NONSTATIONARY;
+  if (!Q || !K || !V || !W1 || !tau || !O || !den || !dO || !dQ || !dK || !dV || !dW1)
+    return FLEX_ERR_INVALID_ARG;
+  if (ns != (W2 != nullptr) || ns != (dW2 != nullptr)) return FLEX_ERR_INVALID_ARG;
+  const void* ptrs[] = {Q, K, V, W1, O, den, dO, dQ, dK, dV, dW1};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return FLEX_ERR_INVALID_ARG;
+  if ((W2 && !aligned16(W2)) || (dW2 && !aligned16(dW2))) return FLEX_ERR_INVALID_ARG;
+  const size_t need = ws_bytes_of(desc, FLEX_PASS_BWD);
+  if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
+  const KernelShape ks = kshape(desc);
+  BwdArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Q = Q; a.K = K; a.V = V; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = O; a.den = den; a.dO = dO;
+  a.dQ = static_cast<float*>(dQ); a.dK = static_cast<float*>(dK); a.dV = static_cast<float*>(dV);
+  a.dW1 = dW1; a.dW2 = dW2; a.dtau = dtau;
+  a.BH = desc->B * desc->H; a.B = desc->B; a.H = desc->H; a.N = desc->N;
+  a.nchunks = nchunks_of(desc);
+  a.segments = pick_segments(desc);
+  a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
+  a.s_const = s_const_of(desc);
+  const size_t bh = (size_t)a.BH, P = (size_t)a.segments;
+  char* base = static_cast<char*>(ws);
+  const size_t sb = align256(bh * P * bwd_state_floats(ks) * sizeof(float));
+  a.sstate = reinterpret_cast<float*>(base);
+  a.rstate = reinterpret_cast<float*>(base + sb);
+  a.dwpart = reinterpret_cast<float*>(base + 2 * sb);
+  a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
+  const hipError_t e = launch_bwd(a, ks, (hipStream_t)stream);
+  return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
+}
+
+}  // extern "C"

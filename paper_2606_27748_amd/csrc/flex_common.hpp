@@ -1,0 +1,230 @@
+// Device building blocks shared by the gfx950 kernels of the RFF linear
+// attention library: MFMA fragments, frequency loading, the projection onto
+// the frequencies and the fused trigonometric feature epilogue.
+//
+// Orientation used throughout ("token-column"): the projection is computed as
+// P^T = W X^T with v_mfma_f32_16x16x32_bf16 (or eight v_mfma_f32_16x16x4f32 on
+// the fp32 path), so a 16x16 accumulator tile holds 16 frequencies x 16 tokens
+// and lane l owns token l%16 and frequencies 4*(l/16)+i, i=0..3.  The feature
+// epilogue turns one such tile into one 8-wide MFMA operand fragment per lane:
+// slots j=0..3 hold the cos (stationary) or cos P1 cos P2 (nonstationary)
+// features of frequencies 4g+j and slots j=4..7 the matching sin /
+// sin P1 cos P2 features (g = l/16).  Both operands of every contraction over
+// features use this same slot -> feature map, so no shuffle is needed.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace flex {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16;
+
+constexpr int WAVE = 64;
+constexpr int CHUNK = 64;          // tokens per chunk
+constexpr int TT = CHUNK / 16;     // token tiles per chunk
+constexpr float INV_2PI = 0.15915494309189535f;
+
+// ---------------------------------------------------------------------------
+// Fragments: 8 operand values per lane.  Lane l supplies row/col l%16 and the
+// contraction indices k(g, j) for g = l/16, j = 0..7.
+// ---------------------------------------------------------------------------
+template <class T> struct Frag;
+template <> struct Frag<__bf16> {
+  bf16x8 v;
+  __device__ void zero() { for (int j = 0; j < 8; ++j) v[j] = (__bf16)0.0f; }
+  __device__ void set(int j, float x) { v[j] = (__bf16)x; }
+  __device__ float get(int j) const { return (float)v[j]; }
+};
+template <> struct Frag<float> {
+  float v[8];
+  __device__ void zero() { for (int j = 0; j < 8; ++j) v[j] = 0.0f; }
+  __device__ void set(int j, float x) { v[j] = x; }
+  __device__ float get(int j) const { return v[j]; }
+};
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+__device__ __forceinline__ void mma(f32x4& c, const Frag<__bf16>& a, const Frag<__bf16>& b) {
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, c, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x4& c, const Frag<float>& a, const Frag<float>& b) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[j], b.v[j], c, 0, 0, 0);
+}
+
+template <class T> struct IsBf16 { static constexpr bool value = false; };
+template <> struct IsBf16<__bf16> { static constexpr bool value = true; };
+
+// Storage type of the io tensors for an operand type.
+template <class T> struct Io;
+template <> struct Io<__bf16> { typedef u16 type; };
+template <> struct Io<float> { typedef float type; };
+
+__device__ __forceinline__ float bf16_bits_to_float(u16 b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+__device__ __forceinline__ u16 float_to_bf16_bits(float x) {
+  __bf16 h = (__bf16)x;
+  return __builtin_bit_cast(u16, h);
+}
+__device__ __forceinline__ float io_to_float(u16 b) { return bf16_bits_to_float(b); }
+__device__ __forceinline__ float io_to_float(float x) { return x; }
+template <class S> __device__ __forceinline__ S float_to_io(float x);
+template <> __device__ __forceinline__ u16 float_to_io<u16>(float x) { return float_to_bf16_bits(x); }
+template <> __device__ __forceinline__ float float_to_io<float>(float x) { return x; }
+
+// Load 8 consecutive io elements starting at p (16-byte aligned for bf16,
+// 32-byte aligned for fp32) into a fragment; `ok` false gives zeros.
+__device__ __forceinline__ void load8(Frag<__bf16>& f, const u16* p, bool ok) {
+  if (ok) {
+    uint4 r = *reinterpret_cast<const uint4*>(p);
+    f.v = __builtin_bit_cast(bf16x8, r);
+  } else {
+    f.zero();
+  }
+}
+__device__ __forceinline__ void load8(Frag<float>& f, const float* p, bool ok) {
+  if (ok) {
+    float4 a = *reinterpret_cast<const float4*>(p);
+    float4 b = *reinterpret_cast<const float4*>(p + 4);
+    f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+    f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+  } else {
+    f.zero();
+  }
+}
+
+// Sum over the four lane groups (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float group_sum(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// Per-wave frequency slice.  A wave owns FW consecutive frequencies starting
+// at f0; its projection rows are those FW rows of W (stationary) or of W'1
+// followed by the same FW rows of W'2 (nonstationary), scaled by 1/(2 pi) so
+// that the projection comes out in revolutions.  On the bf16 path each row is
+// held as a two-term bf16 split hi + lo (about 16 significant bits).
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, bool NS>
+struct FreqSlice {
+  static constexpr int FT = FW / 16;               // frequency tiles
+  static constexpr int PR = NS ? 2 * FT : FT;      // projection row tiles
+  static constexpr int KD = D / 32;                // k-steps over d
+  static constexpr int NSPLIT = IsBf16<T>::value ? 2 : 1;
+  Frag<T> w[NSPLIT][PR][KD];
+
+  // W1, W2: [m, d] fp32 rows of this head.
+  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
+    const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+#pragma unroll
+    for (int pr = 0; pr < PR; ++pr) {
+      const int f = f0 + (pr % FT) * 16 + r;
+      const bool second = pr >= FT;
+#pragma unroll
+      for (int ks = 0; ks < KD; ++ks) {
+        const int c0 = ks * 32 + 8 * g;
+        const float* a = W1 + (size_t)f * D + c0;
+        float x[8];
+        float4 a0 = *reinterpret_cast<const float4*>(a);
+        float4 a1 = *reinterpret_cast<const float4*>(a + 4);
+        x[0] = a0.x; x[1] = a0.y; x[2] = a0.z; x[3] = a0.w;
+        x[4] = a1.x; x[5] = a1.y; x[6] = a1.z; x[7] = a1.w;
+        if (NS) {
+          const float* b = W2 + (size_t)f * D + c0;
+          float4 b0 = *reinterpret_cast<const float4*>(b);
+          float4 b1 = *reinterpret_cast<const float4*>(b + 4);
+          float y[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) x[j] = second ? 0.5f * (x[j] - y[j]) : 0.5f * (x[j] + y[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float v = x[j] * INV_2PI;
+          if (IsBf16<T>::value) {
+            const float hi = (float)(__bf16)v;
+            w[0][pr][ks].set(j, hi);
+            w[NSPLIT - 1][pr][ks].set(j, v - hi);
+          } else {
+            w[0][pr][ks].set(j, v);
+          }
+        }
+      }
+    }
+  }
+};
+
+// Projection of one 16-token tile onto a wave's frequency slice, plus the
+// squared row norm.  X points at the token rows of this (b,h) slice; rows at
+// or beyond n_valid read as zero.  p[pr] receives the P^T tile (revolutions).
+template <class T, int D, int FW, bool NS>
+__device__ __forceinline__ void project_tile(const FreqSlice<T, D, FW, NS>& fs,
+                                             const typename Io<T>::type* __restrict__ X,
+                                             int tok0, int n_valid,
+                                             f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR], float& ssq) {
+  typedef FreqSlice<T, D, FW, NS> FS;
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int tok = tok0 + r;
+  const bool ok = tok < n_valid;
+#pragma unroll
+  for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
+  float s = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < FS::KD; ++ks) {
+    Frag<T> x;
+    load8(x, X + (size_t)tok * D + ks * 32 + 8 * g, ok);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) { const float v = x.get(j); s += v * v; }
+#pragma unroll
+    for (int pr = 0; pr < FS::PR; ++pr)
+#pragma unroll
+      for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], fs.w[sp][pr][ks], x);
+  }
+  ssq = group_sum(s);
+}
+
+// Trigonometric values of a projection in revolutions: cos(2 pi p), sin(2 pi p).
+// v_fract_f32 maps p to [0,1), the domain where v_sin_f32 / v_cos_f32 are exact
+// to about 2.6e-7.
+__device__ __forceinline__ void sincos_rev(float p, float& s, float& c) {
+  const float f = __builtin_amdgcn_fractf(p);
+  s = __builtin_amdgcn_sinf(f);
+  c = __builtin_amdgcn_cosf(f);
+}
+__device__ __forceinline__ float cos_rev(float p) {
+  return __builtin_amdgcn_cosf(__builtin_amdgcn_fractf(p));
+}
+
+// Feature epilogue for one frequency tile ft of one 16-token tile:
+// scale = s * e(x) (0 for rows that are not valid).  Returns the operand
+// fragment [cos-type features 4g..4g+3 | sin-type features 4g..4g+3].
+template <class T, int FT, bool NS>
+__device__ __forceinline__ Frag<T> features(const f32x4 (&p)[NS ? 2 * FT : FT], int ft, float scale) {
+  Frag<T> f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float s1, c1;
+    sincos_rev(p[ft][i], s1, c1);
+    float a = c1 * scale, b = s1 * scale;
+    if (NS) {
+      const float c2 = cos_rev(p[FT + ft][i]);
+      a *= c2;
+      b *= c2;
+    }
+    f.set(i, a);
+    f.set(4 + i, b);
+  }
+  return f;
+}
+
+// Row scale s * exp(||x||^2 / exp(tau)) for valid rows, 0 otherwise.
+__device__ __forceinline__ float row_scale(float ssq, float inv_c, float s_const, bool ok) {
+  return ok ? s_const * __expf(ssq * inv_c) : 0.0f;
+}
+
+}  // namespace flex

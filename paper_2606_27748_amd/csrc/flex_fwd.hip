@@ -1,0 +1,464 @@
+// Forward kernels of the RFF linear attention (Eq.(linear att), Sec. 2.2) with
+// the Flexformer feature maps (Eq.(phi_n) / Eq.(phi_non), Sec. 3.1-3.2).
+//
+// Work decomposition.  A workgroup owns one (b,h) slice and one contiguous
+// segment of 64-token chunks.  Its NW waves split the m frequencies: wave w
+// owns frequencies [w*FW, (w+1)*FW), i.e. 2*FW of the d' = 2m features, and
+// keeps its rows of the state S' = sum_j phi(K_j) [V_j ; 1]^T (d' x (dv+1),
+// fp32) as MFMA accumulators.  Per chunk a wave forms phi(Q), phi(K) for its
+// features on chip (projection + fused trig, never written to memory), adds
+// its partial readout phi(Q) S' plus the intra-chunk masked term
+// tril(phi(Q) phi(K)^T) [V;1], and the partials of the NW waves are summed in
+// LDS before O = num / den is written.
+//
+// Causal sequences are split into segments for occupancy:
+//   k_fwd_state  : segment-local states (one pass over K, V),
+//   k_state_scan : exclusive prefix over segments (causal) or the total
+//                  (non-causal), fixed order, deterministic,
+//   k_fwd_sweep  : per segment, carry-in state + chunk sweep, writes O, den.
+#include "flex_common.hpp"
+#include "flex_kernels.hpp"
+
+namespace flex {
+
+template <class T, int D, int FW, int NW, bool NS>
+struct Shape {
+  static constexpr int M = FW * NW;
+  static constexpr int FT = FW / 16;        // frequency tiles per wave
+  static constexpr int FC = 2 * FT;         // feature tiles per wave
+  static constexpr int DV = D;
+  static constexpr int DVT = DV / 16;       // value tiles
+  static constexpr int DVT1 = DVT + 1;      // + the normaliser tile
+  static constexpr int KT = CHUNK / 32;     // k-steps over the tokens of a chunk
+  static constexpr int PR = NS ? 2 * FT : FT;
+  static constexpr int NT = NW * WAVE;      // threads per workgroup
+  // fp32 floats of one wave's state, one (b,h,segment) block of the workspace
+  static constexpr int WAVE_STATE = FC * DVT1 * WAVE * 4;
+  static constexpr int STATE = NW * WAVE_STATE;
+  // LDS row strides (elements); multiples of 4 keep 8/16-byte alignment
+  static constexpr int TPAD = CHUNK + 4;
+  static constexpr int RPAD = DVT1 * 16 + 4;
+};
+
+typedef Frag<__bf16> FB;
+
+// Fragment with 1 in row/column 0 and 0 elsewhere: as the value operand it
+// appends the ones column of [V | 1] that produces the normaliser.
+template <class T>
+__device__ __forceinline__ Frag<T> ones_col0() {
+  Frag<T> f;
+  const float v = (threadIdx.x % 16) == 0 ? 1.0f : 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f.set(j, v);
+  return f;
+}
+
+// Stage the chunk's value rows into LDS transposed, VT[c][t] = V[tok0+t][c],
+// zero for tokens at or beyond n.  All threads participate.
+template <class T, class SH>
+__device__ __forceinline__ void stage_vt(T* VT, const typename Io<T>::type* __restrict__ V,
+                                         int tok0, int n) {
+  constexpr int PER_ROW = SH::DV / 8;
+  for (int it = threadIdx.x; it < CHUNK * PER_ROW; it += SH::NT) {
+    const int t = it / PER_ROW, c8 = it % PER_ROW;
+    Frag<T> x;
+    load8(x, V + (size_t)(tok0 + t) * SH::DV + 8 * c8, tok0 + t < n);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) VT[(8 * c8 + j) * SH::TPAD + t] = (T)x.get(j);
+  }
+}
+
+// Operand fragment over the chunk's tokens from a token-contiguous LDS row:
+// slots j<4 take tokens 32ks+4g+j, slots j>=4 tokens 32ks+16+4g+j-4.  This is
+// the token order of a pair of accumulator tiles (see pair_tiles).
+template <class T>
+__device__ __forceinline__ Frag<T> lds_tok_frag(const T* row, int ks) {
+  const int g = (threadIdx.x % WAVE) / 16;
+  Frag<T> f;
+  const T* a = row + 32 * ks + 4 * g;
+  const T* b = a + 16;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) { f.set(j, (float)a[j]); f.set(4 + j, (float)b[j]); }
+  return f;
+}
+template <>
+__device__ __forceinline__ Frag<__bf16> lds_tok_frag<__bf16>(const __bf16* row, int ks) {
+  const int g = (threadIdx.x % WAVE) / 16;
+  const __bf16* a = row + 32 * ks + 4 * g;
+  bf16x4 lo = *reinterpret_cast<const bf16x4*>(a);
+  bf16x4 hi = *reinterpret_cast<const bf16x4*>(a + 16);
+  Frag<__bf16> f;
+  f.v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return f;
+}
+
+// Two accumulator tiles whose rows are consecutive 16-blocks of a contraction
+// index, as one operand fragment (slots 0..3 from the first, 4..7 from the second).
+template <class T>
+__device__ __forceinline__ Frag<T> pair_tiles(const f32x4& a, const f32x4& b) {
+  Frag<T> f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { f.set(i, a[i]); f.set(4 + i, b[i]); }
+  return f;
+}
+
+// Write one wave's phi(K) fragment for frequency tile ft and token tile tt
+// into its feature-major LDS block PT[feature][token].
+template <class T, class SH>
+__device__ __forceinline__ void store_phiT(T* PT, const Frag<T>& f, int ft, int tt) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int t = tt * 16 + r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    PT[((2 * ft) * 16 + 4 * g + i) * SH::TPAD + t] = (T)f.get(i);
+    PT[((2 * ft + 1) * 16 + 4 * g + i) * SH::TPAD + t] = (T)f.get(4 + i);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Segment-local state: S'_seg = sum over the segment's tokens of phi(K)[V;1]^T.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS>
+__global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef typename Io<T>::type IO;
+  __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];
+
+  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int w = threadIdx.x / WAVE;
+  const int c0 = seg * a.chunks_per_seg;
+  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
+  const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
+
+  FreqSlice<T, D, FW, NS> fs;
+  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  const float inv_c = __expf(-a.tau[h]);
+
+  f32x4 S[SH::FC][SH::DVT1];
+#pragma unroll
+  for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt) S[fc][dt] = zero4();
+  const Frag<T> ones = ones_col0<T>();
+  const int r = (threadIdx.x % WAVE) % 16;
+
+  for (int c = c0; c < c1; ++c) {
+    const int tok0 = c * CHUNK;
+    __syncthreads();
+    stage_vt<T, SH>(VT, V, tok0, a.N);
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      f32x4 p[SH::PR];
+      float ssq;
+      project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
+      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft)
+        store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < SH::KT; ++ks) {
+      Frag<T> vf[SH::DVT];
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) {
+        const Frag<T> pk = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk, vf[dt]);
+        mma(S[fc][SH::DVT], pk, ones);
+      }
+    }
+  }
+  float* out = a.state + ((size_t)bh * a.segments + seg) * SH::STATE + (size_t)w * SH::WAVE_STATE;
+  const int l = threadIdx.x % WAVE;
+#pragma unroll
+  for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+      *reinterpret_cast<f32x4*>(out + ((fc * SH::DVT1 + dt) * WAVE + l) * 4) = S[fc][dt];
+}
+
+// ---------------------------------------------------------------------------
+// Exclusive prefix over segments (causal) or total into segment 0 (non-causal).
+// state: [BH][P][E] fp32.  Fixed summation order.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_state_scan(float* state, int P, int E, int causal, int reverse) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= E) return;
+  float* s = state + (size_t)blockIdx.y * P * E + e;
+  float acc = 0.f;
+  if (causal) {
+    for (int k = 0; k < P; ++k) {
+      const int p = reverse ? P - 1 - k : k;
+      const float v = s[(size_t)p * E];
+      s[(size_t)p * E] = acc;
+      acc += v;
+    }
+  } else {
+    for (int p = 0; p < P; ++p) acc += s[(size_t)p * E];
+    s[0] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Sweep: carry-in state, then per chunk the readout (and, causal, the
+// intra-chunk term and the state update).  Writes O and den.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG>
+__global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef typename Io<T>::type IO;
+  constexpr int VT_N = CAUSAL ? SH::DV * SH::TPAD : 1;
+  constexpr int PT_N = CAUSAL ? SH::FC * 16 * SH::TPAD : 1;
+  __shared__ __attribute__((aligned(16))) T VT[VT_N];
+  __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
+  __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][SH::RPAD];
+
+  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int c0 = seg * a.chunks_per_seg;
+  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
+  const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
+  const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
+  IO* O = static_cast<IO*>(a.O) + (size_t)bh * a.N * SH::DV;
+  float* den = a.den ? a.den + (size_t)bh * a.N : nullptr;
+
+  FreqSlice<T, D, FW, NS> fs;
+  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  const float inv_c = __expf(-a.tau[h]);
+
+  // carry-in state (exclusive prefix for causal, total for non-causal)
+  f32x4 S[SH::FC][SH::DVT1];
+  {
+    const float* in = a.state + ((size_t)bh * a.segments + (CAUSAL ? seg : 0)) * SH::STATE +
+                      (size_t)w * SH::WAVE_STATE;
+#pragma unroll
+    for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT1; ++dt)
+        S[fc][dt] = *reinterpret_cast<const f32x4*>(in + ((fc * SH::DVT1 + dt) * WAVE + l) * 4);
+  }
+  const Frag<T> ones = ones_col0<T>();
+
+  for (int c = c0; c < c1; ++c) {
+    const int tok0 = c * CHUNK;
+    __syncthreads();
+    if (CAUSAL) stage_vt<T, SH>(VT, V, tok0, a.N);
+
+    Frag<T> pq[SH::FT][TT];
+    Frag<T> pk[SH::FT][TT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      f32x4 p[SH::PR];
+      float ssq;
+      project_tile<T, D, FW, NS>(fs, Q, tok0 + tt * 16, a.N, p, ssq);
+      float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) pq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
+      if (CAUSAL) {
+        project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
+        sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+#pragma unroll
+        for (int ft = 0; ft < SH::FT; ++ft) {
+          pk[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
+          store_phiT<T, SH>(PT[w], pk[ft][tt], ft, tt);
+        }
+      }
+    }
+
+    // state operand for the readout: rows = value columns, k = this wave's features
+    Frag<T> sf[SH::DVT1][SH::FT];
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) sf[dt][ft] = pair_tiles<T>(S[2 * ft][dt], S[2 * ft + 1][dt]);
+
+    // intra-chunk kernel matrix, transposed: AT[tk][tq] rows = key tokens, cols = query tokens
+    Frag<T> ap[CAUSAL ? SH::KT : 1][TT];
+    if (CAUSAL) {
+#pragma unroll
+      for (int tq = 0; tq < TT; ++tq) {
+        f32x4 at[TT];
+#pragma unroll
+        for (int tk = 0; tk < TT; ++tk) {
+          at[tk] = zero4();
+          if (tk <= tq) {
+#pragma unroll
+            for (int ft = 0; ft < SH::FT; ++ft) mma(at[tk], pk[ft][tk], pq[ft][tq]);
+            if (tk == tq) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                if (4 * g + i > r) at[tk][i] = 0.f;
+            }
+          }
+        }
+#pragma unroll
+        for (int ks = 0; ks < SH::KT; ++ks) ap[ks][tq] = pair_tiles<T>(at[2 * ks], at[2 * ks + 1]);
+      }
+    }
+    __syncthreads();
+
+    Frag<T> vf[CAUSAL ? SH::DVT : 1][SH::KT];
+    if (CAUSAL) {
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT; ++dt)
+#pragma unroll
+        for (int ks = 0; ks < SH::KT; ++ks) vf[dt][ks] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+    }
+
+    // readout partials, reduced across waves in groups of QG query tiles
+#pragma unroll
+    for (int q0 = 0; q0 < TT; q0 += QG) {
+      if (q0 > 0) __syncthreads();
+#pragma unroll
+      for (int qq = 0; qq < QG; ++qq) {
+        const int tq = q0 + qq;
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT1; ++dt) {
+          f32x4 acc = zero4();
+          if (CAUSAL) {
+#pragma unroll
+            for (int ks = 0; ks < SH::KT; ++ks)
+              if (32 * ks <= 16 * tq + 15) mma(acc, dt < SH::DVT ? vf[dt][ks] : ones, ap[ks][tq]);
+          }
+#pragma unroll
+          for (int ft = 0; ft < SH::FT; ++ft) mma(acc, sf[dt][ft], pq[ft][tq]);
+          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = acc;
+        }
+      }
+      if (CAUSAL && q0 + QG >= TT) {
+        // state update S' += phi(K)^T [V | 1] with this wave's transposed phi(K)
+#pragma unroll
+        for (int ks = 0; ks < SH::KT; ++ks)
+#pragma unroll
+          for (int fc = 0; fc < SH::FC; ++fc) {
+            const Frag<T> pkt = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+            for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pkt, vf[dt][ks]);
+            mma(S[fc][SH::DVT], pkt, ones);
+          }
+      }
+      __syncthreads();
+      constexpr int C4 = SH::DV / 4;
+      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
+        const int t = it / C4, c4 = it % C4;
+        const int tok = tok0 + q0 * 16 + t;
+        float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+        float dn = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) {
+          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
+          num.x += v.x; num.y += v.y; num.z += v.z; num.w += v.w;
+          dn += RED[ww][t][SH::DV];
+        }
+        if (tok < a.N) {
+          IO* o = O + (size_t)tok * SH::DV + 4 * c4;
+          o[0] = float_to_io<IO>(num.x / dn);
+          o[1] = float_to_io<IO>(num.y / dn);
+          o[2] = float_to_io<IO>(num.z / dn);
+          o[3] = float_to_io<IO>(num.w / dn);
+          if (den && c4 == 0) den[tok] = dn;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Standalone feature map: Phi [B,H,N,2m], [cos | sin] blocks.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS>
+__global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef typename Io<T>::type IO;
+  const int c = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const IO* X = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
+  IO* Phi = static_cast<IO*>(a.O) + (size_t)bh * a.N * (2 * SH::M);
+  FreqSlice<T, D, FW, NS> fs;
+  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  const float inv_c = __expf(-a.tau[h]);
+  const int tok0 = c * CHUNK;
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) {
+    f32x4 p[SH::PR];
+    float ssq;
+    project_tile<T, D, FW, NS>(fs, X, tok0 + tt * 16, a.N, p, ssq);
+    const int tok = tok0 + tt * 16 + r;
+    // the values are produced in fp32 and rounded once to the io dtype
+    const float sc = row_scale(ssq, inv_c, a.s_const, tok < a.N);
+#pragma unroll
+    for (int ft = 0; ft < SH::FT; ++ft) {
+      const Frag<float> f = features<float, SH::FT, NS>(p, ft, sc);
+      if (tok < a.N) {
+        const int f0 = w * FW + ft * 16 + 4 * g;
+        IO* row = Phi + (size_t)tok * (2 * SH::M);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          row[f0 + i] = float_to_io<IO>(f.get(i));
+          row[SH::M + f0 + i] = float_to_io<IO>(f.get(4 + i));
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host-side dispatch.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS>
+static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  constexpr int QG = (SH::DV >= 128) ? 1 : TT;
+  dim3 grid(a.segments, a.BH);
+  k_fwd_state<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
+  dim3 sgrid((SH::STATE + 255) / 256, a.BH);
+  k_state_scan<<<sgrid, 256, 0, st>>>(a.state, a.segments, SH::STATE, causal ? 1 : 0, 0);
+  if (causal)
+    k_fwd_sweep<T, D, FW, NW, NS, true, QG><<<grid, SH::NT, 0, st>>>(a);
+  else
+    k_fwd_sweep<T, D, FW, NW, NS, false, QG><<<grid, SH::NT, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+template <class T, int D, int FW, int NW, bool NS>
+static hipError_t run_fmap_t(const FwdArgs& a, hipStream_t st) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  dim3 grid(a.nchunks, a.BH);
+  k_feature_map<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+template <class T, int D, int FW, int NW>
+static hipError_t run_variant(const FwdArgs& a, bool ns, bool causal, bool fmap, hipStream_t st) {
+  if (fmap) return ns ? run_fmap_t<T, D, FW, NW, true>(a, st) : run_fmap_t<T, D, FW, NW, false>(a, st);
+  return ns ? run_fwd_t<T, D, FW, NW, true>(a, causal, st) : run_fwd_t<T, D, FW, NW, false>(a, causal, st);
+}
+
+hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStream_t st) {
+  const bool ns = ks.nonstationary, causal = ks.causal;
+  if (ks.bf16) {
+    if (ks.d == 32 && ks.m == 64) return run_variant<__bf16, 32, 16, 4>(a, ns, causal, fmap, st);
+    if (ks.d == 64 && ks.m == 64) return run_variant<__bf16, 64, 16, 4>(a, ns, causal, fmap, st);
+    if (ks.d == 64 && ks.m == 128) return run_variant<__bf16, 64, 32, 4>(a, ns, causal, fmap, st);
+    if (ks.d == 128 && ks.m == 256) return run_variant<__bf16, 128, 32, 8>(a, ns, causal, fmap, st);
+  } else {
+    if (ks.d == 32 && ks.m == 64) return run_variant<float, 32, 16, 4>(a, ns, causal, fmap, st);
+    if (ks.d == 64 && ks.m == 64) return run_variant<float, 64, 16, 4>(a, ns, causal, fmap, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+size_t fwd_state_floats(const KernelShape& ks) {
+  const int fw = (ks.m == 64) ? 16 : 32;
+  const int nw = ks.m / fw;
+  const int fc = 2 * (fw / 16);
+  return (size_t)nw * fc * (ks.d / 16 + 1) * WAVE * 4;
+}
+
+}  // namespace flex

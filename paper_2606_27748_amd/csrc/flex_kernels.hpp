@@ -1,0 +1,63 @@
+// Internal interface between the C ABI (flex_api.hip) and the kernel files.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+namespace flex {
+
+struct KernelShape {
+  bool bf16;
+  bool nonstationary;
+  bool causal;
+  int d, m;
+};
+
+struct FwdArgs {
+  const void* Q;      // also the input X of the feature map
+  const void* K;
+  const void* V;
+  const float* W1;
+  const float* W2;
+  const float* tau;
+  void* O;            // also the output Phi of the feature map
+  float* den;
+  float* state;       // [BH][segments][state floats]
+  int BH, H, N;
+  int nchunks, segments, chunks_per_seg;
+  float s_const;      // sigma/sqrt(m) or sigma/(2 sqrt(m))
+};
+
+struct BwdArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  const float* W1;
+  const float* W2;
+  const float* tau;
+  const void* O;
+  const float* den;
+  const void* dO;
+  float* dQ;
+  float* dK;
+  float* dV;
+  float* dW1;
+  float* dW2;
+  float* dtau;
+  float* sstate;      // [BH][segments][state floats]: key-side prefix states
+  float* rstate;      // [BH][segments][state floats]: query-side suffix states
+  float* dwpart;      // [BH][segments][rows][d] frequency-gradient partials
+  float* dtaupart;    // [BH][segments] partial dtau
+  int BH, B, H, N;
+  int nchunks, segments, chunks_per_seg;
+  float s_const;
+};
+
+// fp32 floats of one (b,h,segment) state block for a shape.
+size_t fwd_state_floats(const KernelShape& ks);
+size_t bwd_state_floats(const KernelShape& ks);
+size_t bwd_dw_floats(const KernelShape& ks);
+
+hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);
+hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);
+
+}  // namespace flex

