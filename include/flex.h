@@ -38,8 +38,8 @@
  *   - Results are deterministic (bitwise identical from run to run).
  *   - Supported shapes: N >= 1 (a ragged last chunk is masked); d = dv in
  *     {32, 64, 128}; m in {64, 128, 256} with the combinations
- *     (d, m) = (32, 64), (64, 64), (64, 128), (128, 256); chunk = 64.
- *     Others return FLEX_ERR_UNSUPPORTED.
+ *     (d, m) = (32, 64), (64, 64), (64, 128), (128, 256) with io_dtype FLEX_BF16,
+ *     and (32, 64) with FLEX_F32; chunk = 64.  Others return FLEX_ERR_UNSUPPORTED.
  *   - io_dtype FLEX_F32 computes every contraction in fp32 (MFMA f32);
  *     FLEX_BF16 reads bf16 inputs, projects with a two-term bf16 split of the
  *     frequencies and contracts bf16 features with fp32 accumulation.

@@ -272,5 +272,5 @@ def linattn_bwd(Q, K, V, W1, W2, tau, dO, variant, causal, sigma=1.0, return_aux
     out = dict(dQ=dQ, dK=dK, dV=dV, dW1=dW1q + dW1k,
                dW2=None if dW2q is None else dW2q + dW2k, dtau=dtq + dtk)
     if return_aux:
-        out.update(O=O, den=den, g_q=gq, g_k=gk, G=G)
+        out.update(O=O, den=den, g_q=gq, g_k=gk, G=G, phi_k=pk, dphi_k=dpk)
     return out

@@ -19,11 +19,14 @@ bool shape_supported(const flex_desc* d) {
   if (d->chunk != 0 && d->chunk != kChunk) return false;
   const bool bf = d->io_dtype == FLEX_BF16;
   if (d->d == 32 && d->m == 64) return true;
-  if (d->d == 64 && d->m == 64) return true;
+  if (d->d == 64 && d->m == 64) return bf;
   if (d->d == 64 && d->m == 128) return bf;
   if (d->d == 128 && d->m == 256) return bf;
   return false;
 }
+
+// The backward additionally needs the (d, m) shapes its kernels are built for.
+bool bwd_supported(const flex_desc* d) { return !(d->d == 128 && d->m == 256); }
 
 // 0 = ok, else a flex_status
 int32_t check_desc(const flex_desc* d) {
@@ -90,8 +93,10 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
   const size_t P = (size_t)pick_segments(d);
   if (pass == FLEX_PASS_FEATURE_MAP) return 0;
   if (pass == FLEX_PASS_FWD) return align256(bh * P * fwd_state_floats(ks) * sizeof(float));
-  // backward: key-side and query-side states, frequency-gradient and dtau partials
+  // backward: key-side and query-side states, per-token scalars, frequency-gradient
+  // and dtau partials
   return 2 * align256(bh * P * bwd_state_floats(ks) * sizeof(float)) +
+         align256(bh * (size_t)d->N * 2 * sizeof(float)) +
          align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
 }
 
@@ -174,6 +179,7 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
                          float* dW2, float* dtau, void* ws, size_t ws_bytes, void* stream) {
   const int32_t st = check_desc(desc);
   if (st != FLEX_OK) return st;
+  if (!bwd_supported(desc)) return FLEX_ERR_UNSUPPORTED;
   const bool ns = desc->variant == FLEX_NONSTATIONARY;
   if (!Q || !K || !V || !W1 || !tau || !O || !den || !dO || !dQ || !dK || !dV || !dW1)
     return FLEX_ERR_INVALID_ARG;
@@ -198,10 +204,12 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   const size_t bh = (size_t)a.BH, P = (size_t)a.segments;
   char* base = static_cast<char*>(ws);
   const size_t sb = align256(bh * P * bwd_state_floats(ks) * sizeof(float));
+  const size_t gb = align256(bh * (size_t)a.N * 2 * sizeof(float));
   a.sstate = reinterpret_cast<float*>(base);
   a.rstate = reinterpret_cast<float*>(base + sb);
-  a.dwpart = reinterpret_cast<float*>(base + 2 * sb);
-  a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
+  a.gstats = reinterpret_cast<float*>(base + 2 * sb);
+  a.dwpart = reinterpret_cast<float*>(base + 2 * sb + gb);
+  a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
   const hipError_t e = launch_bwd(a, ks, (hipStream_t)stream);
   return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
 }

@@ -1,11 +1,1011 @@
-// Backward kernels (placeholder until the backward sweep lands).
+// Backward kernels of the RFF linear attention (Eq.(linear att) with the
+// Flexformer feature maps of Eq.(phi_n) / Eq.(phi_non)).  The paper gives no
+// backward; this is the derivative of the forward:
+//
+//   [num|den]_i = sum_j a_ij [V_j ; 1],  a_ij = phi(Q_i).phi(K_j)  (j <= i if causal)
+//   G_i = [dO_i ; -delta_i] / den_i,     delta_i = dO_i . O_i
+//   dphi(Q_i) = S'_i G_i,   S'_i = sum_{j(<=i)} phi(K_j) [V_j;1]^T
+//   dphi(K_j) = R'_j [V_j;1], R'_j = sum_{i(>=j)} phi(Q_i) G_i^T
+//   dV_j = (R'_j^T phi(K_j))[:dv]
+// then the feature-map chain rule (frequencies and norm factor exp(||x||^2/c)).
+//
+// Kernels (per (b,h) slice, sequence split into segments like the forward):
+//   k_bwd_prepass : segment-local S'^T (key side) and R'^T (query side), and the
+//                   per-token scalars 1/den_i, delta_i,
+//   k_state_scan  : prefix of S' and suffix of R' over segments,
+//   k_bwd_dq      : ascending chunk sweep carrying S'; dQ and the query-side
+//                   frequency-gradient partials,
+//   k_bwd_dkv     : descending chunk sweep carrying R'; dK, dV, the key-side
+//                   frequency-gradient partials and dtau partials,
+//   k_bwd_reduce  : fixed-order sums of the partials into dW1, dW2, dtau.
+// Waves split the frequencies as in the forward.  Both states are held as
+// accumulator tiles with value columns as rows ([dv' x features]).
 #include "flex_common.hpp"
 #include "flex_kernels.hpp"
+#include "flex_stage.hpp"
 
 namespace flex {
 
+// Feature fragment (as in the forward) plus, for the nonstationary variant,
+// the fragment of d phi / d P2 up to sign: slots [s e sin P2 cos P1 | s e sin P2 sin P1].
+template <class T, int FT, bool NS>
+__device__ __forceinline__ void features_psi(const f32x4 (&p)[NS ? 2 * FT : FT], int ft, float scale,
+                                             Frag<T>& phi, Frag<T>& psi) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float s1, c1;
+    sincos_rev(p[ft][i], s1, c1);
+    if (NS) {
+      float s2, c2;
+      sincos_rev(p[FT + ft][i], s2, c2);
+      const float sc = scale * c2, ss = scale * s2;
+      phi.set(i, c1 * sc);
+      phi.set(4 + i, s1 * sc);
+      psi.set(i, c1 * ss);
+      psi.set(4 + i, s1 * ss);
+    } else {
+      phi.set(i, c1 * scale);
+      phi.set(4 + i, s1 * scale);
+    }
+  }
+}
+
+// A-operand fragments of W'^T (rows = input dimension d, k = projection rows of
+// this wave, paired tiles) in radians, bf16 hi + lo on the bf16 path.  Used for
+// dX = dP W'.  Projection row tile pr < FT is W'1 (or W), pr >= FT is W'2.
+template <class T, int D, int FW, bool NS>
+struct WTSlice {
+  static constexpr int FT = FW / 16;
+  static constexpr int PR = NS ? 2 * FT : FT;
+  static constexpr int KP = (PR + 1) / 2;      // k-steps over the projection rows
+  static constexpr int DT = D / 16;
+  static constexpr int NSPLIT = IsBf16<T>::value ? 2 : 1;
+  Frag<T> w[NSPLIT][DT][KP];
+
+  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
+    const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int dcol = dt * 16 + r;
+#pragma unroll
+      for (int ks = 0; ks < KP; ++ks) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int pr = 2 * ks + (j >= 4 ? 1 : 0);
+          float v = 0.f;
+          if (pr < PR) {
+            const int f = f0 + (pr % FT) * 16 + 4 * g + (j & 3);
+            const float x = W1[(size_t)f * D + dcol];
+            if (NS) {
+              const float y = W2[(size_t)f * D + dcol];
+              v = pr >= FT ? 0.5f * (x - y) : 0.5f * (x + y);
+            } else {
+              v = x;
+            }
+          }
+          if (IsBf16<T>::value) {
+            const float hi = (float)(__bf16)v;
+            w[0][dt][ks].set(j, hi);
+            w[NSPLIT - 1][dt][ks].set(j, v - hi);
+          } else {
+            w[0][dt][ks].set(j, v);
+          }
+        }
+      }
+    }
+  }
+};
+
+// -x as a two-term operand split (hi, lo): exact to about 16 bits on the bf16
+// path.  The backward states carry the normaliser products in two rows of the
+// normaliser tile (value columns dv and dv+1) so that delta_i is not rounded
+// to bf16 on its way into them.
+template <class T>
+__device__ __forceinline__ void neg_split(float x, float& hi, float& lo) {
+  if (IsBf16<T>::value) {
+    hi = (float)(__bf16)(-x);
+    lo = -x - hi;
+  } else {
+    hi = -x;
+    lo = 0.f;
+  }
+}
+template <class T>
+__device__ __forceinline__ Frag<T> ones_col01() {
+  Frag<T> f;
+  const float v = (threadIdx.x % 16) < 2 ? 1.0f : 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f.set(j, v);
+  return f;
+}
+// Normaliser-row operand over chunk tokens k-step ks: rows dv, dv+1 hold the
+// split of -delta_t for the tokens of the paired-tile order.
+template <class T>
+__device__ __forceinline__ Frag<T> delta_rows(const float (*GS)[2], int ks) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  Frag<T> f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int t = 32 * ks + (j >= 4 ? 16 : 0) + 4 * g + (j & 3);
+    float hi, lo;
+    neg_split<T>(GS[t][1], hi, lo);
+    f.set(j, r == 0 ? hi : (r == 1 ? lo : 0.f));
+  }
+  return f;
+}
+
+// Register-dump layout of a wave's [dv' x features] state: tile (dt, fc).
+template <class SH>
+__device__ __forceinline__ size_t state_off(int w, int dt, int fc, int l) {
+  return (size_t)w * SH::WAVE_STATE + ((size_t)(dt * SH::FC + fc) * WAVE + l) * 4;
+}
+
+// Chain rule through one wave's features for frequency tile ft, token tile tt:
+// dP (per radian) for the projection rows, and <phi, dphi> summed over this
+// lane's slots.
+template <class T, int FT, bool NS>
+__device__ __forceinline__ float feature_grad(const Frag<T>& phi, const Frag<T>& psi,
+                                              const f32x4& da, const f32x4& db, f32x4& dp1, f32x4& dp2) {
+  float gsum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a = phi.get(i), b = phi.get(4 + i);
+    dp1[i] = a * db[i] - b * da[i];
+    if (NS) dp2[i] = -(psi.get(i) * da[i] + psi.get(4 + i) * db[i]);
+    gsum += a * da[i] + b * db[i];
+  }
+  return gsum;
+}
+
+// Write a dP tile (rows = projection rows of tile pr, cols = tokens of tile tt)
+// transposed into the wave's LDS block DPT[row][token].
+template <class T, class SH>
+__device__ __forceinline__ void store_dpT(T* DPT, const f32x4& v, int pr, int tt) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) DPT[(pr * 16 + 4 * g + i) * SH::TPAD + tt * 16 + r] = (T)v[i];
+}
+
+// Write a wave's frequency-gradient partial tiles DW[pr][dt] (rows = projection
+// rows, cols = d) into the canonical layout [matrix][m][d].
+template <class SH, int D, int FW, bool NS>
+__device__ __forceinline__ void dump_dw(float* out, const f32x4 (&DW)[SH::PR][D / 16], int f0) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+#pragma unroll
+  for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int mat = pr >= SH::FT ? 1 : 0;
+        const int f = f0 + (pr % SH::FT) * 16 + 4 * g + i;
+        out[((size_t)mat * SH::M + f) * D + dt * 16 + r] = DW[pr][dt][i];
+      }
+}
+
+// ---------------------------------------------------------------------------
+// Pre-pass: segment-local S'^T = sum [V;1]^T-rows x phi(K) and
+// R'^T = sum [dO;-delta]^T-rows x phi(Q)/den; per-token 1/den and delta.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS>
+__global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef typename Io<T>::type IO;
+  typedef RowStage<IO, D, SH::NT> StX;
+  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XO[StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T DOT[SH::DV * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T PK[NW][SH::FC * 16 * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T PQ[NW][SH::FC * 16 * SH::TPAD];
+  __shared__ float GS[CHUNK][2];
+  __shared__ float DEN[CHUNK];
+
+  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int c0 = seg * a.chunks_per_seg;
+  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
+  const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
+  const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
+  const IO* dO = static_cast<const IO*>(a.dO) + (size_t)bh * a.N * SH::DV;
+  const IO* Ob = static_cast<const IO*>(a.O) + (size_t)bh * a.N * SH::DV;
+  const float* den = a.den + (size_t)bh * a.N;
+  float* gst = a.gstats + (size_t)bh * a.N * 2;
+
+  StX sq, sk;
+  StV sv, sdo, so;
+  float dn_next = 0.f;
+  if (c0 < c1) {
+    sq.fetch(Q, c0 * CHUNK, a.N); sk.fetch(K, c0 * CHUNK, a.N);
+    sv.fetch(V, c0 * CHUNK, a.N); sdo.fetch(dO, c0 * CHUNK, a.N); so.fetch(Ob, c0 * CHUNK, a.N);
+    if (threadIdx.x < CHUNK && c0 * CHUNK + (int)threadIdx.x < a.N) dn_next = den[c0 * CHUNK + threadIdx.x];
+  }
+  FreqSlice<T, D, FW, NS> fs;
+  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  const float inv_c = __expf(-a.tau[h]);
+
+  f32x4 ST[SH::DVT1][SH::FC], RT[SH::DVT1][SH::FC];
+#pragma unroll
+  for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+    for (int fc = 0; fc < SH::FC; ++fc) { ST[dt][fc] = zero4(); RT[dt][fc] = zero4(); }
+  const Frag<T> ones = ones_col01<T>();
+  constexpr int TPT = SH::NT / CHUNK;  // threads per token for the row reductions
+
+  for (int c = c0; c < c1; ++c) {
+    const int tok0 = c * CHUNK;
+    __syncthreads();
+    sq.store(XQ); sk.store(XK); sdo.store(XDO); so.store(XO);
+    sv.template store_t<T, SH::TPAD>(VT);
+    sdo.template store_t<T, SH::TPAD>(DOT);
+    if (threadIdx.x < CHUNK) DEN[threadIdx.x] = dn_next;
+    if (c + 1 < c1) {
+      const int t1 = tok0 + CHUNK;
+      sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N);
+      sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N); so.fetch(Ob, t1, a.N);
+      dn_next = (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N) ? den[t1 + threadIdx.x] : 0.f;
+    }
+    __syncthreads();
+    // per-token 1/den and delta = dO . O
+    {
+      const int t = threadIdx.x / TPT, part = threadIdx.x % TPT;
+      float s = 0.f;
+      for (int cidx = part; cidx < SH::DV; cidx += TPT)
+        s += io_to_float(XDO[t * StV::LD + cidx]) * io_to_float(XO[t * StV::LD + cidx]);
+#pragma unroll
+      for (int o = 1; o < TPT; o <<= 1) s += __shfl_xor(s, o);
+      if (part == 0) {
+        const bool ok = tok0 + t < a.N;
+        const float inv = ok ? 1.0f / DEN[t] : 0.f;
+        GS[t][0] = inv;
+        GS[t][1] = ok ? s : 0.f;
+        if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = s; }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      f32x4 p[SH::PR];
+      float ssq;
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
+      float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PK[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+      sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PQ[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < SH::KT; ++ks) {
+      // value-side operands: rows = value columns, k = chunk tokens
+      Frag<T> vt[SH::DVT1], gt[SH::DVT1];
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT; ++dt) {
+        vt[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        gt[dt] = lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks);
+      }
+      vt[SH::DVT] = ones;
+      gt[SH::DVT] = delta_rows<T>(GS, ks);
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) {
+        const Frag<T> pk = lds_tok_frag<T>(PK[w] + (fc * 16 + r) * SH::TPAD, ks);
+        const Frag<T> pq = lds_tok_frag<T>(PQ[w] + (fc * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT1; ++dt) {
+          mma(ST[dt][fc], vt[dt], pk);
+          mma(RT[dt][fc], gt[dt], pq);
+        }
+      }
+    }
+  }
+  float* so_ = a.sstate + ((size_t)bh * a.segments + seg) * SH::STATE;
+  float* ro_ = a.rstate + ((size_t)bh * a.segments + seg) * SH::STATE;
+#pragma unroll
+  for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+    for (int fc = 0; fc < SH::FC; ++fc) {
+      *reinterpret_cast<f32x4*>(so_ + state_off<SH>(w, dt, fc, l)) = ST[dt][fc];
+      *reinterpret_cast<f32x4*>(ro_ + state_off<SH>(w, dt, fc, l)) = RT[dt][fc];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dQ: ascending sweep with the key-side prefix state S'.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL>
+__global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef typename Io<T>::type IO;
+  typedef RowStage<IO, D, SH::NT> StX;
+  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  typedef WTSlice<T, D, FW, NS> WTS;
+  constexpr int DT = D / 16;
+  constexpr int KG = (SH::DVT1 + 1) / 2;        // k-steps over [dO | -delta]
+  constexpr int QG = 2;                          // token tiles per reduction round
+  constexpr int RP = D + 4;
+  __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T QT[D * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(K)^T, then dP^T
+  __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
+  __shared__ float GS[CHUNK][2];
+
+  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int c0 = seg * a.chunks_per_seg;
+  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
+  const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
+  const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
+  const IO* dO = static_cast<const IO*>(a.dO) + (size_t)bh * a.N * SH::DV;
+  const float* gst = a.gstats + (size_t)bh * a.N * 2;
+  float* dQ = a.dQ + (size_t)bh * a.N * D;
+
+  StX sq, sk;
+  StV sv, sdo;
+  float2 gs_next = make_float2(0.f, 0.f);
+  if (c0 < c1) {
+    sq.fetch(Q, c0 * CHUNK, a.N); sk.fetch(K, c0 * CHUNK, a.N);
+    sv.fetch(V, c0 * CHUNK, a.N); sdo.fetch(dO, c0 * CHUNK, a.N);
+    if (threadIdx.x < CHUNK && c0 * CHUNK + (int)threadIdx.x < a.N)
+      gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(c0 * CHUNK + threadIdx.x) * 2);
+  }
+  const float* W1h = a.W1 + (size_t)h * SH::M * D;
+  const float* W2h = NS ? a.W2 + (size_t)h * SH::M * D : nullptr;
+  FreqSlice<T, D, FW, NS> fs;
+  fs.load(W1h, W2h, w * FW);
+  WTS wt;
+  wt.load(W1h, W2h, w * FW);
+  const float inv_c = __expf(-a.tau[h]);
+
+  f32x4 ST[SH::DVT1][SH::FC];
+  {
+    const float* in = a.sstate + ((size_t)bh * a.segments + (CAUSAL ? seg : 0)) * SH::STATE;
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc)
+        ST[dt][fc] = *reinterpret_cast<const f32x4*>(in + state_off<SH>(w, dt, fc, l));
+  }
+  f32x4 DW[SH::PR][DT];
+#pragma unroll
+  for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) DW[pr][dt] = zero4();
+  const Frag<T> ones = ones_col01<T>();
+
+  for (int c = c0; c < c1; ++c) {
+    const int tok0 = c * CHUNK;
+    __syncthreads();
+    sq.store(XQ); sk.store(XK); sv.store(XV); sdo.store(XDO);
+    sv.template store_t<T, SH::TPAD>(VT);
+    sq.template store_t<T, SH::TPAD>(QT);
+    if (threadIdx.x < CHUNK) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
+    if (c + 1 < c1) {
+      const int t1 = tok0 + CHUNK;
+      sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
+      gs_next = (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N)
+                    ? *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2)
+                    : make_float2(0.f, 0.f);
+    }
+    __syncthreads();
+
+    // phi(K) of this wave's features, transposed into LDS
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      f32x4 p[SH::PR];
+      float ssq;
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
+      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
+    }
+    // phi(Q) and its P2-derivative fragments
+    Frag<T> phq[SH::FT][TT], psq[SH::FT][TT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      f32x4 p[SH::PR];
+      float ssq;
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phq[ft][tt], psq[ft][tt]);
+    }
+    // intra-chunk M^T[j][i] = dO_i . V_j - delta_i for j <= i (1/den_i applied later)
+    Frag<T> mt[CAUSAL ? SH::KT : 1][TT];
+    if (CAUSAL) {
+#pragma unroll
+      for (int tq = 0; tq < TT; ++tq) {
+        const float dl = GS[tq * 16 + r][1];
+        f32x4 m[TT];
+#pragma unroll
+        for (int tk = 0; tk < TT; ++tk) {
+          m[tk] = zero4();
+          if (tk <= tq) {
+#pragma unroll
+            for (int kd = 0; kd < SH::DV / 32; ++kd) {
+              Frag<T> av, bo;
+              lds_row8(av, XV + (tk * 16 + r) * StV::LD, kd * 32 + 8 * g);
+              lds_row8(bo, XDO + (tq * 16 + r) * StV::LD, kd * 32 + 8 * g);
+              mma(m[tk], av, bo);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const bool keep = tk < tq || 4 * g + i <= r;
+              m[tk][i] = keep ? m[tk][i] - dl : 0.f;
+            }
+          }
+        }
+#pragma unroll
+        for (int ks = 0; ks < SH::KT; ++ks) mt[ks][tq] = pair_tiles<T>(m[2 * ks], m[2 * ks + 1]);
+      }
+    }
+    __syncthreads();  // phi(K)^T complete
+
+    // dphi(Q)^T[feature][query] = (phi(K)^T M^T + S'^T-rows x [dO | -delta]) / den
+    f32x4 dph[SH::FC][TT];
+#pragma unroll
+    for (int tq = 0; tq < TT; ++tq) {
+      Frag<T> gf[KG];
+#pragma unroll
+      for (int kd = 0; kd < KG; ++kd) {
+        if (32 * kd < SH::DV) {
+          gf[kd] = lds_tok_frag<T>(reinterpret_cast<const T*>(XDO) + (tq * 16 + r) * StV::LD, kd);
+        } else {
+          Frag<T> f;
+          f.zero();
+          float hi, lo;
+          neg_split<T>(GS[tq * 16 + r][1], hi, lo);
+          if (g == 0) { f.set(0, hi); f.set(1, lo); }
+          gf[kd] = f;
+        }
+      }
+      const float inv = GS[tq * 16 + r][0];
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) {
+        f32x4 acc = zero4();
+        if (CAUSAL) {
+#pragma unroll
+          for (int ks = 0; ks < SH::KT; ++ks)
+            if (32 * ks <= 16 * tq + 15)
+              mma(acc, lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks), mt[ks][tq]);
+        }
+#pragma unroll
+        for (int kd = 0; kd < KG; ++kd) {
+          const f32x4 z = zero4();
+          const Frag<T> sp = pair_tiles<T>(ST[2 * kd][fc], 2 * kd + 1 < SH::DVT1 ? ST[2 * kd + 1][fc] : z);
+          mma(acc, sp, gf[kd]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] *= inv;
+        dph[fc][tq] = acc;
+      }
+    }
+    if (CAUSAL) {
+      // S'^T += [V | 1]^T-rows x phi(K)
+#pragma unroll
+      for (int ks = 0; ks < SH::KT; ++ks) {
+        Frag<T> vt[SH::DVT];
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc) {
+          const Frag<T> pk = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+          for (int dt = 0; dt < SH::DVT; ++dt) mma(ST[dt][fc], vt[dt], pk);
+          mma(ST[SH::DVT][fc], ones, pk);
+        }
+      }
+    }
+    // chain rule through phi(Q): dP per radian, tiles [projection row tile][token tile]
+    f32x4 dp[SH::PR][TT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) {
+        f32x4 d2 = zero4();
+        feature_grad<T, SH::FT, NS>(phq[ft][tt], psq[ft][tt], dph[2 * ft][tt], dph[2 * ft + 1][tt], dp[ft][tt], d2);
+        if (NS) dp[SH::FT + ft][tt] = d2;
+      }
+    // dQ = sum over waves of dP W'; reduced through LDS in rounds of QG token tiles
+#pragma unroll
+    for (int q0 = 0; q0 < TT; q0 += QG) {
+      __syncthreads();
+#pragma unroll
+      for (int qq = 0; qq < QG; ++qq) {
+        const int tt = q0 + qq;
+        Frag<T> dpp[WTS::KP];
+#pragma unroll
+        for (int ks = 0; ks < WTS::KP; ++ks)
+          dpp[ks] = pair_tiles<T>(dp[2 * ks][tt], 2 * ks + 1 < SH::PR ? dp[2 * ks + 1][tt] : zero4());
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int ks = 0; ks < WTS::KP; ++ks)
+#pragma unroll
+            for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wt.w[sp][dt][ks], dpp[ks]);
+          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = acc;
+        }
+      }
+      __syncthreads();
+      constexpr int C4 = D / 4;
+      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
+        const int t = it / C4, c4 = it % C4;
+        const int tok = tok0 + q0 * 16 + t;
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) {
+          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
+          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+        if (tok < a.N) *reinterpret_cast<float4*>(dQ + (size_t)tok * D + 4 * c4) = s;
+      }
+    }
+    __syncthreads();  // every wave is done with phi(K)^T
+#pragma unroll
+    for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
+    __syncthreads();
+    // frequency gradient partial: dW'[rows][d] += dP^T Q
+#pragma unroll
+    for (int ks = 0; ks < SH::KT; ++ks) {
+      Frag<T> xq[DT];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tok_frag<T>(QT + (dt * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+      for (int pr = 0; pr < SH::PR; ++pr) {
+        const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) mma(DW[pr][dt], dpt, xq[dt]);
+      }
+    }
+  }
+  const size_t nmat = NS ? 2 : 1;
+  float* out = a.dwpart + (((size_t)0 * a.BH + bh) * a.segments + seg) * nmat * SH::M * D;
+  dump_dw<SH, D, FW, NS>(out, DW, w * FW);
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV: descending sweep with the query-side suffix state R'.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL>
+__global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef typename Io<T>::type IO;
+  typedef RowStage<IO, D, SH::NT> StX;
+  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  typedef WTSlice<T, D, FW, NS> WTS;
+  constexpr int DT = D / 16;
+  constexpr int KG = (SH::DVT1 + 1) / 2;
+  constexpr int QG = 2;
+  constexpr int RP = (D > SH::DV ? D : SH::DV) + 4;
+  constexpr int RLP = SH::FC * 16 + 4;           // row stride of the transposed R' copy
+  constexpr int RED_BYTES = NW * QG * 16 * RP * 4;
+  constexpr int RL_BYTES = NW * SH::DV * RLP * (int)sizeof(T);
+  __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) T DOT[SH::DV * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T KT[D * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(Q)^T/den, then dP^T
+  __shared__ __attribute__((aligned(16))) char REDRL[RED_BYTES > RL_BYTES ? RED_BYTES : RL_BYTES];
+  __shared__ float GS[CHUNK][2];
+  __shared__ float SSQ[CHUNK];
+  __shared__ float TRED[SH::NT];
+  typedef float RedRow[QG * 16][RP];
+  RedRow* RED = reinterpret_cast<RedRow*>(REDRL);
+  T* RL = reinterpret_cast<T*>(REDRL);
+
+  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int c0 = seg * a.chunks_per_seg;
+  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
+  const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
+  const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
+  const IO* dO = static_cast<const IO*>(a.dO) + (size_t)bh * a.N * SH::DV;
+  const float* gst = a.gstats + (size_t)bh * a.N * 2;
+  float* dK = a.dK + (size_t)bh * a.N * D;
+  float* dV = a.dV + (size_t)bh * a.N * SH::DV;
+
+  StX sq, sk;
+  StV sv, sdo;
+  float2 gs_next = make_float2(0.f, 0.f);
+  if (c0 < c1) {
+    const int t1 = (c1 - 1) * CHUNK;
+    sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
+    if (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N)
+      gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2);
+  }
+  const float* W1h = a.W1 + (size_t)h * SH::M * D;
+  const float* W2h = NS ? a.W2 + (size_t)h * SH::M * D : nullptr;
+  FreqSlice<T, D, FW, NS> fs;
+  fs.load(W1h, W2h, w * FW);
+  WTS wt;
+  wt.load(W1h, W2h, w * FW);
+  const float inv_c = __expf(-a.tau[h]);
+
+  f32x4 RT[SH::DVT1][SH::FC];
+  {
+    const float* in = a.rstate + ((size_t)bh * a.segments + (CAUSAL ? seg : 0)) * SH::STATE;
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc)
+        RT[dt][fc] = *reinterpret_cast<const f32x4*>(in + state_off<SH>(w, dt, fc, l));
+  }
+  f32x4 DW[SH::PR][DT];
+#pragma unroll
+  for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) DW[pr][dt] = zero4();
+  float dtau_acc = 0.f;
+
+  for (int c = c1 - 1; c >= c0; --c) {
+    const int tok0 = c * CHUNK;
+    __syncthreads();
+    sq.store(XQ); sk.store(XK); sv.store(XV); sdo.store(XDO);
+    sdo.template store_t<T, SH::TPAD>(DOT);
+    sk.template store_t<T, SH::TPAD>(KT);
+    if (threadIdx.x < CHUNK) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
+    if (c - 1 >= c0) {
+      const int t1 = tok0 - CHUNK;
+      sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
+      gs_next = (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N)
+                    ? *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2)
+                    : make_float2(0.f, 0.f);
+    }
+    __syncthreads();
+
+    // phi(Q)/den: fragments (for the intra-chunk kernel matrix) and transposed copy
+    // (the non-causal backward of K and V uses only the total R')
+    Frag<T> phq[SH::FT][TT];
+    if (CAUSAL) {
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) {
+        f32x4 p[SH::PR];
+        float ssq;
+        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+        const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
+#pragma unroll
+        for (int ft = 0; ft < SH::FT; ++ft) {
+          phq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
+          store_phiT<T, SH>(PT[w], phq[ft][tt], ft, tt);
+        }
+      }
+    }
+    // phi(K) and its P2-derivative fragments
+    Frag<T> phk[SH::FT][TT], psk[SH::FT][TT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      f32x4 p[SH::PR];
+      float ssq;
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
+      if (w == 0 && g == 0) SSQ[tt * 16 + r] = ssq;
+      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phk[ft][tt], psk[ft][tt]);
+    }
+    // intra-chunk M[i][j] = dO_i . V_j - delta_i and A[i][j] = phi(Q_i)/den_i . phi(K_j), i >= j
+    Frag<T> mp[CAUSAL ? SH::KT : 1][TT], ap[CAUSAL ? SH::KT : 1][TT];
+    if (CAUSAL) {
+#pragma unroll
+      for (int tk = 0; tk < TT; ++tk) {
+        f32x4 m[TT], at[TT];
+#pragma unroll
+        for (int tq = 0; tq < TT; ++tq) {
+          m[tq] = zero4();
+          at[tq] = zero4();
+          if (tq >= tk) {
+#pragma unroll
+            for (int kd = 0; kd < SH::DV / 32; ++kd) {
+              Frag<T> ao, bv;
+              lds_row8(ao, XDO + (tq * 16 + r) * StV::LD, kd * 32 + 8 * g);
+              lds_row8(bv, XV + (tk * 16 + r) * StV::LD, kd * 32 + 8 * g);
+              mma(m[tq], ao, bv);
+            }
+#pragma unroll
+            for (int ft = 0; ft < SH::FT; ++ft) mma(at[tq], phq[ft][tq], phk[ft][tk]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const bool keep = tq > tk || 4 * g + i >= r;
+              m[tq][i] = keep ? m[tq][i] - GS[tq * 16 + 4 * g + i][1] : 0.f;
+              at[tq][i] = keep ? at[tq][i] : 0.f;
+            }
+          }
+        }
+#pragma unroll
+        for (int ks = 0; ks < SH::KT; ++ks) {
+          mp[ks][tk] = pair_tiles<T>(m[2 * ks], m[2 * ks + 1]);
+          ap[ks][tk] = pair_tiles<T>(at[2 * ks], at[2 * ks + 1]);
+        }
+      }
+    }
+    // transposed copy of R' (rows = value columns, cols = this wave's features) for dV
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT; ++dt)
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          RL[(size_t)w * SH::DV * RLP + (dt * 16 + 4 * g + i) * RLP + fc * 16 + r] = (T)RT[dt][fc][i];
+    __syncthreads();  // phi(Q)^T and the R' copy complete
+
+    // dphi(K)^T[feature][key] = phi(Q)^T M + R'^T-rows x [V | 1]
+    f32x4 dph[SH::FC][TT];
+#pragma unroll
+    for (int tk = 0; tk < TT; ++tk) {
+      Frag<T> vf[KG];
+#pragma unroll
+      for (int kd = 0; kd < KG; ++kd) {
+        if (32 * kd < SH::DV) {
+          vf[kd] = lds_tok_frag<T>(reinterpret_cast<const T*>(XV) + (tk * 16 + r) * StV::LD, kd);
+        } else {
+          Frag<T> f;
+          f.zero();
+          if (g == 0) { f.set(0, 1.0f); f.set(1, 1.0f); }
+          vf[kd] = f;
+        }
+      }
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) {
+        f32x4 acc = zero4();
+        if (CAUSAL) {
+#pragma unroll
+          for (int ks = 0; ks < SH::KT; ++ks)
+            if (32 * ks + 31 >= 16 * tk)
+              mma(acc, lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks), mp[ks][tk]);
+        }
+#pragma unroll
+        for (int kd = 0; kd < KG; ++kd) {
+          const Frag<T> rp = pair_tiles<T>(RT[2 * kd][fc], 2 * kd + 1 < SH::DVT1 ? RT[2 * kd + 1][fc] : zero4());
+          mma(acc, rp, vf[kd]);
+        }
+        dph[fc][tk] = acc;
+      }
+    }
+    // dV^T partial[value col][key] = dO^T A/den (intra) + R'[:dv]^T-rows x phi(K)
+    f32x4 dvp[SH::DVT][TT];
+#pragma unroll
+    for (int tk = 0; tk < TT; ++tk)
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT; ++dt) {
+        f32x4 acc = zero4();
+        if (CAUSAL) {
+#pragma unroll
+          for (int ks = 0; ks < SH::KT; ++ks)
+            if (32 * ks + 31 >= 16 * tk) mma(acc, lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks), ap[ks][tk]);
+        }
+#pragma unroll
+        for (int ft = 0; ft < SH::FT; ++ft)
+          mma(acc, lds_tok_frag<T>(RL + (size_t)w * SH::DV * RLP + (dt * 16 + r) * RLP, ft), phk[ft][tk]);
+        dvp[dt][tk] = acc;
+      }
+    // R'^T += [dO | -delta]^T-rows x phi(Q)/den  (after every use of R'_{>c})
+    if (CAUSAL) {
+#pragma unroll
+      for (int ks = 0; ks < SH::KT; ++ks) {
+        Frag<T> gt[SH::DVT1];
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks);
+        gt[SH::DVT] = delta_rows<T>(GS, ks);
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc) {
+          const Frag<T> pq = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+          for (int dt = 0; dt < SH::DVT1; ++dt) mma(RT[dt][fc], gt[dt], pq);
+        }
+      }
+    }
+    // chain rule through phi(K)
+    f32x4 dp[SH::PR][TT];
+    float gp[TT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      float gs = 0.f;
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) {
+        f32x4 d2 = zero4();
+        gs += feature_grad<T, SH::FT, NS>(phk[ft][tt], psk[ft][tt], dph[2 * ft][tt], dph[2 * ft + 1][tt], dp[ft][tt], d2);
+        if (NS) dp[SH::FT + ft][tt] = d2;
+      }
+      gp[tt] = group_sum(gs);
+    }
+    // dV: reduce the per-wave partials
+#pragma unroll
+    for (int q0 = 0; q0 < TT; q0 += QG) {
+      __syncthreads();
+#pragma unroll
+      for (int qq = 0; qq < QG; ++qq)
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt)
+          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = dvp[dt][q0 + qq];
+      __syncthreads();
+      constexpr int C4 = SH::DV / 4;
+      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
+        const int t = it / C4, c4 = it % C4;
+        const int tok = tok0 + q0 * 16 + t;
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) {
+          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
+          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+        if (tok < a.N) *reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4) = s;
+      }
+    }
+    // dK = sum over waves of dP W' + (2/c) g k, g = <phi(K), dphi(K)>; dtau -= g ||k||^2 / c
+#pragma unroll
+    for (int q0 = 0; q0 < TT; q0 += QG) {
+      __syncthreads();
+#pragma unroll
+      for (int qq = 0; qq < QG; ++qq) {
+        const int tt = q0 + qq;
+        Frag<T> dpp[WTS::KP];
+#pragma unroll
+        for (int ks = 0; ks < WTS::KP; ++ks)
+          dpp[ks] = pair_tiles<T>(dp[2 * ks][tt], 2 * ks + 1 < SH::PR ? dp[2 * ks + 1][tt] : zero4());
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int ks = 0; ks < WTS::KP; ++ks)
+#pragma unroll
+            for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wt.w[sp][dt][ks], dpp[ks]);
+          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = acc;
+        }
+        if (g == 0) RED[w][qq * 16 + r][D] = gp[tt];
+      }
+      __syncthreads();
+      constexpr int C4 = D / 4;
+      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
+        const int t = it / C4, c4 = it % C4;
+        const int tl = q0 * 16 + t;
+        const int tok = tok0 + tl;
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        float gg = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) {
+          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
+          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+          gg += RED[ww][t][D];
+        }
+        if (tok < a.N) {
+          const float k2 = 2.0f * inv_c * gg;
+          const IO* kr = XK + tl * StX::LD + 4 * c4;
+          s.x += k2 * io_to_float(kr[0]);
+          s.y += k2 * io_to_float(kr[1]);
+          s.z += k2 * io_to_float(kr[2]);
+          s.w += k2 * io_to_float(kr[3]);
+          *reinterpret_cast<float4*>(dK + (size_t)tok * D + 4 * c4) = s;
+          if (c4 == 0) dtau_acc -= gg * SSQ[tl] * inv_c;
+        }
+      }
+    }
+    __syncthreads();  // every wave is done with phi(Q)^T
+#pragma unroll
+    for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < SH::KT; ++ks) {
+      Frag<T> xk[DT];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tok_frag<T>(KT + (dt * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+      for (int pr = 0; pr < SH::PR; ++pr) {
+        const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) mma(DW[pr][dt], dpt, xk[dt]);
+      }
+    }
+  }
+  const size_t nmat = NS ? 2 : 1;
+  float* out = a.dwpart + (((size_t)1 * a.BH + bh) * a.segments + seg) * nmat * SH::M * D;
+  dump_dw<SH, D, FW, NS>(out, DW, w * FW);
+  // dtau partial of this workgroup: fixed-order tree sum
+  TRED[threadIdx.x] = dtau_acc;
+  __syncthreads();
+  for (int s = SH::NT / 2; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) TRED[threadIdx.x] += TRED[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) a.dtaupart[(size_t)bh * a.segments + seg] = TRED[0];
+}
+
+// ---------------------------------------------------------------------------
+// Fixed-order reduction of the frequency-gradient and dtau partials.
+// dwpart: [2][B*H][P][nmat][m][d].  dW'1, dW'2 -> dW1 = (dW'1+dW'2)/2,
+// dW2 = (dW'1-dW'2)/2 because W'1 = (W1+W2)/2 and W'2 = (W1-W2)/2.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int m, int d, int nmat) {
+  const int md = m * d;
+  const int e = blockIdx.x * 256 + threadIdx.x;   // element (f, k) of one head
+  const int h = blockIdx.y;
+  if (e < md) {
+    float acc[2] = {0.f, 0.f};
+    for (int mat = 0; mat < nmat; ++mat) {
+      float s = 0.f;
+      for (int side = 0; side < 2; ++side)
+        for (int b = 0; b < a.B; ++b)
+          for (int p = 0; p < a.segments; ++p) {
+            const size_t blk = ((size_t)side * a.BH + (size_t)b * a.H + h) * a.segments + p;
+            s += a.dwpart[(blk * nmat + mat) * md + e];
+          }
+      acc[mat] = s;
+    }
+    if (nmat == 2) {
+      a.dW1[(size_t)h * md + e] = 0.5f * (acc[0] + acc[1]);
+      a.dW2[(size_t)h * md + e] = 0.5f * (acc[0] - acc[1]);
+    } else {
+      a.dW1[(size_t)h * md + e] = acc[0];
+    }
+  }
+  if (a.dtau && blockIdx.x == 0 && threadIdx.x == 0) {
+    float s = 0.f;
+    for (int b = 0; b < a.B; ++b)
+      for (int p = 0; p < a.segments; ++p) s += a.dtaupart[((size_t)b * a.H + h) * a.segments + p];
+    a.dtau[h] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host-side dispatch.
+// ---------------------------------------------------------------------------
+template <class T, int D, int FW, int NW, bool NS>
+static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  dim3 grid(a.segments, a.BH);
+  k_bwd_prepass<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
+  hipError_t e = launch_state_scan(a.sstate, a.BH, a.segments, SH::STATE, causal, false, st);
+  if (e != hipSuccess) return e;
+  e = launch_state_scan(a.rstate, a.BH, a.segments, SH::STATE, causal, true, st);
+  if (e != hipSuccess) return e;
+  if (causal) {
+    k_bwd_dq<T, D, FW, NW, NS, true><<<grid, SH::NT, 0, st>>>(a);
+    k_bwd_dkv<T, D, FW, NW, NS, true><<<grid, SH::NT, 0, st>>>(a);
+  } else {
+    k_bwd_dq<T, D, FW, NW, NS, false><<<grid, SH::NT, 0, st>>>(a);
+    k_bwd_dkv<T, D, FW, NW, NS, false><<<grid, SH::NT, 0, st>>>(a);
+  }
+  dim3 rgrid((SH::M * D + 255) / 256, a.H);
+  k_bwd_reduce<<<rgrid, 256, 0, st>>>(a, SH::M, D, NS ? 2 : 1);
+  return hipGetLastError();
+}
+
+template <class T, int D, int FW, int NW>
+static hipError_t run_bwd_v(const BwdArgs& a, bool ns, bool causal, hipStream_t st) {
+  return ns ? run_bwd_t<T, D, FW, NW, true>(a, causal, st) : run_bwd_t<T, D, FW, NW, false>(a, causal, st);
+}
+
+hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st) {
+  if (ks.bf16) {
+    if (ks.d == 32 && ks.m == 64) return run_bwd_v<__bf16, 32, 16, 4>(a, ks.nonstationary, ks.causal, st);
+    if (ks.d == 64 && ks.m == 64) return run_bwd_v<__bf16, 64, 16, 4>(a, ks.nonstationary, ks.causal, st);
+    if (ks.d == 64 && ks.m == 128) return run_bwd_v<__bf16, 64, 32, 4>(a, ks.nonstationary, ks.causal, st);
+  } else {
+    if (ks.d == 32 && ks.m == 64) return run_bwd_v<float, 32, 16, 4>(a, ks.nonstationary, ks.causal, st);
+  }
+  return hipErrorNotSupported;
+}
+
 size_t bwd_state_floats(const KernelShape& ks) { return fwd_state_floats(ks); }
-size_t bwd_dw_floats(const KernelShape& ks) { return (size_t)(ks.nonstationary ? 2 : 1) * ks.m * ks.d; }
-hipError_t launch_bwd(const BwdArgs&, const KernelShape&, hipStream_t) { return hipErrorNotSupported; }
+// both sides (query rows and key rows) of the frequency-gradient partials
+size_t bwd_dw_floats(const KernelShape& ks) {
+  return (size_t)2 * (ks.nonstationary ? 2 : 1) * ks.m * ks.d;
+}
 
 }  // namespace flex

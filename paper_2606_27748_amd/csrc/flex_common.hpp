@@ -37,12 +37,14 @@ template <> struct Frag<__bf16> {
   __device__ void zero() { for (int j = 0; j < 8; ++j) v[j] = (__bf16)0.0f; }
   __device__ void set(int j, float x) { v[j] = (__bf16)x; }
   __device__ float get(int j) const { return (float)v[j]; }
+  __device__ __bf16 raw(int j) const { return v[j]; }   // stored value, no conversion
 };
 template <> struct Frag<float> {
   float v[8];
   __device__ void zero() { for (int j = 0; j < 8; ++j) v[j] = 0.0f; }
   __device__ void set(int j, float x) { v[j] = x; }
   __device__ float get(int j) const { return v[j]; }
+  __device__ float raw(int j) const { return v[j]; }
 };
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
@@ -72,6 +74,11 @@ __device__ __forceinline__ u16 float_to_bf16_bits(float x) {
 }
 __device__ __forceinline__ float io_to_float(u16 b) { return bf16_bits_to_float(b); }
 __device__ __forceinline__ float io_to_float(float x) { return x; }
+// An io element as an operand element of type T (bit copy when the types agree).
+template <class T> __device__ __forceinline__ T io_to_op(u16 b);
+template <> __device__ __forceinline__ __bf16 io_to_op<__bf16>(u16 b) { return __builtin_bit_cast(__bf16, b); }
+template <> __device__ __forceinline__ float io_to_op<float>(u16 b) { return bf16_bits_to_float(b); }
+template <class T> __device__ __forceinline__ T io_to_op(float x) { return (T)x; }
 template <class S> __device__ __forceinline__ S float_to_io(float x);
 template <> __device__ __forceinline__ u16 float_to_io<u16>(float x) { return float_to_bf16_bits(x); }
 template <> __device__ __forceinline__ float float_to_io<float>(float x) { return x; }
@@ -210,14 +217,9 @@ __device__ __forceinline__ Frag<T> features(const f32x4 (&p)[NS ? 2 * FT : FT], 
   for (int i = 0; i < 4; ++i) {
     float s1, c1;
     sincos_rev(p[ft][i], s1, c1);
-    float a = c1 * scale, b = s1 * scale;
-    if (NS) {
-      const float c2 = cos_rev(p[FT + ft][i]);
-      a *= c2;
-      b *= c2;
-    }
-    f.set(i, a);
-    f.set(4 + i, b);
+    const float sc = NS ? scale * cos_rev(p[FT + ft][i]) : scale;
+    f.set(i, c1 * sc);
+    f.set(4 + i, s1 * sc);
   }
   return f;
 }

@@ -18,102 +18,9 @@
 //   k_fwd_sweep  : per segment, carry-in state + chunk sweep, writes O, den.
 #include "flex_common.hpp"
 #include "flex_kernels.hpp"
+#include "flex_stage.hpp"
 
 namespace flex {
-
-template <class T, int D, int FW, int NW, bool NS>
-struct Shape {
-  static constexpr int M = FW * NW;
-  static constexpr int FT = FW / 16;        // frequency tiles per wave
-  static constexpr int FC = 2 * FT;         // feature tiles per wave
-  static constexpr int DV = D;
-  static constexpr int DVT = DV / 16;       // value tiles
-  static constexpr int DVT1 = DVT + 1;      // + the normaliser tile
-  static constexpr int KT = CHUNK / 32;     // k-steps over the tokens of a chunk
-  static constexpr int PR = NS ? 2 * FT : FT;
-  static constexpr int NT = NW * WAVE;      // threads per workgroup
-  // fp32 floats of one wave's state, one (b,h,segment) block of the workspace
-  static constexpr int WAVE_STATE = FC * DVT1 * WAVE * 4;
-  static constexpr int STATE = NW * WAVE_STATE;
-  // LDS row strides (elements); multiples of 4 keep 8/16-byte alignment
-  static constexpr int TPAD = CHUNK + 4;
-  static constexpr int RPAD = DVT1 * 16 + 4;
-};
-
-typedef Frag<__bf16> FB;
-
-// Fragment with 1 in row/column 0 and 0 elsewhere: as the value operand it
-// appends the ones column of [V | 1] that produces the normaliser.
-template <class T>
-__device__ __forceinline__ Frag<T> ones_col0() {
-  Frag<T> f;
-  const float v = (threadIdx.x % 16) == 0 ? 1.0f : 0.0f;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) f.set(j, v);
-  return f;
-}
-
-// Stage the chunk's value rows into LDS transposed, VT[c][t] = V[tok0+t][c],
-// zero for tokens at or beyond n.  All threads participate.
-template <class T, class SH>
-__device__ __forceinline__ void stage_vt(T* VT, const typename Io<T>::type* __restrict__ V,
-                                         int tok0, int n) {
-  constexpr int PER_ROW = SH::DV / 8;
-  for (int it = threadIdx.x; it < CHUNK * PER_ROW; it += SH::NT) {
-    const int t = it / PER_ROW, c8 = it % PER_ROW;
-    Frag<T> x;
-    load8(x, V + (size_t)(tok0 + t) * SH::DV + 8 * c8, tok0 + t < n);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) VT[(8 * c8 + j) * SH::TPAD + t] = (T)x.get(j);
-  }
-}
-
-// Operand fragment over the chunk's tokens from a token-contiguous LDS row:
-// slots j<4 take tokens 32ks+4g+j, slots j>=4 tokens 32ks+16+4g+j-4.  This is
-// the token order of a pair of accumulator tiles (see pair_tiles).
-template <class T>
-__device__ __forceinline__ Frag<T> lds_tok_frag(const T* row, int ks) {
-  const int g = (threadIdx.x % WAVE) / 16;
-  Frag<T> f;
-  const T* a = row + 32 * ks + 4 * g;
-  const T* b = a + 16;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) { f.set(j, (float)a[j]); f.set(4 + j, (float)b[j]); }
-  return f;
-}
-template <>
-__device__ __forceinline__ Frag<__bf16> lds_tok_frag<__bf16>(const __bf16* row, int ks) {
-  const int g = (threadIdx.x % WAVE) / 16;
-  const __bf16* a = row + 32 * ks + 4 * g;
-  bf16x4 lo = *reinterpret_cast<const bf16x4*>(a);
-  bf16x4 hi = *reinterpret_cast<const bf16x4*>(a + 16);
-  Frag<__bf16> f;
-  f.v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  return f;
-}
-
-// Two accumulator tiles whose rows are consecutive 16-blocks of a contraction
-// index, as one operand fragment (slots 0..3 from the first, 4..7 from the second).
-template <class T>
-__device__ __forceinline__ Frag<T> pair_tiles(const f32x4& a, const f32x4& b) {
-  Frag<T> f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { f.set(i, a[i]); f.set(4 + i, b[i]); }
-  return f;
-}
-
-// Write one wave's phi(K) fragment for frequency tile ft and token tile tt
-// into its feature-major LDS block PT[feature][token].
-template <class T, class SH>
-__device__ __forceinline__ void store_phiT(T* PT, const Frag<T>& f, int ft, int tt) {
-  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const int t = tt * 16 + r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    PT[((2 * ft) * 16 + 4 * g + i) * SH::TPAD + t] = (T)f.get(i);
-    PT[((2 * ft + 1) * 16 + 4 * g + i) * SH::TPAD + t] = (T)f.get(4 + i);
-  }
-}
 
 // ---------------------------------------------------------------------------
 // Segment-local state: S'_seg = sum over the segment's tokens of phi(K)[V;1]^T.
@@ -122,6 +29,10 @@ template <class T, int D, int FW, int NW, bool NS>
 __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
+  typedef RowStage<IO, D, SH::NT> StK;
+  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  constexpr bool STX = SH::STAGE_X;
+  __shared__ __attribute__((aligned(16))) IO XK[STX ? StK::LDS_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];
 
@@ -132,6 +43,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
   const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
   const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
 
+  StK sk;
+  StV sv;
+  if (c0 < c1) {
+    if (STX) sk.fetch(K, c0 * CHUNK, a.N);
+    sv.fetch(V, c0 * CHUNK, a.N);
+  }
   FreqSlice<T, D, FW, NS> fs;
   fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
   const float inv_c = __expf(-a.tau[h]);
@@ -147,12 +64,21 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
     __syncthreads();
-    stage_vt<T, SH>(VT, V, tok0, a.N);
+    if (STX) sk.store(XK);
+    sv.template store_t<T, SH::TPAD>(VT);
+    if (c + 1 < c1) {
+      if (STX) sk.fetch(K, tok0 + CHUNK, a.N);
+      sv.fetch(V, tok0 + CHUNK, a.N);
+    }
+    __syncthreads();
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
+      if (STX)
+        project_tile_lds<T, D, FW, NS, StK::LD>(fs, XK, tt, p, ssq);
+      else
+        project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft)
@@ -190,18 +116,30 @@ __global__ __launch_bounds__(256) void k_state_scan(float* state, int P, int E, 
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= E) return;
   float* s = state + (size_t)blockIdx.y * P * E + e;
+  constexpr int BATCH = 16;  // independent loads in flight per thread
   float acc = 0.f;
-  if (causal) {
-    for (int k = 0; k < P; ++k) {
+  for (int k0 = 0; k0 < P; k0 += BATCH) {
+    float v[BATCH];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int k = k0 + j;
       const int p = reverse ? P - 1 - k : k;
-      const float v = s[(size_t)p * E];
-      s[(size_t)p * E] = acc;
-      acc += v;
+      v[j] = k < P ? s[(size_t)p * E] : 0.f;
     }
-  } else {
-    for (int p = 0; p < P; ++p) acc += s[(size_t)p * E];
-    s[0] = acc;
+    if (causal) {
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) {
+        const int k = k0 + j;
+        const int p = reverse ? P - 1 - k : k;
+        if (k < P) s[(size_t)p * E] = acc;
+        acc += v[j];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) acc += v[j];
+    }
   }
+  if (!causal) s[0] = acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -212,8 +150,13 @@ template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG>
 __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
-  constexpr int VT_N = CAUSAL ? SH::DV * SH::TPAD : 1;
-  constexpr int PT_N = CAUSAL ? SH::FC * 16 * SH::TPAD : 1;
+  typedef RowStage<IO, D, SH::NT> StX;
+  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  constexpr bool STX = SH::STAGE_X;
+  constexpr int VT_N = CAUSAL ? SH::DV * SH::TPAD : 8;
+  constexpr int PT_N = CAUSAL ? SH::FC * 16 * SH::TPAD : 8;
+  __shared__ __attribute__((aligned(16))) IO XQ[STX ? StX::LDS_ELEMS : 8];
+  __shared__ __attribute__((aligned(16))) IO XK[(STX && CAUSAL) ? StX::LDS_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) T VT[VT_N];
   __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][SH::RPAD];
@@ -228,6 +171,15 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   IO* O = static_cast<IO*>(a.O) + (size_t)bh * a.N * SH::DV;
   float* den = a.den ? a.den + (size_t)bh * a.N : nullptr;
 
+  StX sq, sk;
+  StV sv;
+  if (c0 < c1) {
+    if (STX) {
+      sq.fetch(Q, c0 * CHUNK, a.N);
+      if (CAUSAL) sk.fetch(K, c0 * CHUNK, a.N);
+    }
+    if (CAUSAL) sv.fetch(V, c0 * CHUNK, a.N);
+  }
   FreqSlice<T, D, FW, NS> fs;
   fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
   const float inv_c = __expf(-a.tau[h]);
@@ -248,20 +200,38 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
     __syncthreads();
-    if (CAUSAL) stage_vt<T, SH>(VT, V, tok0, a.N);
+    if (STX) {
+      sq.store(XQ);
+      if (CAUSAL) sk.store(XK);
+    }
+    if (CAUSAL) sv.template store_t<T, SH::TPAD>(VT);
+    if (c + 1 < c1) {
+      if (STX) {
+        sq.fetch(Q, tok0 + CHUNK, a.N);
+        if (CAUSAL) sk.fetch(K, tok0 + CHUNK, a.N);
+      }
+      if (CAUSAL) sv.fetch(V, tok0 + CHUNK, a.N);
+    }
+    __syncthreads();
 
     Frag<T> pq[SH::FT][TT];
-    Frag<T> pk[SH::FT][TT];
+    Frag<T> pk[CAUSAL ? SH::FT : 1][TT];
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      project_tile<T, D, FW, NS>(fs, Q, tok0 + tt * 16, a.N, p, ssq);
+      if (STX)
+        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+      else
+        project_tile<T, D, FW, NS>(fs, Q, tok0 + tt * 16, a.N, p, ssq);
       float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) pq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
       if (CAUSAL) {
-        project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
+        if (STX)
+          project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
+        else
+          project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
         sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft) {
@@ -278,7 +248,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) sf[dt][ft] = pair_tiles<T>(S[2 * ft][dt], S[2 * ft + 1][dt]);
 
-    // intra-chunk kernel matrix, transposed: AT[tk][tq] rows = key tokens, cols = query tokens
+    // intra-chunk kernel matrix, transposed: rows = key tokens, cols = query tokens
     Frag<T> ap[CAUSAL ? SH::KT : 1][TT];
     if (CAUSAL) {
 #pragma unroll
@@ -301,7 +271,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
         for (int ks = 0; ks < SH::KT; ++ks) ap[ks][tq] = pair_tiles<T>(at[2 * ks], at[2 * ks + 1]);
       }
     }
-    __syncthreads();
+    if (CAUSAL) __syncthreads();  // PT (transposed phi(K)) complete
 
     Frag<T> vf[CAUSAL ? SH::DVT : 1][SH::KT];
     if (CAUSAL) {
@@ -357,11 +327,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
           dn += RED[ww][t][SH::DV];
         }
         if (tok < a.N) {
+          // one reciprocal per row (v_rcp_f32, 1 ulp); den = 0 gives inf/NaN as num/0 does
+          const float inv = __builtin_amdgcn_rcpf(dn);
           IO* o = O + (size_t)tok * SH::DV + 4 * c4;
-          o[0] = float_to_io<IO>(num.x / dn);
-          o[1] = float_to_io<IO>(num.y / dn);
-          o[2] = float_to_io<IO>(num.z / dn);
-          o[3] = float_to_io<IO>(num.w / dn);
+          o[0] = float_to_io<IO>(num.x * inv);
+          o[1] = float_to_io<IO>(num.y * inv);
+          o[2] = float_to_io<IO>(num.z * inv);
+          o[3] = float_to_io<IO>(num.w * inv);
           if (den && c4 == 0) den[tok] = dn;
         }
       }
@@ -449,9 +421,15 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
     if (ks.d == 128 && ks.m == 256) return run_variant<__bf16, 128, 32, 8>(a, ns, causal, fmap, st);
   } else {
     if (ks.d == 32 && ks.m == 64) return run_variant<float, 32, 16, 4>(a, ns, causal, fmap, st);
-    if (ks.d == 64 && ks.m == 64) return run_variant<float, 64, 16, 4>(a, ns, causal, fmap, st);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_state_scan(float* state, int BH, int P, int E, bool causal, bool reverse,
+                             hipStream_t st) {
+  dim3 sgrid((E + 255) / 256, BH);
+  k_state_scan<<<sgrid, 256, 0, st>>>(state, P, E, causal ? 1 : 0, reverse ? 1 : 0);
+  return hipGetLastError();
 }
 
 size_t fwd_state_floats(const KernelShape& ks) {

@@ -45,7 +45,8 @@ struct BwdArgs {
   float* dtau;
   float* sstate;      // [BH][segments][state floats]: key-side prefix states
   float* rstate;      // [BH][segments][state floats]: query-side suffix states
-  float* dwpart;      // [BH][segments][rows][d] frequency-gradient partials
+  float* gstats;      // [BH][N][2]: 1/den_i and delta_i = dO_i . O_i
+  float* dwpart;      // [2 sides][BH][segments][rows][d] frequency-gradient partials
   float* dtaupart;    // [BH][segments] partial dtau
   int BH, B, H, N;
   int nchunks, segments, chunks_per_seg;
@@ -57,6 +58,8 @@ size_t fwd_state_floats(const KernelShape& ks);
 size_t bwd_state_floats(const KernelShape& ks);
 size_t bwd_dw_floats(const KernelShape& ks);
 
+hipError_t launch_state_scan(float* state, int BH, int P, int E, bool causal, bool reverse,
+                             hipStream_t st);
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);
 

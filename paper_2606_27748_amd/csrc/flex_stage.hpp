@@ -1,0 +1,177 @@
+// Chunk staging: the raw rows of one 64-token chunk are fetched from HBM once
+// per workgroup into registers (16 bytes per load, coalesced), one chunk
+// ahead of the computation, then written to LDS where every wave reads the
+// operand fragments it needs.  This hides the global-memory latency behind a
+// whole chunk of work and removes the redundant per-wave reads.
+#pragma once
+#include "flex_common.hpp"
+
+namespace flex {
+
+// Row-major staging of a [64 x COLS] io-typed block with a padded row.
+template <class IO, int COLS, int NT>
+struct RowStage {
+  static constexpr int VEC = 16 / sizeof(IO);           // elements per 16-byte vector
+  static constexpr int VPR = COLS / VEC;                 // vectors per row
+  static constexpr int NV = CHUNK * VPR;                 // vectors per chunk
+  static constexpr int PER = (NV + NT - 1) / NT;         // vectors per thread
+  static constexpr int LD = COLS + VEC;                  // LDS row stride (elements), keeps 16 B alignment
+  static constexpr int LDS_ELEMS = CHUNK * LD;
+  uint4 r[PER];
+
+  // rows: this (b,h) slice's [N, COLS] rows; rows at or beyond n read as zero
+  __device__ __forceinline__ void fetch(const IO* __restrict__ rows, int tok0, int n) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int v = threadIdx.x + i * NT;
+      const int t = v / VPR, c = v % VPR;
+      if (v < NV && tok0 + t < n)
+        r[i] = *reinterpret_cast<const uint4*>(rows + (size_t)(tok0 + t) * COLS + c * VEC);
+      else
+        r[i] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+  __device__ __forceinline__ void store(IO* lds) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int v = threadIdx.x + i * NT;
+      if (v < NV) {
+        const int t = v / VPR, c = v % VPR;
+        *reinterpret_cast<uint4*>(lds + t * LD + c * VEC) = r[i];
+      }
+    }
+  }
+  // transposed store: ldsT[col][token] with row stride LDT (operand type T)
+  template <class T, int LDT>
+  __device__ __forceinline__ void store_t(T* ldsT) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int v = threadIdx.x + i * NT;
+      if (v < NV) {
+        const int t = v / VPR, c = v % VPR;
+        const IO* e = reinterpret_cast<const IO*>(&r[i]);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) ldsT[(c * VEC + j) * LDT + t] = io_to_op<T>(e[j]);
+      }
+    }
+  }
+};
+
+// Operand fragment of 8 consecutive columns [c0, c0+8) of LDS row `row`.
+__device__ __forceinline__ void lds_row8(Frag<__bf16>& f, const u16* row, int c0) {
+  f.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(row + c0));
+}
+__device__ __forceinline__ void lds_row8(Frag<float>& f, const float* row, int c0) {
+  const float4 a = *reinterpret_cast<const float4*>(row + c0);
+  const float4 b = *reinterpret_cast<const float4*>(row + c0 + 4);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
+
+// Projection of one 16-token tile (rows staged in LDS, row stride LD) onto a
+// wave's frequency slice, plus the squared row norm (summed over lane groups).
+template <class T, int D, int FW, bool NS, int LD>
+__device__ __forceinline__ void project_tile_lds(const FreqSlice<T, D, FW, NS>& fs,
+                                                 const typename Io<T>::type* X, int tt,
+                                                 f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR], float& ssq) {
+  typedef FreqSlice<T, D, FW, NS> FS;
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const typename Io<T>::type* row = X + (tt * 16 + r) * LD;
+#pragma unroll
+  for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
+  float s = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < FS::KD; ++ks) {
+    Frag<T> x;
+    lds_row8(x, row, ks * 32 + 8 * g);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) { const float v = x.get(j); s += v * v; }
+#pragma unroll
+    for (int pr = 0; pr < FS::PR; ++pr)
+#pragma unroll
+      for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], fs.w[sp][pr][ks], x);
+  }
+  ssq = group_sum(s);
+}
+
+template <class T, int D, int FW, int NW, bool NS>
+struct Shape {
+  static constexpr int M = FW * NW;
+  static constexpr int FT = FW / 16;        // frequency tiles per wave
+  static constexpr int FC = 2 * FT;         // feature tiles per wave
+  static constexpr int DV = D;
+  static constexpr int DVT = DV / 16;       // value tiles
+  static constexpr int DVT1 = DVT + 1;      // + the normaliser tile
+  static constexpr int KT = CHUNK / 32;     // k-steps over the tokens of a chunk
+  static constexpr int PR = NS ? 2 * FT : FT;
+  static constexpr int NT = NW * WAVE;      // threads per workgroup
+  // fp32 floats of one wave's state, one (b,h,segment) block of the workspace
+  static constexpr int WAVE_STATE = FC * DVT1 * WAVE * 4;
+  static constexpr int STATE = NW * WAVE_STATE;
+  // LDS row strides (elements); multiples of 4 keep 8/16-byte alignment
+  static constexpr int TPAD = CHUNK + 4;
+  static constexpr int RPAD = DVT1 * 16 + 4;
+  // stage the Q/K rows of a chunk through LDS (d = 128 keeps direct loads:
+  // its LDS budget is taken by the larger state operands)
+  static constexpr bool STAGE_X = D <= 64;
+};
+
+// Fragment with 1 in row/column 0 and 0 elsewhere: as the value operand it
+// appends the ones column of [V | 1] that produces the normaliser.
+template <class T>
+__device__ __forceinline__ Frag<T> ones_col0() {
+  Frag<T> f;
+  const float v = (threadIdx.x % 16) == 0 ? 1.0f : 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f.set(j, v);
+  return f;
+}
+
+// Operand fragment over the chunk's tokens from a token-contiguous LDS row:
+// slots j<4 take tokens 32ks+4g+j, slots j>=4 tokens 32ks+16+4g+j-4.  This is
+// the token order of a pair of accumulator tiles (see pair_tiles).
+template <class T>
+__device__ __forceinline__ Frag<T> lds_tok_frag(const T* row, int ks) {
+  const int g = (threadIdx.x % WAVE) / 16;
+  Frag<T> f;
+  const T* a = row + 32 * ks + 4 * g;
+  const T* b = a + 16;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) { f.set(j, (float)a[j]); f.set(4 + j, (float)b[j]); }
+  return f;
+}
+template <>
+__device__ __forceinline__ Frag<__bf16> lds_tok_frag<__bf16>(const __bf16* row, int ks) {
+  const int g = (threadIdx.x % WAVE) / 16;
+  const __bf16* a = row + 32 * ks + 4 * g;
+  bf16x4 lo = *reinterpret_cast<const bf16x4*>(a);
+  bf16x4 hi = *reinterpret_cast<const bf16x4*>(a + 16);
+  Frag<__bf16> f;
+  f.v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return f;
+}
+
+// Two accumulator tiles whose rows are consecutive 16-blocks of a contraction
+// index, as one operand fragment (slots 0..3 from the first, 4..7 from the second).
+template <class T>
+__device__ __forceinline__ Frag<T> pair_tiles(const f32x4& a, const f32x4& b) {
+  Frag<T> f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { f.set(i, a[i]); f.set(4 + i, b[i]); }
+  return f;
+}
+
+// Write one wave's phi(K) fragment for frequency tile ft and token tile tt
+// into its feature-major LDS block PT[feature][token].
+template <class T, class SH>
+__device__ __forceinline__ void store_phiT(T* PT, const Frag<T>& f, int ft, int tt) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int t = tt * 16 + r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    PT[((2 * ft) * 16 + 4 * g + i) * SH::TPAD + t] = f.raw(i);
+    PT[((2 * ft + 1) * 16 + 4 * g + i) * SH::TPAD + t] = f.raw(4 + i);
+  }
+}
+
+}  // namespace flex
