@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""Benchmark of the RFF linear-attention hot path on one MI355X.
+
+One step = one forward + one backward pass of causal nonstationary RFF linear
+attention (feature maps formed on chip, chunked causal forward, backward for
+Q, K, V, both frequency matrices and tau) over one batch of seeded synthetic
+inputs already resident in HBM.  Default workload: B=2, H=16, N=8192, d=64,
+m=128 frequencies per matrix (d'=256), bf16 inputs, fp32 states and gradients.
+
+Prints ONE JSON line: throughput (tokens/s, tokens = B*N per step), the
+roofline position of the dominant kernel (HIP events on its launch stream,
+algorithmic bytes or flops per launch), and the float64 CPU oracle timed on a
+bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tokens/s, causal RFF linear-attn fwd+bwd (N=8192,d=64); % MFMA/HBM roofline"
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP32_TFLOPS = 157.3
+KERNEL_FILES = {"fwd_state": "flex_fwd.hip", "fwd_sweep": "flex_fwd.hip", "scan": "flex_fwd.hip",
+                "bwd_prepass": "flex_bwd.hip", "bwd_dq": "flex_bwd.hip", "bwd_dkv": "flex_bwd.hip",
+                "bwd_reduce": "flex_bwd.hip"}
+
+
+def kernel_work(wl, kernel):
+    """Algorithmic bytes and flops of one launch of a kernel class for a workload:
+    the inputs it must read and the outputs it must write once, and the
+    contractions of the method it performs (no recomputation, intra-chunk
+    masking overhead, state hand-off or padding counted)."""
+    T = wl.B * wl.H * wl.N                        # (b,h,token) rows
+    bio = 2 if wl.io == "bf16" else 4
+    d, dv, dp = wl.d, wl.dv, 2 * wl.m
+    meff = 2 * wl.m if wl.variant == "nonstationary" else wl.m
+    proj = 2 * d * meff                           # one row onto all frequencies
+    state = 2 * dp * (dv + 1)                     # one row into / out of the state
+    if kernel == "fwd_state":
+        return T * 2 * d * bio, T * (proj + state)
+    if kernel == "fwd_sweep":
+        return T * (4 * d * bio + 4), T * (2 * proj + 2 * state)
+    if kernel == "bwd_prepass":
+        return T * (5 * d * bio + 4 + 8), T * (2 * proj + 2 * state)
+    if kernel == "bwd_dq":
+        # reads Q, K, V, dO, 1/den and delta; writes dQ; dphi(Q) = S'G, dQ = dP W', dW' += dP^T Q
+        return T * (4 * d * bio + 8 + 4 * d), T * (state + 2 * proj)
+    if kernel == "bwd_dkv":
+        # reads Q, K, V, dO, 1/den and delta; writes dK, dV; dphi(K), dV, dK, dW' and R'
+        return T * (4 * d * bio + 8 + 8 * d), T * (3 * state + 2 * proj)
+    return 0, 0
+
+
+def source_hash(kernel):
+    path = os.path.join(ROOT, "paper_2606_27748_amd", "csrc", KERNEL_FILES.get(kernel, "flex_fwd.hip"))
+    h = hashlib.sha256()
+    for p in (path, os.path.join(ROOT, "paper_2606_27748_amd", "csrc", "flex_common.hpp"),
+              os.path.join(ROOT, "paper_2606_27748_amd", "csrc", "flex_stage.hpp")):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(wl, kernel):
+    """HBM bytes per launch measured with rocprofv3 counters (committed under
+    profiles/), or None when absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"counters_{kernel}_{wl.name}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_hash") != source_hash(kernel):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, slices, seed_offset=0):
+    """Time the float64 oracle (forward + backward) on `slices` (b,h) slices of
+    the workload at full sequence length; scale to the whole batch."""
+    import numpy as np
+    import oracle
+    import workloads as W
+    sub = wl.scaled(B=1, H=slices)
+    x = W.generate(sub)
+    t0, c0 = time.perf_counter(), time.process_time()
+    oracle.linattn_bwd(x.f64("Q"), x.f64("K"), x.f64("V"), x.W1, x.W2, x.tau, x.f64("dO"),
+                       wl.variant, wl.causal)
+    t1, c1 = time.perf_counter(), time.process_time()
+    per_step = (t1 - t0) * (wl.B * wl.H) / slices
+    return {"value": wl.B * wl.N / per_step, "unit": "tokens/s",
+            "cores": max(1, int(round((c1 - c0) / (t1 - t0)))), "kind": "oracle",
+            "sample": f"{slices} of {wl.B * wl.H} (b,h) slices at N={wl.N}, forward+backward in "
+                      f"float64 ({t1 - t0:.1f} s), scaled by {wl.B * wl.H}/{slices}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="headline_causal_train_d64")
+    ap.add_argument("--cpu-slices", type=int, default=16)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run warmup + steps only (for rocprofv3); no JSON")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported "
+              "(the path has no multi-GPU sharding; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    import paper_2606_27748_amd as F
+
+    wl = W.WORKLOADS[args.workload]
+    dev = "cuda:0"
+    x = W.generate(wl, with_grad=True)
+    dt = torch.bfloat16 if wl.io == "bf16" else torch.float32
+
+    def dev_t(a):
+        import numpy as np
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    Q, K, V, dO = dev_t(x.Q), dev_t(x.K), dev_t(x.V), dev_t(x.dO)
+    W1, W2, tau = dev_t(x.W1), dev_t(x.W2), dev_t(x.tau)
+    desc = F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, wl.causal, wl.io)
+    O = torch.empty_like(V)
+    den = torch.empty(wl.B, wl.H, wl.N, dtype=torch.float32, device=dev)
+    f32 = torch.float32
+    grads = dict(dQ=torch.empty(Q.shape, dtype=f32, device=dev), dK=torch.empty(K.shape, dtype=f32, device=dev),
+                 dV=torch.empty(V.shape, dtype=f32, device=dev),
+                 dW1=torch.empty(W1.shape, dtype=f32, device=dev),
+                 dW2=None if W2 is None else torch.empty(W2.shape, dtype=f32, device=dev),
+                 dtau=torch.empty(tau.shape, dtype=f32, device=dev))
+    ws_f = torch.empty(F.workspace_size(desc, F.FLEX_PASS_FWD) + 256, dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(F.workspace_size(desc, F.FLEX_PASS_BWD) + 256, dtype=torch.uint8, device=dev)
+
+    def step():
+        F.flex_linattn_fwd(desc, Q, K, V, W1, W2, tau, O=O, den=den, ws=ws_f)
+        if wl.backward:
+            F.flex_linattn_bwd(desc, Q, K, V, W1, W2, tau, O, den, dO, ws=ws_b, **grads)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if args.profile_only:
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        return
+
+    # which kernel class dominates (outside the timed region)
+    classes = ["fwd_state", "fwd_sweep", "scan"] + (
+        ["bwd_prepass", "bwd_dq", "bwd_dkv", "bwd_reduce"] if wl.backward else [])
+    share = {}
+    for k in classes:
+        F.flex_timing_enable(k)
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        ms, n = F.flex_timing_read()
+        share[k] = ms / 3
+    dominant = max(share, key=share.get)
+
+    # timed region: exactly K steps, synchronized on both sides, events on the dominant kernel
+    F.flex_timing_enable(dominant)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    k_ms, k_n = F.flex_timing_read()
+    F.flex_timing_enable("none")
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    tokens = wl.B * wl.N
+    value = tokens / (ms_step * 1e-3)
+
+    avg_s = (k_ms / max(k_n, 1)) * 1e-3
+    kbytes, kflops = kernel_work(wl, dominant)
+    ridge = (PEAK_BF16_TFLOPS * 1e12) / (PEAK_HBM_GBS * 1e9)
+    if kbytes and kflops / kbytes >= ridge:
+        roof = {"bound": "mfma", "achieved": kflops / avg_s / 1e12,
+                "peak": PEAK_BF16_TFLOPS if wl.io == "bf16" else PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": kbytes / avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_from_profiles(wl, dominant)
+    roof["kernel"] = dominant
+    roof["kernel_ms"] = avg_s * 1e3
+    roof["kernel_share"] = {k: round(v / sum(share.values()), 4) for k, v in share.items()}
+
+    out = {"metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if wl.io == "bf16" else "f32", "data": "synthetic",
+           "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d, "m": wl.m,
+                      "variant": wl.variant, "causal": wl.causal,
+                      "pass": "fwd+bwd" if wl.backward else "fwd", "parallelism": "single-gpu"},
+           "roofline": roof}
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_slices, wl.B * wl.H))
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -131,6 +131,33 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K,
                          float* dW1, float* dW2, float* dtau,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Kernel timing (profiling aid) --------------------------------------
+ * Kernel classes of the library.  When timing is enabled for one class, every
+ * launch of a kernel of that class is bracketed by two hipEvents recorded on
+ * the launch stream; flex_timing_read() waits for the recorded events and
+ * returns the summed elapsed time.  Timing is off by default and then costs
+ * nothing.  The event objects are created on first use and kept for reuse. */
+typedef enum {
+  FLEX_KERNEL_NONE = 0,
+  FLEX_KERNEL_FWD_STATE = 1,    /* forward segment-state pre-pass            */
+  FLEX_KERNEL_FWD_SWEEP = 2,    /* forward chunk sweep / readout              */
+  FLEX_KERNEL_SCAN = 3,         /* segment prefix / suffix scan               */
+  FLEX_KERNEL_BWD_PREPASS = 4,  /* backward segment-state pre-pass            */
+  FLEX_KERNEL_BWD_DQ = 5,       /* backward query-side sweep (dQ)             */
+  FLEX_KERNEL_BWD_DKV = 6,      /* backward key-side sweep (dK, dV)           */
+  FLEX_KERNEL_BWD_REDUCE = 7,   /* frequency / tau gradient reduction         */
+  FLEX_KERNEL_FEATURE_MAP = 8   /* standalone feature map                     */
+} flex_kernel;
+
+/* Select the kernel class to time (FLEX_KERNEL_NONE disables) and discard
+ * pending records.  Not to be changed while launches are in flight. */
+int32_t flex_timing_enable(int32_t kernel);
+
+/* Wait for the recorded events; *total_ms = summed kernel time and
+ * *launches = number of timed launches since the last enable/read; then clear.
+ * Returns FLEX_ERR_HIP if an event query fails. */
+int32_t flex_timing_read(double* total_ms, int64_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

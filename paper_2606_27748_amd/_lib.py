@@ -18,7 +18,10 @@ FLEX_F32, FLEX_BF16 = 0, 1
 FLEX_STATIONARY, FLEX_NONSTATIONARY = 0, 1
 FLEX_PASS_FEATURE_MAP, FLEX_PASS_FWD, FLEX_PASS_BWD = 0, 1, 2
 EXPORTS = ("flex_abi_version", "flex_status_string", "flex_workspace_size",
-           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_bwd")
+           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_bwd",
+           "flex_timing_enable", "flex_timing_read")
+KERNELS = {"none": 0, "fwd_state": 1, "fwd_sweep": 2, "scan": 3, "bwd_prepass": 4,
+           "bwd_dq": 5, "bwd_dkv": 6, "bwd_reduce": 7, "feature_map": 8}
 
 
 class FlexError(RuntimeError):
@@ -63,6 +66,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flex_linattn_fwd.argtypes = [D, P, P, P, P, P, P, P, P, P, S, P]
     lib.flex_linattn_bwd.restype = I
     lib.flex_linattn_bwd.argtypes = [D] + [P] * 15 + [P, S, P]
+    lib.flex_timing_enable.restype = I
+    lib.flex_timing_enable.argtypes = [I]
+    lib.flex_timing_read.restype = I
+    lib.flex_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
     _lib = lib
     return lib
 
@@ -162,3 +169,16 @@ def flex_linattn_bwd(desc: flex_desc, Q, K, V, W1, W2, tau, O, den, dO, dQ=None,
                                  _ptr(ws), ws.numel(), _stream())
     _check(st, "flex_linattn_bwd")
     return dict(dQ=dQ, dK=dK, dV=dV, dW1=dW1, dW2=dW2, dtau=dtau)
+
+
+def flex_timing_enable(kernel: str) -> None:
+    """Time every launch of one kernel class with HIP events ("none" disables)."""
+    _check(load().flex_timing_enable(KERNELS[kernel]), "flex_timing_enable")
+
+
+def flex_timing_read():
+    """(summed milliseconds, number of launches) since the last enable/read."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(load().flex_timing_read(ctypes.byref(ms), ctypes.byref(n)), "flex_timing_read")
+    return ms.value, n.value

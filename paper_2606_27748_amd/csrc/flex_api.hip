@@ -6,6 +6,9 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+#include <vector>
+
 using namespace flex;
 
 namespace {
@@ -104,9 +107,80 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 }  // namespace
 
+namespace flex {
+
+namespace {
+struct Timing {
+  std::mutex mu;
+  int kernel = 0;
+  std::vector<hipEvent_t> ev;   // pairs (begin, end)
+  size_t used = 0;              // completed pairs
+  bool open = false;
+  bool failed = false;
+};
+Timing& timing() {
+  static Timing t;
+  return t;
+}
+}  // namespace
+
+void timing_mark(int kernel_class, hipStream_t st, bool begin) {
+  Timing& t = timing();
+  if (__atomic_load_n(&t.kernel, __ATOMIC_RELAXED) != kernel_class) return;
+  std::lock_guard<std::mutex> lk(t.mu);
+  if (t.kernel != kernel_class) return;
+  if (begin) {
+    if (2 * t.used + 2 > t.ev.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) { t.failed = true; return; }
+      t.ev.push_back(a);
+      t.ev.push_back(b);
+    }
+    if (hipEventRecord(t.ev[2 * t.used], st) != hipSuccess) t.failed = true;
+    t.open = true;
+  } else if (t.open) {
+    if (hipEventRecord(t.ev[2 * t.used + 1], st) != hipSuccess) t.failed = true;
+    t.open = false;
+    ++t.used;
+  }
+}
+
+}  // namespace flex
+
 extern "C" {
 
 int32_t flex_abi_version(void) { return FLEX_ABI_VERSION; }
+
+int32_t flex_timing_enable(int32_t kernel) {
+  if (kernel < FLEX_KERNEL_NONE || kernel > FLEX_KERNEL_FEATURE_MAP) return FLEX_ERR_INVALID_ARG;
+  Timing& t = timing();
+  std::lock_guard<std::mutex> lk(t.mu);
+  t.kernel = kernel;
+  t.used = 0;
+  t.open = false;
+  t.failed = false;
+  return FLEX_OK;
+}
+
+int32_t flex_timing_read(double* total_ms, int64_t* launches) {
+  if (!total_ms || !launches) return FLEX_ERR_INVALID_ARG;
+  Timing& t = timing();
+  std::lock_guard<std::mutex> lk(t.mu);
+  double sum = 0.0;
+  bool ok = !t.failed;
+  for (size_t i = 0; i < t.used && ok; ++i) {
+    float ms = 0.f;
+    ok = hipEventSynchronize(t.ev[2 * i + 1]) == hipSuccess &&
+         hipEventElapsedTime(&ms, t.ev[2 * i], t.ev[2 * i + 1]) == hipSuccess;
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = (int64_t)t.used;
+  t.used = 0;
+  t.open = false;
+  t.failed = false;
+  return ok ? FLEX_OK : FLEX_ERR_HIP;
+}
 
 const char* flex_status_string(int32_t s) {
   switch (s) {

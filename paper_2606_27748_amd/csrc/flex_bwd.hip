@@ -969,20 +969,29 @@ template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   dim3 grid(a.segments, a.BH);
+  timing_mark(KC_BWD_PREPASS, st, true);
   k_bwd_prepass<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
+  timing_mark(KC_BWD_PREPASS, st, false);
   hipError_t e = launch_state_scan(a.sstate, a.BH, a.segments, SH::STATE, causal, false, st);
   if (e != hipSuccess) return e;
   e = launch_state_scan(a.rstate, a.BH, a.segments, SH::STATE, causal, true, st);
   if (e != hipSuccess) return e;
-  if (causal) {
+  timing_mark(KC_BWD_DQ, st, true);
+  if (causal)
     k_bwd_dq<T, D, FW, NW, NS, true><<<grid, SH::NT, 0, st>>>(a);
-    k_bwd_dkv<T, D, FW, NW, NS, true><<<grid, SH::NT, 0, st>>>(a);
-  } else {
+  else
     k_bwd_dq<T, D, FW, NW, NS, false><<<grid, SH::NT, 0, st>>>(a);
+  timing_mark(KC_BWD_DQ, st, false);
+  timing_mark(KC_BWD_DKV, st, true);
+  if (causal)
+    k_bwd_dkv<T, D, FW, NW, NS, true><<<grid, SH::NT, 0, st>>>(a);
+  else
     k_bwd_dkv<T, D, FW, NW, NS, false><<<grid, SH::NT, 0, st>>>(a);
-  }
+  timing_mark(KC_BWD_DKV, st, false);
   dim3 rgrid((SH::M * D + 255) / 256, a.H);
+  timing_mark(KC_BWD_REDUCE, st, true);
   k_bwd_reduce<<<rgrid, 256, 0, st>>>(a, SH::M, D, NS ? 2 : 1);
+  timing_mark(KC_BWD_REDUCE, st, false);
   return hipGetLastError();
 }
 

@@ -388,13 +388,17 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   constexpr int QG = (SH::DV >= 128) ? 1 : TT;
   dim3 grid(a.segments, a.BH);
+  timing_mark(KC_FWD_STATE, st, true);
   k_fwd_state<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
-  dim3 sgrid((SH::STATE + 255) / 256, a.BH);
-  k_state_scan<<<sgrid, 256, 0, st>>>(a.state, a.segments, SH::STATE, causal ? 1 : 0, 0);
+  timing_mark(KC_FWD_STATE, st, false);
+  const hipError_t e = launch_state_scan(a.state, a.BH, a.segments, SH::STATE, causal, false, st);
+  if (e != hipSuccess) return e;
+  timing_mark(KC_FWD_SWEEP, st, true);
   if (causal)
     k_fwd_sweep<T, D, FW, NW, NS, true, QG><<<grid, SH::NT, 0, st>>>(a);
   else
     k_fwd_sweep<T, D, FW, NW, NS, false, QG><<<grid, SH::NT, 0, st>>>(a);
+  timing_mark(KC_FWD_SWEEP, st, false);
   return hipGetLastError();
 }
 
@@ -402,7 +406,9 @@ template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_fmap_t(const FwdArgs& a, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   dim3 grid(a.nchunks, a.BH);
+  timing_mark(KC_FEATURE_MAP, st, true);
   k_feature_map<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
+  timing_mark(KC_FEATURE_MAP, st, false);
   return hipGetLastError();
 }
 
@@ -428,7 +434,9 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
 hipError_t launch_state_scan(float* state, int BH, int P, int E, bool causal, bool reverse,
                              hipStream_t st) {
   dim3 sgrid((E + 255) / 256, BH);
+  timing_mark(KC_SCAN, st, true);
   k_state_scan<<<sgrid, 256, 0, st>>>(state, P, E, causal ? 1 : 0, reverse ? 1 : 0);
+  timing_mark(KC_SCAN, st, false);
   return hipGetLastError();
 }
 

@@ -53,6 +53,12 @@ struct BwdArgs {
   float s_const;
 };
 
+// Event bracketing of one kernel class (see flex_timing_enable); no-ops unless
+// that class is selected.
+void timing_mark(int kernel_class, hipStream_t st, bool begin);
+enum KernelClass { KC_FWD_STATE = 1, KC_FWD_SWEEP = 2, KC_SCAN = 3, KC_BWD_PREPASS = 4,
+                   KC_BWD_DQ = 5, KC_BWD_DKV = 6, KC_BWD_REDUCE = 7, KC_FEATURE_MAP = 8 };
+
 // fp32 floats of one (b,h,segment) state block for a shape.
 size_t fwd_state_floats(const KernelShape& ks);
 size_t bwd_state_floats(const KernelShape& ks);
