@@ -95,12 +95,13 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
   const size_t bh = (size_t)d->B * d->H;
   const size_t P = (size_t)pick_segments(d);
   if (pass == FLEX_PASS_FEATURE_MAP) return 0;
-  if (pass == FLEX_PASS_FWD) return align256(bh * P * fwd_state_floats(ks) * sizeof(float));
+  const size_t wf = align256(wfrag_bytes(ks, d->H));
+  if (pass == FLEX_PASS_FWD) return align256(bh * P * fwd_state_floats(ks) * sizeof(float)) + wf;
   // backward: key-side and query-side states, per-token scalars, frequency-gradient
   // and dtau partials
   return 2 * align256(bh * P * bwd_state_floats(ks) * sizeof(float)) +
          align256(bh * (size_t)d->N * 2 * sizeof(float)) +
-         align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
+         align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float)) + wf;
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -238,6 +239,8 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
   memset(&a, 0, sizeof(a));
   a.Q = Q; a.K = K; a.V = V; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = O; a.den = den;
   a.state = static_cast<float*>(ws);
+  a.wfrag = static_cast<char*>(ws) +
+            align256((size_t)desc->B * desc->H * pick_segments(desc) * fwd_state_floats(kshape(desc)) * sizeof(float));
   a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
   a.nchunks = nchunks_of(desc);
   a.segments = pick_segments(desc);
@@ -271,7 +274,8 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   a.dQ = static_cast<float*>(dQ); a.dK = static_cast<float*>(dK); a.dV = static_cast<float*>(dV);
   a.dW1 = dW1; a.dW2 = dW2; a.dtau = dtau;
   a.BH = desc->B * desc->H; a.B = desc->B; a.H = desc->H; a.N = desc->N;
-  a.nchunks = nchunks_of(desc);
+  // the backward sweeps use BWD_CHUNK-token chunks over the same segments
+  a.nchunks = (desc->N + BWD_CHUNK - 1) / BWD_CHUNK;
   a.segments = pick_segments(desc);
   a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
   a.s_const = s_const_of(desc);
@@ -284,6 +288,7 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   a.gstats = reinterpret_cast<float*>(base + 2 * sb);
   a.dwpart = reinterpret_cast<float*>(base + 2 * sb + gb);
   a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
+  a.wfrag = base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
   const hipError_t e = launch_bwd(a, ks, (hipStream_t)stream);
   return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
 }

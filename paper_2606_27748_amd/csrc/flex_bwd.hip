@@ -50,52 +50,6 @@ __device__ __forceinline__ void features_psi(const f32x4 (&p)[NS ? 2 * FT : FT],
   }
 }
 
-// A-operand fragments of W'^T (rows = input dimension d, k = projection rows of
-// this wave, paired tiles) in radians, bf16 hi + lo on the bf16 path.  Used for
-// dX = dP W'.  Projection row tile pr < FT is W'1 (or W), pr >= FT is W'2.
-template <class T, int D, int FW, bool NS>
-struct WTSlice {
-  static constexpr int FT = FW / 16;
-  static constexpr int PR = NS ? 2 * FT : FT;
-  static constexpr int KP = (PR + 1) / 2;      // k-steps over the projection rows
-  static constexpr int DT = D / 16;
-  static constexpr int NSPLIT = IsBf16<T>::value ? 2 : 1;
-  Frag<T> w[NSPLIT][DT][KP];
-
-  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
-    const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const int dcol = dt * 16 + r;
-#pragma unroll
-      for (int ks = 0; ks < KP; ++ks) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int pr = 2 * ks + (j >= 4 ? 1 : 0);
-          float v = 0.f;
-          if (pr < PR) {
-            const int f = f0 + (pr % FT) * 16 + 4 * g + (j & 3);
-            const float x = W1[(size_t)f * D + dcol];
-            if (NS) {
-              const float y = W2[(size_t)f * D + dcol];
-              v = pr >= FT ? 0.5f * (x - y) : 0.5f * (x + y);
-            } else {
-              v = x;
-            }
-          }
-          if (IsBf16<T>::value) {
-            const float hi = (float)(__bf16)v;
-            w[0][dt][ks].set(j, hi);
-            w[NSPLIT - 1][dt][ks].set(j, v - hi);
-          } else {
-            w[0][dt][ks].set(j, v);
-          }
-        }
-      }
-    }
-  }
-};
-
 // -x as a two-term operand split (hi, lo): exact to about 16 bits on the bf16
 // path.  The backward states carry the normaliser products in two rows of the
 // normaliser tile (value columns dv and dv+1) so that delta_i is not rounded
@@ -189,10 +143,10 @@ __device__ __forceinline__ void dump_dw(float* out, const f32x4 (&DW)[SH::PR][D 
 // ---------------------------------------------------------------------------
 template <class T, int D, int FW, int NW, bool NS>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
-  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
-  typedef RowStage<IO, D, SH::NT> StX;
-  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  typedef RowStage<IO, D, SH::NT, SH::CH> StX;
+  typedef RowStage<IO, SH::DV, SH::NT, SH::CH> StV;
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
@@ -201,8 +155,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T DOT[SH::DV * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PK[NW][SH::FC * 16 * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PQ[NW][SH::FC * 16 * SH::TPAD];
-  __shared__ float GS[CHUNK][2];
-  __shared__ float DEN[CHUNK];
+  __shared__ float GS[SH::CH][2];
+  __shared__ float DEN[SH::CH];
 
   const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
@@ -220,12 +174,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   StV sv, sdo, so;
   float dn_next = 0.f;
   if (c0 < c1) {
-    sq.fetch(Q, c0 * CHUNK, a.N); sk.fetch(K, c0 * CHUNK, a.N);
-    sv.fetch(V, c0 * CHUNK, a.N); sdo.fetch(dO, c0 * CHUNK, a.N); so.fetch(Ob, c0 * CHUNK, a.N);
-    if (threadIdx.x < CHUNK && c0 * CHUNK + (int)threadIdx.x < a.N) dn_next = den[c0 * CHUNK + threadIdx.x];
+    sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
+    sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N); so.fetch(Ob, c0 * SH::CH, a.N);
+    if (threadIdx.x < SH::CH && c0 * SH::CH + (int)threadIdx.x < a.N) dn_next = den[c0 * SH::CH + threadIdx.x];
   }
-  FreqSlice<T, D, FW, NS> fs;
-  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   f32x4 ST[SH::DVT1][SH::FC], RT[SH::DVT1][SH::FC];
@@ -234,20 +187,20 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 #pragma unroll
     for (int fc = 0; fc < SH::FC; ++fc) { ST[dt][fc] = zero4(); RT[dt][fc] = zero4(); }
   const Frag<T> ones = ones_col01<T>();
-  constexpr int TPT = SH::NT / CHUNK;  // threads per token for the row reductions
+  constexpr int TPT = SH::NT / SH::CH;  // threads per token for the row reductions
 
   for (int c = c0; c < c1; ++c) {
-    const int tok0 = c * CHUNK;
+    const int tok0 = c * SH::CH;
     __syncthreads();
     sq.store(XQ); sk.store(XK); sdo.store(XDO); so.store(XO);
     sv.template store_t<T, SH::TPAD>(VT);
     sdo.template store_t<T, SH::TPAD>(DOT);
-    if (threadIdx.x < CHUNK) DEN[threadIdx.x] = dn_next;
+    if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
     if (c + 1 < c1) {
-      const int t1 = tok0 + CHUNK;
+      const int t1 = tok0 + SH::CH;
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N);
       sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N); so.fetch(Ob, t1, a.N);
-      dn_next = (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N) ? den[t1 + threadIdx.x] : 0.f;
+      dn_next = (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N) ? den[t1 + threadIdx.x] : 0.f;
     }
     __syncthreads();
     // per-token 1/den and delta = dO . O
@@ -267,8 +220,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
       }
     }
     __syncthreads();
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
+    for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
@@ -320,10 +275,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 // ---------------------------------------------------------------------------
 template <class T, int D, int FW, int NW, bool NS, bool CAUSAL>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
-  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
-  typedef RowStage<IO, D, SH::NT> StX;
-  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  typedef RowStage<IO, D, SH::NT, SH::CH> StX;
+  typedef RowStage<IO, SH::DV, SH::NT, SH::CH> StV;
   typedef WTSlice<T, D, FW, NS> WTS;
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;        // k-steps over [dO | -delta]
@@ -337,7 +292,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T QT[D * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(K)^T, then dP^T
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
-  __shared__ float GS[CHUNK][2];
+  __shared__ float GS[SH::CH][2];
 
   const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
@@ -354,17 +309,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   StV sv, sdo;
   float2 gs_next = make_float2(0.f, 0.f);
   if (c0 < c1) {
-    sq.fetch(Q, c0 * CHUNK, a.N); sk.fetch(K, c0 * CHUNK, a.N);
-    sv.fetch(V, c0 * CHUNK, a.N); sdo.fetch(dO, c0 * CHUNK, a.N);
-    if (threadIdx.x < CHUNK && c0 * CHUNK + (int)threadIdx.x < a.N)
-      gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(c0 * CHUNK + threadIdx.x) * 2);
+    sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
+    sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N);
+    if (threadIdx.x < SH::CH && c0 * SH::CH + (int)threadIdx.x < a.N)
+      gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(c0 * SH::CH + threadIdx.x) * 2);
   }
-  const float* W1h = a.W1 + (size_t)h * SH::M * D;
-  const float* W2h = NS ? a.W2 + (size_t)h * SH::M * D : nullptr;
-  FreqSlice<T, D, FW, NS> fs;
-  fs.load(W1h, W2h, w * FW);
-  WTS wt;
-  wt.load(W1h, W2h, w * FW);
+  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
+  const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   f32x4 ST[SH::DVT1][SH::FC];
@@ -384,24 +335,26 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   const Frag<T> ones = ones_col01<T>();
 
   for (int c = c0; c < c1; ++c) {
-    const int tok0 = c * CHUNK;
+    const int tok0 = c * SH::CH;
     __syncthreads();
     sq.store(XQ); sk.store(XK); sv.store(XV); sdo.store(XDO);
     sv.template store_t<T, SH::TPAD>(VT);
     sq.template store_t<T, SH::TPAD>(QT);
-    if (threadIdx.x < CHUNK) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
+    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
     if (c + 1 < c1) {
-      const int t1 = tok0 + CHUNK;
+      const int t1 = tok0 + SH::CH;
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-      gs_next = (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N)
+      gs_next = (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N)
                     ? *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2)
                     : make_float2(0.f, 0.f);
     }
     __syncthreads();
 
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
     // phi(K) of this wave's features, transposed into LDS
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
+    for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
@@ -410,9 +363,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
     }
     // phi(Q) and its P2-derivative fragments
-    Frag<T> phq[SH::FT][TT], psq[SH::FT][TT];
+    Frag<T> phq[SH::FT][SH::TT], psq[SH::FT][SH::TT];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
+    for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
@@ -421,14 +374,14 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phq[ft][tt], psq[ft][tt]);
     }
     // intra-chunk M^T[j][i] = dO_i . V_j - delta_i for j <= i (1/den_i applied later)
-    Frag<T> mt[CAUSAL ? SH::KT : 1][TT];
+    Frag<T> mt[CAUSAL ? SH::KT : 1][SH::TT];
     if (CAUSAL) {
 #pragma unroll
-      for (int tq = 0; tq < TT; ++tq) {
+      for (int tq = 0; tq < SH::TT; ++tq) {
         const float dl = GS[tq * 16 + r][1];
-        f32x4 m[TT];
+        f32x4 m[SH::TT];
 #pragma unroll
-        for (int tk = 0; tk < TT; ++tk) {
+        for (int tk = 0; tk < SH::TT; ++tk) {
           m[tk] = zero4();
           if (tk <= tq) {
 #pragma unroll
@@ -452,9 +405,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     __syncthreads();  // phi(K)^T complete
 
     // dphi(Q)^T[feature][query] = (phi(K)^T M^T + S'^T-rows x [dO | -delta]) / den
-    f32x4 dph[SH::FC][TT];
+    f32x4 dph[SH::FC][SH::TT];
 #pragma unroll
-    for (int tq = 0; tq < TT; ++tq) {
+    for (int tq = 0; tq < SH::TT; ++tq) {
       Frag<T> gf[KG];
 #pragma unroll
       for (int kd = 0; kd < KG; ++kd) {
@@ -507,9 +460,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       }
     }
     // chain rule through phi(Q): dP per radian, tiles [projection row tile][token tile]
-    f32x4 dp[SH::PR][TT];
+    f32x4 dp[SH::PR][SH::TT];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt)
+    for (int tt = 0; tt < SH::TT; ++tt)
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) {
         f32x4 d2 = zero4();
@@ -517,8 +470,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         if (NS) dp[SH::FT + ft][tt] = d2;
       }
     // dQ = sum over waves of dP W'; reduced through LDS in rounds of QG token tiles
+    WTS wt;
+    wt.load_frags(wdx);
 #pragma unroll
-    for (int q0 = 0; q0 < TT; q0 += QG) {
+    for (int q0 = 0; q0 < SH::TT; q0 += QG) {
       __syncthreads();
 #pragma unroll
       for (int qq = 0; qq < QG; ++qq) {
@@ -555,7 +510,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 #pragma unroll
     for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
-      for (int tt = 0; tt < TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
+      for (int tt = 0; tt < SH::TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
     __syncthreads();
     // frequency gradient partial: dW'[rows][d] += dP^T Q
 #pragma unroll
@@ -581,10 +536,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 // ---------------------------------------------------------------------------
 template <class T, int D, int FW, int NW, bool NS, bool CAUSAL>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
-  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
-  typedef RowStage<IO, D, SH::NT> StX;
-  typedef RowStage<IO, SH::DV, SH::NT> StV;
+  typedef RowStage<IO, D, SH::NT, SH::CH> StX;
+  typedef RowStage<IO, SH::DV, SH::NT, SH::CH> StV;
   typedef WTSlice<T, D, FW, NS> WTS;
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;
@@ -601,8 +556,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T KT[D * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(Q)^T/den, then dP^T
   __shared__ __attribute__((aligned(16))) char REDRL[RED_BYTES > RL_BYTES ? RED_BYTES : RL_BYTES];
-  __shared__ float GS[CHUNK][2];
-  __shared__ float SSQ[CHUNK];
+  __shared__ float GS[SH::CH][2];
+  __shared__ float SSQ[SH::CH];
   __shared__ float TRED[SH::NT];
   typedef float RedRow[QG * 16][RP];
   RedRow* RED = reinterpret_cast<RedRow*>(REDRL);
@@ -624,17 +579,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   StV sv, sdo;
   float2 gs_next = make_float2(0.f, 0.f);
   if (c0 < c1) {
-    const int t1 = (c1 - 1) * CHUNK;
+    const int t1 = (c1 - 1) * SH::CH;
     sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-    if (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N)
+    if (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N)
       gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2);
   }
-  const float* W1h = a.W1 + (size_t)h * SH::M * D;
-  const float* W2h = NS ? a.W2 + (size_t)h * SH::M * D : nullptr;
-  FreqSlice<T, D, FW, NS> fs;
-  fs.load(W1h, W2h, w * FW);
-  WTS wt;
-  wt.load(W1h, W2h, w * FW);
+  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
+  const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   f32x4 RT[SH::DVT1][SH::FC];
@@ -654,27 +605,29 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   float dtau_acc = 0.f;
 
   for (int c = c1 - 1; c >= c0; --c) {
-    const int tok0 = c * CHUNK;
+    const int tok0 = c * SH::CH;
     __syncthreads();
     sq.store(XQ); sk.store(XK); sv.store(XV); sdo.store(XDO);
     sdo.template store_t<T, SH::TPAD>(DOT);
     sk.template store_t<T, SH::TPAD>(KT);
-    if (threadIdx.x < CHUNK) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
+    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
     if (c - 1 >= c0) {
-      const int t1 = tok0 - CHUNK;
+      const int t1 = tok0 - SH::CH;
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-      gs_next = (threadIdx.x < CHUNK && t1 + (int)threadIdx.x < a.N)
+      gs_next = (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N)
                     ? *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2)
                     : make_float2(0.f, 0.f);
     }
     __syncthreads();
 
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
     // phi(Q)/den: fragments (for the intra-chunk kernel matrix) and transposed copy
     // (the non-causal backward of K and V uses only the total R')
-    Frag<T> phq[SH::FT][TT];
+    Frag<T> phq[SH::FT][SH::TT];
     if (CAUSAL) {
 #pragma unroll
-      for (int tt = 0; tt < TT; ++tt) {
+      for (int tt = 0; tt < SH::TT; ++tt) {
         f32x4 p[SH::PR];
         float ssq;
         project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
@@ -687,9 +640,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       }
     }
     // phi(K) and its P2-derivative fragments
-    Frag<T> phk[SH::FT][TT], psk[SH::FT][TT];
+    Frag<T> phk[SH::FT][SH::TT], psk[SH::FT][SH::TT];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
+    for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
@@ -699,13 +652,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phk[ft][tt], psk[ft][tt]);
     }
     // intra-chunk M[i][j] = dO_i . V_j - delta_i and A[i][j] = phi(Q_i)/den_i . phi(K_j), i >= j
-    Frag<T> mp[CAUSAL ? SH::KT : 1][TT], ap[CAUSAL ? SH::KT : 1][TT];
+    Frag<T> mp[CAUSAL ? SH::KT : 1][SH::TT], ap[CAUSAL ? SH::KT : 1][SH::TT];
     if (CAUSAL) {
 #pragma unroll
-      for (int tk = 0; tk < TT; ++tk) {
-        f32x4 m[TT], at[TT];
+      for (int tk = 0; tk < SH::TT; ++tk) {
+        f32x4 m[SH::TT], at[SH::TT];
 #pragma unroll
-        for (int tq = 0; tq < TT; ++tq) {
+        for (int tq = 0; tq < SH::TT; ++tq) {
           m[tq] = zero4();
           at[tq] = zero4();
           if (tq >= tk) {
@@ -743,10 +696,50 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
           RL[(size_t)w * SH::DV * RLP + (dt * 16 + 4 * g + i) * RLP + fc * 16 + r] = (T)RT[dt][fc][i];
     __syncthreads();  // phi(Q)^T and the R' copy complete
 
-    // dphi(K)^T[feature][key] = phi(Q)^T M + R'^T-rows x [V | 1]
-    f32x4 dph[SH::FC][TT];
+    // dV^T partial[value col][key] = dO^T A/den (intra) + R'[:dv]^T-rows x phi(K)
+    f32x4 dvp[SH::DVT][SH::TT];
 #pragma unroll
-    for (int tk = 0; tk < TT; ++tk) {
+    for (int tk = 0; tk < SH::TT; ++tk)
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT; ++dt) {
+        f32x4 acc = zero4();
+        if (CAUSAL) {
+#pragma unroll
+          for (int ks = 0; ks < SH::KT; ++ks)
+            if (32 * ks + 31 >= 16 * tk) mma(acc, lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks), ap[ks][tk]);
+        }
+#pragma unroll
+        for (int ft = 0; ft < SH::FT; ++ft)
+          mma(acc, lds_tok_frag<T>(RL + (size_t)w * SH::DV * RLP + (dt * 16 + r) * RLP, ft), phk[ft][tk]);
+        dvp[dt][tk] = acc;
+      }
+    // dV: reduce the per-wave partials
+#pragma unroll
+    for (int q0 = 0; q0 < SH::TT; q0 += QG) {
+      __syncthreads();
+#pragma unroll
+      for (int qq = 0; qq < QG; ++qq)
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt)
+          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = dvp[dt][q0 + qq];
+      __syncthreads();
+      constexpr int C4 = SH::DV / 4;
+      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
+        const int t = it / C4, c4 = it % C4;
+        const int tok = tok0 + q0 * 16 + t;
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) {
+          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
+          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+        if (tok < a.N) *reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4) = s;
+      }
+    }
+    // dphi(K)^T[feature][key] = phi(Q)^T M + R'^T-rows x [V | 1]
+    f32x4 dph[SH::FC][SH::TT];
+#pragma unroll
+    for (int tk = 0; tk < SH::TT; ++tk) {
       Frag<T> vf[KG];
 #pragma unroll
       for (int kd = 0; kd < KG; ++kd) {
@@ -776,23 +769,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         dph[fc][tk] = acc;
       }
     }
-    // dV^T partial[value col][key] = dO^T A/den (intra) + R'[:dv]^T-rows x phi(K)
-    f32x4 dvp[SH::DVT][TT];
-#pragma unroll
-    for (int tk = 0; tk < TT; ++tk)
-#pragma unroll
-      for (int dt = 0; dt < SH::DVT; ++dt) {
-        f32x4 acc = zero4();
-        if (CAUSAL) {
-#pragma unroll
-          for (int ks = 0; ks < SH::KT; ++ks)
-            if (32 * ks + 31 >= 16 * tk) mma(acc, lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks), ap[ks][tk]);
-        }
-#pragma unroll
-        for (int ft = 0; ft < SH::FT; ++ft)
-          mma(acc, lds_tok_frag<T>(RL + (size_t)w * SH::DV * RLP + (dt * 16 + r) * RLP, ft), phk[ft][tk]);
-        dvp[dt][tk] = acc;
-      }
     // R'^T += [dO | -delta]^T-rows x phi(Q)/den  (after every use of R'_{>c})
     if (CAUSAL) {
 #pragma unroll
@@ -810,10 +786,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       }
     }
     // chain rule through phi(K)
-    f32x4 dp[SH::PR][TT];
-    float gp[TT];
+    f32x4 dp[SH::PR][SH::TT];
+    float gp[SH::TT];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
+    for (int tt = 0; tt < SH::TT; ++tt) {
       float gs = 0.f;
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) {
@@ -823,32 +799,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       }
       gp[tt] = group_sum(gs);
     }
-    // dV: reduce the per-wave partials
-#pragma unroll
-    for (int q0 = 0; q0 < TT; q0 += QG) {
-      __syncthreads();
-#pragma unroll
-      for (int qq = 0; qq < QG; ++qq)
-#pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt)
-          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = dvp[dt][q0 + qq];
-      __syncthreads();
-      constexpr int C4 = SH::DV / 4;
-      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
-        const int t = it / C4, c4 = it % C4;
-        const int tok = tok0 + q0 * 16 + t;
-        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int ww = 0; ww < NW; ++ww) {
-          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
-          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-        }
-        if (tok < a.N) *reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4) = s;
-      }
-    }
     // dK = sum over waves of dP W' + (2/c) g k, g = <phi(K), dphi(K)>; dtau -= g ||k||^2 / c
+    WTS wt;
+    wt.load_frags(wdx);
 #pragma unroll
-    for (int q0 = 0; q0 < TT; q0 += QG) {
+    for (int q0 = 0; q0 < SH::TT; q0 += QG) {
       __syncthreads();
 #pragma unroll
       for (int qq = 0; qq < QG; ++qq) {
@@ -898,7 +853,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
     for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
-      for (int tt = 0; tt < TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
+      for (int tt = 0; tt < SH::TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
     __syncthreads();
 #pragma unroll
     for (int ks = 0; ks < SH::KT; ++ks) {
@@ -967,8 +922,9 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int m, int d, int
 // ---------------------------------------------------------------------------
 template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
-  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   dim3 grid(a.segments, a.BH);
+  k_prep_freqs<T, D, FW, NW, NS><<<a.H, SH::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
   timing_mark(KC_BWD_PREPASS, st, true);
   k_bwd_prepass<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
   timing_mark(KC_BWD_PREPASS, st, false);

@@ -164,7 +164,130 @@ struct FreqSlice {
       }
     }
   }
+
+  // Fragments in lane order, [fragment][lane]: one coalesced load per fragment.
+  static constexpr int NFRAG = NSPLIT * PR * KD;
+  __device__ __forceinline__ void store_frags(Frag<T>* out) const {
+    const int l = threadIdx.x % WAVE;
+#pragma unroll
+    for (int sp = 0; sp < NSPLIT; ++sp)
+#pragma unroll
+      for (int pr = 0; pr < PR; ++pr)
+#pragma unroll
+        for (int ks = 0; ks < KD; ++ks) out[((sp * PR + pr) * KD + ks) * WAVE + l] = w[sp][pr][ks];
+  }
+  __device__ __forceinline__ void load_frags(const Frag<T>* in) {
+    const int l = threadIdx.x % WAVE;
+#pragma unroll
+    for (int sp = 0; sp < NSPLIT; ++sp)
+#pragma unroll
+      for (int pr = 0; pr < PR; ++pr)
+#pragma unroll
+        for (int ks = 0; ks < KD; ++ks) w[sp][pr][ks] = in[((sp * PR + pr) * KD + ks) * WAVE + l];
+  }
 };
+
+// A-operand fragments of W'^T (rows = input dimension d, k = projection rows of
+// this wave, paired tiles) in radians, bf16 hi + lo on the bf16 path.  Used for
+// dX = dP W'.  Projection row tile pr < FT is W'1 (or W), pr >= FT is W'2.
+template <class T, int D, int FW, bool NS>
+struct WTSlice {
+  static constexpr int FT = FW / 16;
+  static constexpr int PR = NS ? 2 * FT : FT;
+  static constexpr int KP = (PR + 1) / 2;      // k-steps over the projection rows
+  static constexpr int DT = D / 16;
+  static constexpr int NSPLIT = IsBf16<T>::value ? 2 : 1;
+  Frag<T> w[NSPLIT][DT][KP];
+
+  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
+    const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int dcol = dt * 16 + r;
+#pragma unroll
+      for (int ks = 0; ks < KP; ++ks) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int pr = 2 * ks + (j >= 4 ? 1 : 0);
+          float v = 0.f;
+          if (pr < PR) {
+            const int f = f0 + (pr % FT) * 16 + 4 * g + (j & 3);
+            const float x = W1[(size_t)f * D + dcol];
+            if (NS) {
+              const float y = W2[(size_t)f * D + dcol];
+              v = pr >= FT ? 0.5f * (x - y) : 0.5f * (x + y);
+            } else {
+              v = x;
+            }
+          }
+          if (IsBf16<T>::value) {
+            const float hi = (float)(__bf16)v;
+            w[0][dt][ks].set(j, hi);
+            w[NSPLIT - 1][dt][ks].set(j, v - hi);
+          } else {
+            w[0][dt][ks].set(j, v);
+          }
+        }
+      }
+    }
+  }
+
+  static constexpr int NFRAG = NSPLIT * DT * KP;
+  __device__ __forceinline__ void store_frags(Frag<T>* out) const {
+    const int l = threadIdx.x % WAVE;
+#pragma unroll
+    for (int sp = 0; sp < NSPLIT; ++sp)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int ks = 0; ks < KP; ++ks) out[((sp * DT + dt) * KP + ks) * WAVE + l] = w[sp][dt][ks];
+  }
+  __device__ __forceinline__ void load_frags(const Frag<T>* in) {
+    const int l = threadIdx.x % WAVE;
+#pragma unroll
+    for (int sp = 0; sp < NSPLIT; ++sp)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int ks = 0; ks < KP; ++ks) w[sp][dt][ks] = in[((sp * DT + dt) * KP + ks) * WAVE + l];
+  }
+};
+
+// Per-head frequency fragments prepared once per call: for each wave, the
+// projection fragments (FreqSlice) followed by the dX fragments (WTSlice).
+template <class T, int D, int FW, bool NS>
+struct FragBlock {
+  static constexpr int NP = FreqSlice<T, D, FW, NS>::NFRAG;
+  static constexpr int NT_ = WTSlice<T, D, FW, NS>::NFRAG;
+  static constexpr int PER_WAVE = (NP + NT_) * WAVE;   // fragments per wave
+  __device__ static const Frag<T>* proj(const void* base, int h, int nw, int w) {
+    return static_cast<const Frag<T>*>(base) + ((size_t)h * nw + w) * PER_WAVE;
+  }
+  __device__ static const Frag<T>* dx(const void* base, int h, int nw, int w) {
+    return proj(base, h, nw, w) + NP * WAVE;
+  }
+};
+
+template <class T, int D, int FW, int NW, bool NS>
+__global__ __launch_bounds__(NW * WAVE) void k_prep_freqs(const float* W1, const float* W2, void* out, int M) {
+  typedef FragBlock<T, D, FW, NS> FBk;
+  const int h = blockIdx.x, w = threadIdx.x / WAVE;
+  const float* W1h = W1 + (size_t)h * M * D;
+  const float* W2h = NS ? W2 + (size_t)h * M * D : nullptr;
+  Frag<T>* base = static_cast<Frag<T>*>(out) + ((size_t)h * NW + w) * FBk::PER_WAVE;
+  {
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load(W1h, W2h, w * FW);
+    fs.store_frags(base);
+  }
+  {
+    WTSlice<T, D, FW, NS> wt;
+    wt.load(W1h, W2h, w * FW);
+    wt.store_frags(base + FBk::NP * WAVE);
+  }
+}
+
+
 
 // Projection of one 16-token tile onto a wave's frequency slice, plus the
 // squared row norm.  X points at the token rows of this (b,h) slice; rows at

@@ -49,8 +49,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
     if (STX) sk.fetch(K, c0 * CHUNK, a.N);
     sv.fetch(V, c0 * CHUNK, a.N);
   }
-  FreqSlice<T, D, FW, NS> fs;
-  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   f32x4 S[SH::FC][SH::DVT1];
@@ -71,6 +70,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
       sv.fetch(V, tok0 + CHUNK, a.N);
     }
     __syncthreads();
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
       f32x4 p[SH::PR];
@@ -180,8 +181,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     }
     if (CAUSAL) sv.fetch(V, c0 * CHUNK, a.N);
   }
-  FreqSlice<T, D, FW, NS> fs;
-  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   // carry-in state (exclusive prefix for causal, total for non-causal)
@@ -214,6 +214,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     }
     __syncthreads();
 
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
     Frag<T> pq[SH::FT][TT];
     Frag<T> pk[CAUSAL ? SH::FT : 1][TT];
 #pragma unroll
@@ -388,6 +390,7 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   constexpr int QG = (SH::DV >= 128) ? 1 : TT;
   dim3 grid(a.segments, a.BH);
+  k_prep_freqs<T, D, FW, NW, NS><<<a.H, SH::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
   timing_mark(KC_FWD_STATE, st, true);
   k_fwd_state<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_STATE, st, false);
@@ -438,6 +441,24 @@ hipError_t launch_state_scan(float* state, int BH, int P, int E, bool causal, bo
   k_state_scan<<<sgrid, 256, 0, st>>>(state, P, E, causal ? 1 : 0, reverse ? 1 : 0);
   timing_mark(KC_SCAN, st, false);
   return hipGetLastError();
+}
+
+template <class T, int D, int FW, bool NS>
+static size_t wfrag_bytes_t(int H, int NW) {
+  return (size_t)H * NW * FragBlock<T, D, FW, NS>::PER_WAVE * sizeof(Frag<T>);
+}
+
+size_t wfrag_bytes(const KernelShape& ks, int H) {
+  const bool ns = ks.nonstationary;
+  if (ks.bf16) {
+    if (ks.d == 32 && ks.m == 64) return ns ? wfrag_bytes_t<__bf16, 32, 16, true>(H, 4) : wfrag_bytes_t<__bf16, 32, 16, false>(H, 4);
+    if (ks.d == 64 && ks.m == 64) return ns ? wfrag_bytes_t<__bf16, 64, 16, true>(H, 4) : wfrag_bytes_t<__bf16, 64, 16, false>(H, 4);
+    if (ks.d == 64 && ks.m == 128) return ns ? wfrag_bytes_t<__bf16, 64, 32, true>(H, 4) : wfrag_bytes_t<__bf16, 64, 32, false>(H, 4);
+    if (ks.d == 128 && ks.m == 256) return ns ? wfrag_bytes_t<__bf16, 128, 32, true>(H, 8) : wfrag_bytes_t<__bf16, 128, 32, false>(H, 8);
+  } else {
+    if (ks.d == 32 && ks.m == 64) return ns ? wfrag_bytes_t<float, 32, 16, true>(H, 4) : wfrag_bytes_t<float, 32, 16, false>(H, 4);
+  }
+  return 0;
 }
 
 size_t fwd_state_floats(const KernelShape& ks) {

@@ -5,6 +5,9 @@
 
 namespace flex {
 
+// Chunk length (tokens) of the backward sweeps; the forward uses 64.
+constexpr int BWD_CHUNK = 32;
+
 struct KernelShape {
   bool bf16;
   bool nonstationary;
@@ -22,6 +25,7 @@ struct FwdArgs {
   void* O;            // also the output Phi of the feature map
   float* den;
   float* state;       // [BH][segments][state floats]
+  void* wfrag;        // per-head frequency fragments (prepared by k_prep_freqs)
   int BH, H, N;
   int nchunks, segments, chunks_per_seg;
   float s_const;      // sigma/sqrt(m) or sigma/(2 sqrt(m))
@@ -48,6 +52,7 @@ struct BwdArgs {
   float* gstats;      // [BH][N][2]: 1/den_i and delta_i = dO_i . O_i
   float* dwpart;      // [2 sides][BH][segments][rows][d] frequency-gradient partials
   float* dtaupart;    // [BH][segments] partial dtau
+  void* wfrag;        // per-head frequency fragments (prepared by k_prep_freqs)
   int BH, B, H, N;
   int nchunks, segments, chunks_per_seg;
   float s_const;
@@ -63,6 +68,8 @@ enum KernelClass { KC_FWD_STATE = 1, KC_FWD_SWEEP = 2, KC_SCAN = 3, KC_BWD_PREPA
 size_t fwd_state_floats(const KernelShape& ks);
 size_t bwd_state_floats(const KernelShape& ks);
 size_t bwd_dw_floats(const KernelShape& ks);
+// bytes of the per-head frequency fragments for H heads
+size_t wfrag_bytes(const KernelShape& ks, int H);
 
 hipError_t launch_state_scan(float* state, int BH, int P, int E, bool causal, bool reverse,
                              hipStream_t st);

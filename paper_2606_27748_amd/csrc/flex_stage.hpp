@@ -9,14 +9,14 @@
 namespace flex {
 
 // Row-major staging of a [64 x COLS] io-typed block with a padded row.
-template <class IO, int COLS, int NT>
+template <class IO, int COLS, int NT, int ROWS = CHUNK>
 struct RowStage {
   static constexpr int VEC = 16 / sizeof(IO);           // elements per 16-byte vector
   static constexpr int VPR = COLS / VEC;                 // vectors per row
-  static constexpr int NV = CHUNK * VPR;                 // vectors per chunk
+  static constexpr int NV = ROWS * VPR;                  // vectors per chunk
   static constexpr int PER = (NV + NT - 1) / NT;         // vectors per thread
   static constexpr int LD = COLS + VEC;                  // LDS row stride (elements), keeps 16 B alignment
-  static constexpr int LDS_ELEMS = CHUNK * LD;
+  static constexpr int LDS_ELEMS = ROWS * LD;
   uint4 r[PER];
 
   // rows: this (b,h) slice's [N, COLS] rows; rows at or beyond n read as zero
@@ -94,22 +94,24 @@ __device__ __forceinline__ void project_tile_lds(const FreqSlice<T, D, FW, NS>& 
   ssq = group_sum(s);
 }
 
-template <class T, int D, int FW, int NW, bool NS>
+template <class T, int D, int FW, int NW, bool NS, int CH_ = CHUNK>
 struct Shape {
+  static constexpr int CH = CH_;            // tokens per chunk
+  static constexpr int TT = CH / 16;        // token tiles per chunk
   static constexpr int M = FW * NW;
   static constexpr int FT = FW / 16;        // frequency tiles per wave
   static constexpr int FC = 2 * FT;         // feature tiles per wave
   static constexpr int DV = D;
   static constexpr int DVT = DV / 16;       // value tiles
   static constexpr int DVT1 = DVT + 1;      // + the normaliser tile
-  static constexpr int KT = CHUNK / 32;     // k-steps over the tokens of a chunk
+  static constexpr int KT = CH / 32;        // k-steps over the tokens of a chunk
   static constexpr int PR = NS ? 2 * FT : FT;
   static constexpr int NT = NW * WAVE;      // threads per workgroup
   // fp32 floats of one wave's state, one (b,h,segment) block of the workspace
   static constexpr int WAVE_STATE = FC * DVT1 * WAVE * 4;
   static constexpr int STATE = NW * WAVE_STATE;
   // LDS row strides (elements); multiples of 4 keep 8/16-byte alignment
-  static constexpr int TPAD = CHUNK + 4;
+  static constexpr int TPAD = CH + 4;
   static constexpr int RPAD = DVT1 * 16 + 4;
   // stage the Q/K rows of a chunk through LDS (d = 128 keeps direct loads:
   // its LDS budget is taken by the larger state operands)
