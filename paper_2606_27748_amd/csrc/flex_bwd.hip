@@ -120,21 +120,38 @@ __device__ __forceinline__ void store_dpT(T* DPT, const f32x4& v, int pr, int tt
   for (int i = 0; i < 4; ++i) DPT[(pr * 16 + 4 * g + i) * SH::TPAD + tt * 16 + r] = (T)v[i];
 }
 
+// The per-wave frequency-gradient partial dW'[rows][d] lives in LDS in
+// register-dump order (tile, lane, 4 floats): each chunk's MFMA tiles are added
+// with one 16-byte read and write per lane and tile.
+template <class SH, int D>
+__device__ __forceinline__ void dw_accumulate(float* dwl, const f32x4 (&acc)[SH::PR][D / 16]) {
+  const int l = threadIdx.x % WAVE;
+#pragma unroll
+  for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) {
+      f32x4* p = reinterpret_cast<f32x4*>(dwl + ((pr * (D / 16) + dt) * WAVE + l) * 4);
+      *p += acc[pr][dt];
+    }
+}
+
 // Write a wave's frequency-gradient partial tiles DW[pr][dt] (rows = projection
 // rows, cols = d) into the canonical layout [matrix][m][d].
 template <class SH, int D, int FW, bool NS>
-__device__ __forceinline__ void dump_dw(float* out, const f32x4 (&DW)[SH::PR][D / 16], int f0) {
+__device__ __forceinline__ void dump_dw(float* out, const float* dwl, int f0) {
   const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
 #pragma unroll
   for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt)
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(dwl + ((pr * (D / 16) + dt) * WAVE + l) * 4);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int mat = pr >= SH::FT ? 1 : 0;
         const int f = f0 + (pr % SH::FT) * 16 + 4 * g + i;
-        out[((size_t)mat * SH::M + f) * D + dt * 16 + r] = DW[pr][dt][i];
+        out[((size_t)mat * SH::M + f) * D + dt * 16 + r] = v[i];
       }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -292,6 +309,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T QT[D * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(K)^T, then dP^T
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
+  __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
 
   const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
@@ -327,11 +345,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       for (int fc = 0; fc < SH::FC; ++fc)
         ST[dt][fc] = *reinterpret_cast<const f32x4*>(in + state_off<SH>(w, dt, fc, l));
   }
-  f32x4 DW[SH::PR][DT];
-#pragma unroll
-  for (int pr = 0; pr < SH::PR; ++pr)
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) DW[pr][dt] = zero4();
+  for (int i = l; i < SH::PR * DT * WAVE; i += WAVE)
+    *reinterpret_cast<f32x4*>(&DWL[w][i * 4]) = zero4();
   const Frag<T> ones = ones_col01<T>();
 
   for (int c = c0; c < c1; ++c) {
@@ -513,22 +528,30 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       for (int tt = 0; tt < SH::TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
     __syncthreads();
     // frequency gradient partial: dW'[rows][d] += dP^T Q
+    {
+      f32x4 dw[SH::PR][DT];
 #pragma unroll
-    for (int ks = 0; ks < SH::KT; ++ks) {
-      Frag<T> xq[DT];
+      for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tok_frag<T>(QT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < DT; ++dt) dw[pr][dt] = zero4();
 #pragma unroll
-      for (int pr = 0; pr < SH::PR; ++pr) {
-        const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+      for (int ks = 0; ks < SH::KT; ++ks) {
+        Frag<T> xq[DT];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) mma(DW[pr][dt], dpt, xq[dt]);
+        for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tok_frag<T>(QT + (dt * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int pr = 0; pr < SH::PR; ++pr) {
+          const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) mma(dw[pr][dt], dpt, xq[dt]);
+        }
       }
+      dw_accumulate<SH, D>(DWL[w], dw);
     }
   }
   const size_t nmat = NS ? 2 : 1;
   float* out = a.dwpart + (((size_t)0 * a.BH + bh) * a.segments + seg) * nmat * SH::M * D;
-  dump_dw<SH, D, FW, NS>(out, DW, w * FW);
+  dump_dw<SH, D, FW, NS>(out, DWL[w], w * FW);
 }
 
 // ---------------------------------------------------------------------------
@@ -556,6 +579,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T KT[D * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(Q)^T/den, then dP^T
   __shared__ __attribute__((aligned(16))) char REDRL[RED_BYTES > RL_BYTES ? RED_BYTES : RL_BYTES];
+  __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
   __shared__ float SSQ[SH::CH];
   __shared__ float TRED[SH::NT];
@@ -597,11 +621,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       for (int fc = 0; fc < SH::FC; ++fc)
         RT[dt][fc] = *reinterpret_cast<const f32x4*>(in + state_off<SH>(w, dt, fc, l));
   }
-  f32x4 DW[SH::PR][DT];
-#pragma unroll
-  for (int pr = 0; pr < SH::PR; ++pr)
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) DW[pr][dt] = zero4();
+  for (int i = l; i < SH::PR * DT * WAVE; i += WAVE)
+    *reinterpret_cast<f32x4*>(&DWL[w][i * 4]) = zero4();
   float dtau_acc = 0.f;
 
   for (int c = c1 - 1; c >= c0; --c) {
@@ -855,22 +876,30 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
       for (int tt = 0; tt < SH::TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
     __syncthreads();
+    {
+      f32x4 dw[SH::PR][DT];
 #pragma unroll
-    for (int ks = 0; ks < SH::KT; ++ks) {
-      Frag<T> xk[DT];
+      for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tok_frag<T>(KT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < DT; ++dt) dw[pr][dt] = zero4();
 #pragma unroll
-      for (int pr = 0; pr < SH::PR; ++pr) {
-        const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+      for (int ks = 0; ks < SH::KT; ++ks) {
+        Frag<T> xk[DT];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) mma(DW[pr][dt], dpt, xk[dt]);
+        for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tok_frag<T>(KT + (dt * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int pr = 0; pr < SH::PR; ++pr) {
+          const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) mma(dw[pr][dt], dpt, xk[dt]);
+        }
       }
+      dw_accumulate<SH, D>(DWL[w], dw);
     }
   }
   const size_t nmat = NS ? 2 : 1;
   float* out = a.dwpart + (((size_t)1 * a.BH + bh) * a.segments + seg) * nmat * SH::M * D;
-  dump_dw<SH, D, FW, NS>(out, DW, w * FW);
+  dump_dw<SH, D, FW, NS>(out, DWL[w], w * FW);
   // dtau partial of this workgroup: fixed-order tree sum
   TRED[threadIdx.x] = dtau_acc;
   __syncthreads();
