@@ -17,6 +17,8 @@ FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # never emit packed fp32 arithmetic (v_pk_fma/mul/add_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results that feed VALU code are placed in VGPRs (fewer AGPR copies)
+    # "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
 ]
 

@@ -61,6 +61,16 @@ KernelShape kshape(const flex_desc* d) {
 
 int nchunks_of(const flex_desc* d) { return (d->N + kChunk - 1) / kChunk; }
 
+// Forward state pre-pass workgroups per segment: two (each half a segment)
+// when that still leaves fewer than two workgroups per CU, so that two of them
+// share a CU.
+int fwd_sub_of(const flex_desc* d, int P) {
+  const int nc = nchunks_of(d);
+  const int cps = (nc + P - 1) / P;
+  const long long wgs = (long long)d->B * d->H * P;
+  return (cps % 2 == 0 && wgs < 2LL * kCUs) ? 2 : 1;
+}
+
 // Segments per (b,h): enough workgroups to cover the 256 CUs in whole rounds
 // while keeping the per-segment state traffic small.
 int pick_segments(const flex_desc* d) {
@@ -96,7 +106,8 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
   const size_t P = (size_t)pick_segments(d);
   if (pass == FLEX_PASS_FEATURE_MAP) return 0;
   const size_t wf = align256(wfrag_bytes(ks, d->H));
-  if (pass == FLEX_PASS_FWD) return align256(bh * P * fwd_state_floats(ks) * sizeof(float)) + wf;
+  if (pass == FLEX_PASS_FWD)
+    return align256(bh * P * fwd_sub_of(d, (int)P) * fwd_state_floats(ks) * sizeof(float)) + wf;
   // backward: key-side and query-side states, per-token scalars, frequency-gradient
   // and dtau partials
   return 2 * align256(bh * P * bwd_state_floats(ks) * sizeof(float)) +
@@ -217,7 +228,7 @@ int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1, 
   memset(&a, 0, sizeof(a));
   a.Q = X; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = Phi;
   a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
-  a.nchunks = nchunks_of(desc); a.segments = 1; a.chunks_per_seg = a.nchunks;
+  a.nchunks = nchunks_of(desc); a.segments = 1; a.chunks_per_seg = a.nchunks; a.sub = 1;
   a.s_const = s_const_of(desc);
   const hipError_t e = launch_fwd(a, kshape(desc), true, (hipStream_t)stream);
   return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
@@ -239,12 +250,14 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
   memset(&a, 0, sizeof(a));
   a.Q = Q; a.K = K; a.V = V; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = O; a.den = den;
   a.state = static_cast<float*>(ws);
-  a.wfrag = static_cast<char*>(ws) +
-            align256((size_t)desc->B * desc->H * pick_segments(desc) * fwd_state_floats(kshape(desc)) * sizeof(float));
+  const int P0 = pick_segments(desc);
+  a.wfrag = static_cast<char*>(ws) + align256((size_t)desc->B * desc->H * P0 * fwd_sub_of(desc, P0) *
+                                              fwd_state_floats(kshape(desc)) * sizeof(float));
   a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
   a.nchunks = nchunks_of(desc);
-  a.segments = pick_segments(desc);
+  a.segments = P0;
   a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
+  a.sub = fwd_sub_of(desc, P0);
   a.s_const = s_const_of(desc);
   const hipError_t e = launch_fwd(a, kshape(desc), false, (hipStream_t)stream);
   return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;

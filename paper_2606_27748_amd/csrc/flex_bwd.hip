@@ -174,6 +174,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T PQ[NW][SH::FC * 16 * SH::TPAD];
   __shared__ float GS[SH::CH][2];
   __shared__ float DEN[SH::CH];
+  __shared__ float SSQ[SH::CH], SSK[SH::CH];
 
   const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
     __syncthreads();
-    sq.store(XQ); sk.store(XK); sdo.store(XDO); so.store(XO);
+    sq.store(XQ, SSQ); sk.store(XK, SSK); sdo.store(XDO); so.store(XO);
     sv.template store_t<T, SH::TPAD>(VT);
     sdo.template store_t<T, SH::TPAD>(DOT);
     if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
@@ -226,8 +227,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
       float s = 0.f;
       for (int cidx = part; cidx < SH::DV; cidx += TPT)
         s += io_to_float(XDO[t * StV::LD + cidx]) * io_to_float(XO[t * StV::LD + cidx]);
-#pragma unroll
-      for (int o = 1; o < TPT; o <<= 1) s += __shfl_xor(s, o);
+      s = lane_sum<TPT>(s);
       if (part == 0) {
         const bool ok = tok0 + t < a.N;
         const float inv = ok ? 1.0f / DEN[t] : 0.f;
@@ -243,11 +243,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
       float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PK[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PQ[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
@@ -311,6 +311,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
+  __shared__ float SSQ[SH::CH], SSK[SH::CH];
 
   const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
@@ -352,7 +353,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
     __syncthreads();
-    sq.store(XQ); sk.store(XK); sv.store(XV); sdo.store(XDO);
+    sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
     sv.template store_t<T, SH::TPAD>(VT);
     sq.template store_t<T, SH::TPAD>(QT);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
@@ -372,7 +373,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
@@ -383,7 +384,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phq[ft][tt], psq[ft][tt]);
@@ -581,7 +582,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) char REDRL[RED_BYTES > RL_BYTES ? RED_BYTES : RL_BYTES];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
-  __shared__ float SSQ[SH::CH];
+  __shared__ float SSQ[SH::CH], SSK[SH::CH];
   __shared__ float TRED[SH::NT];
   typedef float RedRow[QG * 16][RP];
   RedRow* RED = reinterpret_cast<RedRow*>(REDRL);
@@ -628,7 +629,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   for (int c = c1 - 1; c >= c0; --c) {
     const int tok0 = c * SH::CH;
     __syncthreads();
-    sq.store(XQ); sk.store(XK); sv.store(XV); sdo.store(XDO);
+    sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
     sdo.template store_t<T, SH::TPAD>(DOT);
     sk.template store_t<T, SH::TPAD>(KT);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
@@ -651,7 +652,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       for (int tt = 0; tt < SH::TT; ++tt) {
         f32x4 p[SH::PR];
         float ssq;
-        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
         const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft) {
@@ -666,8 +667,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     for (int tt = 0; tt < SH::TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
-      if (w == 0 && g == 0) SSQ[tt * 16 + r] = ssq;
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phk[ft][tt], psk[ft][tt]);
@@ -818,7 +818,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         gs += feature_grad<T, SH::FT, NS>(phk[ft][tt], psk[ft][tt], dph[2 * ft][tt], dph[2 * ft + 1][tt], dp[ft][tt], d2);
         if (NS) dp[SH::FT + ft][tt] = d2;
       }
-      gp[tt] = group_sum(gs);
+      gp[tt] = gs;   // this lane group's share; the four shares are summed in the dK reduction
     }
     // dK = sum over waves of dP W' + (2/c) g k, g = <phi(K), dphi(K)>; dtau -= g ||k||^2 / c
     WTS wt;
@@ -842,7 +842,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
             for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wt.w[sp][dt][ks], dpp[ks]);
           *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = acc;
         }
-        if (g == 0) RED[w][qq * 16 + r][D] = gp[tt];
+        RED[w][qq * 16 + r][D + g] = gp[tt];
       }
       __syncthreads();
       constexpr int C4 = D / 4;
@@ -856,7 +856,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         for (int ww = 0; ww < NW; ++ww) {
           const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
           s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-          gg += RED[ww][t][D];
+          gg += (RED[ww][t][D] + RED[ww][t][D + 1]) + (RED[ww][t][D + 2] + RED[ww][t][D + 3]);
         }
         if (tok < a.N) {
           const float k2 = 2.0f * inv_c * gg;
@@ -866,7 +866,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
           s.z += k2 * io_to_float(kr[2]);
           s.w += k2 * io_to_float(kr[3]);
           *reinterpret_cast<float4*>(dK + (size_t)tok * D + 4 * c4) = s;
-          if (c4 == 0) dtau_acc -= gg * SSQ[tl] * inv_c;
+          if (c4 == 0) dtau_acc -= gg * SSK[tl] * inv_c;
         }
       }
     }
@@ -916,26 +916,53 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 // dW2 = (dW'1-dW'2)/2 because W'1 = (W1+W2)/2 and W'2 = (W1-W2)/2.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int m, int d, int nmat) {
+  // 64 elements (f, k) of one head per workgroup; the 4 waves split the list of
+  // partials (side, b, segment) round-robin, loads unrolled so they are in
+  // flight together, then the 4 wave sums are combined in a fixed order.
+  __shared__ float part[2][4][64];
   const int md = m * d;
-  const int e = blockIdx.x * 256 + threadIdx.x;   // element (f, k) of one head
+  const int e = blockIdx.x * 64 + (threadIdx.x % 64);
+  const int q = threadIdx.x / 64;
   const int h = blockIdx.y;
+  const int count = 2 * a.B * a.segments;
+  float acc[2] = {0.f, 0.f};
   if (e < md) {
-    float acc[2] = {0.f, 0.f};
     for (int mat = 0; mat < nmat; ++mat) {
-      float s = 0.f;
-      for (int side = 0; side < 2; ++side)
-        for (int b = 0; b < a.B; ++b)
-          for (int p = 0; p < a.segments; ++p) {
-            const size_t blk = ((size_t)side * a.BH + (size_t)b * a.H + h) * a.segments + p;
-            s += a.dwpart[(blk * nmat + mat) * md + e];
-          }
-      acc[mat] = s;
+      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+      int i = q;
+      for (; i + 12 < count; i += 16) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int j = i + 4 * u;
+          const int side = j / (a.B * a.segments), rem = j % (a.B * a.segments);
+          const int b = rem / a.segments, p = rem % a.segments;
+          const size_t blk = ((size_t)side * a.BH + (size_t)b * a.H + h) * a.segments + p;
+          v[u] = a.dwpart[(blk * nmat + mat) * md + e];
+        }
+        s0 += v[0]; s1 += v[1]; s2 += v[2]; s3 += v[3];
+      }
+      for (; i < count; i += 4) {
+        const int side = i / (a.B * a.segments), rem = i % (a.B * a.segments);
+        const int b = rem / a.segments, p = rem % a.segments;
+        const size_t blk = ((size_t)side * a.BH + (size_t)b * a.H + h) * a.segments + p;
+        s0 += a.dwpart[(blk * nmat + mat) * md + e];
+      }
+      acc[mat] = (s0 + s1) + (s2 + s3);
     }
+  }
+  part[0][q][threadIdx.x % 64] = acc[0];
+  part[1][q][threadIdx.x % 64] = acc[1];
+  __syncthreads();
+  if (q == 0 && e < md) {
+    const int t = threadIdx.x;
+    const float x0 = (part[0][0][t] + part[0][1][t]) + (part[0][2][t] + part[0][3][t]);
+    const float x1 = (part[1][0][t] + part[1][1][t]) + (part[1][2][t] + part[1][3][t]);
     if (nmat == 2) {
-      a.dW1[(size_t)h * md + e] = 0.5f * (acc[0] + acc[1]);
-      a.dW2[(size_t)h * md + e] = 0.5f * (acc[0] - acc[1]);
+      a.dW1[(size_t)h * md + e] = 0.5f * (x0 + x1);
+      a.dW2[(size_t)h * md + e] = 0.5f * (x0 - x1);
     } else {
-      a.dW1[(size_t)h * md + e] = acc[0];
+      a.dW1[(size_t)h * md + e] = x0;
     }
   }
   if (a.dtau && blockIdx.x == 0 && threadIdx.x == 0) {
@@ -957,9 +984,9 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   timing_mark(KC_BWD_PREPASS, st, true);
   k_bwd_prepass<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
   timing_mark(KC_BWD_PREPASS, st, false);
-  hipError_t e = launch_state_scan(a.sstate, a.BH, a.segments, SH::STATE, causal, false, st);
+  hipError_t e = launch_state_scan(a.sstate, a.BH, a.segments, 1, SH::STATE, causal, false, st);
   if (e != hipSuccess) return e;
-  e = launch_state_scan(a.rstate, a.BH, a.segments, SH::STATE, causal, true, st);
+  e = launch_state_scan(a.rstate, a.BH, a.segments, 1, SH::STATE, causal, true, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_BWD_DQ, st, true);
   if (causal)
@@ -973,7 +1000,7 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   else
     k_bwd_dkv<T, D, FW, NW, NS, false><<<grid, SH::NT, 0, st>>>(a);
   timing_mark(KC_BWD_DKV, st, false);
-  dim3 rgrid((SH::M * D + 255) / 256, a.H);
+  dim3 rgrid((SH::M * D + 63) / 64, a.H);
   timing_mark(KC_BWD_REDUCE, st, true);
   k_bwd_reduce<<<rgrid, 256, 0, st>>>(a, SH::M, D, NS ? 2 : 1);
   timing_mark(KC_BWD_REDUCE, st, false);

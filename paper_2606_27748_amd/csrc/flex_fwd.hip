@@ -26,20 +26,23 @@ namespace flex {
 // Segment-local state: S'_seg = sum over the segment's tokens of phi(K)[V;1]^T.
 // ---------------------------------------------------------------------------
 template <class T, int D, int FW, int NW, bool NS>
-__global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
+__global__ __launch_bounds__(NW * WAVE) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 2 : 1, 2)))
+void k_fwd_state(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, SH::NT> StK;
   typedef RowStage<IO, SH::DV, SH::NT> StV;
   constexpr bool STX = SH::STAGE_X;
   __shared__ __attribute__((aligned(16))) IO XK[STX ? StK::LDS_ELEMS : 8];
+  __shared__ float SSK[CHUNK];
   __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];
 
-  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;   // seg: sub-segment
   const int w = threadIdx.x / WAVE;
-  const int c0 = seg * a.chunks_per_seg;
-  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const int cps = a.chunks_per_seg / a.sub;
+  const int c0 = seg * cps;
+  const int c1 = min(c0 + cps, a.nchunks);
   const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
   const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
 
@@ -63,7 +66,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
     __syncthreads();
-    if (STX) sk.store(XK);
+    if (STX) sk.store(XK, SSK);
     sv.template store_t<T, SH::TPAD>(VT);
     if (c + 1 < c1) {
       if (STX) sk.fetch(K, tok0 + CHUNK, a.N);
@@ -77,7 +80,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
       f32x4 p[SH::PR];
       float ssq;
       if (STX)
-        project_tile_lds<T, D, FW, NS, StK::LD>(fs, XK, tt, p, ssq);
+        project_tile_lds<T, D, FW, NS, StK::LD>(fs, XK, SSK, tt, p, ssq);
       else
         project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
       }
     }
   }
-  float* out = a.state + ((size_t)bh * a.segments + seg) * SH::STATE + (size_t)w * SH::WAVE_STATE;
+  float* out = a.state + ((size_t)bh * a.segments * a.sub + seg) * SH::STATE + (size_t)w * SH::WAVE_STATE;
   const int l = threadIdx.x % WAVE;
 #pragma unroll
   for (int fc = 0; fc < SH::FC; ++fc)
@@ -113,26 +116,29 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_state(FwdArgs a) {
 // Exclusive prefix over segments (causal) or total into segment 0 (non-causal).
 // state: [BH][P][E] fp32.  Fixed summation order.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_state_scan(float* state, int P, int E, int causal, int reverse) {
+__global__ __launch_bounds__(256) void k_state_scan(float* state, int P, int sub, int E, int causal,
+                                                    int reverse) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= E) return;
-  float* s = state + (size_t)blockIdx.y * P * E + e;
+  const int n = P * sub;
+  float* s = state + (size_t)blockIdx.y * n * E + e;
   constexpr int BATCH = 16;  // independent loads in flight per thread
   float acc = 0.f;
-  for (int k0 = 0; k0 < P; k0 += BATCH) {
+  for (int k0 = 0; k0 < n; k0 += BATCH) {
     float v[BATCH];
 #pragma unroll
     for (int j = 0; j < BATCH; ++j) {
       const int k = k0 + j;
-      const int p = reverse ? P - 1 - k : k;
-      v[j] = k < P ? s[(size_t)p * E] : 0.f;
+      const int p = reverse ? n - 1 - k : k;
+      v[j] = k < n ? s[(size_t)p * E] : 0.f;
     }
     if (causal) {
 #pragma unroll
       for (int j = 0; j < BATCH; ++j) {
         const int k = k0 + j;
-        const int p = reverse ? P - 1 - k : k;
-        if (k < P) s[(size_t)p * E] = acc;
+        const int p = reverse ? n - 1 - k : k;
+        // first slot of each segment met in scan order: p*sub (prefix) or p*sub+sub-1 (suffix)
+        if (k < n && (reverse ? (p % sub == sub - 1) : (p % sub == 0))) s[(size_t)p * E] = acc;
         acc += v[j];
       }
     } else {
@@ -158,6 +164,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   constexpr int PT_N = CAUSAL ? SH::FC * 16 * SH::TPAD : 8;
   __shared__ __attribute__((aligned(16))) IO XQ[STX ? StX::LDS_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) IO XK[(STX && CAUSAL) ? StX::LDS_ELEMS : 8];
+  __shared__ float SSQ[CHUNK], SSK[CHUNK];
   __shared__ __attribute__((aligned(16))) T VT[VT_N];
   __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][SH::RPAD];
@@ -187,7 +194,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   // carry-in state (exclusive prefix for causal, total for non-causal)
   f32x4 S[SH::FC][SH::DVT1];
   {
-    const float* in = a.state + ((size_t)bh * a.segments + (CAUSAL ? seg : 0)) * SH::STATE +
+    const float* in = a.state + ((size_t)bh * a.segments * a.sub + (CAUSAL ? seg * a.sub : 0)) * SH::STATE +
                       (size_t)w * SH::WAVE_STATE;
 #pragma unroll
     for (int fc = 0; fc < SH::FC; ++fc)
@@ -201,8 +208,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     const int tok0 = c * CHUNK;
     __syncthreads();
     if (STX) {
-      sq.store(XQ);
-      if (CAUSAL) sk.store(XK);
+      sq.store(XQ, SSQ);
+      if (CAUSAL) sk.store(XK, SSK);
     }
     if (CAUSAL) sv.template store_t<T, SH::TPAD>(VT);
     if (c + 1 < c1) {
@@ -223,7 +230,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       f32x4 p[SH::PR];
       float ssq;
       if (STX)
-        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, tt, p, ssq);
+        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       else
         project_tile<T, D, FW, NS>(fs, Q, tok0 + tt * 16, a.N, p, ssq);
       float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
@@ -231,7 +238,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       for (int ft = 0; ft < SH::FT; ++ft) pq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
       if (CAUSAL) {
         if (STX)
-          project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, tt, p, ssq);
+          project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
         else
           project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
         sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
@@ -390,11 +397,12 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   constexpr int QG = (SH::DV >= 128) ? 1 : TT;
   dim3 grid(a.segments, a.BH);
+  dim3 pgrid(a.segments * a.sub, a.BH);
   k_prep_freqs<T, D, FW, NW, NS><<<a.H, SH::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
   timing_mark(KC_FWD_STATE, st, true);
-  k_fwd_state<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
+  k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_STATE, st, false);
-  const hipError_t e = launch_state_scan(a.state, a.BH, a.segments, SH::STATE, causal, false, st);
+  const hipError_t e = launch_state_scan(a.state, a.BH, a.segments, a.sub, SH::STATE, causal, false, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_FWD_SWEEP, st, true);
   if (causal)
@@ -434,11 +442,11 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_state_scan(float* state, int BH, int P, int E, bool causal, bool reverse,
+hipError_t launch_state_scan(float* state, int BH, int P, int sub, int E, bool causal, bool reverse,
                              hipStream_t st) {
   dim3 sgrid((E + 255) / 256, BH);
   timing_mark(KC_SCAN, st, true);
-  k_state_scan<<<sgrid, 256, 0, st>>>(state, P, E, causal ? 1 : 0, reverse ? 1 : 0);
+  k_state_scan<<<sgrid, 256, 0, st>>>(state, P, sub, E, causal ? 1 : 0, reverse ? 1 : 0);
   timing_mark(KC_SCAN, st, false);
   return hipGetLastError();
 }

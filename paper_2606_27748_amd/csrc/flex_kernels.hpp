@@ -24,10 +24,11 @@ struct FwdArgs {
   const float* tau;
   void* O;            // also the output Phi of the feature map
   float* den;
-  float* state;       // [BH][segments][state floats]
+  float* state;       // [BH][segments * sub][state floats]
   void* wfrag;        // per-head frequency fragments (prepared by k_prep_freqs)
   int BH, H, N;
   int nchunks, segments, chunks_per_seg;
+  int sub;            // state pre-pass workgroups per segment (chunks_per_seg % sub == 0)
   float s_const;      // sigma/sqrt(m) or sigma/(2 sqrt(m))
 };
 
@@ -71,7 +72,10 @@ size_t bwd_dw_floats(const KernelShape& ks);
 // bytes of the per-head frequency fragments for H heads
 size_t wfrag_bytes(const KernelShape& ks, int H);
 
-hipError_t launch_state_scan(float* state, int BH, int P, int E, bool causal, bool reverse,
+// state: [BH][P*sub][E]; writes the exclusive prefix (causal) into slot p*sub
+// of every segment p, the exclusive suffix (reverse) into slot p*sub+sub-1, or
+// the total (non-causal) into slot 0.
+hipError_t launch_state_scan(float* state, int BH, int P, int sub, int E, bool causal, bool reverse,
                              hipStream_t st);
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);

@@ -41,6 +41,25 @@ struct RowStage {
       }
     }
   }
+  // store, plus the squared norm of every row into ssq[ROWS] (the VPR vectors
+  // of a row sit in VPR consecutive lanes: summed with lane shuffles)
+  __device__ __forceinline__ void store(IO* lds, float* ssq) const {
+    static_assert(NT % VPR == 0 && VPR <= WAVE, "a row's vectors must share a wave");
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int v = threadIdx.x + i * NT;
+      float s = 0.f;
+      if (v < NV) {
+        const int t = v / VPR, c = v % VPR;
+        *reinterpret_cast<uint4*>(lds + t * LD + c * VEC) = r[i];
+        const IO* e = reinterpret_cast<const IO*>(&r[i]);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) { const float x = io_to_float(e[j]); s += x * x; }
+      }
+      s = lane_sum<VPR>(s);
+      if (v < NV && v % VPR == 0) ssq[v / VPR] = s;
+    }
+  }
   // transposed store: ldsT[col][token] with row stride LDT (operand type T)
   template <class T, int LDT>
   __device__ __forceinline__ void store_t(T* ldsT) const {
@@ -72,26 +91,24 @@ __device__ __forceinline__ void lds_row8(Frag<float>& f, const float* row, int c
 // wave's frequency slice, plus the squared row norm (summed over lane groups).
 template <class T, int D, int FW, bool NS, int LD>
 __device__ __forceinline__ void project_tile_lds(const FreqSlice<T, D, FW, NS>& fs,
-                                                 const typename Io<T>::type* X, int tt,
-                                                 f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR], float& ssq) {
+                                                 const typename Io<T>::type* X, const float* ssq_rows,
+                                                 int tt, f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR],
+                                                 float& ssq) {
   typedef FreqSlice<T, D, FW, NS> FS;
   const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const typename Io<T>::type* row = X + (tt * 16 + r) * LD;
 #pragma unroll
   for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
-  float s = 0.f;
 #pragma unroll
   for (int ks = 0; ks < FS::KD; ++ks) {
     Frag<T> x;
     lds_row8(x, row, ks * 32 + 8 * g);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) { const float v = x.get(j); s += v * v; }
-#pragma unroll
     for (int pr = 0; pr < FS::PR; ++pr)
 #pragma unroll
       for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], fs.w[sp][pr][ks], x);
   }
-  ssq = group_sum(s);
+  ssq = ssq_rows[tt * 16 + r];
 }
 
 template <class T, int D, int FW, int NW, bool NS, int CH_ = CHUNK>

@@ -12,7 +12,7 @@ import pytest
 import oracle as orc
 import workloads as W
 from tests.gpu_util import to_device, to_f64, desc_of
-from tests.parity import check_grads, dtau_scale, KAPPA_MAX, TOL
+from tests.parity import check_grads, dtau_scale, KAPPA_MAX_GRAD as KAPPA_MAX, TOL
 
 pytestmark = pytest.mark.gpu
 
