@@ -62,13 +62,14 @@ KernelShape kshape(const flex_desc* d) {
 int nchunks_of(const flex_desc* d) { return (d->N + kChunk - 1) / kChunk; }
 
 // Forward state pre-pass workgroups per segment: two (each half a segment)
-// when that still leaves fewer than two workgroups per CU, so that two of them
-// share a CU.
+// for 4-wave workgroups when that still leaves fewer than two workgroups per
+// CU, so that two of them share a CU (8-wave workgroups already give each SIMD
+// two waves).
 int fwd_sub_of(const flex_desc* d, int P) {
   const int nc = nchunks_of(d);
   const int cps = (nc + P - 1) / P;
   const long long wgs = (long long)d->B * d->H * P;
-  return (cps % 2 == 0 && wgs < 2LL * kCUs) ? 2 : 1;
+  return (fwd_state_waves(kshape(d)) == 4 && cps % 2 == 0 && wgs < 2LL * kCUs) ? 2 : 1;
 }
 
 // Segments per (b,h): enough workgroups to cover the 256 CUs in whole rounds
@@ -112,7 +113,8 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
   // and dtau partials
   return 2 * align256(bh * P * bwd_state_floats(ks) * sizeof(float)) +
          align256(bh * (size_t)d->N * 2 * sizeof(float)) +
-         align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float)) + wf;
+         align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float)) +
+         (bwd_split_differs(ks) ? 2 : 1) * wf;
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -302,6 +304,7 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   a.dwpart = reinterpret_cast<float*>(base + 2 * sb + gb);
   a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
   a.wfrag = base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
+  a.wfrag_kv = bwd_split_differs(ks) ? static_cast<char*>(a.wfrag) + align256(wfrag_bytes(ks, desc->H)) : a.wfrag;
   const hipError_t e = launch_bwd(a, ks, (hipStream_t)stream);
   return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
 }

@@ -88,10 +88,13 @@ __device__ __forceinline__ Frag<T> delta_rows(const float (*GS)[2], int ks) {
   return f;
 }
 
-// Register-dump layout of a wave's [dv' x features] state: tile (dt, fc).
+// Register-dump layout of the [dv' x features] states: tile (dt, global feature
+// tile w*FC + fc), lane, 4 floats.  It does not depend on how the waves split
+// the frequencies, so kernels with different splits share the states.
 template <class SH>
 __device__ __forceinline__ size_t state_off(int w, int dt, int fc, int l) {
-  return (size_t)w * SH::WAVE_STATE + ((size_t)(dt * SH::FC + fc) * WAVE + l) * 4;
+  constexpr int NFT = SH::M / 8;   // feature tiles of the whole [cos | sin] feature vector
+  return ((size_t)(dt * NFT + w * SH::FC + fc) * WAVE + l) * 4;
 }
 
 // Chain rule through one wave's features for frequency tile ft, token tile tt:
@@ -176,7 +179,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   __shared__ float DEN[SH::CH];
   __shared__ float SSQ[SH::CH], SSK[SH::CH];
 
-  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
+  const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const int c0 = seg * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
@@ -299,7 +303,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   typedef WTSlice<T, D, FW, NS> WTS;
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;        // k-steps over [dO | -delta]
-  constexpr int QG = 2;                          // token tiles per reduction round
+  constexpr int QG = NW >= 8 ? 1 : 2;            // token tiles per reduction round
   constexpr int RP = D + 4;
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
@@ -313,7 +317,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ float GS[SH::CH][2];
   __shared__ float SSQ[SH::CH], SSK[SH::CH];
 
-  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
+  const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const int c0 = seg * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
@@ -567,7 +572,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   typedef WTSlice<T, D, FW, NS> WTS;
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;
-  constexpr int QG = 2;
+  constexpr int QG = NW >= 8 ? 1 : 2;
   constexpr int RP = (D > SH::DV ? D : SH::DV) + 4;
   constexpr int RLP = SH::FC * 16 + 4;           // row stride of the transposed R' copy
   constexpr int RED_BYTES = NW * QG * 16 * RP * 4;
@@ -588,7 +593,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   RedRow* RED = reinterpret_cast<RedRow*>(REDRL);
   T* RL = reinterpret_cast<T*>(REDRL);
 
-  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
+  const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const int c0 = seg * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
@@ -609,8 +615,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     if (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N)
       gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2);
   }
-  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
-  const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, w);
+  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag_kv, h, NW, w);
+  const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag_kv, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   f32x4 RT[SH::DVT1][SH::FC];
@@ -976,52 +982,65 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int m, int d, int
 // ---------------------------------------------------------------------------
 // Host-side dispatch.
 // ---------------------------------------------------------------------------
-template <class T, int D, int FW, int NW, bool NS>
+// Frequencies per wave (FW) and waves per workgroup (NW) of the pre-pass and
+// the dQ sweep (A) and of the dK/dV sweep (B).  The states, the partial sums
+// and the per-token scalars have split-independent layouts; each split has its
+// own prepared fragments.
+template <class T, int D, bool NS, int FWA, int NWA, int FWB, int NWB>
 static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
-  typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
-  dim3 grid(a.segments, a.BH);
-  k_prep_freqs<T, D, FW, NW, NS><<<a.H, SH::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
+  typedef Shape<T, D, FWA, NWA, NS, BWD_CHUNK> SA;
+  typedef Shape<T, D, FWB, NWB, NS, BWD_CHUNK> SB;
+  static_assert(SA::M == SB::M && SA::STATE == SB::STATE, "splits of one shape");
+  const dim3 grid(a.segments * a.BH);
+  k_prep_freqs<T, D, FWA, NWA, NS><<<a.H, SA::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SA::M);
+  if (a.wfrag_kv != a.wfrag)
+    k_prep_freqs<T, D, FWB, NWB, NS><<<a.H, SB::NT, 0, st>>>(a.W1, a.W2, a.wfrag_kv, SB::M);
   timing_mark(KC_BWD_PREPASS, st, true);
-  k_bwd_prepass<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
+  k_bwd_prepass<T, D, FWA, NWA, NS><<<grid, SA::NT, 0, st>>>(a);
   timing_mark(KC_BWD_PREPASS, st, false);
-  hipError_t e = launch_state_scan(a.sstate, a.BH, a.segments, 1, SH::STATE, causal, false, st);
+  hipError_t e = launch_state_scan(a.sstate, a.BH, a.segments, 1, SA::STATE, causal, false, st);
   if (e != hipSuccess) return e;
-  e = launch_state_scan(a.rstate, a.BH, a.segments, 1, SH::STATE, causal, true, st);
+  e = launch_state_scan(a.rstate, a.BH, a.segments, 1, SA::STATE, causal, true, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_BWD_DQ, st, true);
   if (causal)
-    k_bwd_dq<T, D, FW, NW, NS, true><<<grid, SH::NT, 0, st>>>(a);
+    k_bwd_dq<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
   else
-    k_bwd_dq<T, D, FW, NW, NS, false><<<grid, SH::NT, 0, st>>>(a);
+    k_bwd_dq<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
   timing_mark(KC_BWD_DQ, st, false);
   timing_mark(KC_BWD_DKV, st, true);
   if (causal)
-    k_bwd_dkv<T, D, FW, NW, NS, true><<<grid, SH::NT, 0, st>>>(a);
+    k_bwd_dkv<T, D, FWB, NWB, NS, true><<<grid, SB::NT, 0, st>>>(a);
   else
-    k_bwd_dkv<T, D, FW, NW, NS, false><<<grid, SH::NT, 0, st>>>(a);
+    k_bwd_dkv<T, D, FWB, NWB, NS, false><<<grid, SB::NT, 0, st>>>(a);
   timing_mark(KC_BWD_DKV, st, false);
-  dim3 rgrid((SH::M * D + 63) / 64, a.H);
+  dim3 rgrid((SA::M * D + 63) / 64, a.H);
   timing_mark(KC_BWD_REDUCE, st, true);
-  k_bwd_reduce<<<rgrid, 256, 0, st>>>(a, SH::M, D, NS ? 2 : 1);
+  k_bwd_reduce<<<rgrid, 256, 0, st>>>(a, SA::M, D, NS ? 2 : 1);
   timing_mark(KC_BWD_REDUCE, st, false);
   return hipGetLastError();
 }
 
-template <class T, int D, int FW, int NW>
+template <class T, int D, int FWA, int NWA, int FWB, int NWB>
 static hipError_t run_bwd_v(const BwdArgs& a, bool ns, bool causal, hipStream_t st) {
-  return ns ? run_bwd_t<T, D, FW, NW, true>(a, causal, st) : run_bwd_t<T, D, FW, NW, false>(a, causal, st);
+  return ns ? run_bwd_t<T, D, true, FWA, NWA, FWB, NWB>(a, causal, st)
+            : run_bwd_t<T, D, false, FWA, NWA, FWB, NWB>(a, causal, st);
 }
 
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st) {
   if (ks.bf16) {
-    if (ks.d == 32 && ks.m == 64) return run_bwd_v<__bf16, 32, 16, 4>(a, ks.nonstationary, ks.causal, st);
-    if (ks.d == 64 && ks.m == 64) return run_bwd_v<__bf16, 64, 16, 4>(a, ks.nonstationary, ks.causal, st);
-    if (ks.d == 64 && ks.m == 128) return run_bwd_v<__bf16, 64, 32, 4>(a, ks.nonstationary, ks.causal, st);
+    if (ks.d == 32 && ks.m == 64) return run_bwd_v<__bf16, 32, 16, 4, 16, 4>(a, ks.nonstationary, ks.causal, st);
+    if (ks.d == 64 && ks.m == 64) return run_bwd_v<__bf16, 64, 16, 4, 16, 4>(a, ks.nonstationary, ks.causal, st);
+    if (ks.d == 64 && ks.m == 128) return run_bwd_v<__bf16, 64, 16, 8, 32, 4>(a, ks.nonstationary, ks.causal, st);
   } else {
-    if (ks.d == 32 && ks.m == 64) return run_bwd_v<float, 32, 16, 4>(a, ks.nonstationary, ks.causal, st);
+    if (ks.d == 32 && ks.m == 64) return run_bwd_v<float, 32, 16, 4, 16, 4>(a, ks.nonstationary, ks.causal, st);
   }
   return hipErrorNotSupported;
 }
+
+// Whether the dK/dV sweep splits the frequencies differently from the other
+// backward kernels (then it needs a second block of prepared fragments).
+bool bwd_split_differs(const KernelShape& ks) { return ks.bf16 && ks.d == 64 && ks.m == 128; }
 
 size_t bwd_state_floats(const KernelShape& ks) { return fwd_state_floats(ks); }
 // both sides (query rows and key rows) of the frequency-gradient partials

@@ -27,6 +27,24 @@ constexpr int CHUNK = 64;          // tokens per chunk
 constexpr int TT = CHUNK / 16;     // token tiles per chunk
 constexpr float INV_2PI = 0.15915494309189535f;
 
+// Workgroup -> (segment, b*H+h) for a 1-D grid of nseg * BH workgroups.
+// Consecutive workgroup ids are dealt round-robin to the 8 XCDs, each with its
+// own L2; the mapping gives every XCD a contiguous range of the list ordered
+// by (head, batch, segment), so the per-head frequency fragments that every
+// chunk reloads are shared by the workgroups of few heads in each L2.
+constexpr int NUM_XCD = 8;
+struct WgCoord {
+  int seg, bh;
+};
+__device__ __forceinline__ WgCoord wg_coord(int nseg, int H, int BH) {
+  const int T = nseg * BH;
+  const int L = blockIdx.x;
+  const int idx = (T % NUM_XCD == 0) ? (L % NUM_XCD) * (T / NUM_XCD) + L / NUM_XCD : L;
+  const int seg = idx % nseg, t = idx / nseg;
+  const int B = BH / H;
+  return {seg, (t % B) * H + t / B};
+}
+
 // ---------------------------------------------------------------------------
 // Fragments: 8 operand values per lane.  Lane l supplies row/col l%16 and the
 // contraction indices k(g, j) for g = l/16, j = 0..7.

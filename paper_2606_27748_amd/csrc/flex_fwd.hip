@@ -38,7 +38,8 @@ void k_fwd_state(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];
 
-  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;   // seg: sub-segment
+  const WgCoord wc = wg_coord(a.segments * a.sub, a.H, a.BH);   // seg: sub-segment
+  const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE;
   const int cps = a.chunks_per_seg / a.sub;
   const int c0 = seg * cps;
@@ -169,7 +170,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][SH::RPAD];
 
-  const int seg = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
+  const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const int c0 = seg * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
@@ -395,9 +397,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
 template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
-  constexpr int QG = (SH::DV >= 128) ? 1 : TT;
-  dim3 grid(a.segments, a.BH);
-  dim3 pgrid(a.segments * a.sub, a.BH);
+  constexpr int QG = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TT);
+  const dim3 grid(a.segments * a.BH);
+  const dim3 pgrid(a.segments * a.sub * a.BH);
   k_prep_freqs<T, D, FW, NW, NS><<<a.H, SH::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
   timing_mark(KC_FWD_STATE, st, true);
   k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
@@ -434,7 +436,7 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
   if (ks.bf16) {
     if (ks.d == 32 && ks.m == 64) return run_variant<__bf16, 32, 16, 4>(a, ns, causal, fmap, st);
     if (ks.d == 64 && ks.m == 64) return run_variant<__bf16, 64, 16, 4>(a, ns, causal, fmap, st);
-    if (ks.d == 64 && ks.m == 128) return run_variant<__bf16, 64, 32, 4>(a, ns, causal, fmap, st);
+    if (ks.d == 64 && ks.m == 128) return run_variant<__bf16, 64, 16, 8>(a, ns, causal, fmap, st);
     if (ks.d == 128 && ks.m == 256) return run_variant<__bf16, 128, 32, 8>(a, ns, causal, fmap, st);
   } else {
     if (ks.d == 32 && ks.m == 64) return run_variant<float, 32, 16, 4>(a, ns, causal, fmap, st);
@@ -461,12 +463,17 @@ size_t wfrag_bytes(const KernelShape& ks, int H) {
   if (ks.bf16) {
     if (ks.d == 32 && ks.m == 64) return ns ? wfrag_bytes_t<__bf16, 32, 16, true>(H, 4) : wfrag_bytes_t<__bf16, 32, 16, false>(H, 4);
     if (ks.d == 64 && ks.m == 64) return ns ? wfrag_bytes_t<__bf16, 64, 16, true>(H, 4) : wfrag_bytes_t<__bf16, 64, 16, false>(H, 4);
-    if (ks.d == 64 && ks.m == 128) return ns ? wfrag_bytes_t<__bf16, 64, 32, true>(H, 4) : wfrag_bytes_t<__bf16, 64, 32, false>(H, 4);
+    if (ks.d == 64 && ks.m == 128) return ns ? wfrag_bytes_t<__bf16, 64, 16, true>(H, 8) : wfrag_bytes_t<__bf16, 64, 16, false>(H, 8);
     if (ks.d == 128 && ks.m == 256) return ns ? wfrag_bytes_t<__bf16, 128, 32, true>(H, 8) : wfrag_bytes_t<__bf16, 128, 32, false>(H, 8);
   } else {
     if (ks.d == 32 && ks.m == 64) return ns ? wfrag_bytes_t<float, 32, 16, true>(H, 4) : wfrag_bytes_t<float, 32, 16, false>(H, 4);
   }
   return 0;
+}
+
+// Waves per workgroup of the forward kernels of a shape.
+int fwd_state_waves(const KernelShape& ks) {
+  return (ks.bf16 && ((ks.d == 64 && ks.m == 128) || (ks.d == 128 && ks.m == 256))) ? 8 : 4;
 }
 
 size_t fwd_state_floats(const KernelShape& ks) {

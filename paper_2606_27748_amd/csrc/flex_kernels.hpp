@@ -54,6 +54,7 @@ struct BwdArgs {
   float* dwpart;      // [2 sides][BH][segments][rows][d] frequency-gradient partials
   float* dtaupart;    // [BH][segments] partial dtau
   void* wfrag;        // per-head frequency fragments (prepared by k_prep_freqs)
+  void* wfrag_kv;     // fragments of the dK/dV sweep (== wfrag when its split is the same)
   int BH, B, H, N;
   int nchunks, segments, chunks_per_seg;
   float s_const;
@@ -71,6 +72,8 @@ size_t bwd_state_floats(const KernelShape& ks);
 size_t bwd_dw_floats(const KernelShape& ks);
 // bytes of the per-head frequency fragments for H heads
 size_t wfrag_bytes(const KernelShape& ks, int H);
+bool bwd_split_differs(const KernelShape& ks);
+int fwd_state_waves(const KernelShape& ks);
 
 // state: [BH][P*sub][E]; writes the exclusive prefix (causal) into slot p*sub
 // of every segment p, the exclusive suffix (reverse) into slot p*sub+sub-1, or
