@@ -108,7 +108,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="headline_causal_train_d64")
-    ap.add_argument("--cpu-slices", type=int, default=16)
+    ap.add_argument("--cpu-slices", type=int, default=32)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + steps only (for rocprofv3); no JSON")
