@@ -119,8 +119,17 @@ __device__ __forceinline__ float feature_grad(const Frag<T>& phi, const Frag<T>&
 template <class T, class SH>
 __device__ __forceinline__ void store_dpT(T* DPT, const f32x4& v, int pr, int tt) {
   const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  T* o = DPT + (pr * 16 + 4 * g) * SH::TPAD + tt * 16 + r;
+  if constexpr (IsBf16<T>::value) {
+    // two values per conversion instruction, stored as packed halves
+    const bf16x2 a = {(__bf16)v[0], (__bf16)v[1]};
+    const bf16x2 b = {(__bf16)v[2], (__bf16)v[3]};
+    lds_store_halves(o, o + SH::TPAD, __builtin_bit_cast(uint32_t, a));
+    lds_store_halves(o + 2 * SH::TPAD, o + 3 * SH::TPAD, __builtin_bit_cast(uint32_t, b));
+  } else {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) DPT[(pr * 16 + 4 * g + i) * SH::TPAD + tt * 16 + r] = (T)v[i];
+    for (int i = 0; i < 4; ++i) o[i * SH::TPAD] = v[i];
+  }
 }
 
 // The per-wave frequency-gradient partial dW'[rows][d] lives in LDS in
@@ -173,11 +182,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO XO[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T DOT[SH::DV * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T PK[NW][SH::FC * 16 * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T PQ[NW][SH::FC * 16 * SH::TPAD];
   __shared__ float GS[SH::CH][2];
   __shared__ float DEN[SH::CH];
   __shared__ float SSQ[SH::CH], SSK[SH::CH];
+  // per-token feature scales: s e(k) for keys, s e(q) / den for queries
+  __shared__ __attribute__((aligned(16))) float SCK[SH::CH], SCQ[SH::CH];
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -237,46 +246,40 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
         const float inv = ok ? 1.0f / DEN[t] : 0.f;
         GS[t][0] = inv;
         GS[t][1] = ok ? s : 0.f;
+        SCK[t] = row_scale(SSK[t], inv_c, a.s_const, ok);
+        SCQ[t] = row_scale(SSQ[t], inv_c, a.s_const, ok) * inv;
         if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = s; }
       }
     }
     __syncthreads();
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
-#pragma unroll
-    for (int tt = 0; tt < SH::TT; ++tt) {
-      f32x4 p[SH::PR];
-      float ssq;
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
-      float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
-#pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PK[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
-      sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
-#pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PQ[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
-    }
-    __syncthreads();
+    // both feature maps enter only the token sums: token-row features, no
+    // transpose; the key side and the query side one after the other
 #pragma unroll
     for (int ks = 0; ks < SH::KT; ++ks) {
       // value-side operands: rows = value columns, k = chunk tokens
-      Frag<T> vt[SH::DVT1], gt[SH::DVT1];
+      {
+        Frag<T> vt[SH::DVT1], pk[SH::FC];
 #pragma unroll
-      for (int dt = 0; dt < SH::DVT; ++dt) {
-        vt[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
-        gt[dt] = lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        vt[SH::DVT] = ones;
+        feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk);
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+          for (int dt = 0; dt < SH::DVT1; ++dt) mma(ST[dt][fc], vt[dt], pk[fc]);
       }
-      vt[SH::DVT] = ones;
-      gt[SH::DVT] = delta_rows<T>(GS, ks);
+      {
+        Frag<T> gt[SH::DVT1], pq[SH::FC];
 #pragma unroll
-      for (int fc = 0; fc < SH::FC; ++fc) {
-        const Frag<T> pk = lds_tok_frag<T>(PK[w] + (fc * 16 + r) * SH::TPAD, ks);
-        const Frag<T> pq = lds_tok_frag<T>(PQ[w] + (fc * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks);
+        gt[SH::DVT] = delta_rows<T>(GS, ks);
+        feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XQ, SCQ, ks, pq);
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT1; ++dt) {
-          mma(ST[dt][fc], vt[dt], pk);
-          mma(RT[dt][fc], gt[dt], pq);
-        }
+        for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+          for (int dt = 0; dt < SH::DVT1; ++dt) mma(RT[dt][fc], gt[dt], pq[fc]);
       }
     }
   }
@@ -315,7 +318,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
-  __shared__ float SSQ[SH::CH], SSK[SH::CH];
+  __shared__ float SSQ[SH::CH];
+  __shared__ __attribute__((aligned(16))) float SCK[SH::CH];   // per-token key scale s e(k)
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -358,7 +362,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
     __syncthreads();
-    sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
+    sq.store(XQ, SSQ);
+    sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
+    sv.store(XV); sdo.store(XDO);
     sv.template store_t<T, SH::TPAD>(VT);
     sq.template store_t<T, SH::TPAD>(QT);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
@@ -373,16 +379,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
-    // phi(K) of this wave's features, transposed into LDS
+    // phi(K) of this wave's features enters only contractions over the key
+    // tokens: token-row fragments (k = tokens), no transpose
+    Frag<T> pk[SH::KT][SH::FC];
 #pragma unroll
-    for (int tt = 0; tt < SH::TT; ++tt) {
-      f32x4 p[SH::PR];
-      float ssq;
-      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
-      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
-#pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft) store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
-    }
+    for (int ks = 0; ks < SH::KT; ++ks) feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk[ks]);
     // phi(Q) and its P2-derivative fragments
     Frag<T> phq[SH::FT][SH::TT], psq[SH::FT][SH::TT];
 #pragma unroll
@@ -423,8 +424,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         for (int ks = 0; ks < SH::KT; ++ks) mt[ks][tq] = pair_tiles<T>(m[2 * ks], m[2 * ks + 1]);
       }
     }
-    __syncthreads();  // phi(K)^T complete
-
     // dphi(Q)^T[feature][query] = (phi(K)^T M^T + S'^T-rows x [dO | -delta]) / den
     f32x4 dph[SH::FC][SH::TT];
 #pragma unroll
@@ -450,8 +449,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         if (CAUSAL) {
 #pragma unroll
           for (int ks = 0; ks < SH::KT; ++ks)
-            if (32 * ks <= 16 * tq + 15)
-              mma(acc, lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks), mt[ks][tq]);
+            if (32 * ks <= 16 * tq + 15) mma(acc, pk[ks][fc], mt[ks][tq]);
         }
 #pragma unroll
         for (int kd = 0; kd < KG; ++kd) {
@@ -473,10 +471,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc) {
-          const Frag<T> pk = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
 #pragma unroll
-          for (int dt = 0; dt < SH::DVT; ++dt) mma(ST[dt][fc], vt[dt], pk);
-          mma(ST[SH::DVT][fc], ones, pk);
+          for (int dt = 0; dt < SH::DVT; ++dt) mma(ST[dt][fc], vt[dt], pk[ks][fc]);
+          mma(ST[SH::DVT][fc], ones, pk[ks][fc]);
         }
       }
     }
@@ -527,7 +524,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         if (tok < a.N) *reinterpret_cast<float4*>(dQ + (size_t)tok * D + 4 * c4) = s;
       }
     }
-    __syncthreads();  // every wave is done with phi(K)^T
+    // PT[w] is this wave's own block: program order suffices between its uses
 #pragma unroll
     for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll

@@ -34,9 +34,10 @@ void k_fwd_state(FwdArgs a) {
   typedef RowStage<IO, SH::DV, SH::NT> StV;
   constexpr bool STX = SH::STAGE_X;
   __shared__ __attribute__((aligned(16))) IO XK[STX ? StK::LDS_ELEMS : 8];
-  __shared__ float SSK[CHUNK];
+  __shared__ __attribute__((aligned(16))) float SCK[CHUNK];   // staged: per-token scale s e(k)
   __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];
+  // d = 128 (rows read from global memory): phi(K) transposed through LDS
+  __shared__ __attribute__((aligned(16))) T PT[STX ? 1 : NW][STX ? 8 : SH::FC * 16 * SH::TPAD];
 
   const WgCoord wc = wg_coord(a.segments * a.sub, a.H, a.BH);   // seg: sub-segment
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -67,7 +68,8 @@ void k_fwd_state(FwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
     __syncthreads();
-    if (STX) sk.store(XK, SSK);
+    if (STX)
+      sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.template store_t<T, SH::TPAD>(VT);
     if (c + 1 < c1) {
       if (STX) sk.fetch(K, tok0 + CHUNK, a.N);
@@ -76,31 +78,46 @@ void k_fwd_state(FwdArgs a) {
     __syncthreads();
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
+    if constexpr (STX) {
+      // phi(K) with the tokens as the contraction index, straight from registers
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
-      f32x4 p[SH::PR];
-      float ssq;
-      if (STX)
-        project_tile_lds<T, D, FW, NS, StK::LD>(fs, XK, SSK, tt, p, ssq);
-      else
+      for (int ks = 0; ks < SH::KT; ++ks) {
+        Frag<T> pk[SH::FC];
+        feature_frags_rows<T, D, FW, NS, StK::LD>(fs, XK, SCK, ks, pk);
+        Frag<T> vf[SH::DVT];
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc) {
+#pragma unroll
+          for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk[fc], vf[dt]);
+          mma(S[fc][SH::DVT], pk[fc], ones);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) {
+        f32x4 p[SH::PR];
+        float ssq;
         project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
-      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+        const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft)
-        store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
-    }
-    __syncthreads();
+        for (int ft = 0; ft < SH::FT; ++ft)
+          store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
+      }
+      __syncthreads();
 #pragma unroll
-    for (int ks = 0; ks < SH::KT; ++ks) {
-      Frag<T> vf[SH::DVT];
+      for (int ks = 0; ks < SH::KT; ++ks) {
+        Frag<T> vf[SH::DVT];
 #pragma unroll
-      for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
 #pragma unroll
-      for (int fc = 0; fc < SH::FC; ++fc) {
-        const Frag<T> pk = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+        for (int fc = 0; fc < SH::FC; ++fc) {
+          const Frag<T> pk = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk, vf[dt]);
-        mma(S[fc][SH::DVT], pk, ones);
+          for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk, vf[dt]);
+          mma(S[fc][SH::DVT], pk, ones);
+        }
       }
     }
   }

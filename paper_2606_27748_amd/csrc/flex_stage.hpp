@@ -44,6 +44,11 @@ struct RowStage {
   // store, plus the squared norm of every row into ssq[ROWS] (the VPR vectors
   // of a row sit in VPR consecutive lanes: summed with lane shuffles)
   __device__ __forceinline__ void store(IO* lds, float* ssq) const {
+    store(lds, ssq, [](int, float s) { return s; });
+  }
+  // store, plus f(row, squared norm of the row) into out[ROWS]
+  template <class F>
+  __device__ __forceinline__ void store(IO* lds, float* out, F f) const {
     static_assert(NT % VPR == 0 && VPR <= WAVE, "a row's vectors must share a wave");
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
@@ -57,7 +62,7 @@ struct RowStage {
         for (int j = 0; j < VEC; ++j) { const float x = io_to_float(e[j]); s += x * x; }
       }
       s = lane_sum<VPR>(s);
-      if (v < NV && v % VPR == 0) ssq[v / VPR] = s;
+      if (v < NV && v % VPR == 0) out[v / VPR] = f(v / VPR, s);
     }
   }
   // transposed store: ldsT[col][token] with row stride LDT (operand type T)
@@ -180,16 +185,99 @@ __device__ __forceinline__ Frag<T> pair_tiles(const f32x4& a, const f32x4& b) {
   return f;
 }
 
+// Projection of one 16-token tile with the tokens as rows: p[pr] holds rows =
+// tokens tt*16 + 4g + i and cols = frequency (lane % 16) of projection tile
+// pr.  The operands of project_tile_lds are swapped (the register layouts of
+// the two MFMA operands are the same), so the frequency fragments are shared.
+template <class T, int D, int FW, bool NS, int LD>
+__device__ __forceinline__ void project_rows_lds(const FreqSlice<T, D, FW, NS>& fs,
+                                                 const typename Io<T>::type* X, int tt,
+                                                 f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR]) {
+  typedef FreqSlice<T, D, FW, NS> FS;
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const typename Io<T>::type* row = X + (tt * 16 + r) * LD;
+#pragma unroll
+  for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
+#pragma unroll
+  for (int ks = 0; ks < FS::KD; ++ks) {
+    Frag<T> x;
+    lds_row8(x, row, ks * 32 + 8 * g);
+#pragma unroll
+    for (int pr = 0; pr < FS::PR; ++pr)
+#pragma unroll
+      for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], x, fs.w[sp][pr][ks]);
+  }
+}
+
+// Features of a wave's frequency slice for the 32 tokens of k-step ks, with
+// the tokens as the contraction index: out[2ft] (cos-type) and out[2ft+1]
+// (sin-type) have cols = the feature (lane % 16) and k = tokens in the order
+// of pair_tiles / lds_tok_frag.  sc[t] is the per-token scale (0 for tokens
+// past the end).  Used where a feature map only enters contractions over
+// tokens (state sums), which then need no transpose through LDS.
+template <class T, int D, int FW, bool NS, int LD>
+__device__ __forceinline__ void feature_frags_rows(const FreqSlice<T, D, FW, NS>& fs,
+                                                   const typename Io<T>::type* X, const float* sc,
+                                                   int ks, Frag<T> (&out)[2 * (FW / 16)]) {
+  typedef FreqSlice<T, D, FW, NS> FS;
+  constexpr int FT = FW / 16;
+  const int g = (threadIdx.x % WAVE) / 16;
+  f32x4 fc[2][FT], fsn[2][FT];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int tt = 2 * ks + hh;
+    f32x4 p[FS::PR];
+    project_rows_lds<T, D, FW, NS, LD>(fs, X, tt, p);
+    const float4 s4 = *reinterpret_cast<const float4*>(sc + tt * 16 + 4 * g);
+    const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float s1, c1;
+        sincos_rev(p[ft][i], s1, c1);
+        const float m = NS ? sv[i] * cos_rev(p[FT + ft][i]) : sv[i];
+        fc[hh][ft][i] = c1 * m;
+        fsn[hh][ft][i] = s1 * m;
+      }
+  }
+#pragma unroll
+  for (int ft = 0; ft < FT; ++ft) {
+    out[2 * ft] = pair_tiles<T>(fc[0][ft], fc[1][ft]);
+    out[2 * ft + 1] = pair_tiles<T>(fsn[0][ft], fsn[1][ft]);
+  }
+}
+
+// Two packed bf16 values (low half, high half of one register) written to two
+// LDS addresses: the halves are stored as they are, without unpacking and
+// converting the values again.
+__device__ __forceinline__ void lds_store_halves(__bf16* p0, __bf16* p1, uint32_t w) {
+  // opaque to the optimizer, which would otherwise convert each half again
+  asm("" : "+v"(w));
+  *reinterpret_cast<u16*>(p0) = (u16)(w & 0xffffu);
+  *reinterpret_cast<u16*>(p1) = (u16)(w >> 16);
+}
+
 // Write one wave's phi(K) fragment for frequency tile ft and token tile tt
 // into its feature-major LDS block PT[feature][token].
 template <class T, class SH>
 __device__ __forceinline__ void store_phiT(T* PT, const Frag<T>& f, int ft, int tt) {
   const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const int t = tt * 16 + r;
+  T* c = PT + ((2 * ft) * 16 + 4 * g) * SH::TPAD + t;       // cos-type rows
+  T* s = PT + ((2 * ft + 1) * 16 + 4 * g) * SH::TPAD + t;   // sin-type rows
+  if constexpr (IsBf16<T>::value) {
+    const uint4 w = __builtin_bit_cast(uint4, f.v);
+    lds_store_halves(c, c + SH::TPAD, w.x);
+    lds_store_halves(c + 2 * SH::TPAD, c + 3 * SH::TPAD, w.y);
+    lds_store_halves(s, s + SH::TPAD, w.z);
+    lds_store_halves(s + 2 * SH::TPAD, s + 3 * SH::TPAD, w.w);
+  } else {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    PT[((2 * ft) * 16 + 4 * g + i) * SH::TPAD + t] = f.raw(i);
-    PT[((2 * ft + 1) * 16 + 4 * g + i) * SH::TPAD + t] = f.raw(4 + i);
+    for (int i = 0; i < 4; ++i) {
+      c[i * SH::TPAD] = f.raw(i);
+      s[i * SH::TPAD] = f.raw(4 + i);
+    }
   }
 }
 
