@@ -114,24 +114,6 @@ __device__ __forceinline__ float feature_grad(const Frag<T>& phi, const Frag<T>&
   return gsum;
 }
 
-// Write a dP tile (rows = projection rows of tile pr, cols = tokens of tile tt)
-// transposed into the wave's LDS block DPT[row][token].
-template <class T, class SH>
-__device__ __forceinline__ void store_dpT(T* DPT, const f32x4& v, int pr, int tt) {
-  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  T* o = DPT + (pr * 16 + 4 * g) * SH::TPAD + tt * 16 + r;
-  if constexpr (IsBf16<T>::value) {
-    // two values per conversion instruction, stored as packed halves
-    const bf16x2 a = {(__bf16)v[0], (__bf16)v[1]};
-    const bf16x2 b = {(__bf16)v[2], (__bf16)v[3]};
-    lds_store_halves(o, o + SH::TPAD, __builtin_bit_cast(uint32_t, a));
-    lds_store_halves(o + 2 * SH::TPAD, o + 3 * SH::TPAD, __builtin_bit_cast(uint32_t, b));
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[i * SH::TPAD] = v[i];
-  }
-}
-
 // The per-wave frequency-gradient partial dW'[rows][d] lives in LDS in
 // register-dump order (tile, lane, 4 floats): each chunk's MFMA tiles are added
 // with one 16-byte read and write per lane and tile.
@@ -314,7 +296,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T QT[D * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(K)^T, then dP^T
+  constexpr int LDP = SH::FC * 16 + 4;          // row stride of the per-wave [token][row] blocks
+  __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // dP, [token][projection row]
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
@@ -528,7 +511,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 #pragma unroll
     for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
-      for (int tt = 0; tt < SH::TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
+      for (int tt = 0; tt < SH::TT; ++tt) store_tile_nm<T>(PT[w], LDP, tt * 16, pr * 16, dp[pr][tt]);
     __syncthreads();
     // frequency gradient partial: dW'[rows][d] += dP^T Q
     {
@@ -544,7 +527,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tok_frag<T>(QT + (dt * 16 + r) * SH::TPAD, ks);
 #pragma unroll
         for (int pr = 0; pr < SH::PR; ++pr) {
-          const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+          const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, pr * 16);
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) mma(dw[pr][dt], dpt, xq[dt]);
         }
@@ -571,16 +554,17 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int KG = (SH::DVT1 + 1) / 2;
   constexpr int QG = NW >= 8 ? 1 : 2;
   constexpr int RP = (D > SH::DV ? D : SH::DV) + 4;
-  constexpr int RLP = SH::FC * 16 + 4;           // row stride of the transposed R' copy
+  constexpr int RLP = SH::DV + 4;                // row stride of the bf16 R' copy, [feature][value col]
+  constexpr int LDP = SH::FC * 16 + 4;           // row stride of the per-wave [token][row] blocks
   constexpr int RED_BYTES = NW * QG * 16 * RP * 4;
-  constexpr int RL_BYTES = NW * SH::DV * RLP * (int)sizeof(T);
+  constexpr int RL_BYTES = NW * SH::FC * 16 * RLP * (int)sizeof(T);
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) T DOT[SH::DV * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T KT[D * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T PT[NW][SH::FC * 16 * SH::TPAD];   // phi(Q)^T/den, then dP^T
+  __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // phi(Q)/den, then dP: [token][row]
   __shared__ __attribute__((aligned(16))) char REDRL[RED_BYTES > RL_BYTES ? RED_BYTES : RL_BYTES];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
@@ -660,7 +644,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft) {
           phq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
-          store_phiT<T, SH>(PT[w], phq[ft][tt], ft, tt);
+          store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16, phq[ft][tt]);
         }
       }
     }
@@ -710,14 +694,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         }
       }
     }
-    // transposed copy of R' (rows = value columns, cols = this wave's features) for dV
+    // bf16 copy of R' as [feature][value col] for dV (read back transposed)
 #pragma unroll
     for (int dt = 0; dt < SH::DVT; ++dt)
 #pragma unroll
       for (int fc = 0; fc < SH::FC; ++fc)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          RL[(size_t)w * SH::DV * RLP + (dt * 16 + 4 * g + i) * RLP + fc * 16 + r] = (T)RT[dt][fc][i];
+        store_tile_nm<T>(RL + (size_t)w * SH::FC * 16 * RLP, RLP, fc * 16, dt * 16, RT[dt][fc]);
     __syncthreads();  // phi(Q)^T and the R' copy complete
 
     // dV^T partial[value col][key] = dO^T A/den (intra) + R'[:dv]^T-rows x phi(K)
@@ -734,7 +716,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         }
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft)
-          mma(acc, lds_tok_frag<T>(RL + (size_t)w * SH::DV * RLP + (dt * 16 + r) * RLP, ft), phk[ft][tk]);
+          mma(acc, lds_tr_frag<T>(RL + (size_t)w * SH::FC * 16 * RLP, RLP, (2 * ft) * 16 + 4 * g,
+                                  (2 * ft + 1) * 16 + 4 * g, dt * 16), phk[ft][tk]);
         dvp[dt][tk] = acc;
       }
     // dV: reduce the per-wave partials
@@ -783,7 +766,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
           for (int ks = 0; ks < SH::KT; ++ks)
             if (32 * ks + 31 >= 16 * tk)
-              mma(acc, lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks), mp[ks][tk]);
+              mma(acc, lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16), mp[ks][tk]);
         }
 #pragma unroll
         for (int kd = 0; kd < KG; ++kd) {
@@ -803,7 +786,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         gt[SH::DVT] = delta_rows<T>(GS, ks);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc) {
-          const Frag<T> pq = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+          const Frag<T> pq = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16);
 #pragma unroll
           for (int dt = 0; dt < SH::DVT1; ++dt) mma(RT[dt][fc], gt[dt], pq);
         }
@@ -877,7 +860,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
     for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
-      for (int tt = 0; tt < SH::TT; ++tt) store_dpT<T, SH>(PT[w], dp[pr][tt], pr, tt);
+      for (int tt = 0; tt < SH::TT; ++tt) store_tile_nm<T>(PT[w], LDP, tt * 16, pr * 16, dp[pr][tt]);
     __syncthreads();
     {
       f32x4 dw[SH::PR][DT];
@@ -892,7 +875,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tok_frag<T>(KT + (dt * 16 + r) * SH::TPAD, ks);
 #pragma unroll
         for (int pr = 0; pr < SH::PR; ++pr) {
-          const Frag<T> dpt = lds_tok_frag<T>(PT[w] + (pr * 16 + r) * SH::TPAD, ks);
+          const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, pr * 16);
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) mma(dw[pr][dt], dpt, xk[dt]);
         }

@@ -36,8 +36,9 @@ void k_fwd_state(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO XK[STX ? StK::LDS_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) float SCK[CHUNK];   // staged: per-token scale s e(k)
   __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
-  // d = 128 (rows read from global memory): phi(K) transposed through LDS
-  __shared__ __attribute__((aligned(16))) T PT[STX ? 1 : NW][STX ? 8 : SH::FC * 16 * SH::TPAD];
+  // d = 128 (rows read from global memory): phi(K) as [token][feature], read back transposed
+  constexpr int LDP = SH::FC * 16 + 4;
+  __shared__ __attribute__((aligned(16))) T PT[STX ? 1 : NW][STX ? 8 : CHUNK * LDP];
 
   const WgCoord wc = wg_coord(a.segments * a.sub, a.H, a.BH);   // seg: sub-segment
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -63,7 +64,7 @@ void k_fwd_state(FwdArgs a) {
 #pragma unroll
     for (int dt = 0; dt < SH::DVT1; ++dt) S[fc][dt] = zero4();
   const Frag<T> ones = ones_col0<T>();
-  const int r = (threadIdx.x % WAVE) % 16;
+  const int r = (threadIdx.x % WAVE) % 16, g = (threadIdx.x % WAVE) / 16;
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
@@ -103,9 +104,9 @@ void k_fwd_state(FwdArgs a) {
         const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft)
-          store_phiT<T, SH>(PT[w], features<T, SH::FT, NS>(p, ft, sc), ft, tt);
+          store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16,
+                           features<T, SH::FT, NS>(p, ft, sc));
       }
-      __syncthreads();
 #pragma unroll
       for (int ks = 0; ks < SH::KT; ++ks) {
         Frag<T> vf[SH::DVT];
@@ -113,7 +114,7 @@ void k_fwd_state(FwdArgs a) {
         for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc) {
-          const Frag<T> pk = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+          const Frag<T> pk = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16);
 #pragma unroll
           for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk, vf[dt]);
           mma(S[fc][SH::DVT], pk, ones);
@@ -179,7 +180,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   typedef RowStage<IO, SH::DV, SH::NT> StV;
   constexpr bool STX = SH::STAGE_X;
   constexpr int VT_N = CAUSAL ? SH::DV * SH::TPAD : 8;
-  constexpr int PT_N = CAUSAL ? SH::FC * 16 * SH::TPAD : 8;
+  constexpr int LDP = SH::FC * 16 + 4;     // [token][feature] rows of a wave's phi(K) block
+  constexpr int PT_N = CAUSAL ? CHUNK * LDP : 8;
   __shared__ __attribute__((aligned(16))) IO XQ[STX ? StX::LDS_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) IO XK[(STX && CAUSAL) ? StX::LDS_ELEMS : 8];
   __shared__ float SSQ[CHUNK], SSK[CHUNK];
@@ -264,7 +266,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft) {
           pk[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
-          store_phiT<T, SH>(PT[w], pk[ft][tt], ft, tt);
+          store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16, pk[ft][tt]);
         }
       }
     }
@@ -299,7 +301,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
         for (int ks = 0; ks < SH::KT; ++ks) ap[ks][tq] = pair_tiles<T>(at[2 * ks], at[2 * ks + 1]);
       }
     }
-    if (CAUSAL) __syncthreads();  // PT (transposed phi(K)) complete
 
     Frag<T> vf[CAUSAL ? SH::DVT : 1][SH::KT];
     if (CAUSAL) {
@@ -335,7 +336,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
         for (int ks = 0; ks < SH::KT; ++ks)
 #pragma unroll
           for (int fc = 0; fc < SH::FC; ++fc) {
-            const Frag<T> pkt = lds_tok_frag<T>(PT[w] + (fc * 16 + r) * SH::TPAD, ks);
+            const Frag<T> pkt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16);
 #pragma unroll
             for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pkt, vf[dt][ks]);
             mma(S[fc][SH::DVT], pkt, ones);

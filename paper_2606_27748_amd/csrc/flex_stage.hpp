@@ -248,37 +248,71 @@ __device__ __forceinline__ void feature_frags_rows(const FreqSlice<T, D, FW, NS>
   }
 }
 
-// Two packed bf16 values (low half, high half of one register) written to two
-// LDS addresses: the halves are stored as they are, without unpacking and
-// converting the values again.
-__device__ __forceinline__ void lds_store_halves(__bf16* p0, __bf16* p1, uint32_t w) {
-  // opaque to the optimizer, which would otherwise convert each half again
-  asm("" : "+v"(w));
-  *reinterpret_cast<u16*>(p0) = (u16)(w & 0xffffu);
-  *reinterpret_cast<u16*>(p1) = (u16)(w >> 16);
-}
+// ---------------------------------------------------------------------------
+// Transposes through LDS with the gfx950 transpose load.  An accumulator tile
+// holds column n = lane % 16 and rows m = 4g + i (g = lane / 16); written as
+// bf16 into an [n][m]-major block it is one 8-byte store per lane.  Reading
+// that block back with ds_read_b64_tr_b16 gives an operand whose lane is m and
+// whose k index is n: within each group of 16 lanes, slot j of lane i receives
+// element i % 4 of the 4-element row addressed by lane 4j + i / 4, so lane
+// (g, i) addresses row kb + i / 4, columns m0 + 4 (i % 4) .. + 3, and receives
+// column m0 + i of rows kb .. kb + 3.  The fp32 operand type keeps plain
+// element-wise accesses of the same layouts.
+// ---------------------------------------------------------------------------
+typedef short tr_v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) tr_v4i16 lds_tr_v4i16;
 
-// Write one wave's phi(K) fragment for frequency tile ft and token tile tt
-// into its feature-major LDS block PT[feature][token].
-template <class T, class SH>
-__device__ __forceinline__ void store_phiT(T* PT, const Frag<T>& f, int ft, int tt) {
+// Rows 4g..4g+3 of an accumulator tile (values v) into L[n][m0 + 4g + i],
+// n = n0 + lane % 16.
+template <class T>
+__device__ __forceinline__ void store_tile_nm(T* L, int ld, int n0, int m0, const f32x4& v) {
   const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const int t = tt * 16 + r;
-  T* c = PT + ((2 * ft) * 16 + 4 * g) * SH::TPAD + t;       // cos-type rows
-  T* s = PT + ((2 * ft + 1) * 16 + 4 * g) * SH::TPAD + t;   // sin-type rows
+  T* o = L + (n0 + r) * ld + m0 + 4 * g;
   if constexpr (IsBf16<T>::value) {
-    const uint4 w = __builtin_bit_cast(uint4, f.v);
-    lds_store_halves(c, c + SH::TPAD, w.x);
-    lds_store_halves(c + 2 * SH::TPAD, c + 3 * SH::TPAD, w.y);
-    lds_store_halves(s, s + SH::TPAD, w.z);
-    lds_store_halves(s + 2 * SH::TPAD, s + 3 * SH::TPAD, w.w);
+    const bf16x4 b = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+    *reinterpret_cast<bf16x4*>(o) = b;
   } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      c[i * SH::TPAD] = f.raw(i);
-      s[i * SH::TPAD] = f.raw(4 + i);
+    for (int i = 0; i < 4; ++i) o[i] = v[i];
+  }
+}
+
+// The two halves of an operand fragment (slots 0..3 and 4..7, each four rows
+// 4g..4g+3 of one tile) into L[n][m0a + 4g + i] and L[n][m0b + 4g + i].
+template <class T>
+__device__ __forceinline__ void store_frag_nm(T* L, int ld, int n0, int m0a, int m0b, const Frag<T>& f) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  T* row = L + (n0 + r) * ld + 4 * g;
+  if constexpr (IsBf16<T>::value) {
+    const uint4 w = __builtin_bit_cast(uint4, f.v);
+    *reinterpret_cast<uint2*>(row + m0a) = make_uint2(w.x, w.y);
+    *reinterpret_cast<uint2*>(row + m0b) = make_uint2(w.z, w.w);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { row[m0a + i] = f.raw(i); row[m0b + i] = f.raw(4 + i); }
+  }
+}
+
+// Operand fragment with lane m = m0 + lane % 16 and k slots 0..3 = rows
+// kb0 .. kb0+3, slots 4..7 = rows kb1 .. kb1+3 of an [k][m]-major block
+// (kb0, kb1 may differ between lane groups).
+template <class T>
+__device__ __forceinline__ Frag<T> lds_tr_frag(const T* L, int ld, int kb0, int kb1, int m0) {
+  const int i = (threadIdx.x % WAVE) % 16;
+  Frag<T> f;
+  if constexpr (IsBf16<T>::value) {
+    const int off = (i / 4) * ld + m0 + 4 * (i % 4);
+    const tr_v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_tr_v4i16*)(L + kb0 * ld + off));
+    const tr_v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_tr_v4i16*)(L + kb1 * ld + off));
+    f.v = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      f.set(j, L[(kb0 + j) * ld + m0 + i]);
+      f.set(4 + j, L[(kb1 + j) * ld + m0 + i]);
     }
   }
+  return f;
 }
 
 }  // namespace flex
