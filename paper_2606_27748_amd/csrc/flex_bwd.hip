@@ -162,8 +162,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XO[StV::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T DOT[SH::DV * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
   __shared__ float GS[SH::CH][2];
   __shared__ float DEN[SH::CH];
   __shared__ float SSQ[SH::CH], SSK[SH::CH];
@@ -206,8 +205,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     const int tok0 = c * SH::CH;
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sdo.store(XDO); so.store(XO);
-    sv.template store_t<T, SH::TPAD>(VT);
-    sdo.template store_t<T, SH::TPAD>(DOT);
+    sv.store(XV);
     if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
     if (c + 1 < c1) {
       const int t1 = tok0 + SH::CH;
@@ -244,7 +242,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
       {
         Frag<T> vt[SH::DVT1], pk[SH::FC];
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
         vt[SH::DVT] = ones;
         feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk);
 #pragma unroll
@@ -255,7 +253,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
       {
         Frag<T> gt[SH::DVT1], pq[SH::FC];
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XDO), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
         gt[SH::DVT] = delta_rows<T>(GS, ks);
         feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XQ, SCQ, ks, pq);
 #pragma unroll
@@ -294,8 +292,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T QT[D * SH::TPAD];
   constexpr int LDP = SH::FC * 16 + 4;          // row stride of the per-wave [token][row] blocks
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // dP, [token][projection row]
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
@@ -348,8 +344,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     sq.store(XQ, SSQ);
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV); sdo.store(XDO);
-    sv.template store_t<T, SH::TPAD>(VT);
-    sq.template store_t<T, SH::TPAD>(QT);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
     if (c + 1 < c1) {
       const int t1 = tok0 + SH::CH;
@@ -451,7 +445,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       for (int ks = 0; ks < SH::KT; ++ks) {
         Frag<T> vt[SH::DVT];
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc) {
 #pragma unroll
@@ -524,7 +518,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       for (int ks = 0; ks < SH::KT; ++ks) {
         Frag<T> xq[DT];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tok_frag<T>(QT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XQ), StX::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
 #pragma unroll
         for (int pr = 0; pr < SH::PR; ++pr) {
           const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, pr * 16);
@@ -562,8 +556,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) T DOT[SH::DV * SH::TPAD];
-  __shared__ __attribute__((aligned(16))) T KT[D * SH::TPAD];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // phi(Q)/den, then dP: [token][row]
   __shared__ __attribute__((aligned(16))) char REDRL[RED_BYTES > RL_BYTES ? RED_BYTES : RL_BYTES];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
@@ -617,8 +609,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     const int tok0 = c * SH::CH;
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
-    sdo.template store_t<T, SH::TPAD>(DOT);
-    sk.template store_t<T, SH::TPAD>(KT);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
     if (c - 1 >= c0) {
       const int t1 = tok0 - SH::CH;
@@ -712,7 +702,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         if (CAUSAL) {
 #pragma unroll
           for (int ks = 0; ks < SH::KT; ++ks)
-            if (32 * ks + 31 >= 16 * tk) mma(acc, lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks), ap[ks][tk]);
+            if (32 * ks + 31 >= 16 * tk) mma(acc, lds_tr_frag<T>(reinterpret_cast<const T*>(XDO), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16), ap[ks][tk]);
         }
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft)
@@ -782,7 +772,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       for (int ks = 0; ks < SH::KT; ++ks) {
         Frag<T> gt[SH::DVT1];
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tok_frag<T>(DOT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XDO), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
         gt[SH::DVT] = delta_rows<T>(GS, ks);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc) {
@@ -872,7 +862,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       for (int ks = 0; ks < SH::KT; ++ks) {
         Frag<T> xk[DT];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tok_frag<T>(KT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XK), StX::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
 #pragma unroll
         for (int pr = 0; pr < SH::PR; ++pr) {
           const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, pr * 16);
@@ -972,15 +962,13 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FWB, NWB, NS, BWD_CHUNK> SB;
   static_assert(SA::M == SB::M && SA::STATE == SB::STATE, "splits of one shape");
   const dim3 grid(a.segments * a.BH);
-  k_prep_freqs<T, D, FWA, NWA, NS><<<a.H, SA::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SA::M);
+  k_prep_freqs<T, D, FWA, NWA, NS><<<dim3(a.H, NWA, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, SA::M);
   if (a.wfrag_kv != a.wfrag)
-    k_prep_freqs<T, D, FWB, NWB, NS><<<a.H, SB::NT, 0, st>>>(a.W1, a.W2, a.wfrag_kv, SB::M);
+    k_prep_freqs<T, D, FWB, NWB, NS><<<dim3(a.H, NWB, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag_kv, SB::M);
   timing_mark(KC_BWD_PREPASS, st, true);
   k_bwd_prepass<T, D, FWA, NWA, NS><<<grid, SA::NT, 0, st>>>(a);
   timing_mark(KC_BWD_PREPASS, st, false);
-  hipError_t e = launch_state_scan(a.sstate, a.BH, a.segments, 1, SA::STATE, causal, false, st);
-  if (e != hipSuccess) return e;
-  e = launch_state_scan(a.rstate, a.BH, a.segments, 1, SA::STATE, causal, true, st);
+  const hipError_t e = launch_state_scan(a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_BWD_DQ, st, true);
   if (causal)

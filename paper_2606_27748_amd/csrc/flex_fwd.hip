@@ -35,7 +35,7 @@ void k_fwd_state(FwdArgs a) {
   constexpr bool STX = SH::STAGE_X;
   __shared__ __attribute__((aligned(16))) IO XK[STX ? StK::LDS_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) float SCK[CHUNK];   // staged: per-token scale s e(k)
-  __shared__ __attribute__((aligned(16))) T VT[SH::DV * SH::TPAD];
+  __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];   // [token][value col]
   // d = 128 (rows read from global memory): phi(K) as [token][feature], read back transposed
   constexpr int LDP = SH::FC * 16 + 4;
   __shared__ __attribute__((aligned(16))) T PT[STX ? 1 : NW][STX ? 8 : CHUNK * LDP];
@@ -71,7 +71,7 @@ void k_fwd_state(FwdArgs a) {
     __syncthreads();
     if (STX)
       sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
-    sv.template store_t<T, SH::TPAD>(VT);
+    sv.store(XV);
     if (c + 1 < c1) {
       if (STX) sk.fetch(K, tok0 + CHUNK, a.N);
       sv.fetch(V, tok0 + CHUNK, a.N);
@@ -87,7 +87,7 @@ void k_fwd_state(FwdArgs a) {
         feature_frags_rows<T, D, FW, NS, StK::LD>(fs, XK, SCK, ks, pk);
         Frag<T> vf[SH::DVT];
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc) {
 #pragma unroll
@@ -111,7 +111,7 @@ void k_fwd_state(FwdArgs a) {
       for (int ks = 0; ks < SH::KT; ++ks) {
         Frag<T> vf[SH::DVT];
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc) {
           const Frag<T> pk = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16);
@@ -135,12 +135,15 @@ void k_fwd_state(FwdArgs a) {
 // Exclusive prefix over segments (causal) or total into segment 0 (non-causal).
 // state: [BH][P][E] fp32.  Fixed summation order.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_state_scan(float* state, int P, int sub, int E, int causal,
-                                                    int reverse) {
+__global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1, int P, int sub, int E,
+                                                    int causal, int reverse0) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= E) return;
   const int n = P * sub;
-  float* s = state + (size_t)blockIdx.y * n * E + e;
+  // blockIdx.z selects the state array: state0 in the direction reverse0,
+  // state1 (backward only) in the opposite one
+  const int reverse = blockIdx.z == 0 ? reverse0 : 1 - reverse0;
+  float* s = (blockIdx.z == 0 ? state0 : state1) + (size_t)blockIdx.y * n * E + e;
   constexpr int BATCH = 16;  // independent loads in flight per thread
   float acc = 0.f;
   for (int k0 = 0; k0 < n; k0 += BATCH) {
@@ -179,13 +182,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   typedef RowStage<IO, D, SH::NT> StX;
   typedef RowStage<IO, SH::DV, SH::NT> StV;
   constexpr bool STX = SH::STAGE_X;
-  constexpr int VT_N = CAUSAL ? SH::DV * SH::TPAD : 8;
+  constexpr int XV_N = CAUSAL ? StV::LDS_ELEMS : 8;
   constexpr int LDP = SH::FC * 16 + 4;     // [token][feature] rows of a wave's phi(K) block
   constexpr int PT_N = CAUSAL ? CHUNK * LDP : 8;
   __shared__ __attribute__((aligned(16))) IO XQ[STX ? StX::LDS_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) IO XK[(STX && CAUSAL) ? StX::LDS_ELEMS : 8];
   __shared__ float SSQ[CHUNK], SSK[CHUNK];
-  __shared__ __attribute__((aligned(16))) T VT[VT_N];
+  __shared__ __attribute__((aligned(16))) IO XV[XV_N];   // [token][value col]
   __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][SH::RPAD];
 
@@ -232,7 +235,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       sq.store(XQ, SSQ);
       if (CAUSAL) sk.store(XK, SSK);
     }
-    if (CAUSAL) sv.template store_t<T, SH::TPAD>(VT);
+    if (CAUSAL) sv.store(XV);
     if (c + 1 < c1) {
       if (STX) {
         sq.fetch(Q, tok0 + CHUNK, a.N);
@@ -307,7 +310,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
 #pragma unroll
       for (int dt = 0; dt < SH::DVT; ++dt)
 #pragma unroll
-        for (int ks = 0; ks < SH::KT; ++ks) vf[dt][ks] = lds_tok_frag<T>(VT + (dt * 16 + r) * SH::TPAD, ks);
+        for (int ks = 0; ks < SH::KT; ++ks) vf[dt][ks] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
     }
 
     // readout partials, reduced across waves in groups of QG query tiles
@@ -418,11 +421,11 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   constexpr int QG = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TT);
   const dim3 grid(a.segments * a.BH);
   const dim3 pgrid(a.segments * a.sub * a.BH);
-  k_prep_freqs<T, D, FW, NW, NS><<<a.H, SH::NT, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
+  k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
   timing_mark(KC_FWD_STATE, st, true);
   k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_STATE, st, false);
-  const hipError_t e = launch_state_scan(a.state, a.BH, a.segments, a.sub, SH::STATE, causal, false, st);
+  const hipError_t e = launch_state_scan(a.state, nullptr, a.BH, a.segments, a.sub, SH::STATE, causal, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_FWD_SWEEP, st, true);
   if (causal)
@@ -462,11 +465,11 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_state_scan(float* state, int BH, int P, int sub, int E, bool causal, bool reverse,
+hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
                              hipStream_t st) {
-  dim3 sgrid((E + 255) / 256, BH);
+  dim3 sgrid((E + 255) / 256, BH, state_rev ? 2 : 1);
   timing_mark(KC_SCAN, st, true);
-  k_state_scan<<<sgrid, 256, 0, st>>>(state, P, sub, E, causal ? 1 : 0, reverse ? 1 : 0);
+  k_state_scan<<<sgrid, 256, 0, st>>>(state, state_rev, P, sub, E, causal ? 1 : 0, 0);
   timing_mark(KC_SCAN, st, false);
   return hipGetLastError();
 }

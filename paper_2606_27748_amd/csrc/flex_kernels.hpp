@@ -76,9 +76,10 @@ bool bwd_split_differs(const KernelShape& ks);
 int fwd_state_waves(const KernelShape& ks);
 
 // state: [BH][P*sub][E]; writes the exclusive prefix (causal) into slot p*sub
-// of every segment p, the exclusive suffix (reverse) into slot p*sub+sub-1, or
-// the total (non-causal) into slot 0.
-hipError_t launch_state_scan(float* state, int BH, int P, int sub, int E, bool causal, bool reverse,
+// of every segment p, or the total (non-causal) into slot 0.  state_rev (or
+// NULL): [BH][P][E] (sub must be 1), scanned in the same launch in reverse:
+// the exclusive suffix (causal) into slot p, or the total into slot 0.
+hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
                              hipStream_t st);
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);
