@@ -621,9 +621,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
-    // phi(Q)/den: fragments (for the intra-chunk kernel matrix) and transposed copy
-    // (the non-causal backward of K and V uses only the total R')
-    Frag<T> phq[SH::FT][SH::TT];
+    // phi(Q)/den as [token][feature] in the wave's LDS block: read back as it is
+    // for the intra-chunk kernel matrix, transposed for the token sums (the
+    // non-causal backward of K and V uses only the total R')
     if (CAUSAL) {
 #pragma unroll
       for (int tt = 0; tt < SH::TT; ++tt) {
@@ -632,10 +632,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
         const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
 #pragma unroll
-        for (int ft = 0; ft < SH::FT; ++ft) {
-          phq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
-          store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16, phq[ft][tt]);
-        }
+        for (int ft = 0; ft < SH::FT; ++ft)
+          store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16,
+                           features<T, SH::FT, NS>(p, ft, sc));
       }
     }
     // phi(K) and its P2-derivative fragments
@@ -668,7 +667,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
               mma(m[tq], ao, bv);
             }
 #pragma unroll
-            for (int ft = 0; ft < SH::FT; ++ft) mma(at[tq], phq[ft][tq], phk[ft][tk]);
+            for (int ft = 0; ft < SH::FT; ++ft)
+              mma(at[tq], load_frag_nm<T>(PT[w], LDP, tq * 16, (2 * ft) * 16, (2 * ft + 1) * 16), phk[ft][tk]);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const bool keep = tq > tk || 4 * g + i >= r;

@@ -293,6 +293,25 @@ __device__ __forceinline__ void store_frag_nm(T* L, int ld, int n0, int m0a, int
   }
 }
 
+// Operand fragment stored by store_frag_nm, read back in the same layout:
+// lane row n0 + lane % 16, slots 0..3 from columns m0a + 4g .. + 3, slots
+// 4..7 from m0b + 4g .. + 3.
+template <class T>
+__device__ __forceinline__ Frag<T> load_frag_nm(const T* L, int ld, int n0, int m0a, int m0b) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const T* row = L + (n0 + r) * ld + 4 * g;
+  Frag<T> f;
+  if constexpr (IsBf16<T>::value) {
+    const uint2 a = *reinterpret_cast<const uint2*>(row + m0a);
+    const uint2 b = *reinterpret_cast<const uint2*>(row + m0b);
+    f.v = __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { f.set(i, row[m0a + i]); f.set(4 + i, row[m0b + i]); }
+  }
+  return f;
+}
+
 // Operand fragment with lane m = m0 + lane % 16 and k slots 0..3 = rows
 // kb0 .. kb0+3, slots 4..7 = rows kb1 .. kb1+3 of an [k][m]-major block
 // (kb0, kb1 may differ between lane groups).
