@@ -163,7 +163,7 @@ def main():
     def step():
         F.flex_linattn_fwd(desc, Q, K, V, W1, W2, tau, O=O, den=den, ws=ws_f)
         if wl.backward:
-            F.flex_linattn_bwd(desc, Q, K, V, W1, W2, tau, O, den, dO, ws=ws_b, **grads)
+            F.flex_linattn_bwd(desc, Q, K, V, W1, W2, tau, O, den, dO, ws=ws_b, fwd_ws=ws_f, **grads)
 
     for _ in range(args.warmup):
         step()

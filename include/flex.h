@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define FLEX_ABI_VERSION 1
+#define FLEX_ABI_VERSION 2
 
 typedef enum {
   FLEX_OK = 0,
@@ -123,12 +123,21 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K,
  *   dQ, dK [B,H,N,d], dV [B,H,N,dv]   grad_dtype outputs (overwritten)
  *   dW1 [H,m,d] fp32 output (overwritten); dW2 [H,m,d] fp32 output, required for
  *   the nonstationary variant and NULL for the stationary one
- *   dtau [H] fp32 output or NULL (overwritten when given) */
+ *   dtau [H] fp32 output or NULL (overwritten when given)
+ *   fwd_ws, fwd_ws_bytes  optional (NULL, 0): the workspace of the
+ *        flex_linattn_fwd call that produced O and den, with the same
+ *        descriptor and inputs, unchanged since that call.  It holds the
+ *        forward's key-side segment states sum_j phi(K_j) [V_j ; 1]^T; given
+ *        it, the backward reads them instead of recomputing them.  A workspace
+ *        that does not match the call gives wrong gradients (no check is
+ *        possible); one smaller than flex_workspace_size(desc, FLEX_PASS_FWD)
+ *        returns FLEX_ERR_WORKSPACE. */
 int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K,
                          const void* V, const float* W1, const float* W2,
                          const float* tau, const void* O, const float* den,
                          const void* dO, void* dQ, void* dK, void* dV,
                          float* dW1, float* dW2, float* dtau,
+                         const void* fwd_ws, size_t fwd_ws_bytes,
                          void* ws, size_t ws_bytes, void* stream);
 
 /* ---- Kernel timing (profiling aid) --------------------------------------

@@ -65,7 +65,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flex_linattn_fwd.restype = I
     lib.flex_linattn_fwd.argtypes = [D, P, P, P, P, P, P, P, P, P, S, P]
     lib.flex_linattn_bwd.restype = I
-    lib.flex_linattn_bwd.argtypes = [D] + [P] * 15 + [P, S, P]
+    lib.flex_linattn_bwd.argtypes = [D] + [P] * 15 + [P, S] + [P, S, P]
     lib.flex_timing_enable.restype = I
     lib.flex_timing_enable.argtypes = [I]
     lib.flex_timing_read.restype = I
@@ -145,8 +145,12 @@ def flex_linattn_fwd(desc: flex_desc, Q, K, V, W1, W2, tau, O=None, den=None, ws
 
 
 def flex_linattn_bwd(desc: flex_desc, Q, K, V, W1, W2, tau, O, den, dO, dQ=None, dK=None,
-                     dV=None, dW1=None, dW2=None, dtau=None, ws=None, want_dtau=True):
-    """Backward linear attention.  Returns dict of fp32 gradients."""
+                     dV=None, dW1=None, dW2=None, dtau=None, ws=None, want_dtau=True, fwd_ws=None):
+    """Backward linear attention.  Returns dict of fp32 gradients.
+
+    fwd_ws: optionally the workspace tensor of the matching flex_linattn_fwd
+    call (same descriptor and inputs, unchanged since): its segment states are
+    then reused instead of recomputed."""
     import torch
     dev = Q.device
     f32 = torch.float32
@@ -166,6 +170,7 @@ def flex_linattn_bwd(desc: flex_desc, Q, K, V, W1, W2, tau, O, den, dO, dQ=None,
     st = load().flex_linattn_bwd(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(V), _ptr(W1),
                                  _ptr(W2), _ptr(tau), _ptr(O), _ptr(den), _ptr(dO), _ptr(dQ),
                                  _ptr(dK), _ptr(dV), _ptr(dW1), _ptr(dW2), _ptr(dtau),
+                                 _ptr(fwd_ws), 0 if fwd_ws is None else fwd_ws.numel(),
                                  _ptr(ws), ws.numel(), _stream())
     _check(st, "flex_linattn_bwd")
     return dict(dQ=dQ, dK=dK, dV=dV, dW1=dW1, dW2=dW2, dtau=dtau)

@@ -268,7 +268,8 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
 int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, const void* V,
                          const float* W1, const float* W2, const float* tau, const void* O,
                          const float* den, const void* dO, void* dQ, void* dK, void* dV, float* dW1,
-                         float* dW2, float* dtau, void* ws, size_t ws_bytes, void* stream) {
+                         float* dW2, float* dtau, const void* fwd_ws, size_t fwd_ws_bytes, void* ws,
+                         size_t ws_bytes, void* stream) {
   const int32_t st = check_desc(desc);
   if (st != FLEX_OK) return st;
   if (!bwd_supported(desc)) return FLEX_ERR_UNSUPPORTED;
@@ -282,6 +283,8 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   if ((W2 && !aligned16(W2)) || (dW2 && !aligned16(dW2))) return FLEX_ERR_INVALID_ARG;
   const size_t need = ws_bytes_of(desc, FLEX_PASS_BWD);
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
+  if (fwd_ws && (fwd_ws_bytes < ws_bytes_of(desc, FLEX_PASS_FWD) || !aligned16(fwd_ws)))
+    return FLEX_ERR_WORKSPACE;
   const KernelShape ks = kshape(desc);
   BwdArgs a;
   memset(&a, 0, sizeof(a));
@@ -289,10 +292,17 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   a.dQ = static_cast<float*>(dQ); a.dK = static_cast<float*>(dK); a.dV = static_cast<float*>(dV);
   a.dW1 = dW1; a.dW2 = dW2; a.dtau = dtau;
   a.BH = desc->B * desc->H; a.B = desc->B; a.H = desc->H; a.N = desc->N;
-  // the backward sweeps use BWD_CHUNK-token chunks over the same segments
+  // the backward sweeps use BWD_CHUNK-token chunks over the forward's segments
   a.nchunks = (desc->N + BWD_CHUNK - 1) / BWD_CHUNK;
   a.segments = pick_segments(desc);
-  a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
+  {
+    const int fcps = (nchunks_of(desc) + a.segments - 1) / a.segments;   // forward chunks per segment
+    a.chunks_per_seg = fcps * (kChunk / BWD_CHUNK);
+  }
+  if (fwd_ws) {
+    a.fstate = static_cast<const float*>(fwd_ws);
+    a.fsub = fwd_sub_of(desc, a.segments);
+  }
   a.s_const = s_const_of(desc);
   const size_t bh = (size_t)a.BH, P = (size_t)a.segments;
   char* base = static_cast<char*>(ws);

@@ -97,6 +97,29 @@ __device__ __forceinline__ size_t state_off(int w, int dt, int fc, int l) {
   return ((size_t)(dt * NFT + w * SH::FC + fc) * WAVE + l) * 4;
 }
 
+// Tile (dt, fc) of this wave's [dv' x features] key-side state read from a
+// forward segment-state block.  The forward keeps [features x dv'] tiles
+// (feature tile F, value tile dt; rows = features, cols = value columns) in
+// register-dump order, with the normaliser in value column dv; the backward
+// tile is its transpose, with the normaliser in both rows dv and dv+1 (the
+// two rows that take the split of -delta).
+template <class SH>
+__device__ __forceinline__ f32x4 fwd_state_tile_t(const float* blk, int w, int dt, int fc) {
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const float* tile = blk + (size_t)((w * SH::FC + fc) * SH::DVT1 + dt) * WAVE * 4;
+  f32x4 v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int vl = 4 * g + i;                     // value column within tile dt
+    const bool norm = dt == SH::DVT;
+    const int col = norm ? 0 : vl;                // forward column of this value
+    // forward element (feature r, column col): lane col + 16 (r / 4), slot r % 4
+    const float x = tile[(col + 16 * (r / 4)) * 4 + (r % 4)];
+    v[i] = (!norm || vl < 2) ? x : 0.f;
+  }
+  return v;
+}
+
 // Chain rule through one wave's features for frequency tile ft, token tile tt:
 // dP (per radian) for the projection rows, and <phi, dphi> summed over this
 // lane's slots.
@@ -152,7 +175,9 @@ __device__ __forceinline__ void dump_dw(float* out, const float* dwl, int f0) {
 // Pre-pass: segment-local S'^T = sum [V;1]^T-rows x phi(K) and
 // R'^T = sum [dO;-delta]^T-rows x phi(Q)/den; per-token 1/den and delta.
 // ---------------------------------------------------------------------------
-template <class T, int D, int FW, int NW, bool NS>
+// WITH_S: also the key-side states S' (not needed when the forward's segment
+// states are passed in).
+template <class T, int D, int FW, int NW, bool NS, bool WITH_S>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
@@ -239,7 +264,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 #pragma unroll
     for (int ks = 0; ks < SH::KT; ++ks) {
       // value-side operands: rows = value columns, k = chunk tokens
-      {
+      if constexpr (WITH_S) {
         Frag<T> vt[SH::DVT1], pk[SH::FC];
 #pragma unroll
         for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
@@ -269,7 +294,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   for (int dt = 0; dt < SH::DVT1; ++dt)
 #pragma unroll
     for (int fc = 0; fc < SH::FC; ++fc) {
-      *reinterpret_cast<f32x4*>(so_ + state_off<SH>(w, dt, fc, l)) = ST[dt][fc];
+      if (WITH_S) *reinterpret_cast<f32x4*>(so_ + state_off<SH>(w, dt, fc, l)) = ST[dt][fc];
       *reinterpret_cast<f32x4*>(ro_ + state_off<SH>(w, dt, fc, l)) = RT[dt][fc];
     }
 }
@@ -326,7 +351,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   const float inv_c = __expf(-a.tau[h]);
 
   f32x4 ST[SH::DVT1][SH::FC];
-  {
+  if (a.fstate) {
+    const float* in = a.fstate + ((size_t)bh * a.segments * a.fsub + (CAUSAL ? seg * a.fsub : 0)) * SH::STATE;
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) ST[dt][fc] = fwd_state_tile_t<SH>(in, w, dt, fc);
+  } else {
     const float* in = a.sstate + ((size_t)bh * a.segments + (CAUSAL ? seg : 0)) * SH::STATE;
 #pragma unroll
     for (int dt = 0; dt < SH::DVT1; ++dt)
@@ -966,9 +997,13 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   if (a.wfrag_kv != a.wfrag)
     k_prep_freqs<T, D, FWB, NWB, NS><<<dim3(a.H, NWB, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag_kv, SB::M);
   timing_mark(KC_BWD_PREPASS, st, true);
-  k_bwd_prepass<T, D, FWA, NWA, NS><<<grid, SA::NT, 0, st>>>(a);
+  if (a.fstate)
+    k_bwd_prepass<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
+  else
+    k_bwd_prepass<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
   timing_mark(KC_BWD_PREPASS, st, false);
-  const hipError_t e = launch_state_scan(a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st);
+  const hipError_t e =
+      launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_BWD_DQ, st, true);
   if (causal)

@@ -467,9 +467,12 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
 
 hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
                              hipStream_t st) {
-  dim3 sgrid((E + 255) / 256, BH, state_rev ? 2 : 1);
+  dim3 sgrid((E + 255) / 256, BH, (state && state_rev) ? 2 : 1);
   timing_mark(KC_SCAN, st, true);
-  k_state_scan<<<sgrid, 256, 0, st>>>(state, state_rev, P, sub, E, causal ? 1 : 0, 0);
+  if (state)
+    k_state_scan<<<sgrid, 256, 0, st>>>(state, state_rev, P, sub, E, causal ? 1 : 0, 0);
+  else
+    k_state_scan<<<sgrid, 256, 0, st>>>(state_rev, nullptr, P, sub, E, causal ? 1 : 0, 1);
   timing_mark(KC_SCAN, st, false);
   return hipGetLastError();
 }

@@ -5,7 +5,9 @@
 
 namespace flex {
 
-// Chunk length (tokens) of the backward sweeps; the forward uses 64.
+// Chunk length (tokens) of the backward sweeps; the forward uses 64, and a
+// backward segment spans the same tokens as the forward segment (twice as many
+// chunks).
 constexpr int BWD_CHUNK = 32;
 
 struct KernelShape {
@@ -55,6 +57,8 @@ struct BwdArgs {
   float* dtaupart;    // [BH][segments] partial dtau
   void* wfrag;        // per-head frequency fragments (prepared by k_prep_freqs)
   void* wfrag_kv;     // fragments of the dK/dV sweep (== wfrag when its split is the same)
+  const float* fstate; // forward segment states after its scan ([BH][segments*fsub][state]) or NULL
+  int fsub;           // forward pre-pass workgroups per segment
   int BH, B, H, N;
   int nchunks, segments, chunks_per_seg;
   float s_const;
@@ -75,10 +79,11 @@ size_t wfrag_bytes(const KernelShape& ks, int H);
 bool bwd_split_differs(const KernelShape& ks);
 int fwd_state_waves(const KernelShape& ks);
 
-// state: [BH][P*sub][E]; writes the exclusive prefix (causal) into slot p*sub
-// of every segment p, or the total (non-causal) into slot 0.  state_rev (or
-// NULL): [BH][P][E] (sub must be 1), scanned in the same launch in reverse:
-// the exclusive suffix (causal) into slot p, or the total into slot 0.
+// state (or NULL): [BH][P*sub][E]; writes the exclusive prefix (causal) into
+// slot p*sub of every segment p, or the total (non-causal) into slot 0.
+// state_rev (or NULL): [BH][P][E] (sub must then be 1), scanned in the same
+// launch in reverse: the exclusive suffix (causal) into slot p, or the total
+// into slot 0.
 hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
                              hipStream_t st);
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);

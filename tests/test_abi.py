@@ -31,7 +31,7 @@ def test_exports_match_header():
     assert set(names) == set(F.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.flex_abi_version() == 1
+    assert lib.flex_abi_version() == 2
 
 
 def test_status_strings():
@@ -99,13 +99,16 @@ def test_entry_points_reject_bad_arguments():
     assert lib.flex_linattn_fwd(ctypes.byref(dn), P, P, P, P, P, P, P, P, P, 16, None) == 3
     # backward: den, dO and dW2 are required, dW2 must be NULL for stationary
     args = [P] * 15
+    nofwd = [None, 0]
     a = list(args); a[7] = None  # den
-    assert lib.flex_linattn_bwd(ctypes.byref(dn), *a, P, 16, None) == 1
+    assert lib.flex_linattn_bwd(ctypes.byref(dn), *a, *nofwd, P, 16, None) == 1
     a = list(args); a[13] = None  # dW2 missing for nonstationary
-    assert lib.flex_linattn_bwd(ctypes.byref(dn), *a, P, big, None) == 1
+    assert lib.flex_linattn_bwd(ctypes.byref(dn), *a, *nofwd, P, big, None) == 1
     a = list(args); a[4] = None  # W2 NULL, stationary, but dW2 given
-    assert lib.flex_linattn_bwd(ctypes.byref(ds), *a, P, big, None) == 1
-    assert lib.flex_linattn_bwd(ctypes.byref(dn), *args, P, 16, None) == F.FLEX_ERR_WORKSPACE
+    assert lib.flex_linattn_bwd(ctypes.byref(ds), *a, *nofwd, P, big, None) == 1
+    assert lib.flex_linattn_bwd(ctypes.byref(dn), *args, *nofwd, P, 16, None) == F.FLEX_ERR_WORKSPACE
+    # a forward workspace smaller than the forward needs
+    assert lib.flex_linattn_bwd(ctypes.byref(dn), *args, P, 16, P, big, None) == F.FLEX_ERR_WORKSPACE
     # feature map
     assert lib.flex_feature_map(ctypes.byref(dn), None, P, P, P, P, None, 0, None) == 1
     assert lib.flex_feature_map(ctypes.byref(ds), P, P, P, P, P, None, 0, None) == 1

@@ -36,11 +36,16 @@ def masked_inputs(wl, x):
     return keep
 
 
-def gpu_fwd_bwd(F, wl, x, segments=0):
+def gpu_fwd_bwd(F, wl, x, segments=0, reuse=False):
+    """Forward then backward through the C ABI; with reuse=True the backward
+    is given the forward's workspace (its segment states are reused)."""
+    import torch
     t = to_device(x)
     d = desc_of(wl, segments=segments)
-    O, den = F.flex_linattn_fwd(d, t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"])
-    g = F.flex_linattn_bwd(d, t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"], O, den, t["dO"])
+    ws_f = torch.empty(F.workspace_size(d, F.FLEX_PASS_FWD) + 256, dtype=torch.uint8, device=t["Q"].device)
+    O, den = F.flex_linattn_fwd(d, t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"], ws=ws_f)
+    g = F.flex_linattn_bwd(d, t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"], O, den, t["dO"],
+                           fwd_ws=ws_f if reuse else None)
     return {k: (None if v is None else to_f64(v)) for k, v in g.items()}
 
 
@@ -55,37 +60,57 @@ def names_of(wl):
     return ["dQ", "dK", "dV", "dW1", "dtau"] + (["dW2"] if wl.variant == "nonstationary" else [])
 
 
+@pytest.mark.parametrize("reuse", [False, True])
 @pytest.mark.parametrize("io,d,m", SHAPES)
 @pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
 @pytest.mark.parametrize("causal", [False, True])
-def test_backward_small(F, io, d, m, variant, causal):
+def test_backward_small(F, io, d, m, variant, causal, reuse):
     wl = W.Workload("small", 2, 2, 200, d, m, variant, causal, io, True, 21)
     x = W.generate(wl)
     masked_inputs(wl, x)
-    got = gpu_fwd_bwd(F, wl, x)
+    got = gpu_fwd_bwd(F, wl, x, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads(io, got, ref, names_of(wl), sc)
 
 
+@pytest.mark.parametrize("reuse", [False, True])
 @pytest.mark.parametrize("segments", [1, 2, 3])
 @pytest.mark.parametrize("causal", [False, True])
-def test_backward_segments(F, segments, causal):
+def test_backward_segments(F, segments, causal, reuse):
     wl = W.Workload("seg", 1, 2, 330, 64, 128, "nonstationary", causal, "bf16", True, 23)
     x = W.generate(wl)
     masked_inputs(wl, x)
-    got = gpu_fwd_bwd(F, wl, x, segments=segments)
+    got = gpu_fwd_bwd(F, wl, x, segments=segments, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads("bf16", got, ref, names_of(wl), sc)
 
 
-@pytest.mark.parametrize("N", [2, 64, 65])
-def test_backward_edge_lengths(F, N):
+@pytest.mark.parametrize("reuse", [False, True])
+@pytest.mark.parametrize("N", [2, 64, 65, 1050])
+def test_backward_edge_lengths(F, N, reuse):
+    """Ragged lengths; 1050 with 3 segments leaves forward and backward chunk
+    counts whose segment boundaries only agree when the backward follows the
+    forward's segments."""
     wl = W.Workload("edge", 1, 2, N, 64, 64, "nonstationary", True, "bf16", True, 25)
     x = W.generate(wl)
     masked_inputs(wl, x)
-    got = gpu_fwd_bwd(F, wl, x)
+    got = gpu_fwd_bwd(F, wl, x, segments=3 if N > 1000 else 0, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads("bf16", got, ref, names_of(wl), sc)
+
+
+def test_backward_reuse_matches_recompute(F):
+    """The backward with the forward's segment states and the backward that
+    recomputes them differ only in the rounding of those states."""
+    wl = W.Workload("reuse", 2, 2, 700, 64, 128, "nonstationary", True, "bf16", True, 31)
+    x = W.generate(wl)
+    masked_inputs(wl, x)
+    a = gpu_fwd_bwd(F, wl, x, reuse=False)
+    b = gpu_fwd_bwd(F, wl, x, reuse=True)
+    for k in ("dK", "dV"):
+        np.testing.assert_array_equal(a[k], b[k])   # key side: same R' path
+    for k in ("dQ", "dW1", "dW2"):
+        assert np.linalg.norm(a[k] - b[k]) <= 1e-3 * np.linalg.norm(a[k]), k
 
 
 @pytest.mark.parametrize("causal", [False, True])
@@ -155,7 +180,7 @@ def test_backward_full_size_sampled(F, name):
                                x.tau[h:h + 1], wl.variant, wl.causal)[0, 0]
         keep[b, h] = kap <= KAPPA_MAX[wl.io]
     x.dO = x.dO * keep[..., None].astype(x.dO.dtype)
-    got = gpu_fwd_bwd(F, wl, x)
+    got = gpu_fwd_bwd(F, wl, x, reuse=True)
     refs = [_slice_bwd_oracle(wl, x, b, h) for b in range(wl.B)]
     ref = {}
     for n in ("dQ", "dK", "dV"):
