@@ -311,15 +311,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   typedef WTSlice<T, D, FW, NS> WTS;
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;        // k-steps over [dO | -delta]
-  constexpr int QG = NW >= 8 ? 1 : 2;            // token tiles per reduction round
-  constexpr int RP = D + 4;
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
   constexpr int LDP = SH::FC * 16 + 4;          // row stride of the per-wave [token][row] blocks
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // dP, [token][projection row]
-  __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][RP];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
   __shared__ float SSQ[SH::CH];
@@ -495,49 +492,35 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         feature_grad<T, SH::FT, NS>(phq[ft][tt], psq[ft][tt], dph[2 * ft][tt], dph[2 * ft + 1][tt], dp[ft][tt], d2);
         if (NS) dp[SH::FT + ft][tt] = d2;
       }
-    // dQ = sum over waves of dP W'; reduced through LDS in rounds of QG token tiles
-    WTS wt;
-    wt.load_frags(wdx);
-#pragma unroll
-    for (int q0 = 0; q0 < SH::TT; q0 += QG) {
-      __syncthreads();
-#pragma unroll
-      for (int qq = 0; qq < QG; ++qq) {
-        const int tt = q0 + qq;
-        Frag<T> dpp[WTS::KP];
-#pragma unroll
-        for (int ks = 0; ks < WTS::KP; ++ks)
-          dpp[ks] = pair_tiles<T>(dp[2 * ks][tt], 2 * ks + 1 < SH::PR ? dp[2 * ks + 1][tt] : zero4());
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          f32x4 acc = zero4();
-#pragma unroll
-          for (int ks = 0; ks < WTS::KP; ++ks)
-#pragma unroll
-            for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wt.w[sp][dt][ks], dpp[ks]);
-          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = acc;
-        }
-      }
-      __syncthreads();
-      constexpr int C4 = D / 4;
-      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
-        const int t = it / C4, c4 = it % C4;
-        const int tok = tok0 + q0 * 16 + t;
-        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int ww = 0; ww < NW; ++ww) {
-          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
-          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-        }
-        if (tok < a.N) *reinterpret_cast<float4*>(dQ + (size_t)tok * D + 4 * c4) = s;
-      }
-    }
-    // PT[w] is this wave's own block: program order suffices between its uses
+    // dP of this wave as [token][projection row] in its LDS block
 #pragma unroll
     for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
       for (int tt = 0; tt < SH::TT; ++tt) store_tile_nm<T>(PT[w], LDP, tt * 16, pr * 16, dp[pr][tt]);
-    __syncthreads();
+    __syncthreads();   // every wave's dP block complete
+    // dQ = dP W' over all projection rows: each wave computes whole output
+    // tiles dQ^T (d tile, token tile) from every wave's dP block and that
+    // wave's dX fragments, so no cross-wave reduction is needed
+    for (int ot = w; ot < DT * SH::TT; ot += NW) {
+      const int dt = ot % DT, tt = ot / DT;
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) {
+        const Frag<T>* wd = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, ww);
+#pragma unroll
+        for (int ks = 0; ks < WTS::KP; ++ks) {
+          Frag<T> b = load_frag_nm<T>(PT[ww], LDP, tt * 16, (2 * ks) * 16, (2 * ks + 1) * 16);
+          if (2 * ks + 1 >= SH::PR) {   // no second row tile: keep unwritten LDS out of the product
+#pragma unroll
+            for (int j = 4; j < 8; ++j) b.set(j, 0.f);
+          }
+#pragma unroll
+          for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wd[((sp * DT + dt) * WTS::KP + ks) * WAVE + l], b);
+        }
+      }
+      const int tok = tok0 + tt * 16 + r;
+      if (tok < a.N) *reinterpret_cast<f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g) = acc;
+    }
     // frequency gradient partial: dW'[rows][d] += dP^T Q
     {
       f32x4 dw[SH::PR][DT];
