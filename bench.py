@@ -48,6 +48,8 @@ def kernel_work(wl, kernel):
     if kernel == "fwd_state":
         return T * 2 * d * bio, T * (proj + state)
     if kernel == "fwd_sweep":
+        if not wl.causal:   # reads Q, writes O and den; phi(Q) and the readout
+            return T * (2 * d * bio + 4), T * (proj + state)
         return T * (4 * d * bio + 4), T * (2 * proj + 2 * state)
     if kernel == "bwd_prepass":
         return T * (5 * d * bio + 4 + 8), T * (2 * proj + 2 * state)
@@ -102,12 +104,125 @@ def cpu_baseline(wl, slices, seed_offset=0):
                       f"float64 ({t1 - t0:.1f} s), scaled by {wl.B * wl.H}/{slices}"}
 
 
+def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
+    """Time `steps` steps of a workload (after `warmup`), events on the dominant
+    kernel class; returns the JSON record (None with profile_only)."""
+    import torch
+    import workloads as W
+    import paper_2606_27748_amd as F
+
+    dev = "cuda:0"
+    x = W.generate(wl, with_grad=True)
+
+    def dev_t(a):
+        import numpy as np
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    Q, K, V, dO = dev_t(x.Q), dev_t(x.K), dev_t(x.V), dev_t(x.dO)
+    W1, W2, tau = dev_t(x.W1), dev_t(x.W2), dev_t(x.tau)
+    desc = F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, wl.causal, wl.io)
+    O = torch.empty_like(V)
+    den = torch.empty(wl.B, wl.H, wl.N, dtype=torch.float32, device=dev)
+    f32 = torch.float32
+    backward = wl.backward
+    if backward:
+        try:
+            F.workspace_size(desc, F.FLEX_PASS_BWD)
+        except F.FlexError:
+            backward = False        # shape without a backward: forward only, said in the record
+    grads = dict(dQ=torch.empty(Q.shape, dtype=f32, device=dev), dK=torch.empty(K.shape, dtype=f32, device=dev),
+                 dV=torch.empty(V.shape, dtype=f32, device=dev),
+                 dW1=torch.empty(W1.shape, dtype=f32, device=dev),
+                 dW2=None if W2 is None else torch.empty(W2.shape, dtype=f32, device=dev),
+                 dtau=torch.empty(tau.shape, dtype=f32, device=dev))
+    ws_f = torch.empty(F.workspace_size(desc, F.FLEX_PASS_FWD) + 256, dtype=torch.uint8, device=dev)
+    ws_b = (torch.empty(F.workspace_size(desc, F.FLEX_PASS_BWD) + 256, dtype=torch.uint8, device=dev)
+            if backward else None)
+
+    def step():
+        F.flex_linattn_fwd(desc, Q, K, V, W1, W2, tau, O=O, den=den, ws=ws_f)
+        if backward:
+            F.flex_linattn_bwd(desc, Q, K, V, W1, W2, tau, O, den, dO, ws=ws_b, fwd_ws=ws_f, **grads)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if profile_only:
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        return None
+
+    # which kernel class dominates (outside the timed region)
+    classes = ["fwd_state", "fwd_sweep", "scan"] + (
+        ["bwd_prepass", "bwd_dq", "bwd_dkv", "bwd_reduce"] if backward else [])
+    share = {}
+    for k in classes:
+        F.flex_timing_enable(k)
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        ms, n = F.flex_timing_read()
+        share[k] = ms / 3
+    dominant = max(share, key=share.get)
+
+    # timed region: exactly K steps, synchronized on both sides, events on the dominant kernel
+    F.flex_timing_enable(dominant)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    k_ms, k_n = F.flex_timing_read()
+    F.flex_timing_enable("none")
+    ms_step = (t1 - t0) * 1e3 / steps
+    tokens = wl.B * wl.N
+    value = tokens / (ms_step * 1e-3)
+
+    avg_s = (k_ms / max(k_n, 1)) * 1e-3
+    kwl = wl if backward == wl.backward else wl.scaled(backward=False)
+    kbytes, kflops = kernel_work(kwl, dominant)
+    ridge = (PEAK_BF16_TFLOPS * 1e12) / (PEAK_HBM_GBS * 1e9)
+    if kbytes and kflops / kbytes >= ridge:
+        roof = {"bound": "mfma", "achieved": kflops / avg_s / 1e12,
+                "peak": PEAK_BF16_TFLOPS if wl.io == "bf16" else PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": kbytes / avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_from_profiles(wl, dominant)
+    roof["kernel"] = dominant
+    roof["kernel_ms"] = avg_s * 1e3
+    roof["kernel_share"] = {k: round(v / sum(share.values()), 4) for k, v in share.items()}
+
+    out = {"metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+           "warmup": warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if wl.io == "bf16" else "f32", "data": "synthetic",
+           "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d, "m": wl.m,
+                      "variant": wl.variant, "causal": wl.causal,
+                      "pass": "fwd+bwd" if backward else "fwd", "parallelism": "single-gpu"},
+           "roofline": roof}
+    if wl.backward and not backward:
+        out["config"]["note"] = "backward not built for this shape; forward only"
+    if want_cpu:
+        out["cpu_baseline"] = cpu_baseline(wl, min(cpu_slices, wl.B * wl.H))
+    else:
+        out["cpu_baseline"] = None
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="headline_causal_train_d64")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="one JSON line per configured workload (no CPU baseline)")
     ap.add_argument("--cpu-slices", type=int, default=32)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--profile-only", action="store_true",
@@ -129,104 +244,15 @@ def main():
               "(the path has no multi-GPU sharding; see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
 
-    import torch
     import workloads as W
-    import paper_2606_27748_amd as F
-
-    wl = W.WORKLOADS[args.workload]
-    dev = "cuda:0"
-    x = W.generate(wl, with_grad=True)
-    dt = torch.bfloat16 if wl.io == "bf16" else torch.float32
-
-    def dev_t(a):
-        import numpy as np
-        if a is None:
-            return None
-        if a.dtype == np.uint16:
-            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
-        return torch.from_numpy(a).to(dev)
-
-    Q, K, V, dO = dev_t(x.Q), dev_t(x.K), dev_t(x.V), dev_t(x.dO)
-    W1, W2, tau = dev_t(x.W1), dev_t(x.W2), dev_t(x.tau)
-    desc = F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, wl.causal, wl.io)
-    O = torch.empty_like(V)
-    den = torch.empty(wl.B, wl.H, wl.N, dtype=torch.float32, device=dev)
-    f32 = torch.float32
-    grads = dict(dQ=torch.empty(Q.shape, dtype=f32, device=dev), dK=torch.empty(K.shape, dtype=f32, device=dev),
-                 dV=torch.empty(V.shape, dtype=f32, device=dev),
-                 dW1=torch.empty(W1.shape, dtype=f32, device=dev),
-                 dW2=None if W2 is None else torch.empty(W2.shape, dtype=f32, device=dev),
-                 dtau=torch.empty(tau.shape, dtype=f32, device=dev))
-    ws_f = torch.empty(F.workspace_size(desc, F.FLEX_PASS_FWD) + 256, dtype=torch.uint8, device=dev)
-    ws_b = torch.empty(F.workspace_size(desc, F.FLEX_PASS_BWD) + 256, dtype=torch.uint8, device=dev)
-
-    def step():
-        F.flex_linattn_fwd(desc, Q, K, V, W1, W2, tau, O=O, den=den, ws=ws_f)
-        if wl.backward:
-            F.flex_linattn_bwd(desc, Q, K, V, W1, W2, tau, O, den, dO, ws=ws_b, fwd_ws=ws_f, **grads)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    if args.profile_only:
-        for _ in range(args.steps):
-            step()
-        torch.cuda.synchronize()
+    if args.all_configs:
+        for name, wl in W.WORKLOADS.items():
+            print(json.dumps(measure(wl, args.steps, args.warmup, False, 0)), flush=True)
         return
-
-    # which kernel class dominates (outside the timed region)
-    classes = ["fwd_state", "fwd_sweep", "scan"] + (
-        ["bwd_prepass", "bwd_dq", "bwd_dkv", "bwd_reduce"] if wl.backward else [])
-    share = {}
-    for k in classes:
-        F.flex_timing_enable(k)
-        for _ in range(3):
-            step()
-        torch.cuda.synchronize()
-        ms, n = F.flex_timing_read()
-        share[k] = ms / 3
-    dominant = max(share, key=share.get)
-
-    # timed region: exactly K steps, synchronized on both sides, events on the dominant kernel
-    F.flex_timing_enable(dominant)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    k_ms, k_n = F.flex_timing_read()
-    F.flex_timing_enable("none")
-    ms_step = (t1 - t0) * 1e3 / args.steps
-    tokens = wl.B * wl.N
-    value = tokens / (ms_step * 1e-3)
-
-    avg_s = (k_ms / max(k_n, 1)) * 1e-3
-    kbytes, kflops = kernel_work(wl, dominant)
-    ridge = (PEAK_BF16_TFLOPS * 1e12) / (PEAK_HBM_GBS * 1e9)
-    if kbytes and kflops / kbytes >= ridge:
-        roof = {"bound": "mfma", "achieved": kflops / avg_s / 1e12,
-                "peak": PEAK_BF16_TFLOPS if wl.io == "bf16" else PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": kbytes / avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = traffic_from_profiles(wl, dominant)
-    roof["kernel"] = dominant
-    roof["kernel_ms"] = avg_s * 1e3
-    roof["kernel_share"] = {k: round(v / sum(share.values()), 4) for k, v in share.items()}
-
-    out = {"metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
-           "vs_baseline": None, "dtype": "bf16" if wl.io == "bf16" else "f32", "data": "synthetic",
-           "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d, "m": wl.m,
-                      "variant": wl.variant, "causal": wl.causal,
-                      "pass": "fwd+bwd" if wl.backward else "fwd", "parallelism": "single-gpu"},
-           "roofline": roof}
-    if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_slices, wl.B * wl.H))
-    else:
-        out["cpu_baseline"] = None
-    print(json.dumps(out), flush=True)
+    wl = W.WORKLOADS[args.workload]
+    out = measure(wl, args.steps, args.warmup, not args.no_cpu, args.cpu_slices, args.profile_only)
+    if out is not None:
+        print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

@@ -61,6 +61,9 @@ KernelShape kshape(const flex_desc* d) {
 
 int nchunks_of(const flex_desc* d) { return (d->N + kChunk - 1) / kChunk; }
 
+// Chunks per workgroup of the non-causal sweep (its chunks are independent).
+constexpr int kSweepChunks = 8;
+
 // Forward state pre-pass workgroups per segment: two (each half a segment)
 // for 4-wave workgroups when that still leaves fewer than two workgroups per
 // CU, so that two of them share a CU (8-wave workgroups already give each SIMD
@@ -213,6 +216,7 @@ int32_t flex_workspace_size(const flex_desc* desc, int32_t pass, size_t* bytes) 
   if (pass < FLEX_PASS_FEATURE_MAP || pass > FLEX_PASS_BWD) return FLEX_ERR_INVALID_ARG;
   const int32_t st = check_desc(desc);
   if (st != FLEX_OK) return st;
+  if (pass == FLEX_PASS_BWD && !bwd_supported(desc)) return FLEX_ERR_UNSUPPORTED;
   *bytes = ws_bytes_of(desc, pass);
   return FLEX_OK;
 }
@@ -231,6 +235,7 @@ int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1, 
   a.Q = X; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = Phi;
   a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
   a.nchunks = nchunks_of(desc); a.segments = 1; a.chunks_per_seg = a.nchunks; a.sub = 1;
+  a.sweep_groups = 1; a.sweep_cps = a.nchunks;
   a.s_const = s_const_of(desc);
   const hipError_t e = launch_fwd(a, kshape(desc), true, (hipStream_t)stream);
   return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
@@ -260,6 +265,13 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
   a.segments = P0;
   a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
   a.sub = fwd_sub_of(desc, P0);
+  if (desc->causal) {
+    a.sweep_groups = a.segments;
+    a.sweep_cps = a.chunks_per_seg;
+  } else {
+    a.sweep_cps = a.nchunks < kSweepChunks ? a.nchunks : kSweepChunks;
+    a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
+  }
   a.s_const = s_const_of(desc);
   const hipError_t e = launch_fwd(a, kshape(desc), false, (hipStream_t)stream);
   return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;

@@ -192,11 +192,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][SH::RPAD];
 
-  const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
+  // causal: one workgroup per segment; non-causal: per group of chunks (every
+  // chunk reads the same total state)
+  const WgCoord wc = wg_coord(a.sweep_groups, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const int c0 = seg * a.chunks_per_seg;
-  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const int c0 = seg * a.sweep_cps;
+  const int c1 = min(c0 + a.sweep_cps, a.nchunks);
   const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
   const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
   const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
@@ -418,8 +420,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
 template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
+  // token tiles per cross-wave reduction round: fewer rounds where LDS allows;
+  // one for the non-causal sweep, which then fits several workgroups per CU
   constexpr int QG = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TT);
-  const dim3 grid(a.segments * a.BH);
+  const dim3 grid(a.sweep_groups * a.BH);
   const dim3 pgrid(a.segments * a.sub * a.BH);
   k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
   timing_mark(KC_FWD_STATE, st, true);
@@ -431,7 +435,7 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   if (causal)
     k_fwd_sweep<T, D, FW, NW, NS, true, QG><<<grid, SH::NT, 0, st>>>(a);
   else
-    k_fwd_sweep<T, D, FW, NW, NS, false, QG><<<grid, SH::NT, 0, st>>>(a);
+    k_fwd_sweep<T, D, FW, NW, NS, false, 1><<<grid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_SWEEP, st, false);
   return hipGetLastError();
 }

@@ -31,6 +31,8 @@ struct FwdArgs {
   int BH, H, N;
   int nchunks, segments, chunks_per_seg;
   int sub;            // state pre-pass workgroups per segment (chunks_per_seg % sub == 0)
+  int sweep_groups;   // sweep workgroups per (b,h): the segments (causal) or chunk groups (non-causal)
+  int sweep_cps;      // chunks per sweep workgroup
   float s_const;      // sigma/sqrt(m) or sigma/(2 sqrt(m))
 };
 
