@@ -29,7 +29,7 @@ bool shape_supported(const flex_desc* d) {
 }
 
 // The backward additionally needs the (d, m) shapes its kernels are built for.
-bool bwd_supported(const flex_desc* d) { return !(d->d == 128 && d->m == 256); }
+bool bwd_supported(const flex_desc*) { return true; }
 
 // 0 = ok, else a flex_status
 int32_t check_desc(const flex_desc* d) {
@@ -59,6 +59,26 @@ KernelShape kshape(const flex_desc* d) {
   return k;
 }
 
+// Frequency groups of the attention kernels: the (d = 128, m = 256) shape runs
+// as four groups of 64 frequencies (per-workgroup state and frequency-gradient
+// partials of one group fit registers and LDS); the groups' contributions to
+// the numerator, denominator and the Q/K/V/tau gradients are summed in launch
+// order, the frequency gradients of a group are its own rows.
+struct Groups {
+  int n, m;
+};
+Groups groups_of(const flex_desc* d) {
+  if (d->d == 128 && d->m == 256) return Groups{4, 64};
+  return Groups{1, d->m};
+}
+
+// Kernel shape of the attention passes (one frequency group).
+KernelShape attn_shape(const flex_desc* d) {
+  KernelShape k = kshape(d);
+  k.m = groups_of(d).m;
+  return k;
+}
+
 int nchunks_of(const flex_desc* d) { return (d->N + kChunk - 1) / kChunk; }
 
 // Chunks per workgroup of the non-causal sweep (its chunks are independent).
@@ -72,7 +92,7 @@ int fwd_sub_of(const flex_desc* d, int P) {
   const int nc = nchunks_of(d);
   const int cps = (nc + P - 1) / P;
   const long long wgs = (long long)d->B * d->H * P;
-  return (fwd_state_waves(kshape(d)) == 4 && cps % 2 == 0 && wgs < 2LL * kCUs) ? 2 : 1;
+  return (fwd_state_waves(attn_shape(d)) == 4 && cps % 2 == 0 && wgs < 2LL * kCUs) ? 2 : 1;
 }
 
 // Segments per (b,h): enough workgroups to cover the 256 CUs in whole rounds
@@ -104,14 +124,27 @@ float s_const_of(const flex_desc* d) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Forward workspace: the segment states of every frequency group, one block of
+// prepared fragments (reused group after group) and, with several groups, the
+// fp32 numerator / denominator sums.
+size_t fwd_group_state_bytes(const flex_desc* d) {
+  const size_t P = (size_t)pick_segments(d);
+  return align256((size_t)d->B * d->H * P * fwd_sub_of(d, (int)P) * fwd_state_floats(attn_shape(d)) *
+                  sizeof(float));
+}
+size_t fwd_acc_bytes(const flex_desc* d) {
+  if (groups_of(d).n == 1) return 0;
+  const size_t rows = (size_t)d->B * d->H * d->N;
+  return align256(rows * d->dv * sizeof(float)) + align256(rows * sizeof(float));
+}
+
 size_t ws_bytes_of(const flex_desc* d, int pass) {
-  const KernelShape ks = kshape(d);
+  const KernelShape ks = attn_shape(d);
   const size_t bh = (size_t)d->B * d->H;
   const size_t P = (size_t)pick_segments(d);
   if (pass == FLEX_PASS_FEATURE_MAP) return 0;
   const size_t wf = align256(wfrag_bytes(ks, d->H));
-  if (pass == FLEX_PASS_FWD)
-    return align256(bh * P * fwd_sub_of(d, (int)P) * fwd_state_floats(ks) * sizeof(float)) + wf;
+  if (pass == FLEX_PASS_FWD) return groups_of(d).n * fwd_group_state_bytes(d) + wf + fwd_acc_bytes(d);
   // backward: key-side and query-side states, per-token scalars, frequency-gradient
   // and dtau partials
   return 2 * align256(bh * P * bwd_state_floats(ks) * sizeof(float)) +
@@ -255,11 +288,18 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
   FwdArgs a;
   memset(&a, 0, sizeof(a));
-  a.Q = Q; a.K = K; a.V = V; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = O; a.den = den;
-  a.state = static_cast<float*>(ws);
+  a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den;
+  const Groups G = groups_of(desc);
+  const KernelShape ks = attn_shape(desc);
+  const size_t sb = fwd_group_state_bytes(desc);
+  char* base = static_cast<char*>(ws);
+  a.wfrag = base + G.n * sb;
+  if (G.n > 1) {
+    char* acc = base + G.n * sb + align256(wfrag_bytes(ks, desc->H));
+    a.acc_num = reinterpret_cast<float*>(acc);
+    a.acc_den = reinterpret_cast<float*>(acc + align256((size_t)desc->B * desc->H * desc->N * desc->dv * sizeof(float)));
+  }
   const int P0 = pick_segments(desc);
-  a.wfrag = static_cast<char*>(ws) + align256((size_t)desc->B * desc->H * P0 * fwd_sub_of(desc, P0) *
-                                              fwd_state_floats(kshape(desc)) * sizeof(float));
   a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
   a.nchunks = nchunks_of(desc);
   a.segments = P0;
@@ -273,8 +313,19 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
     a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
   }
   a.s_const = s_const_of(desc);
-  const hipError_t e = launch_fwd(a, kshape(desc), false, (hipStream_t)stream);
-  return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
+  a.w_stride = desc->m * desc->d;
+  for (int g = 0; g < G.n; ++g) {
+    const size_t woff = (size_t)g * G.m * desc->d;   // this group's frequency rows
+    a.W1 = W1 + woff;
+    a.W2 = W2 ? W2 + woff : nullptr;
+    a.state = reinterpret_cast<float*>(base + g * sb);
+    a.acc = G.n == 1 ? 0 : (g == 0 ? 1 : 2);
+    const hipError_t e = launch_fwd(a, ks, false, (hipStream_t)stream);
+    if (e != hipSuccess) return FLEX_ERR_HIP;
+  }
+  if (G.n > 1 && launch_fwd_finish(a, ks.bf16, desc->dv, (hipStream_t)stream) != hipSuccess)
+    return FLEX_ERR_HIP;
+  return FLEX_OK;
 }
 
 int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, const void* V,
@@ -297,12 +348,13 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
   if (fwd_ws && (fwd_ws_bytes < ws_bytes_of(desc, FLEX_PASS_FWD) || !aligned16(fwd_ws)))
     return FLEX_ERR_WORKSPACE;
-  const KernelShape ks = kshape(desc);
+  const KernelShape ks = attn_shape(desc);
+  const Groups G = groups_of(desc);
   BwdArgs a;
   memset(&a, 0, sizeof(a));
-  a.Q = Q; a.K = K; a.V = V; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = O; a.den = den; a.dO = dO;
+  a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den; a.dO = dO;
   a.dQ = static_cast<float*>(dQ); a.dK = static_cast<float*>(dK); a.dV = static_cast<float*>(dV);
-  a.dW1 = dW1; a.dW2 = dW2; a.dtau = dtau;
+  a.dtau = dtau;
   a.BH = desc->B * desc->H; a.B = desc->B; a.H = desc->H; a.N = desc->N;
   // the backward sweeps use BWD_CHUNK-token chunks over the forward's segments
   a.nchunks = (desc->N + BWD_CHUNK - 1) / BWD_CHUNK;
@@ -311,10 +363,7 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
     const int fcps = (nchunks_of(desc) + a.segments - 1) / a.segments;   // forward chunks per segment
     a.chunks_per_seg = fcps * (kChunk / BWD_CHUNK);
   }
-  if (fwd_ws) {
-    a.fstate = static_cast<const float*>(fwd_ws);
-    a.fsub = fwd_sub_of(desc, a.segments);
-  }
+  if (fwd_ws) a.fsub = fwd_sub_of(desc, a.segments);
   a.s_const = s_const_of(desc);
   const size_t bh = (size_t)a.BH, P = (size_t)a.segments;
   char* base = static_cast<char*>(ws);
@@ -327,8 +376,20 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
   a.wfrag = base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
   a.wfrag_kv = bwd_split_differs(ks) ? static_cast<char*>(a.wfrag) + align256(wfrag_bytes(ks, desc->H)) : a.wfrag;
-  const hipError_t e = launch_bwd(a, ks, (hipStream_t)stream);
-  return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
+  a.w_stride = desc->m * desc->d;
+  for (int g = 0; g < G.n; ++g) {
+    const size_t woff = (size_t)g * G.m * desc->d;   // this group's frequency rows
+    a.W1 = W1 + woff;
+    a.W2 = W2 ? W2 + woff : nullptr;
+    a.dW1 = dW1 + woff;
+    a.dW2 = dW2 ? dW2 + woff : nullptr;
+    a.acc = g > 0;
+    if (fwd_ws)
+      a.fstate = reinterpret_cast<const float*>(static_cast<const char*>(fwd_ws) + g * fwd_group_state_bytes(desc));
+    const hipError_t e = launch_bwd(a, ks, (hipStream_t)stream);
+    if (e != hipSuccess) return FLEX_ERR_HIP;
+  }
+  return FLEX_OK;
 }
 
 }  // extern "C"

@@ -519,7 +519,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         }
       }
       const int tok = tok0 + tt * 16 + r;
-      if (tok < a.N) *reinterpret_cast<f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g) = acc;
+      if (tok < a.N) {
+        f32x4* o = reinterpret_cast<f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g);
+        *o = a.acc ? *o + acc : acc;   // later frequency groups add their share
+      }
     }
     // frequency gradient partial: dW'[rows][d] += dP^T Q
     {
@@ -560,7 +563,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   typedef WTSlice<T, D, FW, NS> WTS;
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;
-  constexpr int QG = NW >= 8 ? 1 : 2;
+  constexpr int QG = (NW >= 8 || D >= 128) ? 1 : 2;
   constexpr int RP = (D > SH::DV ? D : SH::DV) + 4;
   constexpr int RLP = SH::DV + 4;                // row stride of the bf16 R' copy, [feature][value col]
   constexpr int LDP = SH::FC * 16 + 4;           // row stride of the per-wave [token][row] blocks
@@ -744,7 +747,14 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
           const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
           s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
         }
-        if (tok < a.N) *reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4) = s;
+        if (tok < a.N) {
+          float4* o = reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4);
+          if (a.acc) {
+            const float4 p = *o;
+            s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
+          }
+          *o = s;
+        }
       }
     }
     // dphi(K)^T[feature][key] = phi(Q)^T M + R'^T-rows x [V | 1]
@@ -855,7 +865,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
           s.y += k2 * io_to_float(kr[1]);
           s.z += k2 * io_to_float(kr[2]);
           s.w += k2 * io_to_float(kr[3]);
-          *reinterpret_cast<float4*>(dK + (size_t)tok * D + 4 * c4) = s;
+          float4* o = reinterpret_cast<float4*>(dK + (size_t)tok * D + 4 * c4);
+          if (a.acc) {
+            const float4 p = *o;
+            s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
+          }
+          *o = s;
           if (c4 == 0) dtau_acc -= gg * SSK[tl] * inv_c;
         }
       }
@@ -949,17 +964,17 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int m, int d, int
     const float x0 = (part[0][0][t] + part[0][1][t]) + (part[0][2][t] + part[0][3][t]);
     const float x1 = (part[1][0][t] + part[1][1][t]) + (part[1][2][t] + part[1][3][t]);
     if (nmat == 2) {
-      a.dW1[(size_t)h * md + e] = 0.5f * (x0 + x1);
-      a.dW2[(size_t)h * md + e] = 0.5f * (x0 - x1);
+      a.dW1[(size_t)h * a.w_stride + e] = 0.5f * (x0 + x1);
+      a.dW2[(size_t)h * a.w_stride + e] = 0.5f * (x0 - x1);
     } else {
-      a.dW1[(size_t)h * md + e] = x0;
+      a.dW1[(size_t)h * a.w_stride + e] = x0;
     }
   }
   if (a.dtau && blockIdx.x == 0 && threadIdx.x == 0) {
     float s = 0.f;
     for (int b = 0; b < a.B; ++b)
       for (int p = 0; p < a.segments; ++p) s += a.dtaupart[((size_t)b * a.H + h) * a.segments + p];
-    a.dtau[h] = s;
+    a.dtau[h] = a.acc ? a.dtau[h] + s : s;
   }
 }
 
@@ -976,9 +991,9 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FWB, NWB, NS, BWD_CHUNK> SB;
   static_assert(SA::M == SB::M && SA::STATE == SB::STATE, "splits of one shape");
   const dim3 grid(a.segments * a.BH);
-  k_prep_freqs<T, D, FWA, NWA, NS><<<dim3(a.H, NWA, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, SA::M);
+  k_prep_freqs<T, D, FWA, NWA, NS><<<dim3(a.H, NWA, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
   if (a.wfrag_kv != a.wfrag)
-    k_prep_freqs<T, D, FWB, NWB, NS><<<dim3(a.H, NWB, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag_kv, SB::M);
+    k_prep_freqs<T, D, FWB, NWB, NS><<<dim3(a.H, NWB, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag_kv, a.w_stride);
   timing_mark(KC_BWD_PREPASS, st, true);
   if (a.fstate)
     k_bwd_prepass<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
@@ -1018,6 +1033,7 @@ hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st) {
     if (ks.d == 32 && ks.m == 64) return run_bwd_v<__bf16, 32, 16, 4, 16, 4>(a, ks.nonstationary, ks.causal, st);
     if (ks.d == 64 && ks.m == 64) return run_bwd_v<__bf16, 64, 16, 4, 16, 4>(a, ks.nonstationary, ks.causal, st);
     if (ks.d == 64 && ks.m == 128) return run_bwd_v<__bf16, 64, 16, 8, 32, 4>(a, ks.nonstationary, ks.causal, st);
+    if (ks.d == 128 && ks.m == 64) return run_bwd_v<__bf16, 128, 16, 4, 16, 4>(a, ks.nonstationary, ks.causal, st);
   } else {
     if (ks.d == 32 && ks.m == 64) return run_bwd_v<float, 32, 16, 4, 16, 4>(a, ks.nonstationary, ks.causal, st);
   }

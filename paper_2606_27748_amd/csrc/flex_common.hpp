@@ -317,11 +317,11 @@ struct FragBlock {
 // fragments, part 1 (launched for the backward only) the dX fragments.
 // Grid (H, NW, parts), 64 threads.
 template <class T, int D, int FW, int NW, bool NS>
-__global__ __launch_bounds__(WAVE) void k_prep_freqs(const float* W1, const float* W2, void* out, int M) {
+__global__ __launch_bounds__(WAVE) void k_prep_freqs(const float* W1, const float* W2, void* out, int wstride) {
   typedef FragBlock<T, D, FW, NS> FBk;
   const int h = blockIdx.x, w = blockIdx.y;
-  const float* W1h = W1 + (size_t)h * M * D;
-  const float* W2h = NS ? W2 + (size_t)h * M * D : nullptr;
+  const float* W1h = W1 + (size_t)h * wstride;
+  const float* W2h = NS ? W2 + (size_t)h * wstride : nullptr;
   Frag<T>* base = static_cast<Frag<T>*>(out) + ((size_t)h * NW + w) * FBk::PER_WAVE;
   if (blockIdx.z == 0) {
     FreqSlice<T, D, FW, NS> fs;

@@ -361,14 +361,27 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
           dn += RED[ww][t][SH::DV];
         }
         if (tok < a.N) {
-          // one reciprocal per row (v_rcp_f32, 1 ulp); den = 0 gives inf/NaN as num/0 does
-          const float inv = __builtin_amdgcn_rcpf(dn);
-          IO* o = O + (size_t)tok * SH::DV + 4 * c4;
-          o[0] = float_to_io<IO>(num.x * inv);
-          o[1] = float_to_io<IO>(num.y * inv);
-          o[2] = float_to_io<IO>(num.z * inv);
-          o[3] = float_to_io<IO>(num.w * inv);
-          if (den && c4 == 0) den[tok] = dn;
+          if (a.acc) {
+            // one frequency group's share of the numerator and denominator
+            float4* an = reinterpret_cast<float4*>(a.acc_num + ((size_t)bh * a.N + tok) * SH::DV + 4 * c4);
+            float* ad = a.acc_den + (size_t)bh * a.N + tok;
+            if (a.acc == 2) {
+              const float4 p = *an;
+              num.x += p.x; num.y += p.y; num.z += p.z; num.w += p.w;
+              if (c4 == 0) dn += *ad;
+            }
+            *an = num;
+            if (c4 == 0) *ad = dn;
+          } else {
+            // one reciprocal per row (v_rcp_f32, 1 ulp); den = 0 gives inf/NaN as num/0 does
+            const float inv = __builtin_amdgcn_rcpf(dn);
+            IO* o = O + (size_t)tok * SH::DV + 4 * c4;
+            o[0] = float_to_io<IO>(num.x * inv);
+            o[1] = float_to_io<IO>(num.y * inv);
+            o[2] = float_to_io<IO>(num.z * inv);
+            o[3] = float_to_io<IO>(num.w * inv);
+            if (den && c4 == 0) den[tok] = dn;
+          }
         }
       }
     }
@@ -415,6 +428,39 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// After the last frequency group: O = num / den from the fp32 sums, den out.
+// One thread per 4 value columns of one row.
+// ---------------------------------------------------------------------------
+template <class IO>
+__global__ __launch_bounds__(256) void k_fwd_finish(FwdArgs a, int dv) {
+  const size_t rows = (size_t)a.BH * a.N;
+  const int c4n = dv / 4;
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * c4n) return;
+  const size_t row = i / c4n;
+  const int c4 = (int)(i % c4n);
+  const float4 num = *reinterpret_cast<const float4*>(a.acc_num + row * dv + 4 * c4);
+  const float dn = a.acc_den[row];
+  const float inv = __builtin_amdgcn_rcpf(dn);
+  IO* o = static_cast<IO*>(a.O) + row * dv + 4 * c4;
+  o[0] = float_to_io<IO>(num.x * inv);
+  o[1] = float_to_io<IO>(num.y * inv);
+  o[2] = float_to_io<IO>(num.z * inv);
+  o[3] = float_to_io<IO>(num.w * inv);
+  if (a.den && c4 == 0) a.den[row] = dn;
+}
+
+hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st) {
+  const size_t n = (size_t)a.BH * a.N * (dv / 4);
+  const dim3 grid((unsigned)((n + 255) / 256));
+  if (bf16)
+    k_fwd_finish<u16><<<grid, 256, 0, st>>>(a, dv);
+  else
+    k_fwd_finish<float><<<grid, 256, 0, st>>>(a, dv);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Host-side dispatch.
 // ---------------------------------------------------------------------------
 template <class T, int D, int FW, int NW, bool NS>
@@ -425,7 +471,7 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   constexpr int QG = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TT);
   const dim3 grid(a.sweep_groups * a.BH);
   const dim3 pgrid(a.segments * a.sub * a.BH);
-  k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, SH::M);
+  k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
   timing_mark(KC_FWD_STATE, st, true);
   k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_STATE, st, false);
@@ -451,20 +497,35 @@ static hipError_t run_fmap_t(const FwdArgs& a, hipStream_t st) {
 }
 
 template <class T, int D, int FW, int NW>
-static hipError_t run_variant(const FwdArgs& a, bool ns, bool causal, bool fmap, hipStream_t st) {
-  if (fmap) return ns ? run_fmap_t<T, D, FW, NW, true>(a, st) : run_fmap_t<T, D, FW, NW, false>(a, st);
+static hipError_t run_attn_v(const FwdArgs& a, bool ns, bool causal, hipStream_t st) {
   return ns ? run_fwd_t<T, D, FW, NW, true>(a, causal, st) : run_fwd_t<T, D, FW, NW, false>(a, causal, st);
 }
+template <class T, int D, int FW, int NW>
+static hipError_t run_fmap_v(const FwdArgs& a, bool ns, hipStream_t st) {
+  return ns ? run_fmap_t<T, D, FW, NW, true>(a, st) : run_fmap_t<T, D, FW, NW, false>(a, st);
+}
 
+// Feature map shapes (d, m) and attention shapes (d, m of one frequency group).
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStream_t st) {
   const bool ns = ks.nonstationary, causal = ks.causal;
+  if (fmap) {
+    if (ks.bf16) {
+      if (ks.d == 32 && ks.m == 64) return run_fmap_v<__bf16, 32, 16, 4>(a, ns, st);
+      if (ks.d == 64 && ks.m == 64) return run_fmap_v<__bf16, 64, 16, 4>(a, ns, st);
+      if (ks.d == 64 && ks.m == 128) return run_fmap_v<__bf16, 64, 16, 8>(a, ns, st);
+      if (ks.d == 128 && ks.m == 256) return run_fmap_v<__bf16, 128, 32, 8>(a, ns, st);
+    } else {
+      if (ks.d == 32 && ks.m == 64) return run_fmap_v<float, 32, 16, 4>(a, ns, st);
+    }
+    return hipErrorInvalidValue;
+  }
   if (ks.bf16) {
-    if (ks.d == 32 && ks.m == 64) return run_variant<__bf16, 32, 16, 4>(a, ns, causal, fmap, st);
-    if (ks.d == 64 && ks.m == 64) return run_variant<__bf16, 64, 16, 4>(a, ns, causal, fmap, st);
-    if (ks.d == 64 && ks.m == 128) return run_variant<__bf16, 64, 16, 8>(a, ns, causal, fmap, st);
-    if (ks.d == 128 && ks.m == 256) return run_variant<__bf16, 128, 32, 8>(a, ns, causal, fmap, st);
+    if (ks.d == 32 && ks.m == 64) return run_attn_v<__bf16, 32, 16, 4>(a, ns, causal, st);
+    if (ks.d == 64 && ks.m == 64) return run_attn_v<__bf16, 64, 16, 4>(a, ns, causal, st);
+    if (ks.d == 64 && ks.m == 128) return run_attn_v<__bf16, 64, 16, 8>(a, ns, causal, st);
+    if (ks.d == 128 && ks.m == 64) return run_attn_v<__bf16, 128, 16, 4>(a, ns, causal, st);
   } else {
-    if (ks.d == 32 && ks.m == 64) return run_variant<float, 32, 16, 4>(a, ns, causal, fmap, st);
+    if (ks.d == 32 && ks.m == 64) return run_attn_v<float, 32, 16, 4>(a, ns, causal, st);
   }
   return hipErrorInvalidValue;
 }
@@ -492,17 +553,15 @@ size_t wfrag_bytes(const KernelShape& ks, int H) {
     if (ks.d == 32 && ks.m == 64) return ns ? wfrag_bytes_t<__bf16, 32, 16, true>(H, 4) : wfrag_bytes_t<__bf16, 32, 16, false>(H, 4);
     if (ks.d == 64 && ks.m == 64) return ns ? wfrag_bytes_t<__bf16, 64, 16, true>(H, 4) : wfrag_bytes_t<__bf16, 64, 16, false>(H, 4);
     if (ks.d == 64 && ks.m == 128) return ns ? wfrag_bytes_t<__bf16, 64, 16, true>(H, 8) : wfrag_bytes_t<__bf16, 64, 16, false>(H, 8);
-    if (ks.d == 128 && ks.m == 256) return ns ? wfrag_bytes_t<__bf16, 128, 32, true>(H, 8) : wfrag_bytes_t<__bf16, 128, 32, false>(H, 8);
+    if (ks.d == 128 && ks.m == 64) return ns ? wfrag_bytes_t<__bf16, 128, 16, true>(H, 4) : wfrag_bytes_t<__bf16, 128, 16, false>(H, 4);
   } else {
     if (ks.d == 32 && ks.m == 64) return ns ? wfrag_bytes_t<float, 32, 16, true>(H, 4) : wfrag_bytes_t<float, 32, 16, false>(H, 4);
   }
   return 0;
 }
 
-// Waves per workgroup of the forward kernels of a shape.
-int fwd_state_waves(const KernelShape& ks) {
-  return (ks.bf16 && ((ks.d == 64 && ks.m == 128) || (ks.d == 128 && ks.m == 256))) ? 8 : 4;
-}
+// Waves per workgroup of the forward attention kernels of a shape.
+int fwd_state_waves(const KernelShape& ks) { return (ks.bf16 && ks.d == 64 && ks.m == 128) ? 8 : 4; }
 
 size_t fwd_state_floats(const KernelShape& ks) {
   const int fw = (ks.m == 64) ? 16 : 32;

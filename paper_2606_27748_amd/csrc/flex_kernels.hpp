@@ -34,6 +34,14 @@ struct FwdArgs {
   int sweep_groups;   // sweep workgroups per (b,h): the segments (causal) or chunk groups (non-causal)
   int sweep_cps;      // chunks per sweep workgroup
   float s_const;      // sigma/sqrt(m) or sigma/(2 sqrt(m))
+  // Frequency groups: W1/W2 point at this group's rows, w_stride is the
+  // element stride between heads.  acc = 0 writes O (and den) directly; 1 and
+  // 2 write / add the group's numerator and denominator into acc_num
+  // [BH][N][dv] and acc_den [BH][N] (fp32), which k_fwd_finish divides.
+  int w_stride;
+  int acc;
+  float* acc_num;
+  float* acc_den;
 };
 
 struct BwdArgs {
@@ -64,6 +72,11 @@ struct BwdArgs {
   int BH, B, H, N;
   int nchunks, segments, chunks_per_seg;
   float s_const;
+  // Frequency groups: W1/W2 and dW1/dW2 point at this group's rows, w_stride
+  // is the element stride between heads; acc = 1 adds dQ, dK, dV and dtau to
+  // the outputs (a later group), 0 writes them.
+  int w_stride;
+  int acc;
 };
 
 // Event bracketing of one kernel class (see flex_timing_enable); no-ops unless
@@ -89,6 +102,8 @@ int fwd_state_waves(const KernelShape& ks);
 hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
                              hipStream_t st);
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);
+// O = acc_num / acc_den (io dtype), den = acc_den, after the last frequency group.
+hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);
 
 }  // namespace flex

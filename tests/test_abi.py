@@ -57,10 +57,12 @@ def test_workspace_size():
     assert st == F.FLEX_OK and n0 == 0
     assert _ws(None)[0] == F.FLEX_ERR_INVALID_ARG
     assert _ws(d, 7)[0] == F.FLEX_ERR_INVALID_ARG
-    # a shape with a forward but no backward: the backward query says so
+    # d = 128, m = 256 runs as frequency groups; both passes have a workspace
     d5 = F.make_desc(2, 16, 8192, 128, 256, "nonstationary", True, "bf16")
-    assert _ws(d5)[0] == F.FLEX_OK
-    assert _ws(d5, F.FLEX_PASS_BWD) == (F.FLEX_ERR_UNSUPPORTED, 0)
+    assert _ws(d5)[0] == F.FLEX_OK and _ws(d5, F.FLEX_PASS_BWD)[0] == F.FLEX_OK
+    # an unsupported shape is reported for both passes
+    d6 = F.make_desc(2, 16, 8192, 96, 128, "nonstationary", True, "bf16")
+    assert _ws(d6)[0] == F.FLEX_ERR_UNSUPPORTED and _ws(d6, F.FLEX_PASS_BWD)[0] == F.FLEX_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("field,value,status", [

@@ -16,7 +16,7 @@ from tests.parity import check_grads, dtau_scale, KAPPA_MAX_GRAD as KAPPA_MAX, T
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128)]
+SHAPES = [("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256)]
 
 
 @pytest.fixture(scope="module")
@@ -164,7 +164,7 @@ def _slice_bwd_oracle(wl, x, b, h):
     return ref
 
 
-@pytest.mark.parametrize("name", ["nonstationary_causal_train", "headline_causal_train_d64"])
+@pytest.mark.parametrize("name", ["nonstationary_causal_train", "train_at_scale_d128", "headline_causal_train_d64"])
 def test_backward_full_size_sampled(F, name):
     """Full configured size, default launch configuration.  For one head, every
     slice's dQ, dK, dV rows and the head's dW1, dW2, dtau (sums over its B

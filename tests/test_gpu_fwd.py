@@ -18,7 +18,7 @@ from tests.parity import check_forward, abs_scales, TOL
 pytestmark = pytest.mark.gpu
 
 SHAPES = [  # (io, d, m)
-    ("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128),
+    ("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256),
 ]
 
 
@@ -124,7 +124,7 @@ def test_forward_sigma_invariance(F):
 
 
 FULL_FWD = ["tiny_stationary_noncausal_f32", "lm_stationary_causal", "long_stationary_noncausal",
-            "nonstationary_causal_train", "headline_causal_train_d64"]
+            "nonstationary_causal_train", "train_at_scale_d128", "headline_causal_train_d64"]
 
 
 @pytest.mark.parametrize("name", FULL_FWD)
