@@ -184,7 +184,10 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
     tokens = wl.B * wl.N
     value = tokens / (ms_step * 1e-3)
 
-    avg_s = (k_ms / max(k_n, 1)) * 1e-3
+    # the class's time per step (several launches when the shape runs as
+    # frequency groups) against its algorithmic work per step
+    per_step = max(k_n // steps, 1)
+    avg_s = (k_ms / steps) * 1e-3
     kwl = wl if backward == wl.backward else wl.scaled(backward=False)
     kbytes, kflops = kernel_work(kwl, dominant)
     ridge = (PEAK_BF16_TFLOPS * 1e12) / (PEAK_HBM_GBS * 1e9)
@@ -197,6 +200,7 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
     roof["traffic"] = traffic_from_profiles(wl, dominant)
     roof["kernel"] = dominant
     roof["kernel_ms"] = avg_s * 1e3
+    roof["launches_per_step"] = per_step
     roof["kernel_share"] = {k: round(v / sum(share.values()), 4) for k, v in share.items()}
 
     out = {"metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": steps,

@@ -40,6 +40,9 @@
  *     {32, 64, 128}; m in {64, 128, 256} with the combinations
  *     (d, m) = (32, 64), (64, 64), (64, 128), (128, 256) with io_dtype FLEX_BF16,
  *     and (32, 64) with FLEX_F32; chunk = 64.  Others return FLEX_ERR_UNSUPPORTED.
+ *     Every supported shape has the forward and the backward.  (128, 256) runs
+ *     as four groups of 64 frequencies whose sums are combined in a fixed
+ *     order; its forward workspace holds an fp32 numerator/denominator buffer.
  *   - io_dtype FLEX_F32 computes every contraction in fp32 (MFMA f32);
  *     FLEX_BF16 reads bf16 inputs, projects with a two-term bf16 split of the
  *     frequencies and contracts bf16 features with fp32 accumulation.
