@@ -219,6 +219,45 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
     return out
 
 
+def device_bytes(wl):
+    """Device memory a call needs: inputs, outputs and both workspaces."""
+    import paper_2606_27748_amd as F
+    rows = wl.B * wl.H * wl.N
+    bio = 2 if wl.io == "bf16" else 4
+    nmat = 2 if wl.variant == "nonstationary" else 1
+    desc = F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, wl.causal, wl.io)
+    tensors = rows * wl.d * bio * 4 + rows * 4 + nmat * wl.H * wl.m * wl.d * 4   # Q, K, V, O, den, W
+    ws = F.workspace_size(desc, F.FLEX_PASS_FWD)
+    if wl.backward:
+        tensors += rows * wl.d * bio + rows * wl.d * 4 * 3 + nmat * wl.H * wl.m * wl.d * 4  # dO, dQ/dK/dV, dW
+        ws += F.workspace_size(desc, F.FLEX_PASS_BWD)
+    return tensors, ws
+
+
+def run_sweep(steps, warmup):
+    """Time per step and device memory against the sequence length N (fixed B*H,
+    causal nonstationary d=64, m=128, forward and forward+backward) and against
+    the number of frequencies m (d=64, N=8192): the paper's cost-versus-length
+    and cost-versus-n comparisons, on synthetic inputs, for this implementation
+    only."""
+    import workloads as W
+    base = W.WORKLOADS["headline_causal_train_d64"]
+    cases = []
+    for N in (1024, 2048, 4096, 8192, 16384, 32768):
+        for bwd in (False, True):
+            cases.append(("N", base.scaled(name=f"sweep_N{N}_{'fwdbwd' if bwd else 'fwd'}", N=N, backward=bwd)))
+    for m, variant in ((64, "nonstationary"), (128, "nonstationary"), (64, "stationary"), (128, "stationary")):
+        cases.append(("m", base.scaled(name=f"sweep_m{m}_{variant[:4]}", m=m, variant=variant)))
+    for axis, wl in cases:
+        rec = measure(wl, steps, warmup, False, 0)
+        tensors, ws = device_bytes(wl)
+        print(json.dumps({"axis": axis, "workload": wl.name, "N": wl.N, "m": wl.m, "variant": wl.variant,
+                          "pass": rec["config"]["pass"], "ms_per_step": rec["ms_per_step"],
+                          "tokens_per_s": rec["value"], "device_bytes": tensors + ws,
+                          "workspace_bytes": ws, "dominant_kernel": rec["roofline"]["kernel"],
+                          "roofline_frac": rec["roofline"]["frac"]}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -227,6 +266,8 @@ def main():
     ap.add_argument("--workload", default="headline_causal_train_d64")
     ap.add_argument("--all-configs", action="store_true",
                     help="one JSON line per configured workload (no CPU baseline)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="scaling sweep: time and device memory against N and against m (JSON lines)")
     ap.add_argument("--cpu-slices", type=int, default=32)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--profile-only", action="store_true",
@@ -249,6 +290,9 @@ def main():
         sys.exit(2)
 
     import workloads as W
+    if args.sweep:
+        run_sweep(args.steps, args.warmup)
+        return
     if args.all_configs:
         for name, wl in W.WORKLOADS.items():
             print(json.dumps(measure(wl, args.steps, args.warmup, False, 0)), flush=True)
