@@ -258,6 +258,51 @@ def run_sweep(steps, warmup):
                           "roofline_frac": rec["roofline"]["frac"]}), flush=True)
 
 
+def run_decode(steps, warmup, B=64, H=16, d=64, m=128):
+    """Decode steps of the causal nonstationary attention for a batch of B
+    sequences (one new token each per step) against the resident fp32 state.
+    The state read-modify-write bounds the step: its bytes, the token rows and
+    the frequencies (read once per step) are the algorithmic traffic."""
+    import torch
+    import paper_2606_27748_amd as F
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(7)
+    s = d ** -0.25
+    q = (torch.randn(B, H, d, device=dev, generator=g) * s).to(torch.bfloat16)
+    k = (torch.randn(B, H, d, device=dev, generator=g) * s).to(torch.bfloat16)
+    v = (torch.randn(B, H, d, device=dev, generator=g) * s).to(torch.bfloat16)
+    W1 = torch.randn(H, m, d, device=dev, generator=g)
+    W2 = torch.randn(H, m, d, device=dev, generator=g)
+    tau = torch.full((H,), math.log(2.0), device=dev)
+    state = torch.zeros(B, H, 2 * m, d + 1, device=dev)
+    o = torch.empty(B, H, d, dtype=torch.bfloat16, device=dev)
+    den = torch.empty(B, H, device=dev)
+    desc = F.make_desc(B, H, 1, d, m, "nonstationary", True, "bf16")
+    for _ in range(warmup):
+        F.flex_decode_step(desc, q, k, v, W1, W2, tau, state, o, den)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        F.flex_decode_step(desc, q, k, v, W1, W2, tau, state, o, den)
+    e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / steps
+    kernel_ms = e0.elapsed_time(e1) / steps
+    nbytes = B * H * (2 * m) * (d + 1) * 4 * 2 + B * H * d * 2 * 4 + B * H * 4 + 2 * H * m * d * 4
+    return {"metric": "tokens/s, causal RFF linear-attn decode step", "value": B / (ms * 1e-3),
+            "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
+            "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "decode_nonstationary", "B": B, "H": H, "d": d, "m": m,
+                       "state_bytes": B * H * 2 * m * (d + 1) * 4},
+            "roofline": {"bound": "hbm", "achieved": nbytes / (kernel_ms * 1e-3) / 1e9,
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": nbytes / (kernel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                         "kernel": "decode_step", "kernel_ms": kernel_ms}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,6 +311,8 @@ def main():
     ap.add_argument("--workload", default="headline_causal_train_d64")
     ap.add_argument("--all-configs", action="store_true",
                     help="one JSON line per configured workload (no CPU baseline)")
+    ap.add_argument("--decode", action="store_true",
+                    help="recurrent decode step (one token per sequence against the running state)")
     ap.add_argument("--sweep", action="store_true",
                     help="scaling sweep: time and device memory against N and against m (JSON lines)")
     ap.add_argument("--cpu-slices", type=int, default=32)
@@ -292,6 +339,9 @@ def main():
     import workloads as W
     if args.sweep:
         run_sweep(args.steps, args.warmup)
+        return
+    if args.decode:
+        print(json.dumps(run_decode(args.steps, args.warmup)), flush=True)
         return
     if args.all_configs:
         for name, wl in W.WORKLOADS.items():

@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define FLEX_ABI_VERSION 2
+#define FLEX_ABI_VERSION 3
 
 typedef enum {
   FLEX_OK = 0,
@@ -142,6 +142,27 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K,
                          float* dW1, float* dW2, float* dtau,
                          const void* fwd_ws, size_t fwd_ws_bytes,
                          void* ws, size_t ws_bytes, void* stream);
+
+/* Recurrent decode step (causal attention one token at a time, the
+ * autoregressive language model of Sec. 4.2): for every (b,h) slice, with the
+ * new token's q, k, v,
+ *     S' <- S' + phi(k) [v ; 1]^T,    O = (phi(q)^T S')[:dv] / (phi(q)^T z),
+ * z being the last column of S' (the token attends to itself, as in the
+ * inclusive causal forward).  After t calls from a zero state, O equals row t
+ * of flex_linattn_fwd's causal output for the same tokens.
+ *   q, k [B,H,d], v [B,H,dv]   io_dtype, the new token of each slice
+ *   W1, W2, tau               as for flex_feature_map
+ *   state [B,H,2m,dv+1] fp32  caller-owned, updated in place; feature rows
+ *                             in [cos | sin] order, column dv the normaliser z;
+ *                             all zero for an empty prefix
+ *   o [B,H,dv] io_dtype, den [B,H] fp32 or NULL
+ * desc->N, causal, chunk and segments are ignored.  Shapes: d = dv a multiple
+ * of 4 up to 128, m up to 1024; others return FLEX_ERR_UNSUPPORTED.  The
+ * projection and the features are computed in fp32.  No workspace. */
+int32_t flex_decode_step(const flex_desc* desc, const void* q, const void* k,
+                         const void* v, const float* W1, const float* W2,
+                         const float* tau, float* state, void* o, float* den,
+                         void* stream);
 
 /* ---- Kernel timing (profiling aid) --------------------------------------
  * Kernel classes of the library.  When timing is enabled for one class, every

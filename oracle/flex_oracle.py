@@ -19,6 +19,9 @@ Plain, slow, float64 NumPy.  Every function follows a passage of the paper
                        inclusive).  Evaluated token by token as a running state.
 * backward          -- derived by hand from the two forms above (the paper has
                        no backward); pinned by finite differences in the tests.
+* decode step       -- the causal state form taken one token at a time (the
+                       autoregressive language model of Sec. 4.2); pinned by
+                       brute-force quadratic attention over the prefix.
 
 Readings of the paper taken here (each listed in the design doc):
   * nonstationary scale s = sigma / (2 sqrt(m)) as printed (its derivation
@@ -126,6 +129,25 @@ def attend_features(phi_q, phi_k, V, causal):
             S += phi_k[:, :, i, :, None] * Vp[:, :, i, None, :]
             nd[:, :, i, :] = np.einsum("bhf,bhfv->bhv", phi_q[:, :, i, :], S)
     return nd[..., :-1], nd[..., -1]
+
+
+def decode_step(state, q, k, v, W1, W2, tau, variant, sigma=1.0):
+    """One step of causal attention as a recurrence (the autoregressive use of
+    Eq.(linear att) in Sec. 4.2): the state S' = sum_j phi(k_j) [v_j ; 1]^T
+    takes the new token, then the new query reads it out (inclusive mask).
+
+    state [B,H,2m,dv+1] (feature rows in [cos | sin] order, last column the
+    normaliser z); q, k [B,H,d]; v [B,H,dv].  Returns (o [B,H,dv], den [B,H],
+    new state); the input state is not modified.
+    """
+    q = np.asarray(q, np.float64)[:, :, None, :]
+    k = np.asarray(k, np.float64)[:, :, None, :]
+    phi_q = feature_map(q, W1, W2, tau, variant, sigma)[:, :, 0, :]
+    phi_k = feature_map(k, W1, W2, tau, variant, sigma)[:, :, 0, :]
+    vp = np.concatenate([np.asarray(v, np.float64), np.ones(np.shape(v)[:-1] + (1,))], axis=-1)
+    S = np.asarray(state, np.float64) + phi_k[..., :, None] * vp[..., None, :]
+    nd = np.einsum("bhf,bhfv->bhv", phi_q, S)
+    return nd[..., :-1] / nd[..., -1:], nd[..., -1], S
 
 
 def linattn_fwd(Q, K, V, W1, W2, tau, variant, causal, sigma=1.0):

@@ -18,7 +18,7 @@ FLEX_F32, FLEX_BF16 = 0, 1
 FLEX_STATIONARY, FLEX_NONSTATIONARY = 0, 1
 FLEX_PASS_FEATURE_MAP, FLEX_PASS_FWD, FLEX_PASS_BWD = 0, 1, 2
 EXPORTS = ("flex_abi_version", "flex_status_string", "flex_workspace_size",
-           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_bwd",
+           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_bwd", "flex_decode_step",
            "flex_timing_enable", "flex_timing_read")
 KERNELS = {"none": 0, "fwd_state": 1, "fwd_sweep": 2, "scan": 3, "bwd_prepass": 4,
            "bwd_dq": 5, "bwd_dkv": 6, "bwd_reduce": 7, "feature_map": 8}
@@ -66,6 +66,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flex_linattn_fwd.argtypes = [D, P, P, P, P, P, P, P, P, P, S, P]
     lib.flex_linattn_bwd.restype = I
     lib.flex_linattn_bwd.argtypes = [D] + [P] * 15 + [P, S] + [P, S, P]
+    lib.flex_decode_step.restype = I
+    lib.flex_decode_step.argtypes = [D] + [P] * 10
     lib.flex_timing_enable.restype = I
     lib.flex_timing_enable.argtypes = [I]
     lib.flex_timing_read.restype = I
@@ -174,6 +176,20 @@ def flex_linattn_bwd(desc: flex_desc, Q, K, V, W1, W2, tau, O, den, dO, dQ=None,
                                  _ptr(ws), ws.numel(), _stream())
     _check(st, "flex_linattn_bwd")
     return dict(dQ=dQ, dK=dK, dV=dV, dW1=dW1, dW2=dW2, dtau=dtau)
+
+
+def flex_decode_step(desc: flex_desc, q, k, v, W1, W2, tau, state, o=None, den=None, want_den=True):
+    """One decode step: state (fp32 [B,H,2m,dv+1], updated in place) takes the
+    new token k, v; returns (o, den) for the new token's query q."""
+    import torch
+    if o is None:
+        o = torch.empty(desc.B, desc.H, desc.dv, dtype=q.dtype, device=q.device)
+    if den is None and want_den:
+        den = torch.empty(desc.B, desc.H, dtype=torch.float32, device=q.device)
+    st = load().flex_decode_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(W1), _ptr(W2),
+                                 _ptr(tau), _ptr(state), _ptr(o), _ptr(den), _stream())
+    _check(st, "flex_decode_step")
+    return o, den
 
 
 def flex_timing_enable(kernel: str) -> None:

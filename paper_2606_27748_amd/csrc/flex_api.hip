@@ -31,8 +31,8 @@ bool shape_supported(const flex_desc* d) {
 // The backward additionally needs the (d, m) shapes its kernels are built for.
 bool bwd_supported(const flex_desc*) { return true; }
 
-// 0 = ok, else a flex_status
-int32_t check_desc(const flex_desc* d) {
+// 0 = ok, else a flex_status: the descriptor's fields, without the shape list
+int32_t check_desc_fields(const flex_desc* d) {
   if (!d) return FLEX_ERR_INVALID_ARG;
   if (d->B <= 0 || d->H <= 0 || d->N <= 0 || d->d <= 0 || d->dv <= 0 || d->m <= 0)
     return FLEX_ERR_INVALID_ARG;
@@ -45,8 +45,21 @@ int32_t check_desc(const flex_desc* d) {
   // element counts must fit the 32-bit token and 64-bit element indexing used on device
   const long long bhn = (long long)d->B * d->H * d->N;
   if (bhn > (1LL << 40) || (long long)d->B * d->H > (1LL << 30)) return FLEX_ERR_INVALID_ARG;
+  return FLEX_OK;
+}
+
+// 0 = ok, else a flex_status
+int32_t check_desc(const flex_desc* d) {
+  const int32_t st = check_desc_fields(d);
+  if (st != FLEX_OK) return st;
   if (!shape_supported(d)) return FLEX_ERR_UNSUPPORTED;
   return FLEX_OK;
+}
+
+// Shapes of the decode step (one generic kernel): d = dv, a multiple of 4 up to
+// 128; up to 1024 frequencies.
+bool decode_supported(const flex_desc* d) {
+  return d->dv == d->d && d->d % 4 == 0 && d->d <= 128 && d->m <= 1024 && d->grad_dtype == FLEX_F32;
 }
 
 KernelShape kshape(const flex_desc* d) {
@@ -210,6 +223,26 @@ int32_t flex_timing_enable(int32_t kernel) {
   t.open = false;
   t.failed = false;
   return FLEX_OK;
+}
+
+int32_t flex_decode_step(const flex_desc* desc, const void* q, const void* k, const void* v,
+                         const float* W1, const float* W2, const float* tau, float* state, void* o,
+                         float* den, void* stream) {
+  const int32_t st = check_desc_fields(desc);
+  if (st != FLEX_OK) return st;
+  if (!decode_supported(desc)) return FLEX_ERR_UNSUPPORTED;
+  if (!q || !k || !v || !W1 || !tau || !state || !o) return FLEX_ERR_INVALID_ARG;
+  if ((desc->variant == FLEX_NONSTATIONARY) != (W2 != nullptr)) return FLEX_ERR_INVALID_ARG;
+  if (!aligned16(W1) || (W2 && !aligned16(W2)) || !aligned16(state) || !aligned16(q) || !aligned16(k) ||
+      !aligned16(v) || !aligned16(o) || (den && !aligned16(den)))
+    return FLEX_ERR_INVALID_ARG;
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = q; a.k = k; a.v = v; a.W1 = W1; a.W2 = W2; a.tau = tau; a.state = state; a.o = o; a.den = den;
+  a.BH = desc->B * desc->H; a.H = desc->H; a.d = desc->d; a.dv = desc->dv; a.m = desc->m;
+  a.s_const = s_const_of(desc);
+  const hipError_t e = launch_decode(a, desc->io_dtype == FLEX_BF16, (hipStream_t)stream);
+  return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
 }
 
 int32_t flex_timing_read(double* total_ms, int64_t* launches) {

@@ -86,6 +86,23 @@ enum KernelClass { KC_FWD_STATE = 1, KC_FWD_SWEEP = 2, KC_SCAN = 3, KC_BWD_PREPA
                    KC_BWD_DQ = 5, KC_BWD_DKV = 6, KC_BWD_REDUCE = 7, KC_FEATURE_MAP = 8 };
 
 // fp32 floats of one (b,h,segment) state block for a shape.
+// One decode step: one new token per (b,h) slice against a caller-owned state.
+struct DecodeArgs {
+  const void* q;      // [BH][d] io dtype
+  const void* k;      // [BH][d]
+  const void* v;      // [BH][dv]
+  const float* W1;    // [H][m][d]
+  const float* W2;    // [H][m][d] or NULL (stationary)
+  const float* tau;   // [H]
+  float* state;       // [BH][2m][dv+1] fp32, updated in place
+  void* o;            // [BH][dv] io dtype
+  float* den;         // [BH] or NULL
+  int BH, H, d, dv, m;
+  float s_const;
+};
+size_t decode_smem_bytes(int d, int dv, int m);
+hipError_t launch_decode(const DecodeArgs& a, bool bf16, hipStream_t st);
+
 size_t fwd_state_floats(const KernelShape& ks);
 size_t bwd_state_floats(const KernelShape& ks);
 size_t bwd_dw_floats(const KernelShape& ks);

@@ -1,0 +1,72 @@
+"""GPU parity of the recurrent decode step (flex_decode_step) through the C
+ABI: N steps from a zero state against the float64 oracle's causal attention
+(forward criteria of tests/parity.py), and the final state against the oracle's
+state sum_j phi(K_j)[V_j ; 1]^T."""
+import numpy as np
+import pytest
+
+import oracle as orc
+import workloads as W
+from tests.gpu_util import to_device, to_f64
+from tests.parity import check_forward
+
+pytestmark = pytest.mark.gpu
+
+CASES = [("bf16", 64, 128, "nonstationary"), ("bf16", 32, 64, "stationary"),
+         ("f32", 32, 64, "nonstationary"), ("bf16", 128, 256, "nonstationary")]
+
+
+@pytest.fixture(scope="module")
+def F():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2606_27748_amd as F
+    F.load()
+    return F
+
+
+@pytest.mark.parametrize("io,d,m,variant", CASES)
+def test_decode_steps(F, io, d, m, variant):
+    import torch
+    wl = W.Workload("decode", 2, 3, 48, d, m, variant, True, io, False, 41)
+    x = W.generate(wl)
+    t = to_device(x)
+    desc = F.make_desc(wl.B, wl.H, 1, d, m, variant, True, io)
+    state = torch.zeros(wl.B, wl.H, 2 * m, d + 1, dtype=torch.float32, device="cuda")
+    outs, dens = [], []
+    for i in range(wl.N):
+        o, den = F.flex_decode_step(desc, t["Q"][:, :, i].contiguous(), t["K"][:, :, i].contiguous(),
+                                    t["V"][:, :, i].contiguous(), t["W1"], t["W2"], t["tau"], state)
+        outs.append(o)
+        dens.append(den)
+    O = torch.stack(outs, dim=2)
+    den = torch.stack(dens, dim=2)
+    torch.cuda.synchronize()
+    Q, K, V = x.f64("Q"), x.f64("K"), x.f64("V")
+    ref_O, ref_den = orc.linattn_fwd(Q, K, V, x.W1, x.W2, x.tau, variant, True)
+    kap = orc.conditioning(Q, K, x.W1, x.W2, x.tau, variant, True)
+    check_forward(io, to_f64(O), to_f64(den), ref_O, ref_den, kap)
+    # the state: fp32 features and fp32 sums of 48 terms
+    pk = orc.feature_map(K, x.W1, x.W2, x.tau, variant)
+    Vp = np.concatenate([V, np.ones(V.shape[:-1] + (1,))], axis=-1)
+    ref_S = np.einsum("bhnf,bhnv->bhfv", pk, Vp)
+    got_S = to_f64(state)
+    err = np.linalg.norm(got_S - ref_S) / np.linalg.norm(ref_S)
+    assert err < 2e-5, err
+
+
+def test_decode_rejects_bad_arguments(F):
+    import torch
+    desc = F.make_desc(1, 1, 1, 96 + 2, 64, "stationary", True, "bf16")   # d not a multiple of 4
+    x = torch.zeros(1, 1, 98, dtype=torch.bfloat16, device="cuda")
+    W1 = torch.zeros(1, 64, 98, device="cuda")
+    tau = torch.zeros(1, device="cuda")
+    st = torch.zeros(1, 1, 128, 99, device="cuda")
+    with pytest.raises(F.FlexError):
+        F.flex_decode_step(desc, x, x, x, W1, None, tau, st)
+    desc = F.make_desc(1, 1, 1, 64, 64, "nonstationary", True, "bf16")   # W2 missing
+    x = torch.zeros(1, 1, 64, dtype=torch.bfloat16, device="cuda")
+    W1 = torch.zeros(1, 64, 64, device="cuda")
+    st = torch.zeros(1, 1, 128, 65, device="cuda")
+    with pytest.raises(F.FlexError):
+        F.flex_decode_step(desc, x, x, x, W1, None, tau, st)

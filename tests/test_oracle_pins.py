@@ -165,6 +165,26 @@ def test_state_form_equals_quadratic(variant, causal):
     np.testing.assert_allclose(O * den[..., None], Oq * denq[..., None], rtol=1e-11, atol=1e-11)
 
 
+@pytest.mark.parametrize("variant", [S, NS])
+def test_decode_steps_equal_causal_quadratic(variant):
+    """Recurrent decode (Sec. 4.2's autoregressive use of Eq.(linear att)): t
+    steps from a zero state give row t of the causal brute-force attention, and
+    the state is the plain sum of phi(k_j)[v_j ; 1]^T over the prefix."""
+    Q, K, V, W1, W2, tau = _small_inputs(variant, seed=5, N=11)
+    Oq, denq, _ = _quadratic(Q, K, V, W1, W2, tau, variant, True)
+    B, H, N, d = Q.shape
+    m = W1.shape[1]
+    state = np.zeros((B, H, 2 * m, d + 1))
+    for t in range(N):
+        o, den, state = orc.decode_step(state, Q[:, :, t], K[:, :, t], V[:, :, t], W1, W2, tau, variant)
+        np.testing.assert_allclose(den, denq[:, :, t], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(o * den[..., None], Oq[:, :, t] * denq[:, :, t, None], rtol=1e-11, atol=1e-11)
+    pk = orc.feature_map(K, W1, W2, tau, variant)
+    Vp = np.concatenate([V, np.ones(V.shape[:-1] + (1,))], axis=-1)
+    total = np.einsum("bhnf,bhnv->bhfv", pk, Vp)
+    np.testing.assert_allclose(state, total, rtol=1e-12, atol=1e-12)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_rows_equal_full(causal):
     """The per-row evaluation used for full-size spot checks agrees with the
