@@ -31,7 +31,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_TFLOPS = 157.3
 KERNEL_FILES = {"fwd_state": "flex_fwd.hip", "fwd_sweep": "flex_fwd.hip", "scan": "flex_fwd.hip",
                 "bwd_prepass": "flex_bwd.hip", "bwd_dq": "flex_bwd.hip", "bwd_dkv": "flex_bwd.hip",
-                "bwd_reduce": "flex_bwd.hip"}
+                "bwd_reduce": "flex_bwd.hip", "decode_step": "flex_decode.hip"}
 
 
 def kernel_work(wl, kernel):
@@ -72,10 +72,10 @@ def source_hash(kernel):
     return h.hexdigest()[:16]
 
 
-def traffic_from_profiles(wl, kernel):
+def traffic_from_profiles(workload, kernel):
     """HBM bytes per launch measured with rocprofv3 counters (committed under
     profiles/), or None when absent or taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", f"counters_{kernel}_{wl.name}.json")
+    path = os.path.join(ROOT, "profiles", f"counters_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -197,7 +197,7 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
     else:
         roof = {"bound": "hbm", "achieved": kbytes / avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = traffic_from_profiles(wl, dominant)
+    roof["traffic"] = traffic_from_profiles(wl.name, dominant)
     roof["kernel"] = dominant
     roof["kernel_ms"] = avg_s * 1e3
     roof["launches_per_step"] = per_step
@@ -258,7 +258,7 @@ def run_sweep(steps, warmup):
                           "roofline_frac": rec["roofline"]["frac"]}), flush=True)
 
 
-def run_decode(steps, warmup, B=64, H=16, d=64, m=128):
+def run_decode(steps, warmup, B=256, H=16, d=64, m=128):
     """Decode steps of the causal nonstationary attention for a batch of B
     sequences (one new token each per step) against the resident fp32 state.
     The state read-modify-write bounds the step: its bytes, the token rows and
@@ -274,10 +274,10 @@ def run_decode(steps, warmup, B=64, H=16, d=64, m=128):
     W1 = torch.randn(H, m, d, device=dev, generator=g)
     W2 = torch.randn(H, m, d, device=dev, generator=g)
     tau = torch.full((H,), math.log(2.0), device=dev)
-    state = torch.zeros(B, H, 2 * m, d + 1, device=dev)
+    desc = F.make_desc(B, H, 1, d, m, "nonstationary", True, "bf16")
+    state = F.decode_state(desc)
     o = torch.empty(B, H, d, dtype=torch.bfloat16, device=dev)
     den = torch.empty(B, H, device=dev)
-    desc = F.make_desc(B, H, 1, d, m, "nonstationary", True, "bf16")
     for _ in range(warmup):
         F.flex_decode_step(desc, q, k, v, W1, W2, tau, state, o, den)
     torch.cuda.synchronize()
@@ -291,16 +291,31 @@ def run_decode(steps, warmup, B=64, H=16, d=64, m=128):
     t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / steps
     kernel_ms = e0.elapsed_time(e1) / steps
+    # the practical ceiling: a device copy of the state (read + write), same timing
+    dst = torch.empty_like(state)
+    for _ in range(3):
+        dst.copy_(state)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        dst.copy_(state)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * state.numel() * 4 / (e0.elapsed_time(e1) / steps * 1e-3) / 1e9
+    del dst
     nbytes = B * H * (2 * m) * (d + 1) * 4 * 2 + B * H * d * 2 * 4 + B * H * 4 + 2 * H * m * d * 4
+    workload = f"decode_nonstationary_B{B}_H{H}_d{d}_m{m}"
     return {"metric": "tokens/s, causal RFF linear-attn decode step", "value": B / (ms * 1e-3),
             "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
             "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
-            "config": {"workload": "decode_nonstationary", "B": B, "H": H, "d": d, "m": m,
+            "config": {"workload": workload, "B": B, "H": H, "d": d, "m": m,
                        "state_bytes": B * H * 2 * m * (d + 1) * 4},
             "roofline": {"bound": "hbm", "achieved": nbytes / (kernel_ms * 1e-3) / 1e9,
                          "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": nbytes / (kernel_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
-                         "kernel": "decode_step", "kernel_ms": kernel_ms}}
+                         "traffic": traffic_from_profiles(workload, "decode_step"),
+                         "kernel": "decode_step", "kernel_ms": kernel_ms,
+                         "algorithmic_bytes": nbytes, "state_copy_gbs": copy_gbs}}
 
 
 def main():
@@ -313,6 +328,8 @@ def main():
                     help="one JSON line per configured workload (no CPU baseline)")
     ap.add_argument("--decode", action="store_true",
                     help="recurrent decode step (one token per sequence against the running state)")
+    ap.add_argument("--decode-batch", type=int, default=256,
+                    help="sequences per decode step (the default state, 272 MB, exceeds the 256 MB last-level cache)")
     ap.add_argument("--sweep", action="store_true",
                     help="scaling sweep: time and device memory against N and against m (JSON lines)")
     ap.add_argument("--cpu-slices", type=int, default=32)
@@ -333,7 +350,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported "
-              "(the path has no multi-GPU sharding; see DESIGN.md)", file=sys.stderr)
+              "(the path is built for one GPU; it has no multi-GPU sharding)", file=sys.stderr)
         sys.exit(2)
 
     import workloads as W
@@ -341,7 +358,7 @@ def main():
         run_sweep(args.steps, args.warmup)
         return
     if args.decode:
-        print(json.dumps(run_decode(args.steps, args.warmup)), flush=True)
+        print(json.dumps(run_decode(args.steps, args.warmup, B=args.decode_batch)), flush=True)
         return
     if args.all_configs:
         for name, wl in W.WORKLOADS.items():

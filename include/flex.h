@@ -145,16 +145,19 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K,
 
 /* Recurrent decode step (causal attention one token at a time, the
  * autoregressive language model of Sec. 4.2): for every (b,h) slice, with the
- * new token's q, k, v,
- *     S' <- S' + phi(k) [v ; 1]^T,    O = (phi(q)^T S')[:dv] / (phi(q)^T z),
- * z being the last column of S' (the token attends to itself, as in the
- * inclusive causal forward).  After t calls from a zero state, O equals row t
- * of flex_linattn_fwd's causal output for the same tokens.
+ * new token's q, k, v, the prefix state S' = [S | z] of Eq.(linear att) takes
+ * the token and the query reads it out:
+ *     S <- S + phi(k) v^T,  z <- z + phi(k),  O = (phi(q)^T S) / (phi(q)^T z)
+ * (the token attends to itself, as in the inclusive causal forward).  After t
+ * calls from a zero state, O equals row t of flex_linattn_fwd's causal output
+ * for the same tokens.
  *   q, k [B,H,d], v [B,H,dv]   io_dtype, the new token of each slice
  *   W1, W2, tau               as for flex_feature_map
- *   state [B,H,2m,dv+1] fp32  caller-owned, updated in place; feature rows
- *                             in [cos | sin] order, column dv the normaliser z;
- *                             all zero for an empty prefix
+ *   state fp32, B*H*2m*(dv+1) floats, caller-owned, updated in place; per
+ *                             (b,h) slice S [2m][dv] row-major, then z [2m];
+ *                             feature rows in [cos | sin] order; all zero for
+ *                             an empty prefix.  (S and z are kept apart so
+ *                             that S rows are 16-byte aligned.)
  *   o [B,H,dv] io_dtype, den [B,H] fp32 or NULL
  * desc->N, causal, chunk and segments are ignored.  Shapes: d = dv a multiple
  * of 4 up to 128, m up to 1024; others return FLEX_ERR_UNSUPPORTED.  The

@@ -23,7 +23,7 @@ Plain, slow, float64 NumPy.  Every function follows a passage of the paper
                        autoregressive language model of Sec. 4.2); pinned by
                        brute-force quadratic attention over the prefix.
 
-Readings of the paper taken here (each listed in the design doc):
+Readings of the paper taken here:
   * nonstationary scale s = sigma / (2 sqrt(m)) as printed (its derivation
     drops a factor 4; the constant cancels in O and every gradient);
   * both variants use the norm factor exp(||x||^2 / exp(tau)) with a per-head

@@ -178,10 +178,27 @@ def flex_linattn_bwd(desc: flex_desc, Q, K, V, W1, W2, tau, O, den, dO, dQ=None,
     return dict(dQ=dQ, dK=dK, dV=dV, dW1=dW1, dW2=dW2, dtau=dtau)
 
 
-def flex_decode_step(desc: flex_desc, q, k, v, W1, W2, tau, state, o=None, den=None, want_den=True):
-    """One decode step: state (fp32 [B,H,2m,dv+1], updated in place) takes the
-    new token k, v; returns (o, den) for the new token's query q."""
+def decode_state(desc: flex_desc, device="cuda"):
+    """A zero decode state: fp32 [B,H,2m*dv + 2m], per slice S [2m][dv] then z [2m]."""
     import torch
+    F = 2 * desc.m
+    return torch.zeros(desc.B, desc.H, F * desc.dv + F, dtype=torch.float32, device=device)
+
+
+def decode_state_views(desc: flex_desc, state):
+    """(S [B,H,2m,dv], z [B,H,2m]) views of a decode state."""
+    F = 2 * desc.m
+    st = state.reshape(desc.B, desc.H, F * (desc.dv + 1))
+    return st[..., :F * desc.dv].unflatten(-1, (F, desc.dv)), st[..., F * desc.dv:]
+
+
+def flex_decode_step(desc: flex_desc, q, k, v, W1, W2, tau, state, o=None, den=None, want_den=True):
+    """One decode step: state (fp32, B*H*2m*(dv+1) floats laid out as in
+    decode_state, updated in place) takes the new token k, v; returns (o, den)
+    for the new token's query q."""
+    import torch
+    if state.numel() != desc.B * desc.H * 2 * desc.m * (desc.dv + 1) or state.dtype != torch.float32:
+        raise FlexError(FLEX_ERR_INVALID_ARG, "flex_decode_step: state must hold B*H*2m*(dv+1) fp32")
     if o is None:
         o = torch.empty(desc.B, desc.H, desc.dv, dtype=q.dtype, device=q.device)
     if den is None and want_den:

@@ -32,7 +32,7 @@ def test_decode_steps(F, io, d, m, variant):
     x = W.generate(wl)
     t = to_device(x)
     desc = F.make_desc(wl.B, wl.H, 1, d, m, variant, True, io)
-    state = torch.zeros(wl.B, wl.H, 2 * m, d + 1, dtype=torch.float32, device="cuda")
+    state = F.decode_state(desc)
     outs, dens = [], []
     for i in range(wl.N):
         o, den = F.flex_decode_step(desc, t["Q"][:, :, i].contiguous(), t["K"][:, :, i].contiguous(),
@@ -50,7 +50,8 @@ def test_decode_steps(F, io, d, m, variant):
     pk = orc.feature_map(K, x.W1, x.W2, x.tau, variant)
     Vp = np.concatenate([V, np.ones(V.shape[:-1] + (1,))], axis=-1)
     ref_S = np.einsum("bhnf,bhnv->bhfv", pk, Vp)
-    got_S = to_f64(state)
+    S, z = F.decode_state_views(desc, state)
+    got_S = np.concatenate([to_f64(S), to_f64(z)[..., None]], axis=-1)
     err = np.linalg.norm(got_S - ref_S) / np.linalg.norm(ref_S)
     assert err < 2e-5, err
 
@@ -70,3 +71,28 @@ def test_decode_rejects_bad_arguments(F):
     st = torch.zeros(1, 1, 128, 65, device="cuda")
     with pytest.raises(F.FlexError):
         F.flex_decode_step(desc, x, x, x, W1, None, tau, st)
+    W2 = torch.zeros(1, 64, 64, device="cuda")
+    with pytest.raises(F.FlexError):                                     # state too small
+        F.flex_decode_step(desc, x, x, x, W1, W2, tau, st[..., :64])
+
+
+def test_decode_state_layout(F):
+    """One step from a zero state: S = phi(k) v^T and z = phi(k) land in the
+    documented halves of each slice (S rows first, then z)."""
+    import torch
+    wl = W.Workload("decode1", 2, 2, 1, 32, 64, "stationary", True, "f32", False, 5)
+    x = W.generate(wl)
+    t = to_device(x)
+    desc = F.make_desc(wl.B, wl.H, 1, 32, 64, "stationary", True, "f32")
+    state = F.decode_state(desc)
+    F.flex_decode_step(desc, t["Q"][:, :, 0].contiguous(), t["K"][:, :, 0].contiguous(),
+                       t["V"][:, :, 0].contiguous(), t["W1"], None, t["tau"], state)
+    torch.cuda.synchronize()
+    pk = orc.feature_map(x.f64("K")[:, :, :1], x.W1, None, x.tau, "stationary")[:, :, 0]
+    flat = to_f64(state)
+    Fm = 2 * 64
+    S = flat[..., :Fm * 32].reshape(2, 2, Fm, 32)
+    z = flat[..., Fm * 32:]
+    ref_S = pk[..., :, None] * x.f64("V")[:, :, 0][..., None, :]
+    assert np.linalg.norm(S - ref_S) <= 1e-5 * np.linalg.norm(ref_S)
+    assert np.linalg.norm(z - pk) <= 1e-5 * np.linalg.norm(pk)
