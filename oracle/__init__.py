@@ -6,4 +6,5 @@ benchmark's CPU-baseline leg, never by the product path.
 from .flex_oracle import *  # noqa: F401,F403
 from .flex_oracle import (feature_map, feature_map_parts, linattn_fwd, linattn_fwd_rows,
                           linattn_bwd, attend_features, conditioning, nonstationary_pairs, decode_step,
-                          norm_factor, STATIONARY, NONSTATIONARY)
+                          norm_factor, softmax_weights, awd_loss, awd_grads, STATIONARY,
+                          NONSTATIONARY)

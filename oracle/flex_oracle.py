@@ -22,6 +22,13 @@ Plain, slow, float64 NumPy.  Every function follows a passage of the paper
 * decode step       -- the causal state form taken one token at a time (the
                        autoregressive language model of Sec. 4.2); pinned by
                        brute-force quadratic attention over the prefix.
+* distillation loss -- the attention-weight distillation loss L_awd of
+                       App. A.3 (used in Sec. 4.3): cross-entropy between the
+                       softmax attention weights and the kernel's normalised
+                       weights, and its gradient with respect to the kernel
+                       parameters W1, W2, tau (derived here; pinned by a closed
+                       form at W = 0, softmax recovery at large m, invariances
+                       and finite differences).
 
 Readings of the paper taken here:
   * nonstationary scale s = sigma / (2 sqrt(m)) as printed (its derivation
@@ -29,7 +36,11 @@ Readings of the paper taken here:
   * both variants use the norm factor exp(||x||^2 / exp(tau)) with a per-head
     tau; the frequencies are per head;
   * features are ordered [cos block | sin block] as printed;
-  * no clamp or epsilon on the denominator.
+  * no clamp or epsilon on the denominator;
+  * L_awd: the log of A_ij / sum_l A_il is taken as printed (a non-positive
+    ratio gives NaN or inf for its slice); the softmax target is a constant
+    (only the kernel parameters are trained in the paper's distillation), and
+    its logits are Q_i^T K_j / sqrt(d) as printed.
 
 Every function here is pinned by a test in tests/test_oracle_pins.py; none is
 "parity unpinned".
@@ -296,3 +307,70 @@ def linattn_bwd(Q, K, V, W1, W2, tau, dO, variant, causal, sigma=1.0, return_aux
     if return_aux:
         out.update(O=O, den=den, g_q=gq, g_k=gk, G=G, phi_k=pk, dphi_k=dpk)
     return out
+
+
+# ----------------------------------------------------------------------------
+# Attention-weight distillation loss (App. A.3, used in Sec. 4.3)
+# ----------------------------------------------------------------------------
+
+def softmax_weights(Q, K):
+    """P_ij = exp(Q_i^T K_j / sqrt(d)) / sum_l exp(Q_i^T K_l / sqrt(d)), the
+    target attention weights of L_awd (row-wise softmax of the scaled logits)."""
+    Q = np.asarray(Q, np.float64)
+    K = np.asarray(K, np.float64)
+    S = np.matmul(Q, np.swapaxes(K, -1, -2)) / np.sqrt(Q.shape[-1])
+    S = S - S.max(axis=-1, keepdims=True)
+    E = np.exp(S)
+    return E / E.sum(axis=-1, keepdims=True)
+
+
+def awd_loss(Q, K, W1, W2, tau, variant, sigma=1.0, return_aux=False):
+    """L_awd of App. A.3 for every (b,h) slice:
+
+      L = -(1/N) sum_i sum_j P_ij log( A_ij / sum_l A_il ),
+      P = softmax_weights(Q, K),  A_ij = phi~(Q_i)^T phi~(K_j),
+
+    phi~ being the variant's feature map with its norm factor.  Evaluated as
+    printed (no clamp, no epsilon).  Returns L [B,H] (and the intermediates
+    with return_aux)."""
+    Q = np.asarray(Q, np.float64)
+    K = np.asarray(K, np.float64)
+    N = Q.shape[-2]
+    pq, parts_q = feature_map_parts(Q, W1, W2, tau, variant, sigma)
+    pk, parts_k = feature_map_parts(K, W1, W2, tau, variant, sigma)
+    A = np.matmul(pq, np.swapaxes(pk, -1, -2))
+    P = softmax_weights(Q, K)
+    den = A.sum(axis=-1)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        L = -(P * np.log(A / den[..., None])).sum(axis=-1).sum(axis=-1) / N
+    if return_aux:
+        return L, dict(A=A, P=P, den=den, pq=pq, pk=pk, parts_q=parts_q, parts_k=parts_k)
+    return L
+
+
+def awd_grads(Q, K, W1, W2, tau, variant, sigma=1.0):
+    """Gradients of sum_{b,h} L_awd[b,h] with respect to W1, W2 and tau
+    (derivation; the paper gives none).  With Sigma_j P_ij = 1,
+
+      dL/dA_ij = G_ij = (1/N) (1/den_i - P_ij / A_ij),   den_i = sum_l A_il,
+      dphi(Q_i) = sum_j G_ij phi(K_j),   dphi(K_j) = sum_i G_ij phi(Q_i),
+
+    followed by the feature-map chain rule of the attention backward.
+    Returns dict(loss, dW1, dW2, dtau, dphi_q, dphi_k)."""
+    Q = np.asarray(Q, np.float64)
+    K = np.asarray(K, np.float64)
+    N = Q.shape[-2]
+    L, aux = awd_loss(Q, K, W1, W2, tau, variant, sigma, return_aux=True)
+    A, P, den, pq, pk = aux["A"], aux["P"], aux["den"], aux["pq"], aux["pk"]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        G = (1.0 / den[..., None] - P / A) / N
+    dpq = np.matmul(G, pk)
+    dpk = np.matmul(np.swapaxes(G, -1, -2), pq)
+    parts_q, parts_k = aux["parts_q"], aux["parts_k"]
+    if variant == STATIONARY:
+        parts_q["W"] = np.asarray(W1, np.float64)
+        parts_k["W"] = np.asarray(W1, np.float64)
+    _, dW1q, dW2q, dtq, _ = _feature_map_bwd(Q, parts_q, pq, dpq, variant, tau)
+    _, dW1k, dW2k, dtk, _ = _feature_map_bwd(K, parts_k, pk, dpk, variant, tau)
+    return dict(loss=L, dW1=dW1q + dW1k, dW2=None if dW2q is None else dW2q + dW2k,
+                dtau=dtq + dtk, dphi_q=dpq, dphi_k=dpk)

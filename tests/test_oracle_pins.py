@@ -312,3 +312,118 @@ def test_finite_differences(variant, causal):
         an = g["d" + name]
         rel = np.linalg.norm(an - fd) / np.linalg.norm(fd)
         assert rel < 1e-6, (name, rel)
+
+
+# --- attention-weight distillation loss L_awd (App. A.3, used in Sec. 4.3) ----
+
+def _awd_inputs(variant, seed, B=2, H=2, N=7, d=4, m=5, scale=0.4, wscale=0.5):
+    r = _rng(seed)
+    W1 = r.standard_normal((H, m, d)) * wscale
+    W2 = r.standard_normal((H, m, d)) * wscale if variant == NS else None
+    Q = r.standard_normal((B, H, N, d)) * scale
+    K = r.standard_normal((B, H, N, d)) * scale
+    tau = np.array([math.log(2.0), 0.7])[:H]
+    return Q, K, W1, W2, tau
+
+
+def _entropy_rows(Q, K):
+    """Mean row entropy of the softmax target, from scipy's softmax."""
+    from scipy.special import softmax
+    P = softmax(np.matmul(Q, np.swapaxes(K, -1, -2)) / math.sqrt(Q.shape[-1]), axis=-1)
+    return -(P * np.log(P)).sum(-1).mean(-1), P
+
+
+@pytest.mark.parametrize("variant", [S, NS])
+def test_awd_zero_frequencies_closed_form(variant):
+    """W = 0: every cosine is 1 and every sine 0, so A_ij = s^2 m e(Q_i) e(K_j)
+    and the kernel's normalised weights are softmax_j(||K_j||^2 / c) for every
+    query.  Then L = -(1/N) sum_ij P_ij ||K_j||^2 / c + logsumexp_l ||K_l||^2 / c,
+    and with keys of equal norm L = log N exactly."""
+    from scipy.special import logsumexp
+    Q, K, W1, W2, tau = _awd_inputs(variant, seed=31)
+    W1 = np.zeros_like(W1)
+    W2 = None if W2 is None else np.zeros_like(W2)
+    c = np.exp(tau)[None, :, None]
+    u = (K * K).sum(-1) / c
+    _, P = _entropy_rows(Q, K)
+    expected = -(P * u[..., None, :]).sum(-1).mean(-1) + logsumexp(u, axis=-1)
+    L = orc.awd_loss(Q, K, W1, W2, tau, variant)
+    assert np.allclose(L, expected, rtol=1e-12, atol=1e-12)
+    Ke = K / np.linalg.norm(K, axis=-1, keepdims=True) * 0.7
+    L = orc.awd_loss(Q, Ke, W1, W2, tau, variant)
+    assert np.allclose(L, math.log(Q.shape[-2]), rtol=0, atol=1e-12)
+
+
+def test_awd_large_m_reaches_softmax_entropy():
+    """Gaussian frequencies of variance 1/sqrt(d) with c = 2 sqrt(d) make
+    phi~(x)^T phi~(y) an unbiased estimate of exp(x^T y / sqrt(d)) (the RFA form
+    of the softmax kernel, Sec. 3.1); as m grows the kernel's weights approach
+    the softmax target and L_awd approaches its lower bound, the mean row
+    entropy of the target (Gibbs' inequality).  L >= entropy at every m."""
+    r = _rng(33)
+    B, H, N, d = 1, 1, 8, 4
+    Q = r.standard_normal((B, H, N, d)) * 0.8
+    K = r.standard_normal((B, H, N, d)) * 0.8
+    tau = np.array([math.log(2.0 * math.sqrt(d))])
+    Hm, _ = _entropy_rows(Q, K)
+    gaps = []
+    for m in (16, 2 ** 16):
+        W = r.standard_normal((H, m, d)) * d ** -0.25
+        L = orc.awd_loss(Q, K, W, None, tau, S)
+        assert np.all(L >= Hm - 1e-12)
+        gaps.append(float((L - Hm).max()))
+    assert gaps[1] < 2e-3 < gaps[0]
+
+
+@pytest.mark.parametrize("variant", [S, NS])
+def test_awd_invariances(variant):
+    """Permuting the keys (with their softmax logits) leaves every row's sum
+    over j unchanged; sigma scales every A_ij alike and cancels in A_ij / den_i;
+    Gibbs' inequality bounds L below by the target's mean row entropy."""
+    Q, K, W1, W2, tau = _awd_inputs(variant, seed=35, m=32, wscale=0.4)
+    L = orc.awd_loss(Q, K, W1, W2, tau, variant)
+    assert np.all(np.isfinite(L))
+    perm = _rng(36).permutation(K.shape[-2])
+    assert np.allclose(orc.awd_loss(Q, K[..., perm, :], W1, W2, tau, variant), L, rtol=1e-12, atol=0)
+    assert np.allclose(orc.awd_loss(Q, K, W1, W2, tau, variant, sigma=2.5), L, rtol=1e-12, atol=0)
+    Hm, _ = _entropy_rows(Q, K)
+    assert np.all(L >= Hm - 1e-12)
+
+
+def test_awd_nonpositive_ratio_gives_nan():
+    """The log is taken as printed: one frequency at pi between a query and a
+    key makes a kernel weight negative, and that slice's loss is NaN."""
+    W = np.array([[[1.0]]])
+    Q = np.zeros((1, 1, 2, 1))
+    K = np.array([[[[0.0], [math.pi]]]])
+    L = orc.awd_loss(Q, K, W, None, np.array([3.0]), S)
+    assert np.isnan(L).all()
+
+
+@pytest.mark.parametrize("variant", [S, NS])
+def test_awd_finite_differences(variant):
+    """dW1, dW2 and dtau of sum_{b,h} L_awd match central finite differences."""
+    Q, K, W1, W2, tau = _awd_inputs(variant, seed=37, B=2, H=2, N=5, d=3, m=4, scale=0.4, wscale=0.6)
+    g = orc.awd_grads(Q, K, W1, W2, tau, variant)
+    assert np.all(np.isfinite(g["loss"]))
+    args = dict(W1=W1, W2=W2, tau=tau.astype(np.float64))
+    names = ["W1", "tau"] + (["W2"] if variant == NS else [])
+
+    def total(**kw):
+        return float(orc.awd_loss(Q, K, kw["W1"], kw["W2"], kw["tau"], variant).sum())
+
+    h = 1e-6
+    for name in names:
+        base = args[name]
+        fd = np.zeros_like(base)
+        it = np.nditer(base, flags=["multi_index"])
+        for _ in it:
+            idx = it.multi_index
+            plus = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in args.items()}
+            minus = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in args.items()}
+            plus[name][idx] += h
+            minus[name][idx] -= h
+            fd[idx] = (total(**plus) - total(**minus)) / (2 * h)
+        an = g["d" + name]
+        rel = np.linalg.norm(an - fd) / np.linalg.norm(fd)
+        assert rel < 1e-6, (name, rel)
