@@ -31,7 +31,9 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_TFLOPS = 157.3
 KERNEL_FILES = {"fwd_state": "flex_fwd.hip", "fwd_sweep": "flex_fwd.hip", "scan": "flex_fwd.hip",
                 "bwd_prepass": "flex_bwd.hip", "bwd_dq": "flex_bwd.hip", "bwd_dkv": "flex_bwd.hip",
-                "bwd_reduce": "flex_bwd.hip", "decode_step": "flex_decode.hip"}
+                "bwd_reduce": "flex_bwd.hip", "decode_step": "flex_decode.hip",
+                "awd_fwd": "flex_awd.hip", "awd_bwd_q": "flex_awd.hip", "awd_bwd_k": "flex_awd.hip",
+                "awd_wgrad": "flex_awd.hip"}
 
 
 def kernel_work(wl, kernel):
@@ -258,6 +260,134 @@ def run_sweep(steps, warmup):
                           "roofline_frac": rec["roofline"]["frac"]}), flush=True)
 
 
+AWD_CLASSES = ("feature_map", "awd_fwd", "awd_bwd_q", "awd_bwd_k", "awd_wgrad")
+# transcendental VALU rate: 256 CUs x 4 SIMDs x 16 lanes per clock at quarter
+# rate x 2.4 GHz
+PEAK_TRANS_PER_S = 256 * 4 * 16 / 4 * 2.4e9
+
+
+def awd_kernel_work(wl, kernel):
+    """Algorithmic (bytes, MFMA flops, transcendentals) of one launch of a
+    distillation kernel class: the inputs it must read and the outputs it must
+    write once, and the method's contractions (the logit tile Q K^T, the kernel
+    tile phi phi^T, and G phi for each side), excluding the recomputation of the
+    S and A tiles in the gradient passes."""
+    S, N, d, F = wl.B * wl.H, wl.N, wl.d, 2 * wl.m
+    bio = 2 if wl.io == "bf16" else 4
+    pairs = S * N * N
+    if kernel == "awd_fwd":
+        # reads Q, K, phi(Q), phi(K), z; writes (lse, 1/den) per query
+        return S * (2 * N * d * bio + 2 * N * F * bio + F * 4 + N * 8), pairs * (2 * d + 2 * F), 2 * pairs
+    if kernel in ("awd_bwd_q", "awd_bwd_k"):
+        # reads both sides' rows and features and the statistics; writes dphi (fp32)
+        return (S * (2 * N * d * bio + 2 * N * F * bio + N * 8 + N * F * 4), pairs * 2 * F, 2 * pairs)
+    if kernel == "awd_wgrad":
+        m_eff = wl.m * (2 if wl.variant == "nonstationary" else 1)
+        rows = 2 * S * N
+        return rows * (d * bio + F * 4), rows * (2 * d * m_eff) * 2, rows * (3 if m_eff > wl.m else 2) * wl.m
+    if kernel == "feature_map":
+        m_eff = wl.m * (2 if wl.variant == "nonstationary" else 1)
+        rows = S * N
+        return rows * (d * bio + F * bio), rows * 2 * d * m_eff, rows * (3 if m_eff > wl.m else 2) * wl.m
+    return 0, 0, 0
+
+
+def run_awd(steps, warmup, want_cpu, cpu_batches=2):
+    """One distillation step = flex_awd_loss with gradients (the loss of every
+    (b,h) slice and dW1, dW2, dtau) on the distillation workload, inputs
+    resident in HBM."""
+    import torch
+    import workloads as W
+    import paper_2606_27748_amd as F
+    wl = W.AWD_WORKLOADS[W.AWD_HEADLINE]
+    dev = "cuda:0"
+    x = W.generate_awd(wl)
+
+    def dev_t(a):
+        import numpy as np
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    Q, K, W1, W2, tau = dev_t(x.Q), dev_t(x.K), dev_t(x.W1), dev_t(x.W2), dev_t(x.tau)
+    desc = F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, False, wl.io)
+    f32 = torch.float32
+    outs = dict(loss=torch.empty(wl.B, wl.H, dtype=f32, device=dev),
+                dW1=torch.empty(W1.shape, dtype=f32, device=dev),
+                dW2=None if W2 is None else torch.empty(W2.shape, dtype=f32, device=dev),
+                dtau=torch.empty(tau.shape, dtype=f32, device=dev))
+    ws = torch.empty(F.workspace_size(desc, F.FLEX_PASS_AWD) + 256, dtype=torch.uint8, device=dev)
+
+    def step():
+        F.flex_awd_loss(desc, Q, K, W1, W2, tau, ws=ws, **outs)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    share = {}
+    for k in AWD_CLASSES:
+        F.flex_timing_enable(k)
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        ms, n = F.flex_timing_read()
+        share[k] = ms / 3
+    dominant = max(share, key=share.get)
+    F.flex_timing_enable(dominant)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    k_ms, k_n = F.flex_timing_read()
+    F.flex_timing_enable("none")
+    ms_step = (t1 - t0) * 1e3 / steps
+    avg_s = (k_ms / steps) * 1e-3
+    kb, kf, kt = awd_kernel_work(wl, dominant)
+    peak_f = PEAK_BF16_TFLOPS if wl.io == "bf16" else PEAK_FP32_TFLOPS
+    roofs = {"hbm": kb / (PEAK_HBM_GBS * 1e9), "mfma": kf / (peak_f * 1e12), "alu": kt / PEAK_TRANS_PER_S}
+    bound = max(roofs, key=roofs.get)
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": kb / avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    elif bound == "mfma":
+        roof = {"bound": "mfma", "achieved": kf / avg_s / 1e12, "peak": peak_f, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "alu", "achieved": kt / avg_s / 1e12, "peak": PEAK_TRANS_PER_S / 1e12,
+                "unit": "Ttranscendental/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_from_profiles(wl.name, dominant)
+    roof["kernel"] = dominant
+    roof["kernel_ms"] = avg_s * 1e3
+    roof["launches_per_step"] = max(k_n // steps, 1)
+    roof["roof_us"] = {k: round(v * 1e6, 2) for k, v in roofs.items()}
+    roof["kernel_share"] = {k: round(v / sum(share.values()), 4) for k, v in share.items()}
+    out = {"metric": "tokens/s, attention-weight distillation loss + dW1/dW2/dtau (N=512, d=64)",
+           "value": wl.B * wl.N / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+           "warmup": warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if wl.io == "bf16" else "f32", "data": "synthetic",
+           "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d, "m": wl.m,
+                      "variant": wl.variant, "causal": False, "pass": "loss+grad"},
+           "roofline": roof}
+    if want_cpu:
+        import oracle
+        sub = wl.scaled(B=cpu_batches)
+        xs = W.generate_awd(sub)
+        c0, p0 = time.perf_counter(), time.process_time()
+        oracle.awd_grads(xs.f64("Q"), xs.f64("K"), xs.W1, xs.W2, xs.tau, wl.variant)
+        c1, p1 = time.perf_counter(), time.process_time()
+        per_step = (c1 - c0) * wl.B / cpu_batches
+        out["cpu_baseline"] = {"value": wl.B * wl.N / per_step, "unit": "tokens/s",
+                               "cores": max(1, int(round((p1 - p0) / (c1 - c0)))), "kind": "oracle",
+                               "sample": f"{cpu_batches} of {wl.B} batches (all {wl.H} heads, N={wl.N}): loss "
+                                         f"and gradient in float64 ({c1 - c0:.1f} s), scaled by {wl.B}/{cpu_batches}"}
+    else:
+        out["cpu_baseline"] = None
+    return out
+
+
 def run_decode(steps, warmup, B=256, H=16, d=64, m=128):
     """Decode steps of the causal nonstationary attention for a batch of B
     sequences (one new token each per step) against the resident fp32 state.
@@ -281,16 +411,18 @@ def run_decode(steps, warmup, B=256, H=16, d=64, m=128):
     for _ in range(warmup):
         F.flex_decode_step(desc, q, k, v, W1, W2, tau, state, o, den)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    F.flex_timing_enable("decode_step")
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    e0.record()
     for _ in range(steps):
         F.flex_decode_step(desc, q, k, v, W1, W2, tau, state, o, den)
-    e1.record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    k_ms, _ = F.flex_timing_read()
+    F.flex_timing_enable("none")
     ms = (t1 - t0) * 1e3 / steps
-    kernel_ms = e0.elapsed_time(e1) / steps
+    kernel_ms = k_ms / steps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     # the practical ceiling: a device copy of the state (read + write), same timing
     dst = torch.empty_like(state)
     for _ in range(3):
@@ -326,6 +458,8 @@ def main():
     ap.add_argument("--workload", default="headline_causal_train_d64")
     ap.add_argument("--all-configs", action="store_true",
                     help="one JSON line per configured workload (no CPU baseline)")
+    ap.add_argument("--awd", action="store_true",
+                    help="attention-weight distillation loss and its kernel-parameter gradient")
     ap.add_argument("--decode", action="store_true",
                     help="recurrent decode step (one token per sequence against the running state)")
     ap.add_argument("--decode-batch", type=int, default=256,
@@ -356,6 +490,9 @@ def main():
     import workloads as W
     if args.sweep:
         run_sweep(args.steps, args.warmup)
+        return
+    if args.awd:
+        print(json.dumps(run_awd(args.steps, args.warmup, not args.no_cpu)), flush=True)
         return
     if args.decode:
         print(json.dumps(run_decode(args.steps, args.warmup, B=args.decode_batch)), flush=True)

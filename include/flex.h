@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define FLEX_ABI_VERSION 3
+#define FLEX_ABI_VERSION 4
 
 typedef enum {
   FLEX_OK = 0,
@@ -69,7 +69,8 @@ typedef enum {
 
 typedef enum { FLEX_F32 = 0, FLEX_BF16 = 1 } flex_dtype;
 typedef enum { FLEX_STATIONARY = 0, FLEX_NONSTATIONARY = 1 } flex_variant;
-typedef enum { FLEX_PASS_FEATURE_MAP = 0, FLEX_PASS_FWD = 1, FLEX_PASS_BWD = 2 } flex_pass;
+typedef enum { FLEX_PASS_FEATURE_MAP = 0, FLEX_PASS_FWD = 1, FLEX_PASS_BWD = 2,
+               FLEX_PASS_AWD = 3 } flex_pass;
 
 typedef struct {
   int32_t B, H, N;      /* batch, heads, sequence length                           */
@@ -167,6 +168,36 @@ int32_t flex_decode_step(const flex_desc* desc, const void* q, const void* k,
                          const float* tau, float* state, void* o, float* den,
                          void* stream);
 
+/* Attention-weight distillation loss (App. A.3; the loss Sec. 4.3 uses to
+ * distil softmax attention into the learnable kernel) and its gradient with
+ * respect to the kernel parameters.  For every (b,h) slice, with the softmax
+ * target P_ij = exp(Q_i.K_j/sqrt(d)) / sum_l exp(Q_i.K_l/sqrt(d)) and the
+ * kernel's weights A_ij = phi(Q_i)^T phi(K_j) (flex_feature_map's phi):
+ *     loss[b,h] = -(1/N) sum_i sum_j P_ij log(A_ij / sum_l A_il)
+ * evaluated as printed: no clamp or epsilon, so a non-positive A_ij / den_i
+ * gives NaN (or inf) for its slice.  P is a constant (the paper trains only
+ * the kernel parameters): the gradients are those of sum_{b,h} loss[b,h] with
+ * respect to W1, W2 and tau; there is no dQ or dK.
+ *   Q, K [B,H,N,d]   io_dtype
+ *   W1, W2, tau      as for flex_feature_map
+ *   loss [B,H] fp32  required
+ *   dW1 [H,m,d] fp32 or NULL: NULL computes the loss only (dW2 and dtau are
+ *                    then ignored); otherwise dW2 [H,m,d] is required for the
+ *                    nonstationary variant, and dtau [H] is optional.  The
+ *                    outputs are overwritten.
+ *   ws               flex_workspace_size(desc, FLEX_PASS_AWD) bytes: the
+ *                    features of Q and K, per-query statistics and the
+ *                    gradient partials; nothing of size N x N.
+ * desc->causal must be 0 (the loss sums over every key): 1 returns
+ * FLEX_ERR_UNSUPPORTED; dv, chunk and segments are ignored.  Shapes:
+ * bf16 (d, m) in {(32,64), (64,64), (64,128)} and fp32 (32,64).  Logits, the
+ * log-sum-exp and the logarithms are fp32; A is accumulated in fp32 from
+ * io_dtype features.  Deterministic. */
+int32_t flex_awd_loss(const flex_desc* desc, const void* Q, const void* K,
+                      const float* W1, const float* W2, const float* tau,
+                      float* loss, float* dW1, float* dW2, float* dtau,
+                      void* ws, size_t ws_bytes, void* stream);
+
 /* ---- Kernel timing (profiling aid) --------------------------------------
  * Kernel classes of the library.  When timing is enabled for one class, every
  * launch of a kernel of that class is bracketed by two hipEvents recorded on
@@ -182,7 +213,12 @@ typedef enum {
   FLEX_KERNEL_BWD_DQ = 5,       /* backward query-side sweep (dQ)             */
   FLEX_KERNEL_BWD_DKV = 6,      /* backward key-side sweep (dK, dV)           */
   FLEX_KERNEL_BWD_REDUCE = 7,   /* frequency / tau gradient reduction         */
-  FLEX_KERNEL_FEATURE_MAP = 8   /* standalone feature map                     */
+  FLEX_KERNEL_FEATURE_MAP = 8,  /* standalone feature map                     */
+  FLEX_KERNEL_DECODE = 9,       /* recurrent decode step                      */
+  FLEX_KERNEL_AWD_FWD = 10,     /* distillation loss pass                     */
+  FLEX_KERNEL_AWD_BWD_Q = 11,   /* distillation dphi(Q) pass                  */
+  FLEX_KERNEL_AWD_BWD_K = 12,   /* distillation dphi(K) pass                  */
+  FLEX_KERNEL_AWD_WGRAD = 13    /* distillation chain rule to dW', dtau       */
 } flex_kernel;
 
 /* Select the kernel class to time (FLEX_KERNEL_NONE disables) and discard

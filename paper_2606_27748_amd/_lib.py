@@ -16,12 +16,13 @@ LIB_PATH = os.path.join(HERE, "libflexattn.so")
 FLEX_OK, FLEX_ERR_INVALID_ARG, FLEX_ERR_UNSUPPORTED, FLEX_ERR_WORKSPACE, FLEX_ERR_HIP = range(5)
 FLEX_F32, FLEX_BF16 = 0, 1
 FLEX_STATIONARY, FLEX_NONSTATIONARY = 0, 1
-FLEX_PASS_FEATURE_MAP, FLEX_PASS_FWD, FLEX_PASS_BWD = 0, 1, 2
+FLEX_PASS_FEATURE_MAP, FLEX_PASS_FWD, FLEX_PASS_BWD, FLEX_PASS_AWD = 0, 1, 2, 3
 EXPORTS = ("flex_abi_version", "flex_status_string", "flex_workspace_size",
            "flex_feature_map", "flex_linattn_fwd", "flex_linattn_bwd", "flex_decode_step",
-           "flex_timing_enable", "flex_timing_read")
+           "flex_awd_loss", "flex_timing_enable", "flex_timing_read")
 KERNELS = {"none": 0, "fwd_state": 1, "fwd_sweep": 2, "scan": 3, "bwd_prepass": 4,
-           "bwd_dq": 5, "bwd_dkv": 6, "bwd_reduce": 7, "feature_map": 8}
+           "bwd_dq": 5, "bwd_dkv": 6, "bwd_reduce": 7, "feature_map": 8, "decode_step": 9,
+           "awd_fwd": 10, "awd_bwd_q": 11, "awd_bwd_k": 12, "awd_wgrad": 13}
 
 
 class FlexError(RuntimeError):
@@ -68,6 +69,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flex_linattn_bwd.argtypes = [D] + [P] * 15 + [P, S] + [P, S, P]
     lib.flex_decode_step.restype = I
     lib.flex_decode_step.argtypes = [D] + [P] * 10
+    lib.flex_awd_loss.restype = I
+    lib.flex_awd_loss.argtypes = [D] + [P] * 10 + [S, P]
     lib.flex_timing_enable.restype = I
     lib.flex_timing_enable.argtypes = [I]
     lib.flex_timing_read.restype = I
@@ -207,6 +210,33 @@ def flex_decode_step(desc: flex_desc, q, k, v, W1, W2, tau, state, o=None, den=N
                                  _ptr(tau), _ptr(state), _ptr(o), _ptr(den), _stream())
     _check(st, "flex_decode_step")
     return o, den
+
+
+def flex_awd_loss(desc: flex_desc, Q, K, W1, W2, tau, grads=True, loss=None, dW1=None, dW2=None,
+                  dtau=None, ws=None, want_dtau=True):
+    """Attention-weight distillation loss per (b,h) slice and, with grads, the
+    gradients of its sum over slices with respect to W1, W2 and tau.
+    Returns dict(loss [B,H], dW1, dW2, dtau) (fp32; gradients None without grads)."""
+    import torch
+    dev = Q.device
+    f32 = torch.float32
+    if loss is None:
+        loss = torch.empty(desc.B, desc.H, dtype=f32, device=dev)
+    if grads:
+        if dW1 is None:
+            dW1 = torch.empty(desc.H, desc.m, desc.d, dtype=f32, device=dev)
+        if dW2 is None and desc.variant == FLEX_NONSTATIONARY:
+            dW2 = torch.empty(desc.H, desc.m, desc.d, dtype=f32, device=dev)
+        if dtau is None and want_dtau:
+            dtau = torch.empty(desc.H, dtype=f32, device=dev)
+    else:
+        dW1 = dW2 = dtau = None
+    ws = _workspace(desc, FLEX_PASS_AWD, ws, dev)
+    st = load().flex_awd_loss(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(W1), _ptr(W2), _ptr(tau),
+                              _ptr(loss), _ptr(dW1), _ptr(dW2), _ptr(dtau), _ptr(ws), ws.numel(),
+                              _stream())
+    _check(st, "flex_awd_loss")
+    return dict(loss=loss, dW1=dW1, dW2=dW2, dtau=dtau)
 
 
 def flex_timing_enable(kernel: str) -> None:

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libflexattn.so")
-SOURCES = ["flex_api.hip", "flex_fwd.hip", "flex_bwd.hip", "flex_decode.hip"]
+SOURCES = ["flex_api.hip", "flex_fwd.hip", "flex_bwd.hip", "flex_decode.hip", "flex_awd.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

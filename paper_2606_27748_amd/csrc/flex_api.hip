@@ -168,6 +168,40 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
+// Distillation-loss workspace: features of Q and K (io dtype), z, per-query
+// statistics, loss partials, dphi(Q), dphi(K) (fp32), frequency-gradient and
+// dtau partials.
+struct AwdLayout {
+  size_t phq, phk, z, stats, lpart, dphq, dphk, wpart, dtpart, total;
+};
+int awd_ntile(const flex_desc* d) { return (d->N + 63) / 64; }
+AwdLayout awd_layout(const flex_desc* d) {
+  const size_t bh = (size_t)d->B * d->H, N = (size_t)d->N, F = 2 * (size_t)d->m;
+  const size_t io = d->io_dtype == FLEX_BF16 ? 2 : 4;
+  const size_t nmat = d->variant == FLEX_NONSTATIONARY ? 2 : 1;
+  const size_t parts = (size_t)flex::awd_parts(d->B, d->H, d->N);
+  AwdLayout L;
+  size_t off = 0;
+  L.phq = off;    off += align256(bh * N * F * io);
+  L.phk = off;    off += align256(bh * N * F * io);
+  L.z = off;      off += align256(bh * F * sizeof(float));
+  L.stats = off;  off += align256(bh * N * 2 * sizeof(float));
+  L.lpart = off;  off += align256(bh * (size_t)awd_ntile(d) * sizeof(float));
+  L.dphq = off;   off += align256(bh * N * F * sizeof(float));
+  L.dphk = off;   off += align256(bh * N * F * sizeof(float));
+  L.wpart = off;  off += align256((size_t)d->H * parts * nmat * d->m * d->d * sizeof(float));
+  L.dtpart = off; off += align256((size_t)d->H * parts * sizeof(float));
+  L.total = off;
+  return L;
+}
+int32_t check_awd_desc(const flex_desc* d) {
+  const int32_t st = check_desc_fields(d);
+  if (st != FLEX_OK) return st;
+  if (d->causal != 0) return FLEX_ERR_UNSUPPORTED;
+  if (!flex::awd_shape_supported(d->io_dtype == FLEX_BF16, d->d, d->m)) return FLEX_ERR_UNSUPPORTED;
+  return FLEX_OK;
+}
+
 }  // namespace
 
 namespace flex {
@@ -215,7 +249,7 @@ extern "C" {
 int32_t flex_abi_version(void) { return FLEX_ABI_VERSION; }
 
 int32_t flex_timing_enable(int32_t kernel) {
-  if (kernel < FLEX_KERNEL_NONE || kernel > FLEX_KERNEL_FEATURE_MAP) return FLEX_ERR_INVALID_ARG;
+  if (kernel < FLEX_KERNEL_NONE || kernel > FLEX_KERNEL_AWD_WGRAD) return FLEX_ERR_INVALID_ARG;
   Timing& t = timing();
   std::lock_guard<std::mutex> lk(t.mu);
   t.kernel = kernel;
@@ -223,6 +257,61 @@ int32_t flex_timing_enable(int32_t kernel) {
   t.open = false;
   t.failed = false;
   return FLEX_OK;
+}
+
+int32_t flex_awd_loss(const flex_desc* desc, const void* Q, const void* K, const float* W1,
+                      const float* W2, const float* tau, float* loss, float* dW1, float* dW2,
+                      float* dtau, void* ws, size_t ws_bytes, void* stream) {
+  const int32_t st = check_awd_desc(desc);
+  if (st != FLEX_OK) return st;
+  const bool ns = desc->variant == FLEX_NONSTATIONARY;
+  if (!Q || !K || !W1 || !tau || !loss) return FLEX_ERR_INVALID_ARG;
+  if (ns != (W2 != nullptr)) return FLEX_ERR_INVALID_ARG;
+  const bool grads = dW1 != nullptr;
+  if (grads && ns && !dW2) return FLEX_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(W1) || (W2 && !aligned16(W2)) || !aligned16(loss) ||
+      (grads && (!aligned16(dW1) || (ns && !aligned16(dW2)))))
+    return FLEX_ERR_INVALID_ARG;
+  const AwdLayout L = awd_layout(desc);
+  if (!ws || ws_bytes < L.total || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
+  char* base = static_cast<char*>(ws);
+  const hipStream_t sm = (hipStream_t)stream;
+  // the features of Q and K, written once by the feature-map kernel
+  FwdArgs f;
+  memset(&f, 0, sizeof(f));
+  f.W1 = W1; f.W2 = W2; f.tau = tau;
+  f.BH = desc->B * desc->H; f.H = desc->H; f.N = desc->N;
+  f.nchunks = nchunks_of(desc); f.segments = 1; f.chunks_per_seg = f.nchunks; f.sub = 1;
+  f.sweep_groups = 1; f.sweep_cps = f.nchunks;
+  f.s_const = s_const_of(desc);
+  const KernelShape ks = kshape(desc);
+  f.Q = Q; f.O = base + L.phq;
+  if (launch_fwd(f, ks, true, sm) != hipSuccess) return FLEX_ERR_HIP;
+  f.Q = K; f.O = base + L.phk;
+  if (launch_fwd(f, ks, true, sm) != hipSuccess) return FLEX_ERR_HIP;
+  AwdArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Q = Q; a.K = K; a.W1 = W1; a.W2 = W2; a.tau = tau;
+  a.phq = base + L.phq; a.phk = base + L.phk;
+  a.z = reinterpret_cast<float*>(base + L.z);
+  a.stats = reinterpret_cast<float*>(base + L.stats);
+  a.lpart = reinterpret_cast<float*>(base + L.lpart);
+  a.dphq = reinterpret_cast<float*>(base + L.dphq);
+  a.dphk = reinterpret_cast<float*>(base + L.dphk);
+  a.wpart = reinterpret_cast<float*>(base + L.wpart);
+  a.dtpart = reinterpret_cast<float*>(base + L.dtpart);
+  a.loss = loss;
+  a.dW1 = grads ? dW1 : nullptr;
+  a.dW2 = grads && ns ? dW2 : nullptr;
+  a.dtau = grads ? dtau : nullptr;
+  a.BH = desc->B * desc->H; a.B = desc->B; a.H = desc->H; a.N = desc->N;
+  a.ntile = awd_ntile(desc);
+  a.parts = awd_parts(desc->B, desc->H, desc->N);
+  a.c1 = (float)(1.4426950408889634 / sqrt((double)desc->d));
+  a.log2n = (float)log2((double)desc->N);
+  a.inv_n = (float)(1.0 / (double)desc->N);
+  a.s_const = s_const_of(desc);
+  return launch_awd(a, ks, grads, sm) == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
 }
 
 int32_t flex_decode_step(const flex_desc* desc, const void* q, const void* k, const void* v,
@@ -279,7 +368,13 @@ const char* flex_status_string(int32_t s) {
 int32_t flex_workspace_size(const flex_desc* desc, int32_t pass, size_t* bytes) {
   if (bytes) *bytes = 0;
   if (!bytes) return FLEX_ERR_INVALID_ARG;
-  if (pass < FLEX_PASS_FEATURE_MAP || pass > FLEX_PASS_BWD) return FLEX_ERR_INVALID_ARG;
+  if (pass < FLEX_PASS_FEATURE_MAP || pass > FLEX_PASS_AWD) return FLEX_ERR_INVALID_ARG;
+  if (pass == FLEX_PASS_AWD) {
+    const int32_t sa = check_awd_desc(desc);
+    if (sa != FLEX_OK) return sa;
+    *bytes = awd_layout(desc).total;
+    return FLEX_OK;
+  }
   const int32_t st = check_desc(desc);
   if (st != FLEX_OK) return st;
   if (pass == FLEX_PASS_BWD && !bwd_supported(desc)) return FLEX_ERR_UNSUPPORTED;

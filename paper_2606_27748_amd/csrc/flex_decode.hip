@@ -213,10 +213,12 @@ size_t decode_smem_bytes(int d, int dv, int m) {
 
 hipError_t launch_decode(const DecodeArgs& a, bool bf16, hipStream_t st) {
   const size_t smem = decode_smem_bytes(a.d, a.dv, a.m);
+  timing_mark(KC_DECODE, st, true);
   if (bf16)
     k_decode_step<u16><<<a.BH, DEC_NT, smem, st>>>(a);
   else
     k_decode_step<float><<<a.BH, DEC_NT, smem, st>>>(a);
+  timing_mark(KC_DECODE, st, false);
   return hipGetLastError();
 }
 

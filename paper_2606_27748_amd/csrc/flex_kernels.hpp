@@ -83,9 +83,10 @@ struct BwdArgs {
 // that class is selected.
 void timing_mark(int kernel_class, hipStream_t st, bool begin);
 enum KernelClass { KC_FWD_STATE = 1, KC_FWD_SWEEP = 2, KC_SCAN = 3, KC_BWD_PREPASS = 4,
-                   KC_BWD_DQ = 5, KC_BWD_DKV = 6, KC_BWD_REDUCE = 7, KC_FEATURE_MAP = 8 };
+                   KC_BWD_DQ = 5, KC_BWD_DKV = 6, KC_BWD_REDUCE = 7, KC_FEATURE_MAP = 8,
+                   KC_DECODE = 9, KC_AWD_FWD = 10, KC_AWD_BWD_Q = 11, KC_AWD_BWD_K = 12,
+                   KC_AWD_WGRAD = 13 };
 
-// fp32 floats of one (b,h,segment) state block for a shape.
 // One decode step: one new token per (b,h) slice against a caller-owned state.
 struct DecodeArgs {
   const void* q;      // [BH][d] io dtype
@@ -94,7 +95,7 @@ struct DecodeArgs {
   const float* W1;    // [H][m][d]
   const float* W2;    // [H][m][d] or NULL (stationary)
   const float* tau;   // [H]
-  float* state;       // [BH][2m][dv+1] fp32, updated in place
+  float* state;       // per slice S [2m][dv] then z [2m], fp32, updated in place
   void* o;            // [BH][dv] io dtype
   float* den;         // [BH] or NULL
   int BH, H, d, dv, m;
@@ -103,6 +104,39 @@ struct DecodeArgs {
 size_t decode_smem_bytes(int d, int dv, int m);
 hipError_t launch_decode(const DecodeArgs& a, bool bf16, hipStream_t st);
 
+// Attention-weight distillation loss and its kernel-parameter gradient.
+struct AwdArgs {
+  const void* Q;      // [BH][N][d] io dtype
+  const void* K;      // [BH][N][d]
+  const float* W1;    // [H][m][d]
+  const float* W2;    // [H][m][d] or NULL (stationary)
+  const float* tau;   // [H]
+  const void* phq;    // [BH][N][2m] io dtype: phi(Q), written by the feature map
+  const void* phk;    // [BH][N][2m]: phi(K)
+  float* z;           // [BH][2m] column sums of phi(K)
+  float* stats;       // [BH][N][2]: (lse2_i + log2 N, 1 / (N den_i)) per query
+  float* lpart;       // [BH][ntile] loss partial per 64-query tile
+  float* dphq;        // [BH][N][2m] fp32 dL/dphi(Q)
+  float* dphk;        // [BH][N][2m] fp32 dL/dphi(K)
+  float* wpart;       // [H][parts][nmat][m][d] frequency-gradient partials
+  float* dtpart;      // [H][parts] dtau partials
+  float* loss;        // [BH]
+  float* dW1;         // [H][m][d] or NULL (loss only)
+  float* dW2;         // [H][m][d] or NULL
+  float* dtau;        // [H] or NULL
+  int BH, B, H, N, ntile, parts;
+  float c1;           // log2(e) / sqrt(d): scaled logits in base 2
+  float log2n;        // log2(N)
+  float inv_n;        // 1 / N
+  float s_const;
+};
+int awd_parts(int B, int H, int N);
+// Supported (d, m) of the distillation loss; the launch returns
+// hipErrorInvalidValue for any other shape.
+bool awd_shape_supported(bool bf16, int d, int m);
+hipError_t launch_awd(const AwdArgs& a, const KernelShape& ks, bool grads, hipStream_t st);
+
+// fp32 floats of one (b,h,segment) state block for a shape.
 size_t fwd_state_floats(const KernelShape& ks);
 size_t bwd_state_floats(const KernelShape& ks);
 size_t bwd_dw_floats(const KernelShape& ks);

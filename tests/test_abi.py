@@ -31,7 +31,7 @@ def test_exports_match_header():
     assert set(names) == set(F.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.flex_abi_version() == 3
+    assert lib.flex_abi_version() == 4
 
 
 def test_status_strings():
@@ -63,6 +63,21 @@ def test_workspace_size():
     # an unsupported shape is reported for both passes
     d6 = F.make_desc(2, 16, 8192, 96, 128, "nonstationary", True, "bf16")
     assert _ws(d6)[0] == F.FLEX_ERR_UNSUPPORTED and _ws(d6, F.FLEX_PASS_BWD)[0] == F.FLEX_ERR_UNSUPPORTED
+
+
+def test_awd_workspace_size():
+    """The distillation loss pass: non-causal only, its own shape set."""
+    d = F.make_desc(32, 8, 512, 64, 64, "nonstationary", False, "bf16")
+    st, n = _ws(d, F.FLEX_PASS_AWD)
+    assert st == F.FLEX_OK
+    # at least the two feature blocks (bf16) and the two fp32 feature gradients
+    assert n >= 32 * 8 * 512 * 128 * (2 + 2 + 4 + 4)
+    dc = F.make_desc(32, 8, 512, 64, 64, "nonstationary", True, "bf16")
+    assert _ws(dc, F.FLEX_PASS_AWD)[0] == F.FLEX_ERR_UNSUPPORTED
+    d5 = F.make_desc(2, 16, 8192, 128, 256, "nonstationary", False, "bf16")
+    assert _ws(d5, F.FLEX_PASS_AWD)[0] == F.FLEX_ERR_UNSUPPORTED
+    df = F.make_desc(2, 2, 100, 32, 64, "stationary", False, "f32")
+    assert _ws(df, F.FLEX_PASS_AWD)[0] == F.FLEX_OK
 
 
 @pytest.mark.parametrize("field,value,status", [
@@ -118,3 +133,15 @@ def test_entry_points_reject_bad_arguments():
     # feature map
     assert lib.flex_feature_map(ctypes.byref(dn), None, P, P, P, P, None, 0, None) == 1
     assert lib.flex_feature_map(ctypes.byref(ds), P, P, P, P, P, None, 0, None) == 1
+    # distillation loss: loss is required, W2 matches the variant, dW2 is
+    # required with gradients of the nonstationary variant, non-causal only,
+    # and the workspace is checked
+    an = F.make_desc(1, 2, 100, 64, 128, "nonstationary", False, "bf16")
+    ast = F.make_desc(1, 2, 100, 64, 128, "stationary", False, "bf16")
+    assert lib.flex_awd_loss(ctypes.byref(an), P, P, P, P, P, None, P, P, P, P, big, None) == 1
+    assert lib.flex_awd_loss(ctypes.byref(an), P, P, P, None, P, P, P, P, P, P, big, None) == 1
+    assert lib.flex_awd_loss(ctypes.byref(ast), P, P, P, P, P, P, P, None, P, P, big, None) == 1
+    assert lib.flex_awd_loss(ctypes.byref(an), P, P, P, P, P, P, P, None, P, P, big, None) == 1
+    assert lib.flex_awd_loss(ctypes.byref(dn), P, P, P, P, P, P, P, P, P, P, big, None) == 2
+    assert lib.flex_awd_loss(ctypes.byref(an), P, P, P, P, P, P, P, P, P, P, 16, None) == 3
+    assert lib.flex_awd_loss(ctypes.byref(an), P, P, P, P, P, P, None, None, None, None, big, None) == 3

@@ -390,6 +390,22 @@ def test_awd_invariances(variant):
     assert np.all(L >= Hm - 1e-12)
 
 
+@pytest.mark.parametrize("variant", [S, NS])
+def test_awd_query_norm_gradient_vanishes(variant):
+    """L_awd depends on A_ij / sum_l A_il only, which no rescaling of phi(Q_i)
+    changes: <phi(Q_i), dL/dphi(Q_i)> = 0 for every query, so the query norm
+    factor contributes nothing to dtau (the key side does)."""
+    Q, K, W1, W2, tau = _awd_inputs(variant, seed=39, m=32, wscale=0.4)
+    g = orc.awd_grads(Q, K, W1, W2, tau, variant)
+    pq = orc.feature_map(Q, W1, W2, tau, variant)
+    pk = orc.feature_map(K, W1, W2, tau, variant)
+    gq = (pq * g["dphi_q"]).sum(-1)
+    gk = (pk * g["dphi_k"]).sum(-1)
+    scale = np.abs(pq * g["dphi_q"]).sum(-1).max()
+    assert np.abs(gq).max() <= 1e-12 * scale
+    assert np.abs(gk).max() > 1e-3 * np.abs(pk * g["dphi_k"]).sum(-1).max()
+
+
 def test_awd_nonpositive_ratio_gives_nan():
     """The log is taken as printed: one frequency at pi between a query and a
     key makes a kernel weight negative, and that slice's loss is NaN."""

@@ -81,6 +81,19 @@ WORKLOADS = {
 }
 HEADLINE = "headline_causal_train_d64"
 
+# Attention-weight distillation (the loss of App. A.3, used in Sec. 4.3):
+# non-causal, the softmax target from the same Q and K.  Stand-in for the
+# paper's GLUE distillation of a RoBERTa-size encoder (8 heads of d = 64,
+# batch 32, n = d frequencies, sequences up to 512 tokens); those data are not
+# available here and are not needed: the loss and its gradient cost the same
+# for any values.
+AWD_WORKLOADS = {
+    "distill_glue_B32_H8_N512_d64_m64": Workload(
+        "distill_glue_B32_H8_N512_d64_m64", 32, 8, 512, 64, 64,
+        "nonstationary", False, "bf16", True, 2001),
+}
+AWD_HEADLINE = "distill_glue_B32_H8_N512_d64_m64"
+
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bfloat16 (round-to-nearest-even); uint16 bits."""
@@ -145,3 +158,29 @@ def generate(wl: Workload, seed: int | None = None, with_grad: bool | None = Non
     dO = _store(rng.standard_normal((wl.B, wl.H, wl.N, wl.dv)), wl.io) if want_grad else None
     tau = np.full((H,), math.log(2.0), dtype=np.float32)
     return Inputs(wl, W1, W2, tau, Q, K, V, dO)
+
+
+def generate_awd(wl: Workload, seed: int | None = None) -> Inputs:
+    """Seeded inputs of a distillation-loss workload.
+
+    A ``numpy.random.default_rng(seed)`` draws, in this order and each standard
+    normal float64 in C order, W1 [H,m,d], W2 [H,m,d] (nonstationary only), Q
+    and K [B,H,N,d].  W is multiplied by 0.5 / sqrt(d) and rounded to fp32; Q
+    and K keep unit-variance entries (logits Q.K / sqrt(d) of unit variance,
+    as in a trained attention layer) and are rounded to the storage dtype;
+    tau = ln(2d) for every head.  With these frequencies and this bandwidth the
+    projections stay within about one radian, so every kernel weight
+    phi(Q_i)^T phi(K_j) is positive and the loss's logarithm is defined: a
+    kernel initialised near a wide Gaussian before distillation.  No V or dO.
+    """
+    rng = np.random.default_rng(wl.seed if seed is None else seed)
+    H, m, d = wl.H, wl.m, wl.d
+    ws = 0.5 / math.sqrt(d)
+    W1 = (rng.standard_normal((H, m, d)) * ws).astype(np.float32)
+    W2 = ((rng.standard_normal((H, m, d)) * ws).astype(np.float32)
+          if wl.variant == "nonstationary" else None)
+    shp = (wl.B, wl.H, wl.N, wl.d)
+    Q = _store(rng.standard_normal(shp), wl.io)
+    K = _store(rng.standard_normal(shp), wl.io)
+    tau = np.full((H,), math.log(2.0 * d), dtype=np.float32)
+    return Inputs(wl, W1, W2, tau, Q, K, None, None)
