@@ -168,9 +168,19 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-// Distillation-loss workspace: features of Q and K (io dtype), z, per-query
-// statistics, loss partials, dphi(Q), dphi(K) (fp32), frequency-gradient and
-// dtau partials.
+// Chunks per workgroup of the standalone feature map: about 1024 workgroups
+// in all (each builds its frequency fragments once), at least one chunk each.
+int fmap_chunks_per_wg(const flex_desc* d) {
+  const long long total = (long long)nchunks_of(d) * d->B * d->H;
+  long long c = total / 1024;
+  if (c < 1) c = 1;
+  if (c > nchunks_of(d)) c = nchunks_of(d);
+  return (int)c;
+}
+
+// Distillation-loss workspace: features of Q and K, z, per-query statistics,
+// loss partials, dphi(Q), dphi(K) (io dtype), frequency-gradient and dtau
+// partials.
 struct AwdLayout {
   size_t phq, phk, z, stats, lpart, dphq, dphk, wpart, dtpart, total;
 };
@@ -187,8 +197,8 @@ AwdLayout awd_layout(const flex_desc* d) {
   L.z = off;      off += align256(bh * F * sizeof(float));
   L.stats = off;  off += align256(bh * N * 2 * sizeof(float));
   L.lpart = off;  off += align256(bh * (size_t)awd_ntile(d) * sizeof(float));
-  L.dphq = off;   off += align256(bh * N * F * sizeof(float));
-  L.dphk = off;   off += align256(bh * N * F * sizeof(float));
+  L.dphq = off;   off += align256(bh * N * F * io);
+  L.dphk = off;   off += align256(bh * N * F * io);
   L.wpart = off;  off += align256((size_t)d->H * parts * nmat * d->m * d->d * sizeof(float));
   L.dtpart = off; off += align256((size_t)d->H * parts * sizeof(float));
   L.total = off;
@@ -281,7 +291,7 @@ int32_t flex_awd_loss(const flex_desc* desc, const void* Q, const void* K, const
   memset(&f, 0, sizeof(f));
   f.W1 = W1; f.W2 = W2; f.tau = tau;
   f.BH = desc->B * desc->H; f.H = desc->H; f.N = desc->N;
-  f.nchunks = nchunks_of(desc); f.segments = 1; f.chunks_per_seg = f.nchunks; f.sub = 1;
+  f.nchunks = nchunks_of(desc); f.segments = 1; f.chunks_per_seg = fmap_chunks_per_wg(desc); f.sub = 1;
   f.sweep_groups = 1; f.sweep_cps = f.nchunks;
   f.s_const = s_const_of(desc);
   const KernelShape ks = kshape(desc);
@@ -296,8 +306,8 @@ int32_t flex_awd_loss(const flex_desc* desc, const void* Q, const void* K, const
   a.z = reinterpret_cast<float*>(base + L.z);
   a.stats = reinterpret_cast<float*>(base + L.stats);
   a.lpart = reinterpret_cast<float*>(base + L.lpart);
-  a.dphq = reinterpret_cast<float*>(base + L.dphq);
-  a.dphk = reinterpret_cast<float*>(base + L.dphk);
+  a.dphq = base + L.dphq;
+  a.dphk = base + L.dphk;
   a.wpart = reinterpret_cast<float*>(base + L.wpart);
   a.dtpart = reinterpret_cast<float*>(base + L.dtpart);
   a.loss = loss;
@@ -395,7 +405,7 @@ int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1, 
   memset(&a, 0, sizeof(a));
   a.Q = X; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = Phi;
   a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
-  a.nchunks = nchunks_of(desc); a.segments = 1; a.chunks_per_seg = a.nchunks; a.sub = 1;
+  a.nchunks = nchunks_of(desc); a.segments = 1; a.chunks_per_seg = fmap_chunks_per_wg(desc); a.sub = 1;
   a.sweep_groups = 1; a.sweep_cps = a.nchunks;
   a.s_const = s_const_of(desc);
   const hipError_t e = launch_fwd(a, kshape(desc), true, (hipStream_t)stream);

@@ -43,6 +43,14 @@ __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ float log2_fast(float x) { return __builtin_amdgcn_logf(x); }
 __device__ __forceinline__ float rcp_fast(float x) { return __builtin_amdgcn_rcpf(x); }
 
+// Waves per SIMD the quadratic passes are compiled for: the bf16 shapes with
+// up to 128 features fit 3 (4 for the d = 64 loss pass) without spilling; the
+// others keep the compiler's choice.
+template <class T, int D, int F, bool GRAD>
+struct AwdOcc {
+  static constexpr int value = (IsBf16<T>::value && F <= 128) ? ((GRAD || D < 64) ? 3 : 4) : 1;
+};
+
 // Operand fragments of one row (COLS columns, k = columns) of a row-major
 // [N][COLS] io block; rows past the end read as zero.
 template <class T, int COLS>
@@ -130,7 +138,8 @@ __global__ __launch_bounds__(256) void k_awd_colsum(const IO* __restrict__ phk, 
 // 2^(x - max) and the sum of 2^(x - max) log2(A/den) over its own key subset
 // (keys 4g + i of every 16-key block); the four lane groups merge at the end.
 template <class T, int D, int F>
-__global__ __launch_bounds__(AWD_NT) void k_awd_fwd(AwdArgs a) {
+__global__ __launch_bounds__(AWD_NT) __attribute__((amdgpu_waves_per_eu(AwdOcc<T, D, F, false>::value)))
+void k_awd_fwd(AwdArgs a) {
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, AWD_NT> StX;
   typedef RowStage<IO, F, AWD_NT> StP;
@@ -176,30 +185,43 @@ __global__ __launch_bounds__(AWD_NT) void k_awd_fwd(AwdArgs a) {
     f32x4 s[4], av[4];
     tile_products<T, D, F, StX::LD, StP::LD>(XL, PL, xf, pf, s, av);
     const int kb = kt * AWD_TILE + 4 * g;
+    // whole tiles (every tile but a ragged last one) skip the key masks
+    const bool full = (kt + 1) * AWD_TILE <= a.N;
+    // running maximum of the raw logits (c1 > 0 scales them into base 2)
     float tmax = -INFINITY;
 #pragma unroll
     for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float x = s[sub][i] * a.c1;
-        s[sub][i] = x;
-        if (kb + sub * 16 + i < a.N) tmax = fmaxf(tmax, x);
-      }
+      for (int i = 0; i < 4; ++i)
+        if (full || kb + sub * 16 + i < a.N) tmax = fmaxf(tmax, s[sub][i]);
+    tmax *= a.c1;
     if (tmax > mx) {
       const float sc = exp2_fast(mx - tmax);   // 0 while mx is -inf
       Z *= sc;
       LS *= sc;
       mx = tmax;
     }
+    const float nm = -mx;
+    if (full) {
 #pragma unroll
-    for (int sub = 0; sub < 4; ++sub)
+      for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (kb + sub * 16 + i < a.N) {
-          const float e = exp2_fast(s[sub][i] - mx);
+        for (int i = 0; i < 4; ++i) {
+          const float e = exp2_fast(fmaf(s[sub][i], a.c1, nm));
           Z += e;
-          LS += e * log2_fast(av[sub][i] * rden);
+          LS = fmaf(e, log2_fast(av[sub][i] * rden), LS);
         }
+    } else {
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (kb + sub * 16 + i < a.N) {
+            const float e = exp2_fast(fmaf(s[sub][i], a.c1, nm));
+            Z += e;
+            LS = fmaf(e, log2_fast(av[sub][i] * rden), LS);
+          }
+    }
   }
   // merge the four lane groups of each query
 #pragma unroll
@@ -232,7 +254,8 @@ __global__ __launch_bounds__(AWD_NT) void k_awd_fwd(AwdArgs a) {
 // dphi(own) += G . Phi(streamed) on MFMA with the streamed features read
 // through the transpose load.
 template <class T, int D, int F, int MODE>
-__global__ __launch_bounds__(AWD_NT) void k_awd_bwd(AwdArgs a) {
+__global__ __launch_bounds__(AWD_NT) __attribute__((amdgpu_waves_per_eu(AwdOcc<T, D, F, true>::value)))
+void k_awd_bwd(AwdArgs a) {
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, AWD_NT> StX;
   typedef RowStage<IO, F, AWD_NT> StP;
@@ -301,13 +324,15 @@ __global__ __launch_bounds__(AWD_NT) void k_awd_bwd(AwdArgs a) {
                            ft * 16));
     }
   }
-  float* dst = (MODE == 0 ? a.dphq : a.dphk) + po;
+  // dphi is stored in the io dtype: its rounding (2^-9 relative on the bf16
+  // path) is below that of the bf16 features the passes already use
+  IO* dst = static_cast<IO*>(MODE == 0 ? a.dphq : a.dphk) + po;
 #pragma unroll
   for (int ft = 0; ft < F / 16; ++ft)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = tile * AWD_TILE + w * 16 + 4 * g + i;
-      if (row < a.N) dst[(size_t)row * F + ft * 16 + r] = acc[ft][i];
+      if (row < a.N) dst[(size_t)row * F + ft * 16 + r] = float_to_io<IO>(acc[ft][i]);
     }
 }
 
@@ -328,8 +353,10 @@ __global__ __launch_bounds__(M / 16 * WAVE) void k_awd_wgrad(AwdArgs a) {
   typedef typename Io<T>::type IO;
   constexpr int NW = M / 16, NT = NW * WAVE, F = 2 * M, ROWS = 32;
   typedef RowStage<IO, D, NT, ROWS> StX;
+  typedef RowStage<IO, F, NT, ROWS> StD;
   typedef FreqSlice<T, D, 16, NS> FS;
   __shared__ __align__(16) IO XL[StX::LDS_ELEMS];
+  __shared__ __align__(16) IO DL[StD::LDS_ELEMS];
   __shared__ float SSQ[ROWS];
   __shared__ float TRED[NW];
   const int h = blockIdx.x, part = blockIdx.y;
@@ -346,37 +373,41 @@ __global__ __launch_bounds__(M / 16 * WAVE) void k_awd_wgrad(AwdArgs a) {
     for (int dt = 0; dt < D / 16; ++dt) dw[pr][dt] = zero4();
   float gt = 0.f;
   // chunk u -> rows n0.. of side (0: Q, 1: K) of slice (b, h)
-  auto rows_of = [&](int u, const IO*& X, const float*& dph, int& n0, int& side) {
+  auto rows_of = [&](int u, const IO*& X, const IO*& dph, int& n0, int& side) {
     side = u / per_side;
     const int rem = u % per_side, b = rem / nch;
     const size_t bh = (size_t)b * a.H + h;
     X = static_cast<const IO*>(side ? a.K : a.Q) + bh * a.N * D;
-    dph = (side ? a.dphk : a.dphq) + bh * a.N * F;
+    dph = static_cast<const IO*>(side ? a.dphk : a.dphq) + bh * a.N * F;
     n0 = (rem % nch) * ROWS;
   };
   StX sx;
+  StD sd;
   if (u0 < u1) {
     const IO* X;
-    const float* dph;
+    const IO* dph;
     int n0, side;
     rows_of(u0, X, dph, n0, side);
     sx.fetch(X, n0, a.N);
+    sd.fetch(dph, n0, a.N);
   }
   for (int u = u0; u < u1; ++u) {
     const IO* X;
-    const float* dph;
+    const IO* dph;
     int n0, side;
     rows_of(u, X, dph, n0, side);
     const float gw = side ? 1.f : 0.f;   // dtau takes the K rows only
     __syncthreads();
     sx.store(XL, SSQ);
+    sd.store(DL);
     __syncthreads();
     if (u + 1 < u1) {
       const IO* Xn;
-      const float* dn;
+      const IO* dn;
       int nn, sn;
       rows_of(u + 1, Xn, dn, nn, sn);
       sx.fetch(Xn, nn, a.N);
+      sd.fetch(dn, nn, a.N);
     }
     f32x4 dp[2][FS::PR];
 #pragma unroll
@@ -390,8 +421,9 @@ __global__ __launch_bounds__(M / 16 * WAVE) void k_awd_wgrad(AwdArgs a) {
         const float ssq = SSQ[tl];
         const float sc = ok ? a.s_const * __expf(ssq * inv_c) : 0.f;
         const int f = w * 16 + r;
-        const float da = ok ? dph[(size_t)tok * F + f] : 0.f;
-        const float db = ok ? dph[(size_t)tok * F + M + f] : 0.f;
+        // rows past the end were staged as zeros
+        const float da = io_to_float(DL[tl * StD::LD + f]);
+        const float db = io_to_float(DL[tl * StD::LD + M + f]);
         float s1, c1;
         sincos_rev(p[0][i], s1, c1);
         if (NS) {
@@ -442,22 +474,36 @@ __global__ __launch_bounds__(M / 16 * WAVE) void k_awd_wgrad(AwdArgs a) {
 
 // Fixed-order sums: dW'1, dW'2 -> dW1 = (dW'1 + dW'2)/2, dW2 = (dW'1 - dW'2)/2
 // (W'1 = (W1 + W2)/2, W'2 = (W1 - W2)/2); dtau; loss = (1/N) sum of the tile
-// partials.  Grid (element blocks, H).
+// partials.  Grid (element blocks of 64, H): the four waves of a block take
+// every fourth partial of the block's 64 elements, then combine in order.
+constexpr int AWD_RED_E = 64;
 template <bool NS>
 __global__ __launch_bounds__(256) void k_awd_reduce(AwdArgs a, int M, int D) {
-  const int h = blockIdx.y, e = blockIdx.x * 256 + threadIdx.x, MD = M * D, nmat = NS ? 2 : 1;
-  if (a.dW1 && e < MD) {
+  __shared__ float R[2][4][AWD_RED_E];
+  const int h = blockIdx.y, w = threadIdx.x / WAVE, l = threadIdx.x % WAVE;
+  const int e = blockIdx.x * AWD_RED_E + l, MD = M * D, nmat = NS ? 2 : 1;
+  if (a.dW1) {
     float x0 = 0.f, x1 = 0.f;
-    for (int p = 0; p < a.parts; ++p) {
-      const float* src = a.wpart + ((size_t)h * a.parts + p) * nmat * MD;
-      x0 += src[e];
-      if (NS) x1 += src[MD + e];
+    if (e < MD) {
+#pragma unroll 4
+      for (int p = w; p < a.parts; p += 4) {
+        const float* src = a.wpart + ((size_t)h * a.parts + p) * nmat * MD;
+        x0 += src[e];
+        if (NS) x1 += src[MD + e];
+      }
     }
-    if (NS) {
-      a.dW1[(size_t)h * MD + e] = 0.5f * (x0 + x1);
-      a.dW2[(size_t)h * MD + e] = 0.5f * (x0 - x1);
-    } else {
-      a.dW1[(size_t)h * MD + e] = x0;
+    R[0][w][l] = x0;
+    R[1][w][l] = x1;
+    __syncthreads();
+    if (w == 0 && e < MD) {
+      const float y0 = ((R[0][0][l] + R[0][1][l]) + R[0][2][l]) + R[0][3][l];
+      if (NS) {
+        const float y1 = ((R[1][0][l] + R[1][1][l]) + R[1][2][l]) + R[1][3][l];
+        a.dW1[(size_t)h * MD + e] = 0.5f * (y0 + y1);
+        a.dW2[(size_t)h * MD + e] = 0.5f * (y0 - y1);
+      } else {
+        a.dW1[(size_t)h * MD + e] = y0;
+      }
     }
   }
   if (blockIdx.x != 0) return;
@@ -499,7 +545,7 @@ hipError_t run_awd(const AwdArgs& a, bool ns, bool grads, hipStream_t st) {
       k_awd_wgrad<T, D, M, false><<<wg, M / 16 * WAVE, 0, st>>>(a);
     timing_mark(KC_AWD_WGRAD, st, false);
   }
-  const dim3 rg(grads ? (M * D + 255) / 256 : 1, a.H);
+  const dim3 rg(grads ? (M * D + AWD_RED_E - 1) / AWD_RED_E : 1, a.H);
   if (ns)
     k_awd_reduce<true><<<rg, 256, 0, st>>>(a, M, D);
   else

@@ -389,38 +389,57 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Standalone feature map: Phi [B,H,N,2m], [cos | sin] blocks.
+// Standalone feature map: Phi [B,H,N,2m], [cos | sin] blocks.  A workgroup
+// walks a.chunks_per_seg consecutive chunks of one (b,h) slice with its
+// frequency fragments built once; each lane writes its four consecutive
+// features of a block as one vector store.
 // ---------------------------------------------------------------------------
+template <class IO>
+__device__ __forceinline__ void store4(IO* p, const float (&v)[4]);
+template <>
+__device__ __forceinline__ void store4<u16>(u16* p, const float (&v)[4]) {
+  const uint2 w = make_uint2((uint32_t)float_to_bf16_bits(v[0]) | ((uint32_t)float_to_bf16_bits(v[1]) << 16),
+                             (uint32_t)float_to_bf16_bits(v[2]) | ((uint32_t)float_to_bf16_bits(v[3]) << 16));
+  *reinterpret_cast<uint2*>(p) = w;
+}
+template <>
+__device__ __forceinline__ void store4<float>(float* p, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+
 template <class T, int D, int FW, int NW, bool NS>
 __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
-  const int c = blockIdx.x, bh = blockIdx.y, h = bh % a.H;
+  const int bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const IO* X = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
   IO* Phi = static_cast<IO*>(a.O) + (size_t)bh * a.N * (2 * SH::M);
   FreqSlice<T, D, FW, NS> fs;
   fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
   const float inv_c = __expf(-a.tau[h]);
-  const int tok0 = c * CHUNK;
+  const int c0 = blockIdx.x * a.chunks_per_seg;
+  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  for (int c = c0; c < c1; ++c) {
+    const int tok0 = c * CHUNK;
 #pragma unroll
-  for (int tt = 0; tt < TT; ++tt) {
-    f32x4 p[SH::PR];
-    float ssq;
-    project_tile<T, D, FW, NS>(fs, X, tok0 + tt * 16, a.N, p, ssq);
-    const int tok = tok0 + tt * 16 + r;
-    // the values are produced in fp32 and rounded once to the io dtype
-    const float sc = row_scale(ssq, inv_c, a.s_const, tok < a.N);
+    for (int tt = 0; tt < TT; ++tt) {
+      f32x4 p[SH::PR];
+      float ssq;
+      project_tile<T, D, FW, NS>(fs, X, tok0 + tt * 16, a.N, p, ssq);
+      const int tok = tok0 + tt * 16 + r;
+      // the values are produced in fp32 and rounded once to the io dtype
+      const float sc = row_scale(ssq, inv_c, a.s_const, tok < a.N);
 #pragma unroll
-    for (int ft = 0; ft < SH::FT; ++ft) {
-      const Frag<float> f = features<float, SH::FT, NS>(p, ft, sc);
-      if (tok < a.N) {
-        const int f0 = w * FW + ft * 16 + 4 * g;
-        IO* row = Phi + (size_t)tok * (2 * SH::M);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          row[f0 + i] = float_to_io<IO>(f.get(i));
-          row[SH::M + f0 + i] = float_to_io<IO>(f.get(4 + i));
+      for (int ft = 0; ft < SH::FT; ++ft) {
+        const Frag<float> f = features<float, SH::FT, NS>(p, ft, sc);
+        if (tok < a.N) {
+          const int f0 = w * FW + ft * 16 + 4 * g;
+          IO* row = Phi + (size_t)tok * (2 * SH::M);
+          const float cv[4] = {f.get(0), f.get(1), f.get(2), f.get(3)};
+          const float sv[4] = {f.get(4), f.get(5), f.get(6), f.get(7)};
+          store4<IO>(row + f0, cv);
+          store4<IO>(row + SH::M + f0, sv);
         }
       }
     }
@@ -489,7 +508,7 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
 template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_fmap_t(const FwdArgs& a, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
-  dim3 grid(a.nchunks, a.BH);
+  dim3 grid((a.nchunks + a.chunks_per_seg - 1) / a.chunks_per_seg, a.BH);
   timing_mark(KC_FEATURE_MAP, st, true);
   k_feature_map<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FEATURE_MAP, st, false);

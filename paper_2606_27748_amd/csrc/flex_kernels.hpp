@@ -116,8 +116,8 @@ struct AwdArgs {
   float* z;           // [BH][2m] column sums of phi(K)
   float* stats;       // [BH][N][2]: (lse2_i + log2 N, 1 / (N den_i)) per query
   float* lpart;       // [BH][ntile] loss partial per 64-query tile
-  float* dphq;        // [BH][N][2m] fp32 dL/dphi(Q)
-  float* dphk;        // [BH][N][2m] fp32 dL/dphi(K)
+  void* dphq;         // [BH][N][2m] io dtype: dL/dphi(Q)
+  void* dphk;         // [BH][N][2m] io dtype: dL/dphi(K)
   float* wpart;       // [H][parts][nmat][m][d] frequency-gradient partials
   float* dtpart;      // [H][parts] dtau partials
   float* loss;        // [BH]

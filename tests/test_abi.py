@@ -70,8 +70,8 @@ def test_awd_workspace_size():
     d = F.make_desc(32, 8, 512, 64, 64, "nonstationary", False, "bf16")
     st, n = _ws(d, F.FLEX_PASS_AWD)
     assert st == F.FLEX_OK
-    # at least the two feature blocks (bf16) and the two fp32 feature gradients
-    assert n >= 32 * 8 * 512 * 128 * (2 + 2 + 4 + 4)
+    # at least the two feature blocks and the two feature gradients (bf16)
+    assert n >= 32 * 8 * 512 * 128 * (2 + 2 + 2 + 2)
     dc = F.make_desc(32, 8, 512, 64, 64, "nonstationary", True, "bf16")
     assert _ws(dc, F.FLEX_PASS_AWD)[0] == F.FLEX_ERR_UNSUPPORTED
     d5 = F.make_desc(2, 16, 8192, 128, 256, "nonstationary", False, "bf16")
