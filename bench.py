@@ -279,12 +279,12 @@ def awd_kernel_work(wl, kernel):
         # reads Q, K, phi(Q), phi(K), z; writes (lse, 1/den) per query
         return S * (2 * N * d * bio + 2 * N * F * bio + F * 4 + N * 8), pairs * (2 * d + 2 * F), 2 * pairs
     if kernel in ("awd_bwd_q", "awd_bwd_k"):
-        # reads both sides' rows and features and the statistics; writes dphi (fp32)
-        return (S * (2 * N * d * bio + 2 * N * F * bio + N * 8 + N * F * 4), pairs * 2 * F, 2 * pairs)
+        # reads both sides' rows and features and the statistics; writes dphi (io dtype)
+        return (S * (2 * N * d * bio + 2 * N * F * bio + N * 8 + N * F * bio), pairs * 2 * F, 2 * pairs)
     if kernel == "awd_wgrad":
         m_eff = wl.m * (2 if wl.variant == "nonstationary" else 1)
         rows = 2 * S * N
-        return rows * (d * bio + F * 4), rows * (2 * d * m_eff) * 2, rows * (3 if m_eff > wl.m else 2) * wl.m
+        return rows * (d * bio + F * bio), rows * (2 * d * m_eff) * 2, rows * (3 if m_eff > wl.m else 2) * wl.m
     if kernel == "feature_map":
         m_eff = wl.m * (2 if wl.variant == "nonstationary" else 1)
         rows = S * N
@@ -292,7 +292,7 @@ def awd_kernel_work(wl, kernel):
     return 0, 0, 0
 
 
-def run_awd(steps, warmup, want_cpu, cpu_batches=2):
+def run_awd(steps, warmup, want_cpu, cpu_batches=32):
     """One distillation step = flex_awd_loss with gradients (the loss of every
     (b,h) slice and dW1, dW2, dtau) on the distillation workload, inputs
     resident in HBM."""
