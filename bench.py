@@ -32,7 +32,7 @@ PEAK_FP32_TFLOPS = 157.3
 KERNEL_FILES = {"fwd_state": "flex_fwd.hip", "fwd_sweep": "flex_fwd.hip", "scan": "flex_fwd.hip",
                 "bwd_prepass": "flex_bwd.hip", "bwd_dq": "flex_bwd.hip", "bwd_dkv": "flex_bwd.hip",
                 "bwd_reduce": "flex_bwd.hip", "decode_step": "flex_decode.hip",
-                "awd_fwd": "flex_awd.hip", "awd_bwd_q": "flex_awd.hip", "awd_bwd_k": "flex_awd.hip",
+                "awd_fwd": "flex_awd.hip", "awd_bwd_k": "flex_awd.hip",
                 "awd_wgrad": "flex_awd.hip"}
 
 
@@ -104,6 +104,33 @@ def cpu_baseline(wl, slices, seed_offset=0):
             "cores": max(1, int(round((c1 - c0) / (t1 - t0)))), "kind": "oracle",
             "sample": f"{slices} of {wl.B * wl.H} (b,h) slices at N={wl.N}, forward+backward in "
                       f"float64 ({t1 - t0:.1f} s), scaled by {wl.B * wl.H}/{slices}"}
+
+
+FLUSH_BYTES = 512 << 20   # twice the 256 MB last-level cache
+
+
+def step_stats(step, reps, cold):
+    """Per-step time (ms) of `reps` single steps, each bracketed by events on
+    the current stream; cold: a 512 MiB buffer is written before each step so
+    that no input of the step is left in the last-level cache.  Returns the
+    median and the 10th / 90th percentiles."""
+    import torch
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda:0") if cold else None
+    times = []
+    for _ in range(reps):
+        if cold:
+            flush.fill_(1.0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        step()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    times.sort()
+
+    def pct(q):
+        return times[min(len(times) - 1, int(round(q * (len(times) - 1))))]
+    return {"median_ms": pct(0.5), "p10_ms": pct(0.1), "p90_ms": pct(0.9), "reps": reps}
 
 
 def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
@@ -212,6 +239,8 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
                       "variant": wl.variant, "causal": wl.causal,
                       "pass": "fwd+bwd" if backward else "fwd", "parallelism": "single-gpu"},
            "roofline": roof}
+    out["step_timing"] = {"warm": step_stats(step, 20, False), "cold": step_stats(step, 20, True),
+                          "flush_bytes": FLUSH_BYTES}
     if wl.backward and not backward:
         out["config"]["note"] = "backward not built for this shape; forward only"
     if want_cpu:
@@ -260,7 +289,7 @@ def run_sweep(steps, warmup):
                           "roofline_frac": rec["roofline"]["frac"]}), flush=True)
 
 
-AWD_CLASSES = ("feature_map", "awd_fwd", "awd_bwd_q", "awd_bwd_k", "awd_wgrad")
+AWD_CLASSES = ("feature_map", "awd_fwd", "awd_bwd_k", "awd_wgrad")
 # transcendental VALU rate: 256 CUs x 4 SIMDs x 16 lanes per clock at quarter
 # rate x 2.4 GHz
 PEAK_TRANS_PER_S = 256 * 4 * 16 / 4 * 2.4e9
@@ -276,9 +305,11 @@ def awd_kernel_work(wl, kernel):
     bio = 2 if wl.io == "bf16" else 4
     pairs = S * N * N
     if kernel == "awd_fwd":
-        # reads Q, K, phi(Q), phi(K), z; writes (lse, 1/den) per query
-        return S * (2 * N * d * bio + 2 * N * F * bio + F * 4 + N * 8), pairs * (2 * d + 2 * F), 2 * pairs
-    if kernel in ("awd_bwd_q", "awd_bwd_k"):
+        # reads Q, K, phi(Q), phi(K), z; writes (lse, 1/den) per query and dphi(Q);
+        # the logit and kernel tiles and G phi(K); exp, log and a reciprocal per pair
+        return (S * (2 * N * d * bio + 2 * N * F * bio + F * 4 + N * 8 + N * F * bio),
+                pairs * (2 * d + 4 * F), 3 * pairs)
+    if kernel == "awd_bwd_k":
         # reads both sides' rows and features and the statistics; writes dphi (io dtype)
         return (S * (2 * N * d * bio + 2 * N * F * bio + N * 8 + N * F * bio), pairs * 2 * F, 2 * pairs)
     if kernel == "awd_wgrad":
@@ -370,7 +401,9 @@ def run_awd(steps, warmup, want_cpu, cpu_batches=32):
            "vs_baseline": None, "dtype": "bf16" if wl.io == "bf16" else "f32", "data": "synthetic",
            "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d, "m": wl.m,
                       "variant": wl.variant, "causal": False, "pass": "loss+grad"},
-           "roofline": roof}
+           "roofline": roof,
+           "step_timing": {"warm": step_stats(step, 20, False), "cold": step_stats(step, 20, True),
+                           "flush_bytes": FLUSH_BYTES}}
     if want_cpu:
         import oracle
         sub = wl.scaled(B=cpu_batches)

@@ -215,10 +215,9 @@ typedef enum {
   FLEX_KERNEL_BWD_REDUCE = 7,   /* frequency / tau gradient reduction         */
   FLEX_KERNEL_FEATURE_MAP = 8,  /* standalone feature map                     */
   FLEX_KERNEL_DECODE = 9,       /* recurrent decode step                      */
-  FLEX_KERNEL_AWD_FWD = 10,     /* distillation loss pass                     */
-  FLEX_KERNEL_AWD_BWD_Q = 11,   /* distillation dphi(Q) pass                  */
-  FLEX_KERNEL_AWD_BWD_K = 12,   /* distillation dphi(K) pass                  */
-  FLEX_KERNEL_AWD_WGRAD = 13    /* distillation chain rule to dW', dtau       */
+  FLEX_KERNEL_AWD_FWD = 10,     /* distillation loss (and dphi(Q)) pass       */
+  FLEX_KERNEL_AWD_BWD_K = 11,   /* distillation dphi(K) pass                  */
+  FLEX_KERNEL_AWD_WGRAD = 12    /* distillation chain rule to dW', dtau       */
 } flex_kernel;
 
 /* Select the kernel class to time (FLEX_KERNEL_NONE disables) and discard

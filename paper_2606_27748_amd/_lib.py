@@ -22,7 +22,7 @@ EXPORTS = ("flex_abi_version", "flex_status_string", "flex_workspace_size",
            "flex_awd_loss", "flex_timing_enable", "flex_timing_read")
 KERNELS = {"none": 0, "fwd_state": 1, "fwd_sweep": 2, "scan": 3, "bwd_prepass": 4,
            "bwd_dq": 5, "bwd_dkv": 6, "bwd_reduce": 7, "feature_map": 8, "decode_step": 9,
-           "awd_fwd": 10, "awd_bwd_q": 11, "awd_bwd_k": 12, "awd_wgrad": 13}
+           "awd_fwd": 10, "awd_bwd_k": 11, "awd_wgrad": 12}
 
 
 class FlexError(RuntimeError):

@@ -17,9 +17,9 @@
 //   k_awd_colsum  z = sum_j phi(K_j) per slice, so that den_i = phi(Q_i)^T z
 //   k_awd_fwd     per 64-query tile: online base-2 log-sum-exp of the scaled
 //                 logits and the P-weighted sum of log2(A_ij / den_i) per
-//                 query; a loss partial per tile, (lse, 1/den) per query
-//   k_awd_bwd<0>  dphi(Q) per 64-query tile, streaming the key tiles
-//   k_awd_bwd<1>  dphi(K) per 64-key tile, streaming the query tiles
+//                 query; a loss partial per tile, (lse, 1/den) per query; with
+//                 gradients also dphi(Q) in the same sweep
+//   k_awd_bwd_k   dphi(K) per 64-key tile, streaming the query tiles
 //   k_awd_wgrad   chain rule through phi for the Q and K rows of one head:
 //                 dW' and dtau partials
 //   k_awd_reduce  fixed-order sums into loss [B,H], dW1, dW2 and dtau
@@ -134,11 +134,18 @@ __global__ __launch_bounds__(256) void k_awd_colsum(const IO* __restrict__ phk, 
 }
 
 // Loss pass: one workgroup per (b,h, 64-query tile); wave w owns queries
-// tile*64 + 16w + (lane % 16).  Each lane keeps a running maximum, the sum of
-// 2^(x - max) and the sum of 2^(x - max) log2(A/den) over its own key subset
-// (keys 4g + i of every 16-key block); the four lane groups merge at the end.
-template <class T, int D, int F>
-__global__ __launch_bounds__(AWD_NT) __attribute__((amdgpu_waves_per_eu(AwdOcc<T, D, F, false>::value)))
+// tile*64 + 16w + (lane % 16).  The four lane groups of a query share one
+// running maximum of its scaled logits (a cross-group max per key tile); each
+// lane sums 2^(x - max) (Z) and 2^(x - max) log2(A/den) (LS) over its own keys
+// (4g + i of every 16-key block), merged at the end.
+//
+// DPHI also forms dphi(Q) in the same sweep (flash style):
+//   dphi(Q_i) = (1/N) (z / den_i - U_i / Z_i),  U_i = sum_j 2^(x_ij - max) / A_ij phi(K_j),
+// with U rescaled whenever the maximum grows.  The two terms cancel to the
+// extent the kernel's weights match the target, so e/A enters the MFMA as a
+// bf16 hi + lo pair (about 16 bits), not rounded to bf16.
+template <class T, int D, int F, bool DPHI>
+__global__ __launch_bounds__(AWD_NT) __attribute__((amdgpu_waves_per_eu(AwdOcc<T, D, F, DPHI>::value)))
 void k_awd_fwd(AwdArgs a) {
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, AWD_NT> StX;
@@ -169,6 +176,9 @@ void k_awd_fwd(AwdArgs a) {
   const float rden = 1.0f / den;
 
   float mx = -INFINITY, Z = 0.f, LS = 0.f;
+  f32x4 U[DPHI ? F / 16 : 1];
+#pragma unroll
+  for (int ft = 0; ft < (DPHI ? F / 16 : 1); ++ft) U[ft] = zero4();
   StX sx;
   StP sp;
   sx.fetch(K, 0, a.N);
@@ -187,58 +197,82 @@ void k_awd_fwd(AwdArgs a) {
     const int kb = kt * AWD_TILE + 4 * g;
     // whole tiles (every tile but a ragged last one) skip the key masks
     const bool full = (kt + 1) * AWD_TILE <= a.N;
-    // running maximum of the raw logits (c1 > 0 scales them into base 2)
+    // the query's maximum over this tile's valid keys, shared by its four
+    // lane groups (c1 > 0 scales raw logits into base 2)
     float tmax = -INFINITY;
 #pragma unroll
     for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         if (full || kb + sub * 16 + i < a.N) tmax = fmaxf(tmax, s[sub][i]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
     tmax *= a.c1;
-    if (tmax > mx) {
-      const float sc = exp2_fast(mx - tmax);   // 0 while mx is -inf
-      Z *= sc;
-      LS *= sc;
-      mx = tmax;
+    const float mn = fmaxf(mx, tmax);
+    const float al = mn > mx ? exp2_fast(mx - mn) : 1.f;   // 0 while mx is -inf
+    Z *= al;
+    LS *= al;
+    if (DPHI && __any(al != 1.f)) {
+      // rows 4g + i of U belong to queries 4g + i, whose factors sit in lanes 4g + i
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float ai = __shfl(al, 4 * g + i);
+#pragma unroll
+        for (int ft = 0; ft < (DPHI ? F / 16 : 1); ++ft) U[ft][i] *= ai;
+      }
     }
+    mx = mn;
     const float nm = -mx;
-    if (full) {
+    f32x4 H[DPHI ? 4 : 1];
 #pragma unroll
-      for (int sub = 0; sub < 4; ++sub)
+    for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float e = exp2_fast(fmaf(s[sub][i], a.c1, nm));
-          Z += e;
-          LS = fmaf(e, log2_fast(av[sub][i] * rden), LS);
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = full || kb + sub * 16 + i < a.N;
+        const float e = ok ? exp2_fast(fmaf(s[sub][i], a.c1, nm)) : 0.f;
+        Z += e;
+        if (ok) LS = fmaf(e, log2_fast(av[sub][i] * rden), LS);
+        if (DPHI) H[sub][i] = ok ? e * rcp_fast(av[sub][i]) : 0.f;
+      }
+    if (DPHI) {
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp) {
+        Frag<T> hi, lo;
+        split_pair<T>(H[2 * kp], H[2 * kp + 1], hi, lo);
+#pragma unroll
+        for (int ft = 0; ft < F / 16; ++ft) {
+          const Frag<T> pb = lds_tr_frag<T>(reinterpret_cast<const T*>(PL), StP::LD, 32 * kp + 4 * g,
+                                            32 * kp + 16 + 4 * g, ft * 16);
+          mma(U[ft], hi, pb);
+          if (IsBf16<T>::value) mma(U[ft], lo, pb);
         }
-    } else {
-#pragma unroll
-      for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (kb + sub * 16 + i < a.N) {
-            const float e = exp2_fast(fmaf(s[sub][i], a.c1, nm));
-            Z += e;
-            LS = fmaf(e, log2_fast(av[sub][i] * rden), LS);
-          }
+      }
     }
   }
-  // merge the four lane groups of each query
-#pragma unroll
-  for (int off = 16; off <= 32; off <<= 1) {
-    const float om = __shfl_xor(mx, off), oz = __shfl_xor(Z, off), ol = __shfl_xor(LS, off);
-    const float M = fmaxf(mx, om);
-    const float f1 = mx == -INFINITY ? 0.f : exp2_fast(mx - M);
-    const float f2 = om == -INFINITY ? 0.f : exp2_fast(om - M);
-    Z = Z * f1 + oz * f2;
-    LS = LS * f1 + ol * f2;
-    mx = M;
-  }
+  // the four lane groups of a query share its maximum: plain sums
+  Z += __shfl_xor(Z, 16);
+  Z += __shfl_xor(Z, 32);
+  LS += __shfl_xor(LS, 16);
+  LS += __shfl_xor(LS, 32);
   if (g == 0) {
     if (qok)
       reinterpret_cast<float2*>(a.stats)[(size_t)bh * a.N + q] =
           make_float2(mx + log2_fast(Z) + a.log2n, rden * a.inv_n);
     LP[w * 16 + r] = qok ? -LN2 * LS / Z : 0.f;
+  }
+  if (DPHI) {
+    IO* dst = static_cast<IO*>(a.dphq) + (size_t)bh * a.N * F;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float zi = __shfl(Z, 4 * g + i), ri = __shfl(rden, 4 * g + i);
+      const float iz = 1.0f / zi;
+      const int row = tile * AWD_TILE + w * 16 + 4 * g + i;
+#pragma unroll
+      for (int ft = 0; ft < F / 16; ++ft) {
+        const float v = a.inv_n * (ri * z[ft * 16 + r] - U[ft][i] * iz);
+        if (row < a.N) dst[(size_t)row * F + ft * 16 + r] = float_to_io<IO>(v);
+      }
+    }
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -248,14 +282,13 @@ void k_awd_fwd(AwdArgs a) {
   }
 }
 
-// Gradient pass for one side: MODE 0 computes dphi(Q) for a 64-query tile
-// (streaming key tiles), MODE 1 dphi(K) for a 64-key tile (streaming query
-// tiles, with their statistics).  G = (1/N)(1/den - P/A) per pair, then
-// dphi(own) += G . Phi(streamed) on MFMA with the streamed features read
-// through the transpose load.
-template <class T, int D, int F, int MODE>
+// Key-side gradient pass: dphi(K) for a 64-key tile, streaming the query tiles
+// with their statistics.  G = (1/N)(1/den - P/A) per pair, then
+// dphi(K) += G^T . Phi(Q) on MFMA with the streamed features read through the
+// transpose load.  (dphi(Q) comes out of the loss pass.)
+template <class T, int D, int F>
 __global__ __launch_bounds__(AWD_NT) __attribute__((amdgpu_waves_per_eu(AwdOcc<T, D, F, true>::value)))
-void k_awd_bwd(AwdArgs a) {
+void k_awd_bwd_k(AwdArgs a) {
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, AWD_NT> StX;
   typedef RowStage<IO, F, AWD_NT> StP;
@@ -266,18 +299,16 @@ void k_awd_bwd(AwdArgs a) {
   const int tile = wc.seg, bh = wc.bh;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const size_t xo = (size_t)bh * a.N * D, po = (size_t)bh * a.N * F;
-  const IO* Xown = static_cast<const IO*>(MODE == 0 ? a.Q : a.K) + xo;
-  const IO* Pown = static_cast<const IO*>(MODE == 0 ? a.phq : a.phk) + po;
-  const IO* Xoth = static_cast<const IO*>(MODE == 0 ? a.K : a.Q) + xo;
-  const IO* Poth = static_cast<const IO*>(MODE == 0 ? a.phk : a.phq) + po;
+  const IO* Xown = static_cast<const IO*>(a.K) + xo;
+  const IO* Pown = static_cast<const IO*>(a.phk) + po;
+  const IO* Xoth = static_cast<const IO*>(a.Q) + xo;
+  const IO* Poth = static_cast<const IO*>(a.phq) + po;
   const float2* stats = reinterpret_cast<const float2*>(a.stats) + (size_t)bh * a.N;
   const int o = tile * AWD_TILE + w * 16 + r;
   const bool ook = o < a.N;
   Frag<T> xf[D / 32], pf[F / 32];
   own_frags<T, D>(xf, Xown, o, ook);
   own_frags<T, F>(pf, Pown, o, ook);
-  float2 qst = make_float2(0.f, 0.f);
-  if (MODE == 0 && ook) qst = stats[o];
   f32x4 acc[F / 16];
 #pragma unroll
   for (int ft = 0; ft < F / 16; ++ft) acc[ft] = zero4();
@@ -287,18 +318,18 @@ void k_awd_bwd(AwdArgs a) {
   float2 sr = make_float2(0.f, 0.f);
   sx.fetch(Xoth, 0, a.N);
   sp.fetch(Poth, 0, a.N);
-  if (MODE == 1 && threadIdx.x < AWD_TILE && (int)threadIdx.x < a.N) sr = stats[threadIdx.x];
+  if (threadIdx.x < AWD_TILE && (int)threadIdx.x < a.N) sr = stats[threadIdx.x];
   for (int ot = 0; ot < a.ntile; ++ot) {
     __syncthreads();
     sx.store(XL);
     sp.store(PL);
-    if (MODE == 1 && threadIdx.x < AWD_TILE) SL[threadIdx.x] = sr;
+    if (threadIdx.x < AWD_TILE) SL[threadIdx.x] = sr;
     __syncthreads();
     if (ot + 1 < a.ntile) {
       const int n1 = (ot + 1) * AWD_TILE;
       sx.fetch(Xoth, n1, a.N);
       sp.fetch(Poth, n1, a.N);
-      if (MODE == 1 && threadIdx.x < AWD_TILE)
+      if (threadIdx.x < AWD_TILE)
         sr = n1 + (int)threadIdx.x < a.N ? stats[n1 + threadIdx.x] : make_float2(0.f, 0.f);
     }
     f32x4 s[4], av[4];
@@ -309,7 +340,7 @@ void k_awd_bwd(AwdArgs a) {
     for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float2 st = MODE == 0 ? qst : SL[sub * 16 + 4 * g + i];
+        const float2 st = SL[sub * 16 + 4 * g + i];
         const float p = exp2_fast(s[sub][i] * a.c1 - st.x);
         const float gv = st.y - p * rcp_fast(av[sub][i]);
         G[sub][i] = (ook && ob + sub * 16 + i < a.N) ? gv : 0.f;
@@ -326,7 +357,7 @@ void k_awd_bwd(AwdArgs a) {
   }
   // dphi is stored in the io dtype: its rounding (2^-9 relative on the bf16
   // path) is below that of the bf16 features the passes already use
-  IO* dst = static_cast<IO*>(MODE == 0 ? a.dphq : a.dphk) + po;
+  IO* dst = static_cast<IO*>(a.dphk) + po;
 #pragma unroll
   for (int ft = 0; ft < F / 16; ++ft)
 #pragma unroll
@@ -528,14 +559,14 @@ hipError_t run_awd(const AwdArgs& a, bool ns, bool grads, hipStream_t st) {
   const int nwg = a.BH * a.ntile;
   k_awd_colsum<IO, F><<<a.BH, 256, 0, st>>>(static_cast<const IO*>(a.phk), a.z, a.N);
   timing_mark(KC_AWD_FWD, st, true);
-  k_awd_fwd<T, D, F><<<nwg, AWD_NT, 0, st>>>(a);
+  if (grads)
+    k_awd_fwd<T, D, F, true><<<nwg, AWD_NT, 0, st>>>(a);   // loss and dphi(Q)
+  else
+    k_awd_fwd<T, D, F, false><<<nwg, AWD_NT, 0, st>>>(a);
   timing_mark(KC_AWD_FWD, st, false);
   if (grads) {
-    timing_mark(KC_AWD_BWD_Q, st, true);
-    k_awd_bwd<T, D, F, 0><<<nwg, AWD_NT, 0, st>>>(a);
-    timing_mark(KC_AWD_BWD_Q, st, false);
     timing_mark(KC_AWD_BWD_K, st, true);
-    k_awd_bwd<T, D, F, 1><<<nwg, AWD_NT, 0, st>>>(a);
+    k_awd_bwd_k<T, D, F><<<nwg, AWD_NT, 0, st>>>(a);
     timing_mark(KC_AWD_BWD_K, st, false);
     const dim3 wg(a.H, a.parts);
     timing_mark(KC_AWD_WGRAD, st, true);

@@ -84,8 +84,7 @@ struct BwdArgs {
 void timing_mark(int kernel_class, hipStream_t st, bool begin);
 enum KernelClass { KC_FWD_STATE = 1, KC_FWD_SWEEP = 2, KC_SCAN = 3, KC_BWD_PREPASS = 4,
                    KC_BWD_DQ = 5, KC_BWD_DKV = 6, KC_BWD_REDUCE = 7, KC_FEATURE_MAP = 8,
-                   KC_DECODE = 9, KC_AWD_FWD = 10, KC_AWD_BWD_Q = 11, KC_AWD_BWD_K = 12,
-                   KC_AWD_WGRAD = 13 };
+                   KC_DECODE = 9, KC_AWD_FWD = 10, KC_AWD_BWD_K = 11, KC_AWD_WGRAD = 12 };
 
 // One decode step: one new token per (b,h) slice against a caller-owned state.
 struct DecodeArgs {
