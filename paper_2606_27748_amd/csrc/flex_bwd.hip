@@ -228,6 +228,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
+    // this chunk's projection fragments: in flight across the staging barriers
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sdo.store(XDO); so.store(XO);
     sv.store(XV);
@@ -257,8 +260,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
       }
     }
     __syncthreads();
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
     // both feature maps enter only the token sums: token-row features, no
     // transpose; the key side and the query side one after the other
 #pragma unroll
@@ -368,6 +369,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
+    // this chunk's projection fragments: in flight across the staging barriers
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
     __syncthreads();
     sq.store(XQ, SSQ);
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
@@ -382,8 +386,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     }
     __syncthreads();
 
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
     // phi(K) of this wave's features enters only contractions over the key
     // tokens: token-row fragments (k = tokens), no transpose
     Frag<T> pk[SH::KT][SH::FC];
@@ -564,7 +566,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;
   constexpr int QG = (NW >= 8 || D >= 128) ? 1 : 2;
-  constexpr int RP = (D > SH::DV ? D : SH::DV) + 4;
+  constexpr int RP = SH::DV + 4;                 // row stride of the dV reduction rows
   constexpr int RLP = SH::DV + 4;                // row stride of the bf16 R' copy, [feature][value col]
   constexpr int LDP = SH::FC * 16 + 4;           // row stride of the per-wave [token][row] blocks
   constexpr int RED_BYTES = NW * QG * 16 * RP * 4;
@@ -579,6 +581,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   __shared__ float GS[SH::CH][2];
   __shared__ float SSQ[SH::CH], SSK[SH::CH];
   __shared__ float TRED[SH::NT];
+  __shared__ __attribute__((aligned(16))) float GP[SH::CH][NW][4];   // per-lane-group shares of g
   typedef float RedRow[QG * 16][RP];
   RedRow* RED = reinterpret_cast<RedRow*>(REDRL);
   T* RL = reinterpret_cast<T*>(REDRL);
@@ -606,7 +609,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag_kv, h, NW, w);
-  const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag_kv, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   f32x4 RT[SH::DVT1][SH::FC];
@@ -624,6 +626,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 
   for (int c = c1 - 1; c >= c0; --c) {
     const int tok0 = c * SH::CH;
+    // this chunk's projection fragments: in flight across the staging barriers
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
@@ -636,8 +641,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     }
     __syncthreads();
 
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
     // phi(Q)/den as [token][feature] in the wave's LDS block: read back as it is
     // for the intra-chunk kernel matrix, transposed for the token sums (the
     // non-causal backward of K and V uses only the total R')
@@ -820,67 +823,72 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       }
       gp[tt] = gs;   // this lane group's share; the four shares are summed in the dK reduction
     }
-    // dK = sum over waves of dP W' + (2/c) g k, g = <phi(K), dphi(K)>; dtau -= g ||k||^2 / c
-    WTS wt;
-    wt.load_frags(wdx);
+    // dK = dP W' over all projection rows + (2/c) g k, g = <phi(K), dphi(K)>;
+    // dtau -= g ||k||^2 / c.  Each wave computes whole output tiles (d tile,
+    // token tile) from every wave's dP block and that wave's dX fragments, so
+    // no cross-wave reduction is needed.  Wave w takes the d tiles
+    // dt = w mod DT (+ NW, ...) and, when there are fewer d tiles than waves,
+    // the token tiles tt = w / DT (+ NW / DT, ...).  The dX fragments of its
+    // first d tile are loaded before the barrier, so their latency overlaps it.
+    Frag<T> wf[NW][WTS::KP][WTS::NSPLIT];
+    auto load_wf = [&](int dt) {
 #pragma unroll
-    for (int q0 = 0; q0 < SH::TT; q0 += QG) {
-      __syncthreads();
-#pragma unroll
-      for (int qq = 0; qq < QG; ++qq) {
-        const int tt = q0 + qq;
-        Frag<T> dpp[WTS::KP];
+      for (int ww = 0; ww < NW; ++ww) {
+        const Frag<T>* wd = FragBlock<T, D, FW, NS>::dx(a.wfrag_kv, h, NW, ww);
 #pragma unroll
         for (int ks = 0; ks < WTS::KP; ++ks)
-          dpp[ks] = pair_tiles<T>(dp[2 * ks][tt], 2 * ks + 1 < SH::PR ? dp[2 * ks + 1][tt] : zero4());
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          f32x4 acc = zero4();
-#pragma unroll
-          for (int ks = 0; ks < WTS::KP; ++ks)
-#pragma unroll
-            for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wt.w[sp][dt][ks], dpp[ks]);
-          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = acc;
-        }
-        RED[w][qq * 16 + r][D + g] = gp[tt];
+          for (int sp = 0; sp < WTS::NSPLIT; ++sp) wf[ww][ks][sp] = wd[((sp * DT + dt) * WTS::KP + ks) * WAVE + l];
       }
-      __syncthreads();
-      constexpr int C4 = D / 4;
-      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
-        const int t = it / C4, c4 = it % C4;
-        const int tl = q0 * 16 + t;
-        const int tok = tok0 + tl;
-        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-        float gg = 0.f;
-#pragma unroll
-        for (int ww = 0; ww < NW; ++ww) {
-          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
-          s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-          gg += (RED[ww][t][D] + RED[ww][t][D + 1]) + (RED[ww][t][D + 2] + RED[ww][t][D + 3]);
-        }
-        if (tok < a.N) {
-          const float k2 = 2.0f * inv_c * gg;
-          const IO* kr = XK + tl * StX::LD + 4 * c4;
-          s.x += k2 * io_to_float(kr[0]);
-          s.y += k2 * io_to_float(kr[1]);
-          s.z += k2 * io_to_float(kr[2]);
-          s.w += k2 * io_to_float(kr[3]);
-          float4* o = reinterpret_cast<float4*>(dK + (size_t)tok * D + 4 * c4);
-          if (a.acc) {
-            const float4 p = *o;
-            s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
-          }
-          *o = s;
-          if (c4 == 0) dtau_acc -= gg * SSK[tl] * inv_c;
-        }
-      }
-    }
-    __syncthreads();  // every wave is done with phi(Q)^T
+    };
+    load_wf(w % DT);
+    // dP of this wave as [token][projection row] in its LDS block (its own reads
+    // of phi(Q)/den there are done: one wave's LDS accesses complete in order),
+    // and this lane's share of g per token
 #pragma unroll
     for (int pr = 0; pr < SH::PR; ++pr)
 #pragma unroll
       for (int tt = 0; tt < SH::TT; ++tt) store_tile_nm<T>(PT[w], LDP, tt * 16, pr * 16, dp[pr][tt]);
-    __syncthreads();
+#pragma unroll
+    for (int tt = 0; tt < SH::TT; ++tt) GP[tt * 16 + r][w][g] = gp[tt];
+    __syncthreads();   // every wave's dP block and g shares complete
+    constexpr int TT0STEP = DT < NW ? NW / DT : 1;
+    for (int dt = w % DT; dt < DT; dt += NW) {
+      if (dt != w % DT) load_wf(dt);
+      for (int tt = DT < NW ? w / DT : 0; tt < SH::TT; tt += TT0STEP) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) {
+#pragma unroll
+        for (int ks = 0; ks < WTS::KP; ++ks) {
+          Frag<T> b = load_frag_nm<T>(PT[ww], LDP, tt * 16, (2 * ks) * 16, (2 * ks + 1) * 16);
+          if (2 * ks + 1 >= SH::PR) {   // no second row tile: keep unwritten LDS out of the product
+#pragma unroll
+            for (int j = 4; j < 8; ++j) b.set(j, 0.f);
+          }
+#pragma unroll
+          for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wf[ww][ks][sp], b);
+        }
+      }
+      const int tl = tt * 16 + r, tok = tok0 + tl;
+      float gg = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) {
+        const float4 v = *reinterpret_cast<const float4*>(&GP[tl][ww][0]);
+        gg += (v.x + v.y) + (v.z + v.w);
+      }
+      if (tok < a.N) {
+        const float k2 = 2.0f * inv_c * gg;
+        const IO* kr = XK + tl * StX::LD + dt * 16 + 4 * g;
+        f32x4 s;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s[i] = acc[i] + k2 * io_to_float(kr[i]);
+        f32x4* o = reinterpret_cast<f32x4*>(dK + (size_t)tok * D + dt * 16 + 4 * g);
+        *o = a.acc ? *o + s : s;   // later frequency groups add their share
+        if (dt == 0 && g == 0) dtau_acc -= gg * SSK[tl] * inv_c;
+      }
+      }
+    }
     {
       f32x4 dw[SH::PR][DT];
 #pragma unroll

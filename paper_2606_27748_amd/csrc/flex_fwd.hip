@@ -68,6 +68,9 @@ void k_fwd_state(FwdArgs a) {
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
+    // this chunk's projection fragments: in flight across the staging barriers
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
     __syncthreads();
     if (STX)
       sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
@@ -77,8 +80,6 @@ void k_fwd_state(FwdArgs a) {
       sv.fetch(V, tok0 + CHUNK, a.N);
     }
     __syncthreads();
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
     if constexpr (STX) {
       // phi(K) with the tokens as the contraction index, straight from registers
 #pragma unroll
@@ -246,9 +247,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       if (CAUSAL) sv.fetch(V, tok0 + CHUNK, a.N);
     }
     __syncthreads();
-
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
+
     Frag<T> pq[SH::FT][TT];
     Frag<T> pk[CAUSAL ? SH::FT : 1][TT];
 #pragma unroll
