@@ -88,6 +88,15 @@ __device__ __forceinline__ Frag<T> delta_rows(const float (*GS)[2], int ks) {
   return f;
 }
 
+// Per-token (1/den, delta) of token tok0 + (thread mod ch), loaded from a
+// clamped in-range index so that the load is unconditional (ok: the thread
+// holds a token of the chunk below n; others are zeroed where they are stored).
+__device__ __forceinline__ float2 load_gs(const float* gst, int tok0, int n, int ch, bool& ok) {
+  const int t = tok0 + (int)(threadIdx.x % ch);
+  ok = (int)threadIdx.x < ch && t < n;
+  return *reinterpret_cast<const float2*>(gst + (size_t)min(t, n - 1) * 2);
+}
+
 // Register-dump layout of the [dv' x features] states: tile (dt, global feature
 // tile w*FC + fc), lane, 4 floats.  It does not depend on how the waves split
 // the frequencies, so kernels with different splits share the states.
@@ -213,7 +222,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   if (c0 < c1) {
     sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
     sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N); so.fetch(Ob, c0 * SH::CH, a.N);
-    if (threadIdx.x < SH::CH && c0 * SH::CH + (int)threadIdx.x < a.N) dn_next = den[c0 * SH::CH + threadIdx.x];
+    dn_next = den[min(c0 * SH::CH + (int)(threadIdx.x % SH::CH), a.N - 1)];   // rows past N unused
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
@@ -239,7 +248,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
       const int t1 = tok0 + SH::CH;
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N);
       sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N); so.fetch(Ob, t1, a.N);
-      dn_next = (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N) ? den[t1 + threadIdx.x] : 0.f;
+      dn_next = den[min(t1 + (int)(threadIdx.x % SH::CH), a.N - 1)];   // unconditional: no wait on the load
     }
     __syncthreads();
     // per-token 1/den and delta = dO . O
@@ -338,11 +347,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   StX sq, sk;
   StV sv, sdo;
   float2 gs_next = make_float2(0.f, 0.f);
+  bool gs_ok = false;
   if (c0 < c1) {
     sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
     sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N);
-    if (threadIdx.x < SH::CH && c0 * SH::CH + (int)threadIdx.x < a.N)
-      gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(c0 * SH::CH + threadIdx.x) * 2);
+    gs_next = load_gs(gst, c0 * SH::CH, a.N, SH::CH, gs_ok);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, w);
@@ -376,13 +385,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     sq.store(XQ, SSQ);
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV); sdo.store(XDO);
-    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
+    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
     if (c + 1 < c1) {
       const int t1 = tok0 + SH::CH;
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-      gs_next = (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N)
-                    ? *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2)
-                    : make_float2(0.f, 0.f);
+      gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
     }
     __syncthreads();
 
@@ -602,11 +609,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   StX sq, sk;
   StV sv, sdo;
   float2 gs_next = make_float2(0.f, 0.f);
+  bool gs_ok = false;
   if (c0 < c1) {
     const int t1 = (c1 - 1) * SH::CH;
     sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-    if (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N)
-      gs_next = *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2);
+    gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag_kv, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
@@ -631,13 +638,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     fs.load_frags(wproj);
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
-    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_next.x; GS[threadIdx.x][1] = gs_next.y; }
+    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
     if (c - 1 >= c0) {
       const int t1 = tok0 - SH::CH;
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-      gs_next = (threadIdx.x < SH::CH && t1 + (int)threadIdx.x < a.N)
-                    ? *reinterpret_cast<const float2*>(gst + (size_t)(t1 + threadIdx.x) * 2)
-                    : make_float2(0.f, 0.f);
+      gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
     }
     __syncthreads();
 

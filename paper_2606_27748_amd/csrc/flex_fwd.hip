@@ -239,6 +239,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       if (CAUSAL) sk.store(XK, SSK);
     }
     if (CAUSAL) sv.store(XV);
+    __syncthreads();
+    FreqSlice<T, D, FW, NS> fs;
+    fs.load_frags(wproj);
+    // next chunk's rows, issued after the fragments: loads retire in order, so
+    // the wait for the fragments does not wait for them
     if (c + 1 < c1) {
       if (STX) {
         sq.fetch(Q, tok0 + CHUNK, a.N);
@@ -246,9 +251,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       }
       if (CAUSAL) sv.fetch(V, tok0 + CHUNK, a.N);
     }
-    __syncthreads();
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
 
     Frag<T> pq[SH::FT][TT];
     Frag<T> pk[CAUSAL ? SH::FT : 1][TT];

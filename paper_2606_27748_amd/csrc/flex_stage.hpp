@@ -18,18 +18,27 @@ struct RowStage {
   static constexpr int LD = COLS + VEC;                  // LDS row stride (elements), keeps 16 B alignment
   static constexpr int LDS_ELEMS = ROWS * LD;
   uint4 r[PER];
+  uint32_t okm;   // bit i: vector i belongs to this thread and to a row below n
 
-  // rows: this (b,h) slice's [N, COLS] rows; rows at or beyond n read as zero
+  // rows: this (b,h) slice's [N, COLS] rows; rows at or beyond n read as zero.
+  // The loads are unconditional, from a clamped in-range row, so that nothing
+  // writes their destination registers while they are in flight (a zeroing
+  // branch would make the compiler wait for each load right away); the
+  // out-of-range vectors are zeroed when they are stored.  n >= 1.
   __device__ __forceinline__ void fetch(const IO* __restrict__ rows, int tok0, int n) {
+    okm = 0u;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int v = threadIdx.x + i * NT;
+      const int v0 = threadIdx.x + i * NT;
+      const int v = v0 < NV ? v0 : NV - 1;
       const int t = v / VPR, c = v % VPR;
-      if (v < NV && tok0 + t < n)
-        r[i] = *reinterpret_cast<const uint4*>(rows + (size_t)(tok0 + t) * COLS + c * VEC);
-      else
-        r[i] = make_uint4(0u, 0u, 0u, 0u);
+      const int row = tok0 + t < n ? tok0 + t : n - 1;
+      r[i] = *reinterpret_cast<const uint4*>(rows + (size_t)row * COLS + c * VEC);
+      if (v0 < NV && tok0 + t < n) okm |= 1u << i;
     }
+  }
+  __device__ __forceinline__ uint4 vec(int i) const {
+    return ((okm >> i) & 1u) ? r[i] : make_uint4(0u, 0u, 0u, 0u);
   }
   __device__ __forceinline__ void store(IO* lds) const {
 #pragma unroll
@@ -37,7 +46,7 @@ struct RowStage {
       const int v = threadIdx.x + i * NT;
       if (v < NV) {
         const int t = v / VPR, c = v % VPR;
-        *reinterpret_cast<uint4*>(lds + t * LD + c * VEC) = r[i];
+        *reinterpret_cast<uint4*>(lds + t * LD + c * VEC) = vec(i);
       }
     }
   }
@@ -56,10 +65,11 @@ struct RowStage {
       float s = 0.f;
       if (v < NV) {
         const int t = v / VPR, c = v % VPR;
-        *reinterpret_cast<uint4*>(lds + t * LD + c * VEC) = r[i];
-        const IO* e = reinterpret_cast<const IO*>(&r[i]);
+        const uint4 x = vec(i);
+        *reinterpret_cast<uint4*>(lds + t * LD + c * VEC) = x;
+        const IO* e = reinterpret_cast<const IO*>(&x);
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) { const float x = io_to_float(e[j]); s += x * x; }
+        for (int j = 0; j < VEC; ++j) { const float y = io_to_float(e[j]); s += y * y; }
       }
       s = lane_sum<VPR>(s);
       if (v < NV && v % VPR == 0) out[v / VPR] = f(v / VPR, s);
@@ -73,7 +83,8 @@ struct RowStage {
       const int v = threadIdx.x + i * NT;
       if (v < NV) {
         const int t = v / VPR, c = v % VPR;
-        const IO* e = reinterpret_cast<const IO*>(&r[i]);
+        const uint4 x = vec(i);
+        const IO* e = reinterpret_cast<const IO*>(&x);
 #pragma unroll
         for (int j = 0; j < VEC; ++j) ldsT[(c * VEC + j) * LDT + t] = io_to_op<T>(e[j]);
       }
