@@ -233,15 +233,19 @@ struct FreqSlice {
 };
 
 // A-operand fragments of W'^T (rows = input dimension d, k = projection rows of
-// this wave, paired tiles) in radians, bf16 hi + lo on the bf16 path.  Used for
+// this wave, paired tiles) in radians, in the operand type.  Used for
 // dX = dP W'.  Projection row tile pr < FT is W'1 (or W), pr >= FT is W'2.
+// One term (no hi + lo split, unlike the projection fragments): dP is itself
+// rounded to the operand type in this product, and a relative rounding of W'
+// of the same size only enters dX linearly, whereas the projection's phase
+// error is multiplied by |P| inside the trigonometric functions.
 template <class T, int D, int FW, bool NS>
 struct WTSlice {
   static constexpr int FT = FW / 16;
   static constexpr int PR = NS ? 2 * FT : FT;
   static constexpr int KP = (PR + 1) / 2;      // k-steps over the projection rows
   static constexpr int DT = D / 16;
-  static constexpr int NSPLIT = IsBf16<T>::value ? 2 : 1;
+  static constexpr int NSPLIT = 1;
   Frag<T> w[NSPLIT][DT][KP];
 
   __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
@@ -265,13 +269,7 @@ struct WTSlice {
               v = x;
             }
           }
-          if (IsBf16<T>::value) {
-            const float hi = (float)(__bf16)v;
-            w[0][dt][ks].set(j, hi);
-            w[NSPLIT - 1][dt][ks].set(j, v - hi);
-          } else {
-            w[0][dt][ks].set(j, v);
-          }
+          w[0][dt][ks].set(j, v);   // rounded to the operand type (RNE)
         }
       }
     }
