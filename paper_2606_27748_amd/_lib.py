@@ -52,6 +52,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         raise FileNotFoundError(
             f"{path} not found: build it with `python -m paper_2606_27748_amd.build` "
             "or __graft_entry__.build()")
+    # The calls take device pointers and streams from torch, so the library must
+    # bind to the HIP runtime torch loads (torch ships its own copy): importing
+    # torch first makes the dynamic linker reuse that runtime.  Loaded the other
+    # way round, torch brings a second runtime whose streams the library's
+    # launches reject.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P, S, I = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
     D = ctypes.POINTER(flex_desc)
