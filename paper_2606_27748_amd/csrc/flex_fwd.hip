@@ -32,13 +32,9 @@ void k_fwd_state(FwdArgs a) {
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, SH::NT> StK;
   typedef RowStage<IO, SH::DV, SH::NT> StV;
-  constexpr bool STX = SH::STAGE_X;
-  __shared__ __attribute__((aligned(16))) IO XK[STX ? StK::LDS_ELEMS : 8];
+  __shared__ __attribute__((aligned(16))) IO XK[StK::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) float SCK[CHUNK];   // staged: per-token scale s e(k)
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];   // [token][value col]
-  // d = 128 (rows read from global memory): phi(K) as [token][feature], read back transposed
-  constexpr int LDP = SH::FC * 16 + 4;
-  __shared__ __attribute__((aligned(16))) T PT[STX ? 1 : NW][STX ? 8 : CHUNK * LDP];
 
   const WgCoord wc = wg_coord(a.segments * a.sub, a.H, a.BH);   // seg: sub-segment
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -52,7 +48,7 @@ void k_fwd_state(FwdArgs a) {
   StK sk;
   StV sv;
   if (c0 < c1) {
-    if (STX) sk.fetch(K, c0 * CHUNK, a.N);
+    sk.fetch(K, c0 * CHUNK, a.N);
     sv.fetch(V, c0 * CHUNK, a.N);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
@@ -64,7 +60,7 @@ void k_fwd_state(FwdArgs a) {
 #pragma unroll
     for (int dt = 0; dt < SH::DVT1; ++dt) S[fc][dt] = zero4();
   const Frag<T> ones = ones_col0<T>();
-  const int r = (threadIdx.x % WAVE) % 16, g = (threadIdx.x % WAVE) / 16;
+  const int g = (threadIdx.x % WAVE) / 16;
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
@@ -72,54 +68,26 @@ void k_fwd_state(FwdArgs a) {
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
     __syncthreads();
-    if (STX)
-      sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
+    sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV);
     if (c + 1 < c1) {
-      if (STX) sk.fetch(K, tok0 + CHUNK, a.N);
+      sk.fetch(K, tok0 + CHUNK, a.N);
       sv.fetch(V, tok0 + CHUNK, a.N);
     }
     __syncthreads();
-    if constexpr (STX) {
-      // phi(K) with the tokens as the contraction index, straight from registers
+    // phi(K) with the tokens as the contraction index, straight from registers
 #pragma unroll
-      for (int ks = 0; ks < SH::KT; ++ks) {
-        Frag<T> pk[SH::FC];
-        feature_frags_rows<T, D, FW, NS, StK::LD>(fs, XK, SCK, ks, pk);
-        Frag<T> vf[SH::DVT];
+    for (int ks = 0; ks < SH::KT; ++ks) {
+      Frag<T> pk[SH::FC];
+      feature_frags_rows<T, D, FW, NS, StK::LD>(fs, XK, SCK, ks, pk);
+      Frag<T> vf[SH::DVT];
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
+      for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
 #pragma unroll
-        for (int fc = 0; fc < SH::FC; ++fc) {
+      for (int fc = 0; fc < SH::FC; ++fc) {
 #pragma unroll
-          for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk[fc], vf[dt]);
-          mma(S[fc][SH::DVT], pk[fc], ones);
-        }
-      }
-    } else {
-#pragma unroll
-      for (int tt = 0; tt < TT; ++tt) {
-        f32x4 p[SH::PR];
-        float ssq;
-        project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
-        const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
-#pragma unroll
-        for (int ft = 0; ft < SH::FT; ++ft)
-          store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16,
-                           features<T, SH::FT, NS>(p, ft, sc));
-      }
-#pragma unroll
-      for (int ks = 0; ks < SH::KT; ++ks) {
-        Frag<T> vf[SH::DVT];
-#pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
-#pragma unroll
-        for (int fc = 0; fc < SH::FC; ++fc) {
-          const Frag<T> pk = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16);
-#pragma unroll
-          for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk, vf[dt]);
-          mma(S[fc][SH::DVT], pk, ones);
-        }
+        for (int dt = 0; dt < SH::DVT; ++dt) mma(S[fc][dt], pk[fc], vf[dt]);
+        mma(S[fc][SH::DVT], pk[fc], ones);
       }
     }
   }
@@ -182,12 +150,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, SH::NT> StX;
   typedef RowStage<IO, SH::DV, SH::NT> StV;
-  constexpr bool STX = SH::STAGE_X;
   constexpr int XV_N = CAUSAL ? StV::LDS_ELEMS : 8;
   constexpr int LDP = SH::FC * 16 + 4;     // [token][feature] rows of a wave's phi(K) block
   constexpr int PT_N = CAUSAL ? CHUNK * LDP : 8;
-  __shared__ __attribute__((aligned(16))) IO XQ[STX ? StX::LDS_ELEMS : 8];
-  __shared__ __attribute__((aligned(16))) IO XK[(STX && CAUSAL) ? StX::LDS_ELEMS : 8];
+  __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK[CAUSAL ? StX::LDS_ELEMS : 8];
   __shared__ float SSQ[CHUNK], SSK[CHUNK];
   __shared__ __attribute__((aligned(16))) IO XV[XV_N];   // [token][value col]
   __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
@@ -209,10 +176,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   StX sq, sk;
   StV sv;
   if (c0 < c1) {
-    if (STX) {
-      sq.fetch(Q, c0 * CHUNK, a.N);
-      if (CAUSAL) sk.fetch(K, c0 * CHUNK, a.N);
-    }
+    sq.fetch(Q, c0 * CHUNK, a.N);
+    if (CAUSAL) sk.fetch(K, c0 * CHUNK, a.N);
     if (CAUSAL) sv.fetch(V, c0 * CHUNK, a.N);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
@@ -234,10 +199,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
     __syncthreads();
-    if (STX) {
-      sq.store(XQ, SSQ);
-      if (CAUSAL) sk.store(XK, SSK);
-    }
+    sq.store(XQ, SSQ);
+    if (CAUSAL) sk.store(XK, SSK);
     if (CAUSAL) sv.store(XV);
     __syncthreads();
     FreqSlice<T, D, FW, NS> fs;
@@ -245,10 +208,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     // next chunk's rows, issued after the fragments: loads retire in order, so
     // the wait for the fragments does not wait for them
     if (c + 1 < c1) {
-      if (STX) {
-        sq.fetch(Q, tok0 + CHUNK, a.N);
-        if (CAUSAL) sk.fetch(K, tok0 + CHUNK, a.N);
-      }
+      sq.fetch(Q, tok0 + CHUNK, a.N);
+      if (CAUSAL) sk.fetch(K, tok0 + CHUNK, a.N);
       if (CAUSAL) sv.fetch(V, tok0 + CHUNK, a.N);
     }
 
@@ -258,18 +219,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     for (int tt = 0; tt < TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      if (STX)
-        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
-      else
-        project_tile<T, D, FW, NS>(fs, Q, tok0 + tt * 16, a.N, p, ssq);
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) pq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
       if (CAUSAL) {
-        if (STX)
-          project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
-        else
-          project_tile<T, D, FW, NS>(fs, K, tok0 + tt * 16, a.N, p, ssq);
+        project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
         sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft) {

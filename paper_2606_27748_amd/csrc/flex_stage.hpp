@@ -146,9 +146,6 @@ struct Shape {
   // LDS row strides (elements); multiples of 4 keep 8/16-byte alignment
   static constexpr int TPAD = CH + 4;
   static constexpr int RPAD = DVT1 * 16 + 4;
-  // stage the Q/K rows of a chunk through LDS (d = 128 keeps direct loads:
-  // its LDS budget is taken by the larger state operands)
-  static constexpr bool STAGE_X = D <= 64;
 };
 
 // Fragment with 1 in row/column 0 and 0 elsewhere: as the value operand it
