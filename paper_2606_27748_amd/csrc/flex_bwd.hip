@@ -235,11 +235,14 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   const Frag<T> ones = ones_col01<T>();
   constexpr int TPT = SH::NT / SH::CH;  // threads per token for the row reductions
 
+  // projection fragments: held for the whole sweep on the query-side-only
+  // pass at d <= 64, else reloaded per chunk ahead of the staging barriers
+  constexpr bool KEEP_FS = D <= 64 && !WITH_S;
+  FreqSlice<T, D, FW, NS> fs;
+  if (KEEP_FS) fs.load_frags(wproj);
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
-    // this chunk's projection fragments: in flight across the staging barriers
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
+    if (!KEEP_FS) fs.load_frags(wproj);
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sdo.store(XDO); so.store(XO);
     sv.store(XV);

@@ -62,11 +62,14 @@ void k_fwd_state(FwdArgs a) {
   const Frag<T> ones = ones_col0<T>();
   const int g = (threadIdx.x % WAVE) / 16;
 
+  // projection fragments: held for the whole sweep where registers allow
+  // (d <= 64), else reloaded per chunk ahead of the staging barriers
+  constexpr bool KEEP_FS = D <= 64;
+  FreqSlice<T, D, FW, NS> fs;
+  if (KEEP_FS) fs.load_frags(wproj);
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
-    // this chunk's projection fragments: in flight across the staging barriers
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
+    if (!KEEP_FS) fs.load_frags(wproj);
     __syncthreads();
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV);
