@@ -486,8 +486,8 @@ def run_decode(steps, warmup, B=256, H=16, d=64, m=128):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="headline_causal_train_d64")
     ap.add_argument("--all-configs", action="store_true",
                     help="one JSON line per configured workload (no CPU baseline)")

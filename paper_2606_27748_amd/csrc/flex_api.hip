@@ -109,11 +109,21 @@ int fwd_sub_of(const flex_desc* d, int P) {
 }
 
 // Segments per (b,h): enough workgroups to cover the 256 CUs in whole rounds
-// while keeping the per-segment state traffic small.
+// while keeping the per-segment state traffic small.  Costs are in units of
+// one sweep chunk: the sweep's rounds of chunks (a pre-pass adds about a third
+// of a chunk), the hand-off, and the segment states' HBM traffic (written by
+// the pre-pass, read and written by the scan, read by the sweep).  A chunk's
+// time is estimated from its MFMA work relative to the d = 64, m = 128
+// nonstationary shape, measured at about 6.7 us per 64-token chunk.
 int pick_segments(const flex_desc* d) {
   const int nc = nchunks_of(d);
   if (d->segments > 0) return d->segments < nc ? d->segments : nc;
   const long long bh = (long long)d->B * d->H;
+  const KernelShape ks = attn_shape(d);
+  const double m_eff = ks.nonstationary ? 2.0 * ks.m : ks.m;
+  const double work = 2.0 * ks.d * m_eff + 4.0 * ks.m * (d->dv + 1);   // MFMA flop per token
+  const double t_chunk = 6.7e-6 * work / 66048.0;
+  const double state_bytes = (double)fwd_state_floats(ks) * sizeof(float);
   int best = 1;
   double best_cost = 1e30;
   for (int p = 1; p <= nc && p <= 64; ++p) {
@@ -122,8 +132,8 @@ int pick_segments(const flex_desc* d) {
     if (used != p) continue;
     const long long wgs = bh * p;
     const long long rounds = (wgs + kCUs - 1) / kCUs;
-    // sweep chunks per CU + pre-pass (about a third of a sweep chunk) + state hand-off
-    const double cost = rounds * (double)cps * (p > 1 || !d->causal ? 1.35 : 1.0) + 0.5 * p * bh / kCUs;
+    const double traffic = 4.0 * p * bh * state_bytes / 5.0e12 / t_chunk;
+    const double cost = rounds * (double)cps * (p > 1 || !d->causal ? 1.35 : 1.0) + 0.5 * p * bh / kCUs + traffic;
     if (cost < best_cost - 1e-9) { best_cost = cost; best = p; }
   }
   return best;
