@@ -45,7 +45,9 @@
  *     order; its forward workspace holds an fp32 numerator/denominator buffer.
  *   - io_dtype FLEX_F32 computes every contraction in fp32 (MFMA f32);
  *     FLEX_BF16 reads bf16 inputs, projects with a two-term bf16 split of the
- *     frequencies and contracts bf16 features with fp32 accumulation.
+ *     frequencies and contracts bf16 features with fp32 accumulation (the
+ *     backward's dX = dP W' takes the frequencies rounded once to bf16, like
+ *     dP itself).
  */
 #ifndef FLEX_H
 #define FLEX_H
