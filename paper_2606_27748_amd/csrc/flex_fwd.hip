@@ -198,6 +198,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
         S[fc][dt] = *reinterpret_cast<const f32x4*>(in + ((fc * SH::DVT1 + dt) * WAVE + l) * 4);
   }
   const Frag<T> ones = ones_col0<T>();
+  // projection fragments, held for the whole sweep
+  FreqSlice<T, D, FW, NS> fs;
+  fs.load_frags(wproj);
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
@@ -206,10 +209,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     if (CAUSAL) sk.store(XK, SSK);
     if (CAUSAL) sv.store(XV);
     __syncthreads();
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
-    // next chunk's rows, issued after the fragments: loads retire in order, so
-    // the wait for the fragments does not wait for them
+    // next chunk's rows
     if (c + 1 < c1) {
       sq.fetch(Q, tok0 + CHUNK, a.N);
       if (CAUSAL) sk.fetch(K, tok0 + CHUNK, a.N);
