@@ -379,11 +379,14 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     *reinterpret_cast<f32x4*>(&DWL[w][i * 4]) = zero4();
   const Frag<T> ones = ones_col01<T>();
 
+  // projection fragments: held for the whole sweep at d <= 64, else reloaded
+  // per chunk ahead of the staging barriers
+  constexpr bool KEEP_FS = D <= 64;
+  FreqSlice<T, D, FW, NS> fs;
+  if (KEEP_FS) fs.load_frags(wproj);
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
-    // this chunk's projection fragments: in flight across the staging barriers
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
+    if (!KEEP_FS) fs.load_frags(wproj);
     __syncthreads();
     sq.store(XQ, SSQ);
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
