@@ -637,6 +637,20 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     *reinterpret_cast<f32x4*>(&DWL[w][i * 4]) = zero4();
   float dtau_acc = 0.f;
 
+  // dX fragments of this wave's d tile: held for the whole sweep when every
+  // wave has one d tile (DT <= NW), else loaded per chunk ahead of the barrier
+  Frag<T> wf[NW][WTS::KP][WTS::NSPLIT];
+  auto load_wf = [&](int dt) {
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) {
+      const Frag<T>* wd = FragBlock<T, D, FW, NS>::dx(a.wfrag_kv, h, NW, ww);
+#pragma unroll
+      for (int ks = 0; ks < WTS::KP; ++ks)
+#pragma unroll
+        for (int sp = 0; sp < WTS::NSPLIT; ++sp) wf[ww][ks][sp] = wd[((sp * DT + dt) * WTS::KP + ks) * WAVE + l];
+    }
+  };
+  if (DT <= NW) load_wf(w % DT);
   for (int c = c1 - 1; c >= c0; --c) {
     const int tok0 = c * SH::CH;
     // this chunk's projection fragments: in flight across the staging barriers
@@ -841,18 +855,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     // dt = w mod DT (+ NW, ...) and, when there are fewer d tiles than waves,
     // the token tiles tt = w / DT (+ NW / DT, ...).  The dX fragments of its
     // first d tile are loaded before the barrier, so their latency overlaps it.
-    Frag<T> wf[NW][WTS::KP][WTS::NSPLIT];
-    auto load_wf = [&](int dt) {
-#pragma unroll
-      for (int ww = 0; ww < NW; ++ww) {
-        const Frag<T>* wd = FragBlock<T, D, FW, NS>::dx(a.wfrag_kv, h, NW, ww);
-#pragma unroll
-        for (int ks = 0; ks < WTS::KP; ++ks)
-#pragma unroll
-          for (int sp = 0; sp < WTS::NSPLIT; ++sp) wf[ww][ks][sp] = wd[((sp * DT + dt) * WTS::KP + ks) * WAVE + l];
-      }
-    };
-    load_wf(w % DT);
+    if (DT > NW) load_wf(w % DT);
     // dP of this wave as [token][projection row] in its LDS block (its own reads
     // of phi(Q)/den there are done: one wave's LDS accesses complete in order),
     // and this lane's share of g per token
