@@ -1013,9 +1013,11 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FWB, NWB, NS, BWD_CHUNK> SB;
   static_assert(SA::M == SB::M && SA::STATE == SB::STATE, "splits of one shape");
   const dim3 grid(a.segments * a.BH);
-  k_prep_freqs<T, D, FWA, NWA, NS><<<dim3(a.H, NWA, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
-  if (a.wfrag_kv != a.wfrag)
-    k_prep_freqs<T, D, FWB, NWB, NS><<<dim3(a.H, NWB, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag_kv, a.w_stride);
+  if (a.wfrag_kv != a.wfrag)   // both splits' fragments in one launch
+    k_prep_freqs2<T, D, FWA, NWA, FWB, NWB, NS><<<dim3(a.H, NWA > NWB ? NWA : NWB, 4), WAVE, 0, st>>>(
+        a.W1, a.W2, a.wfrag, a.wfrag_kv, a.w_stride);
+  else
+    k_prep_freqs<T, D, FWA, NWA, NS><<<dim3(a.H, NWA, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
   timing_mark(KC_BWD_PREPASS, st, true);
   if (a.fstate)
     k_bwd_prepass<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);

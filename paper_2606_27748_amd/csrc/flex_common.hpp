@@ -313,15 +313,14 @@ struct FragBlock {
 
 // One wave per (head, wave slice, part): part 0 writes the projection
 // fragments, part 1 (launched for the backward only) the dX fragments.
-// Grid (H, NW, parts), 64 threads.
 template <class T, int D, int FW, int NW, bool NS>
-__global__ __launch_bounds__(WAVE) void k_prep_freqs(const float* W1, const float* W2, void* out, int wstride) {
+__device__ __forceinline__ void prep_freqs_part(const float* W1, const float* W2, void* out, int wstride,
+                                                int h, int w, int part) {
   typedef FragBlock<T, D, FW, NS> FBk;
-  const int h = blockIdx.x, w = blockIdx.y;
   const float* W1h = W1 + (size_t)h * wstride;
   const float* W2h = NS ? W2 + (size_t)h * wstride : nullptr;
   Frag<T>* base = static_cast<Frag<T>*>(out) + ((size_t)h * NW + w) * FBk::PER_WAVE;
-  if (blockIdx.z == 0) {
+  if (part == 0) {
     FreqSlice<T, D, FW, NS> fs;
     fs.load(W1h, W2h, w * FW);
     fs.store_frags(base);
@@ -329,6 +328,23 @@ __global__ __launch_bounds__(WAVE) void k_prep_freqs(const float* W1, const floa
     WTSlice<T, D, FW, NS> wt;
     wt.load(W1h, W2h, w * FW);
     wt.store_frags(base + FBk::NP * WAVE);
+  }
+}
+// Grid (H, NW, parts), 64 threads.
+template <class T, int D, int FW, int NW, bool NS>
+__global__ __launch_bounds__(WAVE) void k_prep_freqs(const float* W1, const float* W2, void* out, int wstride) {
+  prep_freqs_part<T, D, FW, NW, NS>(W1, W2, out, wstride, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+// Both parts for two wave splits A and B in one launch: grid (H, max(NWA,
+// NWB), 4); blockIdx.z = 2 * split + part.
+template <class T, int D, int FWA, int NWA, int FWB, int NWB, bool NS>
+__global__ __launch_bounds__(WAVE) void k_prep_freqs2(const float* W1, const float* W2, void* outA, void* outB,
+                                                      int wstride) {
+  const int w = blockIdx.y, part = blockIdx.z % 2;
+  if (blockIdx.z < 2) {
+    if (w < NWA) prep_freqs_part<T, D, FWA, NWA, NS>(W1, W2, outA, wstride, blockIdx.x, w, part);
+  } else {
+    if (w < NWB) prep_freqs_part<T, D, FWB, NWB, NS>(W1, W2, outB, wstride, blockIdx.x, w, part);
   }
 }
 
