@@ -188,9 +188,10 @@ void k_awd_fwd(AwdArgs a) {
     sx.store(XL);
     sp.store(PL);
     __syncthreads();
-    if (kt + 1 < a.ntile) {
-      sx.fetch(K, (kt + 1) * AWD_TILE, a.N);
-      sp.fetch(PK, (kt + 1) * AWD_TILE, a.N);
+    {
+      const int n1 = (kt + 1 < a.ntile ? kt + 1 : kt) * AWD_TILE;   // the last tile refetches itself (unused)
+      sx.fetch(K, n1, a.N);
+      sp.fetch(PK, n1, a.N);
     }
     f32x4 s[4], av[4];
     tile_products<T, D, F, StX::LD, StP::LD>(XL, PL, xf, pf, s, av);
@@ -315,22 +316,24 @@ void k_awd_bwd_k(AwdArgs a) {
 
   StX sx;
   StP sp;
-  float2 sr = make_float2(0.f, 0.f);
   sx.fetch(Xoth, 0, a.N);
   sp.fetch(Poth, 0, a.N);
-  if (threadIdx.x < AWD_TILE && (int)threadIdx.x < a.N) sr = stats[threadIdx.x];
+  // per-row statistics: loaded unconditionally from a clamped row, zeroed past N when stored
+  bool sr_ok = (int)threadIdx.x < a.N;
+  float2 sr = stats[min((int)threadIdx.x % AWD_TILE, a.N - 1)];
   for (int ot = 0; ot < a.ntile; ++ot) {
     __syncthreads();
     sx.store(XL);
     sp.store(PL);
-    if (threadIdx.x < AWD_TILE) SL[threadIdx.x] = sr;
+    if (threadIdx.x < AWD_TILE) SL[threadIdx.x] = sr_ok ? sr : make_float2(0.f, 0.f);
     __syncthreads();
-    if (ot + 1 < a.ntile) {
-      const int n1 = (ot + 1) * AWD_TILE;
+    {
+      const int n1 = (ot + 1 < a.ntile ? ot + 1 : ot) * AWD_TILE;   // the last tile refetches itself (unused)
       sx.fetch(Xoth, n1, a.N);
       sp.fetch(Poth, n1, a.N);
-      if (threadIdx.x < AWD_TILE)
-        sr = n1 + (int)threadIdx.x < a.N ? stats[n1 + threadIdx.x] : make_float2(0.f, 0.f);
+      const int row = n1 + (int)threadIdx.x % AWD_TILE;
+      sr_ok = row < a.N;
+      sr = stats[min(row, a.N - 1)];
     }
     f32x4 s[4], av[4];
     tile_products<T, D, F, StX::LD, StP::LD>(XL, PL, xf, pf, s, av);
@@ -432,11 +435,11 @@ __global__ __launch_bounds__(M / 16 * WAVE) void k_awd_wgrad(AwdArgs a) {
     sx.store(XL, SSQ);
     sd.store(DL);
     __syncthreads();
-    if (u + 1 < u1) {
+    {
       const IO* Xn;
       const IO* dn;
       int nn, sn;
-      rows_of(u + 1, Xn, dn, nn, sn);
+      rows_of(u + 1 < u1 ? u + 1 : u, Xn, dn, nn, sn);   // the last unit refetches itself (unused)
       sx.fetch(Xn, nn, a.N);
       sd.fetch(dn, nn, a.N);
     }

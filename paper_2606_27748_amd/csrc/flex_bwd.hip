@@ -247,11 +247,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     sq.store(XQ, SSQ); sk.store(XK, SSK); sdo.store(XDO); so.store(XO);
     sv.store(XV);
     if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
-    if (c + 1 < c1) {
-      const int t1 = tok0 + SH::CH;
+    {
+      const int t1 = c + 1 < c1 ? tok0 + SH::CH : tok0;   // the last chunk refetches itself (unused)
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N);
       sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N); so.fetch(Ob, t1, a.N);
-      dn_next = den[min(t1 + (int)(threadIdx.x % SH::CH), a.N - 1)];   // unconditional: no wait on the load
+      dn_next = den[min(t1 + (int)(threadIdx.x % SH::CH), a.N - 1)];
     }
     __syncthreads();
     // per-token 1/den and delta = dO . O
@@ -392,8 +392,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV); sdo.store(XDO);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
-    if (c + 1 < c1) {
-      const int t1 = tok0 + SH::CH;
+    {
+      const int t1 = c + 1 < c1 ? tok0 + SH::CH : tok0;   // the last chunk refetches itself (unused)
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
       gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
     }
@@ -659,8 +659,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
-    if (c - 1 >= c0) {
-      const int t1 = tok0 - SH::CH;
+    {
+      const int t1 = c - 1 >= c0 ? tok0 - SH::CH : tok0;   // the last chunk refetches itself (unused)
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
       gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
     }

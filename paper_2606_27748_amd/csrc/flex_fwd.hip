@@ -73,9 +73,10 @@ void k_fwd_state(FwdArgs a) {
     __syncthreads();
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV);
-    if (c + 1 < c1) {
-      sk.fetch(K, tok0 + CHUNK, a.N);
-      sv.fetch(V, tok0 + CHUNK, a.N);
+    {
+      const int t1 = c + 1 < c1 ? tok0 + CHUNK : tok0;   // the last chunk refetches itself (unused)
+      sk.fetch(K, t1, a.N);
+      sv.fetch(V, t1, a.N);
     }
     __syncthreads();
     // phi(K) with the tokens as the contraction index, straight from registers
@@ -210,10 +211,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     if (CAUSAL) sv.store(XV);
     __syncthreads();
     // next chunk's rows
-    if (c + 1 < c1) {
-      sq.fetch(Q, tok0 + CHUNK, a.N);
-      if (CAUSAL) sk.fetch(K, tok0 + CHUNK, a.N);
-      if (CAUSAL) sv.fetch(V, tok0 + CHUNK, a.N);
+    {
+      const int t1 = c + 1 < c1 ? tok0 + CHUNK : tok0;   // the last chunk refetches itself (unused)
+      sq.fetch(Q, t1, a.N);
+      if (CAUSAL) sk.fetch(K, t1, a.N);
+      if (CAUSAL) sv.fetch(V, t1, a.N);
     }
 
     Frag<T> pq[SH::FT][TT];
