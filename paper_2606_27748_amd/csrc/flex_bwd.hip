@@ -582,22 +582,26 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int RP = SH::DV + 4;                 // row stride of the dV reduction rows
   constexpr int RLP = SH::DV + 4;                // row stride of the bf16 R' copy, [feature][value col]
   constexpr int LDP = SH::FC * 16 + 4;           // row stride of the per-wave [token][row] blocks
-  constexpr int RED_BYTES = NW * QG * 16 * RP * 4;
-  constexpr int RL_BYTES = NW * SH::FC * 16 * RLP * (int)sizeof(T);
+  // Each wave owns one slot of REDRL: its bf16 copy of R' and, once its own
+  // reads of that copy are done, its dV partials.  No other wave touches the
+  // slot between the staging barriers and the dV reduction, so neither the
+  // copy nor the partials need a barrier before they are written.
+  constexpr int RED_W = QG * 16 * RP * 4;
+  constexpr int RL_W = SH::FC * 16 * RLP * (int)sizeof(T);
+  constexpr int SLOT = RED_W > RL_W ? RED_W : RL_W;
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // phi(Q)/den, then dP: [token][row]
-  __shared__ __attribute__((aligned(16))) char REDRL[RED_BYTES > RL_BYTES ? RED_BYTES : RL_BYTES];
+  __shared__ __attribute__((aligned(16))) char REDRL[NW * SLOT];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS[SH::CH][2];
   __shared__ float SSQ[SH::CH], SSK[SH::CH];
   __shared__ float TRED[SH::NT];
   __shared__ __attribute__((aligned(16))) float GP[SH::CH][NW][4];   // per-lane-group shares of g
   typedef float RedRow[QG * 16][RP];
-  RedRow* RED = reinterpret_cast<RedRow*>(REDRL);
-  T* RL = reinterpret_cast<T*>(REDRL);
+  auto RED = [&](int ww) -> RedRow& { return *reinterpret_cast<RedRow*>(REDRL + ww * SLOT); };
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -610,6 +614,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   const IO* dO = static_cast<const IO*>(a.dO) + (size_t)bh * a.N * SH::DV;
   const float* gst = a.gstats + (size_t)bh * a.N * 2;
   float* dK = a.dK + (size_t)bh * a.N * D;
+  T* RLw = reinterpret_cast<T*>(REDRL + w * SLOT);   // this wave's R' copy
   float* dV = a.dV + (size_t)bh * a.N * SH::DV;
 
   StX sq, sk;
@@ -734,8 +739,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     for (int dt = 0; dt < SH::DVT; ++dt)
 #pragma unroll
       for (int fc = 0; fc < SH::FC; ++fc)
-        store_tile_nm<T>(RL + (size_t)w * SH::FC * 16 * RLP, RLP, fc * 16, dt * 16, RT[dt][fc]);
-    __syncthreads();  // phi(Q)^T and the R' copy complete
+        store_tile_nm<T>(RLw, RLP, fc * 16, dt * 16, RT[dt][fc]);
 
     // dV^T partial[value col][key] = dO^T A/den (intra) + R'[:dv]^T-rows x phi(K)
     f32x4 dvp[SH::DVT][SH::TT];
@@ -751,19 +755,19 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         }
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft)
-          mma(acc, lds_tr_frag<T>(RL + (size_t)w * SH::FC * 16 * RLP, RLP, (2 * ft) * 16 + 4 * g,
-                                  (2 * ft + 1) * 16 + 4 * g, dt * 16), phk[ft][tk]);
+          mma(acc, lds_tr_frag<T>(RLw, RLP, (2 * ft) * 16 + 4 * g, (2 * ft + 1) * 16 + 4 * g, dt * 16),
+              phk[ft][tk]);
         dvp[dt][tk] = acc;
       }
     // dV: reduce the per-wave partials
 #pragma unroll
     for (int q0 = 0; q0 < SH::TT; q0 += QG) {
-      __syncthreads();
+      if (q0 > 0) __syncthreads();   // the previous round's reads of every slot are done
 #pragma unroll
       for (int qq = 0; qq < QG; ++qq)
 #pragma unroll
         for (int dt = 0; dt < SH::DVT; ++dt)
-          *reinterpret_cast<f32x4*>(&RED[w][qq * 16 + r][dt * 16 + 4 * g]) = dvp[dt][q0 + qq];
+          *reinterpret_cast<f32x4*>(&RED(w)[qq * 16 + r][dt * 16 + 4 * g]) = dvp[dt][q0 + qq];
       __syncthreads();
       constexpr int C4 = SH::DV / 4;
       for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
@@ -772,7 +776,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) {
-          const float4 v = *reinterpret_cast<const float4*>(&RED[ww][t][4 * c4]);
+          const float4 v = *reinterpret_cast<const float4*>(&RED(ww)[t][4 * c4]);
           s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
         }
         if (tok < a.N) {
