@@ -315,7 +315,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // dQ: ascending sweep with the key-side prefix state S'.
 // ---------------------------------------------------------------------------
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL>
+// ACC: add dQ to the values an earlier frequency group stored (loaded at the
+// start of each chunk, ahead of the next chunk's prefetch).
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
@@ -324,6 +326,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   typedef WTSlice<T, D, FW, NS> WTS;
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;        // k-steps over [dO | -delta]
+  constexpr int NOT = (DT * SH::TT + NW - 1) / NW;   // dQ tiles per wave (at most)
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
@@ -387,6 +390,16 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * SH::CH;
     if (!KEEP_FS) fs.load_frags(wproj);
+    // an earlier group's dQ of this chunk (rows past N read row N-1, unused)
+    f32x4 old_q[ACC ? NOT : 1];
+    if (ACC) {
+#pragma unroll
+      for (int k = 0; k < NOT; ++k) {
+        const int ot = w + k * NW, dt = ot % DT, tt = ot / DT;
+        const int tok = min(tok0 + tt * 16 + r, a.N - 1);
+        if (ot < DT * SH::TT) old_q[k] = *reinterpret_cast<const f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g);
+      }
+    }
     __syncthreads();
     sq.store(XQ, SSQ);
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
@@ -516,7 +529,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     // dQ = dP W' over all projection rows: each wave computes whole output
     // tiles dQ^T (d tile, token tile) from every wave's dP block and that
     // wave's dX fragments, so no cross-wave reduction is needed
-    for (int ot = w; ot < DT * SH::TT; ot += NW) {
+#pragma unroll
+    for (int k = 0; k < NOT; ++k) {
+      const int ot = w + k * NW;
+      if (ot >= DT * SH::TT) break;
       const int dt = ot % DT, tt = ot / DT;
       f32x4 acc = zero4();
 #pragma unroll
@@ -535,8 +551,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       }
       const int tok = tok0 + tt * 16 + r;
       if (tok < a.N) {
-        f32x4* o = reinterpret_cast<f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g);
-        *o = a.acc ? *o + acc : acc;   // later frequency groups add their share
+        if (ACC) acc += old_q[k];   // later frequency groups add their share
+        *reinterpret_cast<f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g) = acc;
       }
     }
     // frequency gradient partial: dW'[rows][d] += dP^T Q
@@ -569,7 +585,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // dK, dV: descending sweep with the query-side suffix state R'.
 // ---------------------------------------------------------------------------
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL>
+// ACC: add dK and dV to the values an earlier frequency group stored.  The
+// old values are loaded at the start of each chunk, ahead of the next chunk's
+// prefetch, so waiting for them never waits for that prefetch.
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
@@ -580,6 +599,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int KG = (SH::DVT1 + 1) / 2;
   constexpr int QG = (NW >= 8 || D >= 128) ? 1 : 2;
   constexpr int RP = SH::DV + 4;                 // row stride of the dV reduction rows
+  constexpr int C4 = SH::DV / 4;                 // float4 columns of a dV row
+  constexpr int NIT = (QG * 16 * C4 + SH::NT - 1) / SH::NT;   // dV items per thread and round
+  constexpr int TT0STEP = DT < NW ? NW / DT : 1; // token-tile step of a wave's dK tiles
+  constexpr int NDK = (DT + NW - 1) / NW;        // d tiles per wave (at most)
+  constexpr int NTK = DT < NW ? (SH::TT + TT0STEP - 1) / TT0STEP : SH::TT;   // token tiles per d tile
   constexpr int RLP = SH::DV + 4;                // row stride of the bf16 R' copy, [feature][value col]
   constexpr int LDP = SH::FC * 16 + 4;           // row stride of the per-wave [token][row] blocks
   // Each wave owns one slot of REDRL: its bf16 copy of R' and, once its own
@@ -661,6 +685,29 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     // this chunk's projection fragments: in flight across the staging barriers
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
+    // an earlier group's dK and dV of this chunk (rows past N read row N-1, unused)
+    f32x4 old_k[ACC ? NDK : 1][ACC ? NTK : 1];
+    float4 old_v[ACC ? SH::TT / QG : 1][ACC ? NIT : 1];
+    if (ACC) {
+#pragma unroll
+      for (int kd = 0; kd < NDK; ++kd)
+#pragma unroll
+        for (int kt = 0; kt < NTK; ++kt) {
+          const int dt = w % DT + kd * NW, tt = (DT < NW ? w / DT : 0) + kt * TT0STEP;
+          const int tok = min(tok0 + tt * 16 + r, a.N - 1);
+          if (dt < DT && tt < SH::TT)
+            old_k[kd][kt] = *reinterpret_cast<const f32x4*>(dK + (size_t)tok * D + dt * 16 + 4 * g);
+        }
+#pragma unroll
+      for (int q = 0; q < SH::TT / QG; ++q)
+#pragma unroll
+        for (int k = 0; k < NIT; ++k) {
+          const int it = threadIdx.x + k * SH::NT;
+          const int tok = min(tok0 + q * QG * 16 + it / C4, a.N - 1);
+          if (it < QG * 16 * C4)
+            old_v[q][k] = *reinterpret_cast<const float4*>(dV + (size_t)tok * SH::DV + 4 * (it % C4));
+        }
+    }
     __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
@@ -769,24 +816,20 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         for (int dt = 0; dt < SH::DVT; ++dt)
           *reinterpret_cast<f32x4*>(&RED(w)[qq * 16 + r][dt * 16 + 4 * g]) = dvp[dt][q0 + qq];
       __syncthreads();
-      constexpr int C4 = SH::DV / 4;
-      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
+#pragma unroll
+      for (int k = 0; k < NIT; ++k) {
+        const int it = threadIdx.x + k * SH::NT;
+        if (it >= QG * 16 * C4) break;
         const int t = it / C4, c4 = it % C4;
         const int tok = tok0 + q0 * 16 + t;
         float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (ACC) s = old_v[q0 / QG][k];   // later frequency groups add their share
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) {
           const float4 v = *reinterpret_cast<const float4*>(&RED(ww)[t][4 * c4]);
           s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
         }
-        if (tok < a.N) {
-          float4* o = reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4);
-          if (a.acc) {
-            const float4 p = *o;
-            s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
-          }
-          *o = s;
-        }
+        if (tok < a.N) *reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4) = s;
       }
     }
     // dphi(K)^T[feature][key] = phi(Q)^T M + R'^T-rows x [V | 1]
@@ -870,10 +913,15 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
     for (int tt = 0; tt < SH::TT; ++tt) GP[tt * 16 + r][w][g] = gp[tt];
     __syncthreads();   // every wave's dP block and g shares complete
-    constexpr int TT0STEP = DT < NW ? NW / DT : 1;
-    for (int dt = w % DT; dt < DT; dt += NW) {
-      if (dt != w % DT) load_wf(dt);
-      for (int tt = DT < NW ? w / DT : 0; tt < SH::TT; tt += TT0STEP) {
+#pragma unroll
+    for (int kd = 0; kd < NDK; ++kd) {
+      const int dt = w % DT + kd * NW;
+      if (dt >= DT) break;
+      if (kd > 0) load_wf(dt);
+#pragma unroll
+      for (int kt = 0; kt < NTK; ++kt) {
+      const int tt = (DT < NW ? w / DT : 0) + kt * TT0STEP;
+      if (tt >= SH::TT) break;
       f32x4 acc = zero4();
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) {
@@ -901,8 +949,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         f32x4 s;
 #pragma unroll
         for (int i = 0; i < 4; ++i) s[i] = acc[i] + k2 * io_to_float(kr[i]);
-        f32x4* o = reinterpret_cast<f32x4*>(dK + (size_t)tok * D + dt * 16 + 4 * g);
-        *o = a.acc ? *o + s : s;   // later frequency groups add their share
+        if (ACC) s += old_k[kd][kt];   // later frequency groups add their share
+        *reinterpret_cast<f32x4*>(dK + (size_t)tok * D + dt * 16 + 4 * g) = s;
         if (dt == 0 && g == 0) dtau_acc -= gg * SSK[tl] * inv_c;
       }
       }
@@ -1032,16 +1080,32 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
       launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_BWD_DQ, st, true);
-  if (causal)
-    k_bwd_dq<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
-  else
-    k_bwd_dq<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
+  // only the frequency-group shape (d = 128) adds into an earlier group's outputs
+  constexpr bool GROUPED = D == 128;
+  if (GROUPED && a.acc) {
+    if (causal)
+      k_bwd_dq<T, D, FWA, NWA, NS, true, GROUPED><<<grid, SA::NT, 0, st>>>(a);
+    else
+      k_bwd_dq<T, D, FWA, NWA, NS, false, GROUPED><<<grid, SA::NT, 0, st>>>(a);
+  } else {
+    if (causal)
+      k_bwd_dq<T, D, FWA, NWA, NS, true, false><<<grid, SA::NT, 0, st>>>(a);
+    else
+      k_bwd_dq<T, D, FWA, NWA, NS, false, false><<<grid, SA::NT, 0, st>>>(a);
+  }
   timing_mark(KC_BWD_DQ, st, false);
   timing_mark(KC_BWD_DKV, st, true);
-  if (causal)
-    k_bwd_dkv<T, D, FWB, NWB, NS, true><<<grid, SB::NT, 0, st>>>(a);
-  else
-    k_bwd_dkv<T, D, FWB, NWB, NS, false><<<grid, SB::NT, 0, st>>>(a);
+  if (GROUPED && a.acc) {
+    if (causal)
+      k_bwd_dkv<T, D, FWB, NWB, NS, true, GROUPED><<<grid, SB::NT, 0, st>>>(a);
+    else
+      k_bwd_dkv<T, D, FWB, NWB, NS, false, GROUPED><<<grid, SB::NT, 0, st>>>(a);
+  } else {
+    if (causal)
+      k_bwd_dkv<T, D, FWB, NWB, NS, true, false><<<grid, SB::NT, 0, st>>>(a);
+    else
+      k_bwd_dkv<T, D, FWB, NWB, NS, false, false><<<grid, SB::NT, 0, st>>>(a);
+  }
   timing_mark(KC_BWD_DKV, st, false);
   dim3 rgrid((SA::M * D + 63) / 64, a.H);
   timing_mark(KC_BWD_REDUCE, st, true);

@@ -148,7 +148,10 @@ __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1
 // Sweep: carry-in state, then per chunk the readout (and, causal, the
 // intra-chunk term and the state update).  Writes O and den.
 // ---------------------------------------------------------------------------
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG>
+// ADD: add this frequency group's numerator and denominator to the sums the
+// earlier groups stored; the old sums are loaded at the start of each chunk,
+// so their latency overlaps the chunk's work.
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG, bool ADD>
 __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
@@ -157,6 +160,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   constexpr int XV_N = CAUSAL ? StV::LDS_ELEMS : 8;
   constexpr int LDP = SH::FC * 16 + 4;     // [token][feature] rows of a wave's phi(K) block
   constexpr int PT_N = CAUSAL ? CHUNK * LDP : 8;
+  constexpr int C4 = SH::DV / 4;                                // float4 columns of a row
+  constexpr int NIT = (QG * 16 * C4 + SH::NT - 1) / SH::NT;    // readout items per thread and round
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[CAUSAL ? StX::LDS_ELEMS : 8];
   __shared__ float SSQ[CHUNK], SSK[CHUNK];
@@ -216,6 +221,22 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       sq.fetch(Q, t1, a.N);
       if (CAUSAL) sk.fetch(K, t1, a.N);
       if (CAUSAL) sv.fetch(V, t1, a.N);
+    }
+    // the earlier groups' sums for this chunk (rows past N read row N-1, unused)
+    float4 old_n[ADD ? TT / QG : 1][ADD ? NIT : 1];
+    float old_d[ADD ? TT / QG : 1][ADD ? NIT : 1];
+    if (ADD) {
+#pragma unroll
+      for (int q = 0; q < TT / QG; ++q)
+#pragma unroll
+        for (int k = 0; k < NIT; ++k) {
+          const int it = threadIdx.x + k * SH::NT;
+          const size_t row = (size_t)bh * a.N + min(tok0 + q * QG * 16 + it / C4, a.N - 1);
+          if (it < QG * 16 * C4) {
+            old_n[q][k] = *reinterpret_cast<const float4*>(a.acc_num + row * SH::DV + 4 * (it % C4));
+            old_d[q][k] = a.acc_den[row];
+          }
+        }
     }
 
     Frag<T> pq[SH::FT][TT];
@@ -311,8 +332,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
           }
       }
       __syncthreads();
-      constexpr int C4 = SH::DV / 4;
-      for (int it = threadIdx.x; it < QG * 16 * C4; it += SH::NT) {
+#pragma unroll
+      for (int k = 0; k < NIT; ++k) {
+        const int it = threadIdx.x + k * SH::NT;
+        if (it >= QG * 16 * C4) break;
         const int t = it / C4, c4 = it % C4;
         const int tok = tok0 + q0 * 16 + t;
         float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -324,14 +347,14 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
           dn += RED[ww][t][SH::DV];
         }
         if (tok < a.N) {
-          if (a.acc) {
+          if (ADD || a.acc) {
             // one frequency group's share of the numerator and denominator
             float4* an = reinterpret_cast<float4*>(a.acc_num + ((size_t)bh * a.N + tok) * SH::DV + 4 * c4);
             float* ad = a.acc_den + (size_t)bh * a.N + tok;
-            if (a.acc == 2) {
-              const float4 p = *an;
+            if (ADD) {
+              const float4 p = old_n[q0 / QG][k];
               num.x += p.x; num.y += p.y; num.z += p.z; num.w += p.w;
-              if (c4 == 0) dn += *ad;
+              dn += old_d[q0 / QG][k];
             }
             *an = num;
             if (c4 == 0) *ad = dn;
@@ -460,10 +483,19 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   const hipError_t e = launch_state_scan(a.state, nullptr, a.BH, a.segments, a.sub, SH::STATE, causal, st);
   if (e != hipSuccess) return e;
   timing_mark(KC_FWD_SWEEP, st, true);
-  if (causal)
-    k_fwd_sweep<T, D, FW, NW, NS, true, QG><<<grid, SH::NT, 0, st>>>(a);
-  else
-    k_fwd_sweep<T, D, FW, NW, NS, false, 1><<<grid, SH::NT, 0, st>>>(a);
+  // only the frequency-group shape (d = 128) adds to an earlier group's sums
+  constexpr bool GROUPED = D == 128;
+  if (GROUPED && a.acc == 2) {
+    if (causal)
+      k_fwd_sweep<T, D, FW, NW, NS, true, QG, GROUPED><<<grid, SH::NT, 0, st>>>(a);
+    else
+      k_fwd_sweep<T, D, FW, NW, NS, false, 1, GROUPED><<<grid, SH::NT, 0, st>>>(a);
+  } else {
+    if (causal)
+      k_fwd_sweep<T, D, FW, NW, NS, true, QG, false><<<grid, SH::NT, 0, st>>>(a);
+    else
+      k_fwd_sweep<T, D, FW, NW, NS, false, 1, false><<<grid, SH::NT, 0, st>>>(a);
+  }
   timing_mark(KC_FWD_SWEEP, st, false);
   return hipGetLastError();
 }
