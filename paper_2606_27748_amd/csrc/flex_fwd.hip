@@ -110,22 +110,24 @@ void k_fwd_state(FwdArgs a) {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1, int P, int sub, int E,
                                                     int causal, int reverse0) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= E) return;
+  // one thread per 4 consecutive elements (E is a multiple of 256)
+  const int e4 = blockIdx.x * 256 + threadIdx.x;
+  if (4 * e4 >= E) return;
   const int n = P * sub;
   // blockIdx.z selects the state array: state0 in the direction reverse0,
   // state1 (backward only) in the opposite one
   const int reverse = blockIdx.z == 0 ? reverse0 : 1 - reverse0;
-  float* s = (blockIdx.z == 0 ? state0 : state1) + (size_t)blockIdx.y * n * E + e;
+  float4* s = reinterpret_cast<float4*>((blockIdx.z == 0 ? state0 : state1) + (size_t)blockIdx.y * n * E) + e4;
+  const size_t E4 = E / 4;
   constexpr int BATCH = 16;  // independent loads in flight per thread
-  float acc = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int k0 = 0; k0 < n; k0 += BATCH) {
-    float v[BATCH];
+    float4 v[BATCH];
 #pragma unroll
     for (int j = 0; j < BATCH; ++j) {
       const int k = k0 + j;
       const int p = reverse ? n - 1 - k : k;
-      v[j] = k < n ? s[(size_t)p * E] : 0.f;
+      v[j] = k < n ? s[(size_t)p * E4] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (causal) {
 #pragma unroll
@@ -133,12 +135,12 @@ __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1
         const int k = k0 + j;
         const int p = reverse ? n - 1 - k : k;
         // first slot of each segment met in scan order: p*sub (prefix) or p*sub+sub-1 (suffix)
-        if (k < n && (reverse ? (p % sub == sub - 1) : (p % sub == 0))) s[(size_t)p * E] = acc;
-        acc += v[j];
+        if (k < n && (reverse ? (p % sub == sub - 1) : (p % sub == 0))) s[(size_t)p * E4] = acc;
+        acc.x += v[j].x; acc.y += v[j].y; acc.z += v[j].z; acc.w += v[j].w;
       }
     } else {
 #pragma unroll
-      for (int j = 0; j < BATCH; ++j) acc += v[j];
+      for (int j = 0; j < BATCH; ++j) { acc.x += v[j].x; acc.y += v[j].y; acc.z += v[j].z; acc.w += v[j].w; }
     }
   }
   if (!causal) s[0] = acc;
@@ -546,7 +548,8 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
 
 hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
                              hipStream_t st) {
-  dim3 sgrid((E + 255) / 256, BH, (state && state_rev) ? 2 : 1);
+  if (E % 4 != 0) return hipErrorInvalidValue;   // the scan moves 4 floats per thread
+  dim3 sgrid((E / 4 + 255) / 256, BH, (state && state_rev) ? 2 : 1);
   timing_mark(KC_SCAN, st, true);
   if (state)
     k_state_scan<<<sgrid, 256, 0, st>>>(state, state_rev, P, sub, E, causal ? 1 : 0, 0);
