@@ -994,54 +994,66 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 // dwpart: [2][B*H][P][nmat][m][d].  dW'1, dW'2 -> dW1 = (dW'1+dW'2)/2,
 // dW2 = (dW'1-dW'2)/2 because W'1 = (W1+W2)/2 and W'2 = (W1-W2)/2.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int m, int d, int nmat) {
-  // 64 elements (f, k) of one head per workgroup; the 4 waves split the list of
-  // partials (side, b, segment) round-robin, loads unrolled so they are in
-  // flight together, then the 4 wave sums are combined in a fixed order.
-  __shared__ float part[2][4][64];
-  const int md = m * d;
-  const int e = blockIdx.x * 64 + (threadIdx.x % 64);
+template <int NMAT>
+__global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int md4) {
+  // 256 elements (f, k) of one head per workgroup, 4 consecutive per thread;
+  // the 4 waves split the list of partials (side, b, segment) round-robin and
+  // issue a batch of loads of every matrix before summing it (a partial past
+  // the list reads the last one, added as zero), then the 4 wave sums are
+  // combined in a fixed order.
+  constexpr int BATCH = 8;
+  __shared__ float4 part[NMAT][4][64];
+  const int e4 = blockIdx.x * 64 + (threadIdx.x % 64);
   const int q = threadIdx.x / 64;
   const int h = blockIdx.y;
   const int count = 2 * a.B * a.segments;
-  float acc[2] = {0.f, 0.f};
-  if (e < md) {
-    for (int mat = 0; mat < nmat; ++mat) {
-      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-      int i = q;
-      for (; i + 12 < count; i += 16) {
-        float v[4];
+  const float4* src = reinterpret_cast<const float4*>(a.dwpart);
+  float4 acc[NMAT];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int j = i + 4 * u;
-          const int side = j / (a.B * a.segments), rem = j % (a.B * a.segments);
-          const int b = rem / a.segments, p = rem % a.segments;
-          const size_t blk = ((size_t)side * a.BH + (size_t)b * a.H + h) * a.segments + p;
-          v[u] = a.dwpart[(blk * nmat + mat) * md + e];
-        }
-        s0 += v[0]; s1 += v[1]; s2 += v[2]; s3 += v[3];
-      }
-      for (; i < count; i += 4) {
-        const int side = i / (a.B * a.segments), rem = i % (a.B * a.segments);
+  for (int mat = 0; mat < NMAT; ++mat) acc[mat] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (e4 < md4) {
+    for (int i0 = q; i0 < count; i0 += 4 * BATCH) {
+      float4 v[BATCH][NMAT];
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const int j = min(i0 + 4 * u, count - 1);
+        const int side = j / (a.B * a.segments), rem = j % (a.B * a.segments);
         const int b = rem / a.segments, p = rem % a.segments;
         const size_t blk = ((size_t)side * a.BH + (size_t)b * a.H + h) * a.segments + p;
-        s0 += a.dwpart[(blk * nmat + mat) * md + e];
+#pragma unroll
+        for (int mat = 0; mat < NMAT; ++mat) v[u][mat] = src[(blk * NMAT + mat) * md4 + e4];
       }
-      acc[mat] = (s0 + s1) + (s2 + s3);
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const float k = i0 + 4 * u < count ? 1.f : 0.f;
+#pragma unroll
+        for (int mat = 0; mat < NMAT; ++mat) {
+          acc[mat].x += k * v[u][mat].x; acc[mat].y += k * v[u][mat].y;
+          acc[mat].z += k * v[u][mat].z; acc[mat].w += k * v[u][mat].w;
+        }
+      }
     }
   }
-  part[0][q][threadIdx.x % 64] = acc[0];
-  part[1][q][threadIdx.x % 64] = acc[1];
+#pragma unroll
+  for (int mat = 0; mat < NMAT; ++mat) part[mat][q][threadIdx.x % 64] = acc[mat];
   __syncthreads();
-  if (q == 0 && e < md) {
+  if (q == 0 && e4 < md4) {
     const int t = threadIdx.x;
-    const float x0 = (part[0][0][t] + part[0][1][t]) + (part[0][2][t] + part[0][3][t]);
-    const float x1 = (part[1][0][t] + part[1][1][t]) + (part[1][2][t] + part[1][3][t]);
-    if (nmat == 2) {
-      a.dW1[(size_t)h * a.w_stride + e] = 0.5f * (x0 + x1);
-      a.dW2[(size_t)h * a.w_stride + e] = 0.5f * (x0 - x1);
+    float4 x[NMAT];
+#pragma unroll
+    for (int mat = 0; mat < NMAT; ++mat) {
+      const float4 p0 = part[mat][0][t], p1 = part[mat][1][t], p2 = part[mat][2][t], p3 = part[mat][3][t];
+      x[mat] = make_float4((p0.x + p1.x) + (p2.x + p3.x), (p0.y + p1.y) + (p2.y + p3.y),
+                           (p0.z + p1.z) + (p2.z + p3.z), (p0.w + p1.w) + (p2.w + p3.w));
+    }
+    float4* o1 = reinterpret_cast<float4*>(a.dW1 + (size_t)h * a.w_stride) + e4;
+    if (NMAT == 2) {
+      float4* o2 = reinterpret_cast<float4*>(a.dW2 + (size_t)h * a.w_stride) + e4;
+      const float4 u = x[0], w = x[NMAT - 1];
+      *o1 = make_float4(0.5f * (u.x + w.x), 0.5f * (u.y + w.y), 0.5f * (u.z + w.z), 0.5f * (u.w + w.w));
+      *o2 = make_float4(0.5f * (u.x - w.x), 0.5f * (u.y - w.y), 0.5f * (u.z - w.z), 0.5f * (u.w - w.w));
     } else {
-      a.dW1[(size_t)h * a.w_stride + e] = x0;
+      *o1 = x[0];
     }
   }
   if (a.dtau && blockIdx.x == 0 && threadIdx.x == 0) {
@@ -1107,9 +1119,11 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
       k_bwd_dkv<T, D, FWB, NWB, NS, false, false><<<grid, SB::NT, 0, st>>>(a);
   }
   timing_mark(KC_BWD_DKV, st, false);
-  dim3 rgrid((SA::M * D + 63) / 64, a.H);
+  static_assert((SA::M * D) % 4 == 0, "the reduce moves 4 floats per thread");
+  constexpr int MD4 = SA::M * D / 4;
+  dim3 rgrid((MD4 + 63) / 64, a.H);
   timing_mark(KC_BWD_REDUCE, st, true);
-  k_bwd_reduce<<<rgrid, 256, 0, st>>>(a, SA::M, D, NS ? 2 : 1);
+  k_bwd_reduce<NS ? 2 : 1><<<rgrid, 256, 0, st>>>(a, MD4);
   timing_mark(KC_BWD_REDUCE, st, false);
   return hipGetLastError();
 }
