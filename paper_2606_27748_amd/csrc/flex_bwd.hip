@@ -529,12 +529,15 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     // dQ = dP W' over all projection rows: each wave computes whole output
     // tiles dQ^T (d tile, token tile) from every wave's dP block and that
     // wave's dX fragments, so no cross-wave reduction is needed
+    // (every tile's products first, then the stores: the dX fragment loads of
+    // a later tile never wait behind an earlier tile's stores)
+    f32x4 acc[NOT];
 #pragma unroll
     for (int k = 0; k < NOT; ++k) {
       const int ot = w + k * NW;
-      if (ot >= DT * SH::TT) break;
+      acc[k] = zero4();
+      if (ot >= DT * SH::TT) continue;
       const int dt = ot % DT, tt = ot / DT;
-      f32x4 acc = zero4();
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) {
         const Frag<T>* wd = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, ww);
@@ -546,13 +549,19 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
             for (int j = 4; j < 8; ++j) b.set(j, 0.f);
           }
 #pragma unroll
-          for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wd[((sp * DT + dt) * WTS::KP + ks) * WAVE + l], b);
+          for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc[k], wd[((sp * DT + dt) * WTS::KP + ks) * WAVE + l], b);
         }
       }
+    }
+#pragma unroll
+    for (int k = 0; k < NOT; ++k) {
+      const int ot = w + k * NW;
+      if (ot >= DT * SH::TT) continue;
+      const int dt = ot % DT, tt = ot / DT;
       const int tok = tok0 + tt * 16 + r;
       if (tok < a.N) {
-        if (ACC) acc += old_q[k];   // later frequency groups add their share
-        *reinterpret_cast<f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g) = acc;
+        if (ACC) acc[k] += old_q[k];   // later frequency groups add their share
+        *reinterpret_cast<f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g) = acc[k];
       }
     }
     // frequency gradient partial: dW'[rows][d] += dP^T Q
@@ -917,42 +926,50 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     for (int kd = 0; kd < NDK; ++kd) {
       const int dt = w % DT + kd * NW;
       if (dt >= DT) break;
-      if (kd > 0) load_wf(dt);
+      f32x4 acc[NTK];
 #pragma unroll
       for (int kt = 0; kt < NTK; ++kt) {
-      const int tt = (DT < NW ? w / DT : 0) + kt * TT0STEP;
-      if (tt >= SH::TT) break;
-      f32x4 acc = zero4();
+        const int tt = (DT < NW ? w / DT : 0) + kt * TT0STEP;
+        acc[kt] = zero4();
+        if (tt >= SH::TT) continue;
 #pragma unroll
-      for (int ww = 0; ww < NW; ++ww) {
+        for (int ww = 0; ww < NW; ++ww) {
 #pragma unroll
-        for (int ks = 0; ks < WTS::KP; ++ks) {
-          Frag<T> b = load_frag_nm<T>(PT[ww], LDP, tt * 16, (2 * ks) * 16, (2 * ks + 1) * 16);
-          if (2 * ks + 1 >= SH::PR) {   // no second row tile: keep unwritten LDS out of the product
+          for (int ks = 0; ks < WTS::KP; ++ks) {
+            Frag<T> b = load_frag_nm<T>(PT[ww], LDP, tt * 16, (2 * ks) * 16, (2 * ks + 1) * 16);
+            if (2 * ks + 1 >= SH::PR) {   // no second row tile: keep unwritten LDS out of the product
 #pragma unroll
-            for (int j = 4; j < 8; ++j) b.set(j, 0.f);
+              for (int j = 4; j < 8; ++j) b.set(j, 0.f);
+            }
+#pragma unroll
+            for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc[kt], wf[ww][ks][sp], b);
           }
-#pragma unroll
-          for (int sp = 0; sp < WTS::NSPLIT; ++sp) mma(acc, wf[ww][ks][sp], b);
         }
       }
-      const int tl = tt * 16 + r, tok = tok0 + tl;
-      float gg = 0.f;
+      // the next d tile's dX fragments, issued ahead of this tile's stores so
+      // that waiting for them does not wait for the stores
+      if (kd + 1 < NDK && dt + NW < DT) load_wf(dt + NW);
 #pragma unroll
-      for (int ww = 0; ww < NW; ++ww) {
-        const float4 v = *reinterpret_cast<const float4*>(&GP[tl][ww][0]);
-        gg += (v.x + v.y) + (v.z + v.w);
-      }
-      if (tok < a.N) {
-        const float k2 = 2.0f * inv_c * gg;
-        const IO* kr = XK + tl * StX::LD + dt * 16 + 4 * g;
-        f32x4 s;
+      for (int kt = 0; kt < NTK; ++kt) {
+        const int tt = (DT < NW ? w / DT : 0) + kt * TT0STEP;
+        if (tt >= SH::TT) continue;
+        const int tl = tt * 16 + r, tok = tok0 + tl;
+        float gg = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) s[i] = acc[i] + k2 * io_to_float(kr[i]);
-        if (ACC) s += old_k[kd][kt];   // later frequency groups add their share
-        *reinterpret_cast<f32x4*>(dK + (size_t)tok * D + dt * 16 + 4 * g) = s;
-        if (dt == 0 && g == 0) dtau_acc -= gg * SSK[tl] * inv_c;
-      }
+        for (int ww = 0; ww < NW; ++ww) {
+          const float4 v = *reinterpret_cast<const float4*>(&GP[tl][ww][0]);
+          gg += (v.x + v.y) + (v.z + v.w);
+        }
+        if (tok < a.N) {
+          const float k2 = 2.0f * inv_c * gg;
+          const IO* kr = XK + tl * StX::LD + dt * 16 + 4 * g;
+          f32x4 s;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) s[i] = acc[kt][i] + k2 * io_to_float(kr[i]);
+          if (ACC) s += old_k[kd][kt];   // later frequency groups add their share
+          *reinterpret_cast<f32x4*>(dK + (size_t)tok * D + dt * 16 + 4 * g) = s;
+          if (dt == 0 && g == 0) dtau_acc -= gg * SSK[tl] * inv_c;
+        }
       }
     }
     {
