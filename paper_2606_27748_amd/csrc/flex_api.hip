@@ -178,11 +178,11 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-// Chunks per workgroup of the standalone feature map: about 1024 workgroups
+// Chunks per workgroup of the standalone feature map: about 512 workgroups
 // in all (each builds its frequency fragments once), at least one chunk each.
 int fmap_chunks_per_wg(const flex_desc* d) {
   const long long total = (long long)nchunks_of(d) * d->B * d->H;
-  long long c = total / 1024;
+  long long c = total / 512;
   if (c < 1) c = 1;
   if (c > nchunks_of(d)) c = nchunks_of(d);
   return (int)c;

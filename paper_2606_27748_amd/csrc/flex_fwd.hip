@@ -395,41 +395,64 @@ __device__ __forceinline__ void store4<float>(float* p, const float (&v)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
+// The chunk's X rows are staged through LDS (prefetched a chunk ahead), every
+// wave projects them for its frequency slice, and the features are gathered
+// as [token][feature] rows in LDS, then written out as whole 16-byte vectors.
 template <class T, int D, int FW, int NW, bool NS>
 __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
+  typedef RowStage<IO, D, SH::NT> StX;
+  constexpr int F = 2 * SH::M;                 // features per row
+  constexpr int VEC = 16 / (int)sizeof(IO);    // elements per 16-byte vector
+  constexpr int LDF = F + VEC;                 // row stride of the staged features
+  constexpr int NVO = CHUNK * F / VEC;         // output vectors per chunk
+  __shared__ __attribute__((aligned(16))) IO XL[StX::LDS_ELEMS];
+  __shared__ float SSQ[CHUNK];
+  __shared__ __attribute__((aligned(16))) IO PH[CHUNK * LDF];
   const int bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   const IO* X = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
-  IO* Phi = static_cast<IO*>(a.O) + (size_t)bh * a.N * (2 * SH::M);
+  IO* Phi = static_cast<IO*>(a.O) + (size_t)bh * a.N * F;
+  const int c0 = blockIdx.x * a.chunks_per_seg;
+  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  StX sx;
+  if (c0 < c1) sx.fetch(X, c0 * CHUNK, a.N);
   FreqSlice<T, D, FW, NS> fs;
   fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
   const float inv_c = __expf(-a.tau[h]);
-  const int c0 = blockIdx.x * a.chunks_per_seg;
-  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
+    __syncthreads();   // the previous chunk's reads of XL and PH are done
+    sx.store(XL, SSQ);
+    sx.fetch(X, c + 1 < c1 ? tok0 + CHUNK : tok0, a.N);   // the last chunk refetches itself (unused)
+    __syncthreads();
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
       f32x4 p[SH::PR];
       float ssq;
-      project_tile<T, D, FW, NS>(fs, X, tok0 + tt * 16, a.N, p, ssq);
-      const int tok = tok0 + tt * 16 + r;
+      project_tile_lds<T, D, FW, NS, StX::LD>(fs, XL, SSQ, tt, p, ssq);
       // the values are produced in fp32 and rounded once to the io dtype
-      const float sc = row_scale(ssq, inv_c, a.s_const, tok < a.N);
+      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+      IO* row = PH + (tt * 16 + r) * LDF;
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) {
         const Frag<float> f = features<float, SH::FT, NS>(p, ft, sc);
-        if (tok < a.N) {
-          const int f0 = w * FW + ft * 16 + 4 * g;
-          IO* row = Phi + (size_t)tok * (2 * SH::M);
-          const float cv[4] = {f.get(0), f.get(1), f.get(2), f.get(3)};
-          const float sv[4] = {f.get(4), f.get(5), f.get(6), f.get(7)};
-          store4<IO>(row + f0, cv);
-          store4<IO>(row + SH::M + f0, sv);
-        }
+        const int f0 = w * FW + ft * 16 + 4 * g;
+        const float cv[4] = {f.get(0), f.get(1), f.get(2), f.get(3)};
+        const float sv[4] = {f.get(4), f.get(5), f.get(6), f.get(7)};
+        store4<IO>(row + f0, cv);
+        store4<IO>(row + SH::M + f0, sv);
       }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < (NVO + SH::NT - 1) / SH::NT; ++i) {
+      const int v = threadIdx.x + i * SH::NT;
+      const int t = v / (F / VEC), cv = v % (F / VEC);
+      if (v < NVO && tok0 + t < a.N)
+        *reinterpret_cast<uint4*>(Phi + (size_t)(tok0 + t) * F + cv * VEC) =
+            *reinterpret_cast<const uint4*>(PH + t * LDF + cv * VEC);
     }
   }
 }
