@@ -66,7 +66,8 @@ void k_fwd_state(FwdArgs a) {
   // (d <= 64), else reloaded per chunk ahead of the staging barriers
   constexpr bool KEEP_FS = D <= 64;
   FreqSlice<T, D, FW, NS> fs;
-  if (KEEP_FS) fs.load_frags(wproj);
+  // held for the whole sweep: built from W by each wave (no prepared copy is needed)
+  if (KEEP_FS) fs.load(a.W1 + (size_t)h * a.w_stride, NS ? a.W2 + (size_t)h * a.w_stride : nullptr, w * FW);
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
     if (!KEEP_FS) fs.load_frags(wproj);
@@ -191,7 +192,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     if (CAUSAL) sk.fetch(K, c0 * CHUNK, a.N);
     if (CAUSAL) sv.fetch(V, c0 * CHUNK, a.N);
   }
-  const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const float inv_c = __expf(-a.tau[h]);
 
   // carry-in state (exclusive prefix for causal, total for non-causal)
@@ -206,9 +206,16 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
         S[fc][dt] = *reinterpret_cast<const f32x4*>(in + ((fc * SH::DVT1 + dt) * WAVE + l) * 4);
   }
   const Frag<T> ones = ones_col0<T>();
-  // projection fragments, held for the whole sweep
+  // projection fragments, held for the whole sweep: built from W by each wave
   FreqSlice<T, D, FW, NS> fs;
-  fs.load_frags(wproj);
+  fs.load(a.W1 + (size_t)h * a.w_stride, NS ? a.W2 + (size_t)h * a.w_stride : nullptr, w * FW);
+  Frag<T> sf[SH::DVT1][SH::FT];
+  if (!CAUSAL) {
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int ft = 0; ft < SH::FT; ++ft) sf[dt][ft] = pair_tiles<T>(S[2 * ft][dt], S[2 * ft + 1][dt]);
+  }
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
@@ -262,12 +269,14 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       }
     }
 
-    // state operand for the readout: rows = value columns, k = this wave's features
-    Frag<T> sf[SH::DVT1][SH::FT];
+    // state operand for the readout: rows = value columns, k = this wave's
+    // features (the non-causal total state is converted once, before the loop)
+    if (CAUSAL) {
 #pragma unroll
-    for (int dt = 0; dt < SH::DVT1; ++dt)
+      for (int dt = 0; dt < SH::DVT1; ++dt)
 #pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft) sf[dt][ft] = pair_tiles<T>(S[2 * ft][dt], S[2 * ft + 1][dt]);
+        for (int ft = 0; ft < SH::FT; ++ft) sf[dt][ft] = pair_tiles<T>(S[2 * ft][dt], S[2 * ft + 1][dt]);
+    }
 
     // intra-chunk kernel matrix, transposed: rows = key tokens, cols = query tokens
     Frag<T> ap[CAUSAL ? SH::KT : 1][TT];
@@ -501,7 +510,9 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   constexpr int QG = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TT);
   const dim3 grid(a.sweep_groups * a.BH);
   const dim3 pgrid(a.segments * a.sub * a.BH);
-  k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
+  // prepared fragments serve the state pre-pass at d > 64, which reloads them
+  // per chunk; the other forward kernels build theirs from W once
+  if (D > 64) k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
   timing_mark(KC_FWD_STATE, st, true);
   k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_STATE, st, false);
