@@ -192,16 +192,17 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, SH::NT, SH::CH> StX;
   typedef RowStage<IO, SH::DV, SH::NT, SH::CH> StV;
-  __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XO[StV::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
-  __shared__ float GS[SH::CH][2];
-  __shared__ float DEN[SH::CH];
-  __shared__ float SSQ[SH::CH], SSK[SH::CH];
+  // staging (and the per-token scalars) double-buffered by chunk parity
+  __shared__ __attribute__((aligned(16))) IO XQ2[2][StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK2[2][StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XDO2[2][StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XO2[2][StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XV2[2][StV::LDS_ELEMS];
+  __shared__ float GS2[2][SH::CH][2];
+  __shared__ float DEN2[2][SH::CH];
+  __shared__ float SSQ2[2][SH::CH], SSK2[2][SH::CH];
   // per-token feature scales: s e(k) for keys, s e(q) / den for queries
-  __shared__ __attribute__((aligned(16))) float SCK[SH::CH], SCQ[SH::CH];
+  __shared__ __attribute__((aligned(16))) float SCK2[2][SH::CH], SCQ2[2][SH::CH];
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -241,9 +242,23 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   FreqSlice<T, D, FW, NS> fs;
   if (KEEP_FS) fs.load_frags(wproj);
   for (int c = c0; c < c1; ++c) {
+    // This chunk's buffers.  They need no barrier before they are written:
+    // the chunk that last read them (two back) is separated from this point
+    // by the previous chunk's barriers.
+    const int par = (c - c0) & 1;
+    IO* XQ = XQ2[par];
+    IO* XK = XK2[par];
+    IO* XDO = XDO2[par];
+    IO* XO = XO2[par];
+    IO* XV = XV2[par];
+    float (*GS)[2] = GS2[par];
+    float* DEN = DEN2[par];
+    float* SSQ = SSQ2[par];
+    float* SSK = SSK2[par];
+    float* SCK = SCK2[par];
+    float* SCQ = SCQ2[par];
     const int tok0 = c * SH::CH;
     if (!KEEP_FS) fs.load_frags(wproj);
-    __syncthreads();
     sq.store(XQ, SSQ); sk.store(XK, SSK); sdo.store(XDO); so.store(XO);
     sv.store(XV);
     if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
@@ -327,16 +342,18 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   constexpr int DT = D / 16;
   constexpr int KG = (SH::DVT1 + 1) / 2;        // k-steps over [dO | -delta]
   constexpr int NOT = (DT * SH::TT + NW - 1) / NW;   // dQ tiles per wave (at most)
-  __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
+  // staging is double-buffered by chunk parity where LDS allows (d <= 64)
+  constexpr int NBUF = D <= 64 ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) IO XQ2[NBUF][StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK2[NBUF][StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XV2[NBUF][StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XDO2[NBUF][StV::LDS_ELEMS];
   constexpr int LDP = SH::FC * 16 + 4;          // row stride of the per-wave [token][row] blocks
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // dP, [token][projection row]
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
-  __shared__ float GS[SH::CH][2];
-  __shared__ float SSQ[SH::CH];
-  __shared__ __attribute__((aligned(16))) float SCK[SH::CH];   // per-token key scale s e(k)
+  __shared__ float GS2[NBUF][SH::CH][2];
+  __shared__ float SSQ2[NBUF][SH::CH];
+  __shared__ __attribute__((aligned(16))) float SCK2[NBUF][SH::CH];   // per-token key scale s e(k)
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -388,6 +405,17 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   FreqSlice<T, D, FW, NS> fs;
   if (KEEP_FS) fs.load_frags(wproj);
   for (int c = c0; c < c1; ++c) {
+    // This chunk's staging buffers.  Double-buffered, they need no barrier
+    // before they are written: the chunk that last read them (two back) is
+    // separated from this point by the previous chunk's barriers.
+    const int par = NBUF == 2 ? (c - c0) & 1 : 0;
+    IO* XQ = XQ2[par];
+    IO* XK = XK2[par];
+    IO* XV = XV2[par];
+    IO* XDO = XDO2[par];
+    float (*GS)[2] = GS2[par];
+    float* SSQ = SSQ2[par];
+    float* SCK = SCK2[par];
     const int tok0 = c * SH::CH;
     if (!KEEP_FS) fs.load_frags(wproj);
     // an earlier group's dQ of this chunk (rows past N read row N-1, unused)
@@ -400,7 +428,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         if (ot < DT * SH::TT) old_q[k] = *reinterpret_cast<const f32x4*>(dQ + (size_t)tok * D + dt * 16 + 4 * g);
       }
     }
-    __syncthreads();
+    if (NBUF == 1) __syncthreads();   // single buffer: the previous chunk's reads are done
     sq.store(XQ, SSQ);
     sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV); sdo.store(XDO);
@@ -622,15 +650,17 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int RED_W = QG * 16 * RP * 4;
   constexpr int RL_W = SH::FC * 16 * RLP * (int)sizeof(T);
   constexpr int SLOT = RED_W > RL_W ? RED_W : RL_W;
-  __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XK[StX::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XDO[StV::LDS_ELEMS];
+  // staging is double-buffered by chunk parity where LDS allows (d <= 64)
+  constexpr int NBUF = D <= 64 ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) IO XQ2[NBUF][StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK2[NBUF][StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XV2[NBUF][StV::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XDO2[NBUF][StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // phi(Q)/den, then dP: [token][row]
   __shared__ __attribute__((aligned(16))) char REDRL[NW * SLOT];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
-  __shared__ float GS[SH::CH][2];
-  __shared__ float SSQ[SH::CH], SSK[SH::CH];
+  __shared__ float GS2[NBUF][SH::CH][2];
+  __shared__ float SSQ2[NBUF][SH::CH], SSK2[NBUF][SH::CH];
   __shared__ float TRED[SH::NT];
   __shared__ __attribute__((aligned(16))) float GP[SH::CH][NW][4];   // per-lane-group shares of g
   typedef float RedRow[QG * 16][RP];
@@ -690,6 +720,17 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   };
   if (DT <= NW) load_wf(w % DT);
   for (int c = c1 - 1; c >= c0; --c) {
+    // This chunk's staging buffers.  Double-buffered, they need no barrier
+    // before they are written: the chunk that last read them (two back) is
+    // separated from this point by the previous chunk's barriers.
+    const int par = NBUF == 2 ? (c1 - 1 - c) & 1 : 0;
+    IO* XQ = XQ2[par];
+    IO* XK = XK2[par];
+    IO* XV = XV2[par];
+    IO* XDO = XDO2[par];
+    float (*GS)[2] = GS2[par];
+    float* SSQ = SSQ2[par];
+    float* SSK = SSK2[par];
     const int tok0 = c * SH::CH;
     // this chunk's projection fragments: in flight across the staging barriers
     FreqSlice<T, D, FW, NS> fs;
@@ -717,7 +758,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
             old_v[q][k] = *reinterpret_cast<const float4*>(dV + (size_t)tok * SH::DV + 4 * (it % C4));
         }
     }
-    __syncthreads();
+    if (NBUF == 1) __syncthreads();   // single buffer: the previous chunk's reads are done
     sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
     {
