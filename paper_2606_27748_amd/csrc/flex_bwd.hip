@@ -259,8 +259,14 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     float* SCQ = SCQ2[par];
     const int tok0 = c * SH::CH;
     if (!KEEP_FS) fs.load_frags(wproj);
-    sq.store(XQ, SSQ); sk.store(XK, SSK); sdo.store(XDO); so.store(XO);
-    sv.store(XV);
+    sq.store(XQ, SSQ); sdo.store(XDO); so.store(XO);
+    if (WITH_S) {
+      sk.store(XK, SSK);
+      sv.store(XV);
+    } else {   // K and V only warm the caches for the sweeps that follow
+      sk.touch();
+      sv.touch();
+    }
     if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
     {
       const int t1 = c + 1 < c1 ? tok0 + SH::CH : tok0;   // the last chunk refetches itself (unused)
@@ -281,7 +287,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
         const float inv = ok ? 1.0f / DEN[t] : 0.f;
         GS[t][0] = inv;
         GS[t][1] = ok ? s : 0.f;
-        SCK[t] = row_scale(SSK[t], inv_c, a.s_const, ok);
+        if (WITH_S) SCK[t] = row_scale(SSK[t], inv_c, a.s_const, ok);
         SCQ[t] = row_scale(SSQ[t], inv_c, a.s_const, ok) * inv;
         if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = s; }
       }

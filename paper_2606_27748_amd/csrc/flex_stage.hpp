@@ -40,6 +40,12 @@ struct RowStage {
   __device__ __forceinline__ uint4 vec(int i) const {
     return ((okm >> i) & 1u) ? r[i] : make_uint4(0u, 0u, 0u, 0u);
   }
+  // keeps the fetched rows' loads without storing them anywhere (loads whose
+  // only purpose is to bring the rows into the caches for a later kernel)
+  __device__ __forceinline__ void touch() const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) asm volatile("" ::"v"(r[i].x), "v"(r[i].y), "v"(r[i].z), "v"(r[i].w));
+  }
   __device__ __forceinline__ void store(IO* lds) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
