@@ -249,7 +249,11 @@ void timing_mark(int kernel_class, hipStream_t st, bool begin) {
   if (begin) {
     if (2 * t.used + 2 > t.ev.size()) {
       hipEvent_t a, b;
-      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) { t.failed = true; return; }
+      // timing-only events: no system-scope fence (cache writeback and
+      // invalidation) when they are recorded, which would otherwise stall
+      // the kernel that follows for several microseconds
+      if (hipEventCreateWithFlags(&a, hipEventDisableSystemFence) != hipSuccess ||
+          hipEventCreateWithFlags(&b, hipEventDisableSystemFence) != hipSuccess) { t.failed = true; return; }
       t.ev.push_back(a);
       t.ev.push_back(b);
     }
