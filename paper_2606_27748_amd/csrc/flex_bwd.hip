@@ -651,7 +651,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int LDP = SH::FC * 16 + 4;           // row stride of the per-wave [token][row] blocks
   // Each wave owns one slot of REDRL: its bf16 copy of R' and, once its own
   // reads of that copy are done, its dV partials.  No other wave touches the
-  // slot between the staging barriers and the dV reduction, so neither the
+  // slot between the chunk's staging barrier and its dV reduction, so neither the
   // copy nor the partials need a barrier before they are written.
   constexpr int RED_W = QG * 16 * RP * 4;
   constexpr int RL_W = SH::FC * 16 * RLP * (int)sizeof(T);
@@ -738,7 +738,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     float* SSQ = SSQ2[par];
     float* SSK = SSK2[par];
     const int tok0 = c * SH::CH;
-    // this chunk's projection fragments: in flight across the staging barriers
+    // this chunk's projection fragments: in flight across the staging barrier
     FreqSlice<T, D, FW, NS> fs;
     fs.load_frags(wproj);
     // an earlier group's dK and dV of this chunk (rows past N read row N-1, unused)
