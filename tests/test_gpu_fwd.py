@@ -59,6 +59,21 @@ def test_feature_map(F, io, d, m, variant):
     assert err <= tol, err
 
 
+@pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
+def test_feature_map_several_chunks_per_workgroup(F, variant):
+    """Enough chunks (8 x 8 slices x 24) that each workgroup maps several in
+    turn, prefetching the next one; N = 1500 leaves a ragged last chunk."""
+    wl = W.Workload("fmap_many", 8, 8, 1500, 64, 64, variant, False, "bf16", True, 17)
+    x = W.generate(wl)
+    t = to_device(x)
+    Phi = F.flex_feature_map(desc_of(wl), t["Q"], t["W1"], t["W2"], t["tau"])
+    got = to_f64(Phi)
+    ref = orc.feature_map(x.f64("Q"), x.W1, x.W2, x.tau, variant)
+    s = 1 / math.sqrt(wl.m) if variant == "stationary" else 1 / (2 * math.sqrt(wl.m))
+    scale = s * orc.norm_factor(x.f64("Q"), x.tau)[..., None]
+    assert np.max(np.abs(got - ref) / scale) <= 2.0 ** -8
+
+
 @pytest.mark.parametrize("io,d,m", SHAPES)
 @pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
 @pytest.mark.parametrize("causal", [False, True])
