@@ -86,6 +86,18 @@ def test_backward_segments(F, segments, causal, reuse):
 
 
 @pytest.mark.parametrize("reuse", [False, True])
+def test_backward_many_partials(F, reuse):
+    """B = 3 and 7 segments give 42 frequency-gradient partials per head: the
+    reduce takes them in two batches, the second one partly past the list."""
+    wl = W.Workload("partials", 3, 2, 500, 64, 64, "nonstationary", True, "bf16", True, 33)
+    x = W.generate(wl)
+    masked_inputs(wl, x)
+    got = gpu_fwd_bwd(F, wl, x, segments=7, reuse=reuse)
+    ref, sc = oracle_bwd(wl, x)
+    check_grads("bf16", got, ref, names_of(wl), sc)
+
+
+@pytest.mark.parametrize("reuse", [False, True])
 @pytest.mark.parametrize("N", [2, 64, 65, 1050])
 def test_backward_edge_lengths(F, N, reuse):
     """Ragged lengths; 1050 with 3 segments leaves forward and backward chunk
