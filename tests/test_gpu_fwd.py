@@ -85,6 +85,17 @@ def test_forward_small(F, io, d, m, variant, causal):
     check_forward(io, to_f64(O), to_f64(den), O_ref, den_ref, kap, sc)
 
 
+@pytest.mark.parametrize("causal", [False, True])
+def test_forward_many_segments(F, causal):
+    """20 segments: the segment scan takes its states in two batches."""
+    wl, x = small("bf16", 64, 64, "nonstationary", causal, B=1, H=2, N=1350, seed=13)
+    t = to_device(x)
+    O, den = F.flex_linattn_fwd(desc_of(wl, segments=20), t["Q"], t["K"], t["V"],
+                                t["W1"], t["W2"], t["tau"])
+    O_ref, den_ref, kap, sc = oracle_fwd(x, wl)
+    check_forward("bf16", to_f64(O), to_f64(den), O_ref, den_ref, kap, sc)
+
+
 @pytest.mark.parametrize("segments", [1, 2, 3, 5])
 @pytest.mark.parametrize("causal", [False, True])
 def test_forward_segments(F, segments, causal):
