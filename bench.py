@@ -318,7 +318,7 @@ def awd_kernel_work(wl, kernel):
         return rows * (d * bio + F * bio), rows * (2 * d * m_eff) * 2, rows * (3 if m_eff > wl.m else 2) * wl.m
     if kernel == "feature_map":
         m_eff = wl.m * (2 if wl.variant == "nonstationary" else 1)
-        rows = S * N
+        rows = 2 * S * N   # the rows of Q and of K, mapped in one launch
         return rows * (d * bio + F * bio), rows * 2 * d * m_eff, rows * (3 if m_eff > wl.m else 2) * wl.m
     return 0, 0, 0
 

@@ -309,9 +309,8 @@ int32_t flex_awd_loss(const flex_desc* desc, const void* Q, const void* K, const
   f.sweep_groups = 1; f.sweep_cps = f.nchunks;
   f.s_const = s_const_of(desc);
   const KernelShape ks = kshape(desc);
-  f.Q = Q; f.O = base + L.phq;
-  if (launch_fwd(f, ks, true, sm) != hipSuccess) return FLEX_ERR_HIP;
-  f.Q = K; f.O = base + L.phk;
+  f.Q = Q; f.O = base + L.phq;   // both matrices in one launch
+  f.K = K; f.O2 = base + L.phk;
   if (launch_fwd(f, ks, true, sm) != hipSuccess) return FLEX_ERR_HIP;
   AwdArgs a;
   memset(&a, 0, sizeof(a));

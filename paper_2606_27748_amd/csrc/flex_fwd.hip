@@ -421,8 +421,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO PH[CHUNK * LDF];
   const int bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const IO* X = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
-  IO* Phi = static_cast<IO*>(a.O) + (size_t)bh * a.N * F;
+  const IO* X = static_cast<const IO*>(blockIdx.z ? a.K : a.Q) + (size_t)bh * a.N * D;
+  IO* Phi = static_cast<IO*>(blockIdx.z ? a.O2 : a.O) + (size_t)bh * a.N * F;
   const int c0 = blockIdx.x * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
   StX sx;
@@ -539,7 +539,7 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
 template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_fmap_t(const FwdArgs& a, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
-  dim3 grid((a.nchunks + a.chunks_per_seg - 1) / a.chunks_per_seg, a.BH);
+  dim3 grid((a.nchunks + a.chunks_per_seg - 1) / a.chunks_per_seg, a.BH, a.K ? 2 : 1);
   timing_mark(KC_FEATURE_MAP, st, true);
   k_feature_map<T, D, FW, NW, NS><<<grid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FEATURE_MAP, st, false);

@@ -42,6 +42,9 @@ struct FwdArgs {
   int acc;
   float* acc_num;
   float* acc_den;
+  // feature map of a second input in the same launch (grid.z = 2): X = K,
+  // Phi = O2; nullptr K maps Q only
+  void* O2;
 };
 
 struct BwdArgs {
