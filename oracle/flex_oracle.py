@@ -195,18 +195,21 @@ def linattn_fwd_rows(Q, K, V, W1, W2, tau, variant, causal, rows, sigma=1.0):
     return out_O, out_den
 
 
-def conditioning(Q, K, W1, W2, tau, variant, causal, sigma=1.0):
+def conditioning(Q, K, W1, W2, tau, variant, causal, sigma=1.0, return_den=False):
     """kappa_i = sum_k |phi(Q_i)_k z_ik| / |den_i|, z_i = sum_{j(<=i)} phi(K_j):
     the condition number of the denominator's dot product.  With trigonometric
     features den is sign-indefinite, and a row's rounding error grows with
-    kappa_i; parity tests weight rows by it."""
+    kappa_i; parity tests weight rows by it.  With return_den, also the
+    den_i = sum_k phi(Q_i)_k z_ik the condition numbers belong to."""
     pq = feature_map(Q, W1, W2, tau, variant, sigma)
     pk = feature_map(K, W1, W2, tau, variant, sigma)
     z = np.cumsum(pk, axis=-2) if causal else np.broadcast_to(
         pk.sum(axis=-2, keepdims=True), pk.shape)
     t = pq * z
+    den = t.sum(-1)
     with np.errstate(divide="ignore", invalid="ignore"):
-        return np.abs(t).sum(-1) / np.abs(t.sum(-1))
+        kappa = np.abs(t).sum(-1) / np.abs(den)
+    return (kappa, den) if return_den else kappa
 
 
 # ----------------------------------------------------------------------------

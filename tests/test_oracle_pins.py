@@ -263,6 +263,44 @@ def test_conditioning_bounds():
     np.testing.assert_allclose(kap0, 1.0, rtol=1e-12)
 
 
+@pytest.mark.parametrize("variant", [S, NS])
+@pytest.mark.parametrize("causal", [False, True])
+def test_conditioning_den_is_attention_den(variant, causal):
+    """The dot products whose condition numbers kappa_i measures are the
+    denominators of Eq.(linear att): phi(Q_i)^T z_i with z_i the sum of phi(K_j)
+    over j <= i (causal, inclusive) or over all j.  Their sum must equal the
+    quadratic form's row sums (brute force, independent of the state form), so
+    an exclusive, shifted or non-cumulative z fails."""
+    Q, K, V, W1, W2, tau = _small_inputs(variant, seed=14)
+    kap, den = orc.conditioning(Q, K, W1, W2, tau, variant, causal, return_den=True)
+    _, denq, _ = _quadratic(Q, K, V, W1, W2, tau, variant, causal)
+    np.testing.assert_allclose(den, denq, rtol=1e-12, atol=1e-13)
+    assert np.all(kap >= 1 - 1e-12)
+
+
+def test_conditioning_two_tokens_closed_form():
+    """Two tokens, one frequency w = 1, d = 1, tau -> inf (norm factor 1), so
+    phi(x) = [cos x, sin x] (Eq.(phi_n) with m = 1, sigma = 1).  Keys k_1 = 0,
+    k_2 = pi/2 give phi(k_1) = (1, 0), phi(k_2) = (0, 1); queries q_1 = 5 pi/6,
+    q_2 = 2 pi/3.  Causal: z_1 = (1, 0) gives den_1 = -sqrt(3)/2 and kappa_1 = 1;
+    z_2 = (1, 1) gives den_2 = -1/2 + sqrt(3)/2 and kappa_2 = (1/2 + sqrt(3)/2) /
+    (sqrt(3)/2 - 1/2) = 2 + sqrt(3).  Non-causal: z = (1, 1) for both rows, and
+    kappa_1 = (sqrt(3)/2 + 1/2) / (sqrt(3)/2 - 1/2) = 2 + sqrt(3) as well.  An
+    exclusive prefix (z_2 = (1, 0)) or a non-cumulative z (z_2 = (0, 1)) would
+    give kappa_2 = 1."""
+    W = np.ones((1, 1, 1))
+    tau = np.array([math.inf])
+    Q = np.array([5 * math.pi / 6, 2 * math.pi / 3]).reshape(1, 1, 2, 1)
+    K = np.array([0.0, math.pi / 2]).reshape(1, 1, 2, 1)
+    r3 = math.sqrt(3.0)
+    kap, den = orc.conditioning(Q, K, W, None, tau, S, True, return_den=True)
+    np.testing.assert_allclose(den[0, 0], [-r3 / 2, -0.5 + r3 / 2], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(kap[0, 0], [1.0, 2 + r3], rtol=1e-13)
+    kap, den = orc.conditioning(Q, K, W, None, tau, S, False, return_den=True)
+    np.testing.assert_allclose(den[0, 0], [-r3 / 2 + 0.5, -0.5 + r3 / 2], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(kap[0, 0], [2 + r3, 2 + r3], rtol=1e-13)
+
+
 # --- backward: closed form in V and finite differences --------------------------------
 
 @pytest.mark.parametrize("variant", [S, NS])
