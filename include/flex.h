@@ -27,6 +27,9 @@
  *     den [B,H,N]; W1, W2 [H,m,d] fp32 (one frequency matrix per head, as in the
  *     paper's parameter analysis, Appendix B); tau [H] fp32; Phi [B,H,N,2m] with
  *     features ordered [cos block | sin block] as printed in Eq.(phi_n)/(phi_non).
+ *     The frequencies are always per head, so the descriptor has no head stride
+ *     for W1/W2: a caller who shares one matrix across heads passes it H times
+ *     (H*m*d floats); dW1/dW2 are then per head and the caller sums them.
  *   - Pointers must be 16-byte aligned.
  *   - The workspace `ws` is caller-owned device memory of at least
  *     flex_workspace_size() bytes for the same descriptor and pass; its contents
@@ -39,7 +42,8 @@
  *   - Supported shapes: N >= 1 (a ragged last chunk is masked); d = dv in
  *     {32, 64, 128}; m in {64, 128, 256} with the combinations
  *     (d, m) = (32, 64), (64, 64), (64, 128), (128, 256) with io_dtype FLEX_BF16,
- *     and (32, 64) with FLEX_F32; chunk = 64.  Others return FLEX_ERR_UNSUPPORTED.
+ *     and (32, 64) with FLEX_F32; chunk in {0, 16, 32, 64}.  Others return
+ *     FLEX_ERR_UNSUPPORTED.
  *     Every supported shape has the forward and the backward.  (128, 256) runs
  *     as four groups of 64 frequencies whose sums are combined in a fixed
  *     order; its forward workspace holds an fp32 numerator/denominator buffer.
@@ -80,7 +84,12 @@ typedef struct {
   int32_t m;            /* frequencies per matrix (the paper's n); d' = 2m          */
   int32_t variant;      /* flex_variant                                             */
   int32_t causal;       /* 0: all j; 1: j <= i                                      */
-  int32_t chunk;        /* causal chunk length; 0 selects 64; only 64 is supported  */
+  int32_t chunk;        /* causal chunk length C in {16, 32, 64}; 0 selects 64.  The
+                           causal forward forms tril(phi(Q_c) phi(K_c)^T)[V_c ; 1]
+                           inside each C-token chunk and carries earlier tokens
+                           in the running state; results agree across C up to
+                           rounding.  The non-causal forward, the backward and
+                           the segment split do not depend on it.               */
   int32_t segments;     /* sequence segments per (b,h); 0 selects a heuristic       */
   int32_t io_dtype;     /* flex_dtype of Q, K, V, O, dO and Phi                     */
   int32_t grad_dtype;   /* flex_dtype of dQ, dK, dV; only FLEX_F32 is supported     */
@@ -105,7 +114,8 @@ int32_t flex_workspace_size(const flex_desc* desc, int32_t pass, size_t* bytes);
  *   W2  [H,m,d]     fp32, omega_2; must be NULL for the stationary variant
  *   tau [H]         fp32, log of the norm-factor scale
  *   Phi [B,H,N,2m]  io_dtype output, [cos | sin] feature blocks
- * `causal` and `dv` are ignored. */
+ * `dv`, `causal`, `chunk`, `segments` and `grad_dtype` are ignored (any value
+ * is accepted); the workspace may be NULL (flex_workspace_size gives 0). */
 int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1,
                          const float* W2, const float* tau, void* Phi,
                          void* ws, size_t ws_bytes, void* stream);

@@ -16,10 +16,16 @@ namespace {
 constexpr int kChunk = 64;
 constexpr int kCUs = 256;
 
+// Chunk lengths of the causal forward sweep.  The segment split, the state
+// pre-pass and the non-causal sweep work in 64-token chunks whatever the
+// chunk; the backward in 32-token chunks.
+bool chunk_supported(int c) { return c == 0 || c == 16 || c == 32 || c == 64; }
+int chunk_of(const flex_desc* d) { return d->chunk == 0 ? kChunk : d->chunk; }
+
 bool shape_supported(const flex_desc* d) {
   if (d->dv != d->d) return false;
   if (d->grad_dtype != FLEX_F32) return false;
-  if (d->chunk != 0 && d->chunk != kChunk) return false;
+  if (!chunk_supported(d->chunk)) return false;
   const bool bf = d->io_dtype == FLEX_BF16;
   if (d->d == 32 && d->m == 64) return true;
   if (d->d == 64 && d->m == 64) return bf;
@@ -27,9 +33,6 @@ bool shape_supported(const flex_desc* d) {
   if (d->d == 128 && d->m == 256) return bf;
   return false;
 }
-
-// The backward additionally needs the (d, m) shapes its kernels are built for.
-bool bwd_supported(const flex_desc*) { return true; }
 
 // 0 = ok, else a flex_status: the descriptor's fields, without the shape list
 int32_t check_desc_fields(const flex_desc* d) {
@@ -54,6 +57,19 @@ int32_t check_desc(const flex_desc* d) {
   if (st != FLEX_OK) return st;
   if (!shape_supported(d)) return FLEX_ERR_UNSUPPORTED;
   return FLEX_OK;
+}
+
+// The feature map ignores dv, causal, chunk, segments and grad_dtype: the
+// descriptor is checked with those fields set to values every shape accepts.
+int32_t check_fmap_desc(const flex_desc* d) {
+  if (!d) return FLEX_ERR_INVALID_ARG;
+  flex_desc c = *d;
+  c.dv = c.d;
+  c.causal = 0;
+  c.chunk = 0;
+  c.segments = 0;
+  c.grad_dtype = FLEX_F32;
+  return check_desc(&c);
 }
 
 // Shapes of the decode step (one generic kernel): d = dv, a multiple of 4 up to
@@ -398,9 +414,8 @@ int32_t flex_workspace_size(const flex_desc* desc, int32_t pass, size_t* bytes) 
     *bytes = awd_layout(desc).total;
     return FLEX_OK;
   }
-  const int32_t st = check_desc(desc);
+  const int32_t st = pass == FLEX_PASS_FEATURE_MAP ? check_fmap_desc(desc) : check_desc(desc);
   if (st != FLEX_OK) return st;
-  if (pass == FLEX_PASS_BWD && !bwd_supported(desc)) return FLEX_ERR_UNSUPPORTED;
   *bytes = ws_bytes_of(desc, pass);
   return FLEX_OK;
 }
@@ -408,7 +423,7 @@ int32_t flex_workspace_size(const flex_desc* desc, int32_t pass, size_t* bytes) 
 int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1, const float* W2,
                          const float* tau, void* Phi, void* ws, size_t ws_bytes, void* stream) {
   (void)ws; (void)ws_bytes;
-  const int32_t st = check_desc(desc);
+  const int32_t st = check_fmap_desc(desc);
   if (st != FLEX_OK) return st;
   if (!X || !W1 || !tau || !Phi) return FLEX_ERR_INVALID_ARG;
   if ((desc->variant == FLEX_NONSTATIONARY) != (W2 != nullptr)) return FLEX_ERR_INVALID_ARG;
@@ -457,9 +472,13 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
   a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
   a.sub = fwd_sub_of(desc, P0);
   if (desc->causal) {
+    // the sweep's chunks of chunk_of(desc) tokens: a segment spans the same
+    // tokens as its 64-token pre-pass chunks
+    a.sweep_chunk = chunk_of(desc);
     a.sweep_groups = a.segments;
-    a.sweep_cps = a.chunks_per_seg;
+    a.sweep_cps = a.chunks_per_seg * (kChunk / a.sweep_chunk);
   } else {
+    a.sweep_chunk = kChunk;
     a.sweep_cps = a.nchunks < kSweepChunks ? a.nchunks : kSweepChunks;
     a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
   }
@@ -486,7 +505,6 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
                          size_t ws_bytes, void* stream) {
   const int32_t st = check_desc(desc);
   if (st != FLEX_OK) return st;
-  if (!bwd_supported(desc)) return FLEX_ERR_UNSUPPORTED;
   const bool ns = desc->variant == FLEX_NONSTATIONARY;
   if (!Q || !K || !V || !W1 || !tau || !O || !den || !dO || !dQ || !dK || !dV || !dW1)
     return FLEX_ERR_INVALID_ARG;

@@ -391,13 +391,13 @@ __global__ __launch_bounds__(M / 16 * WAVE) void k_awd_wgrad(AwdArgs a) {
   typedef FreqSlice<T, D, 16, NS> FS;
   __shared__ __align__(16) IO XL[StX::LDS_ELEMS];
   __shared__ __align__(16) IO DL[StD::LDS_ELEMS];
-  __shared__ float SSQ[ROWS];
+  __shared__ typename StX::Ssq SSQ[ROWS];
   __shared__ float TRED[NW];
   const int h = blockIdx.x, part = blockIdx.y;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
   FS fs;
   fs.load(a.W1 + (size_t)h * M * D, NS ? a.W2 + (size_t)h * M * D : nullptr, w * 16);
-  const float inv_c = __expf(-a.tau[h]);
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
   const int nch = (a.N + ROWS - 1) / ROWS, per_side = a.B * nch, U = 2 * per_side;
   const int u0 = (int)((long long)U * part / a.parts), u1 = (int)((long long)U * (part + 1) / a.parts);
   f32x4 dw[FS::PR][D / 16];
@@ -446,14 +446,14 @@ __global__ __launch_bounds__(M / 16 * WAVE) void k_awd_wgrad(AwdArgs a) {
     f32x4 dp[2][FS::PR];
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
-      f32x4 p[FS::PR];
+      ProjT<T> p[FS::PR];
       project_rows_lds<T, D, 16, NS, StX::LD>(fs, XL, tt, p);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int tl = tt * 16 + 4 * g + i, tok = n0 + tl;
         const bool ok = tok < a.N;
-        const float ssq = SSQ[tl];
-        const float sc = ok ? a.s_const * __expf(ssq * inv_c) : 0.f;
+        const auto ssq = SSQ[tl];
+        const float sc = row_scale(ssq, inv_c, a.s_const, ok);
         const int f = w * 16 + r;
         // rows past the end were staged as zeros
         const float da = io_to_float(DL[tl * StD::LD + f]);

@@ -28,8 +28,8 @@ namespace flex {
 
 // Feature fragment (as in the forward) plus, for the nonstationary variant,
 // the fragment of d phi / d P2 up to sign: slots [s e sin P2 cos P1 | s e sin P2 sin P1].
-template <class T, int FT, bool NS>
-__device__ __forceinline__ void features_psi(const f32x4 (&p)[NS ? 2 * FT : FT], int ft, float scale,
+template <class T, int FT, bool NS, class P>
+__device__ __forceinline__ void features_psi(const P (&p)[NS ? 2 * FT : FT], int ft, float scale,
                                              Frag<T>& phi, Frag<T>& psi) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) IO XV2[2][StV::LDS_ELEMS];
   __shared__ float GS2[2][SH::CH][2];
   __shared__ float DEN2[2][SH::CH];
-  __shared__ float SSQ2[2][SH::CH], SSK2[2][SH::CH];
+  __shared__ typename StX::Ssq SSQ2[2][SH::CH], SSK2[2][SH::CH];
   // per-token feature scales: s e(k) for keys, s e(q) / den for queries
   __shared__ __attribute__((aligned(16))) float SCK2[2][SH::CH], SCQ2[2][SH::CH];
 
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     dn_next = den[min(c0 * SH::CH + (int)(threadIdx.x % SH::CH), a.N - 1)];   // rows past N unused
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
-  const float inv_c = __expf(-a.tau[h]);
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
 
   f32x4 ST[SH::DVT1][SH::FC], RT[SH::DVT1][SH::FC];
 #pragma unroll
@@ -253,8 +253,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     IO* XV = XV2[par];
     float (*GS)[2] = GS2[par];
     float* DEN = DEN2[par];
-    float* SSQ = SSQ2[par];
-    float* SSK = SSK2[par];
+    typename StX::Ssq* SSQ = SSQ2[par];
+    typename StX::Ssq* SSK = SSK2[par];
     float* SCK = SCK2[par];
     float* SCQ = SCQ2[par];
     const int tok0 = c * SH::CH;
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // dP, [token][projection row]
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS2[NBUF][SH::CH][2];
-  __shared__ float SSQ2[NBUF][SH::CH];
+  __shared__ typename StX::Ssq SSQ2[NBUF][SH::CH];
   __shared__ __attribute__((aligned(16))) float SCK2[NBUF][SH::CH];   // per-token key scale s e(k)
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
@@ -384,7 +384,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, w);
-  const float inv_c = __expf(-a.tau[h]);
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
 
   f32x4 ST[SH::DVT1][SH::FC];
   if (a.fstate) {
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     IO* XV = XV2[par];
     IO* XDO = XDO2[par];
     float (*GS)[2] = GS2[par];
-    float* SSQ = SSQ2[par];
+    typename StX::Ssq* SSQ = SSQ2[par];
     float* SCK = SCK2[par];
     const int tok0 = c * SH::CH;
     if (!KEEP_FS) fs.load_frags(wproj);
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     }
     if (NBUF == 1) __syncthreads();   // single buffer: the previous chunk's reads are done
     sq.store(XQ, SSQ);
-    sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
+    sk.store(XK, SCK, [&](int t, auto ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV); sdo.store(XDO);
     if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
     {
@@ -455,8 +455,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     Frag<T> phq[SH::FT][SH::TT], psq[SH::FT][SH::TT];
 #pragma unroll
     for (int tt = 0; tt < SH::TT; ++tt) {
-      f32x4 p[SH::PR];
-      float ssq;
+      ProjT<T> p[SH::PR];
+      typename StX::Ssq ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
@@ -666,7 +666,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) char REDRL[NW * SLOT];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS2[NBUF][SH::CH][2];
-  __shared__ float SSQ2[NBUF][SH::CH], SSK2[NBUF][SH::CH];
+  __shared__ typename StX::Ssq SSQ2[NBUF][SH::CH], SSK2[NBUF][SH::CH];
   __shared__ float TRED[SH::NT];
   __shared__ __attribute__((aligned(16))) float GP[SH::CH][NW][4];   // per-lane-group shares of g
   typedef float RedRow[QG * 16][RP];
@@ -696,7 +696,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag_kv, h, NW, w);
-  const float inv_c = __expf(-a.tau[h]);
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
 
   f32x4 RT[SH::DVT1][SH::FC];
   {
@@ -735,8 +735,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     IO* XV = XV2[par];
     IO* XDO = XDO2[par];
     float (*GS)[2] = GS2[par];
-    float* SSQ = SSQ2[par];
-    float* SSK = SSK2[par];
+    typename StX::Ssq* SSQ = SSQ2[par];
+    typename StX::Ssq* SSK = SSK2[par];
     const int tok0 = c * SH::CH;
     // this chunk's projection fragments: in flight across the staging barrier
     FreqSlice<T, D, FW, NS> fs;
@@ -780,8 +780,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     if (CAUSAL) {
 #pragma unroll
       for (int tt = 0; tt < SH::TT; ++tt) {
-        f32x4 p[SH::PR];
-        float ssq;
+        ProjT<T> p[SH::PR];
+        typename StX::Ssq ssq;
         project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
         const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
 #pragma unroll
@@ -794,8 +794,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     Frag<T> phk[SH::FT][SH::TT], psk[SH::FT][SH::TT];
 #pragma unroll
     for (int tt = 0; tt < SH::TT; ++tt) {
-      f32x4 p[SH::PR];
-      float ssq;
+      ProjT<T> p[SH::PR];
+      typename StX::Ssq ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll

@@ -21,6 +21,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16;
 
 constexpr int WAVE = 64;
@@ -78,6 +79,16 @@ __device__ __forceinline__ void mma(f32x4& c, const Frag<float>& a, const Frag<f
 
 template <class T> struct IsBf16 { static constexpr bool value = false; };
 template <> struct IsBf16<__bf16> { static constexpr bool value = true; };
+
+// Projection tiles and squared row norms by operand type.  The bf16 path
+// projects on MFMA in fp32 (revolutions); the fp32 path forms the projection
+// and the squared norms in float64, so that the phase handed to the
+// trigonometric functions is exact to float64 rounding whatever its size.
+template <class T> struct ProjTile { typedef f32x4 type; };
+template <> struct ProjTile<float> { typedef f64x4 type; };
+template <class T> using ProjT = typename ProjTile<T>::type;
+template <class T> struct SsqType { typedef float type; };
+template <> struct SsqType<float> { typedef double type; };
 
 // Storage type of the io tensors for an operand type.
 template <class T> struct Io;
@@ -232,6 +243,41 @@ struct FreqSlice {
   }
 };
 
+// fp32 path: the wave's frequency rows themselves (no operand fragments).  The
+// projection is formed in float64 on the vector ALU from these rows (W'1, W'2
+// exactly as (w1 +- w2)/2 in float64), so no frequency is rounded before it
+// multiplies x.  The rows of matrix 1 start at `a`, those of matrix 2 at `b`,
+// both with row stride D.  A prepared block holds the same rows as plain
+// floats, [matrix][FW][D], in the space the generic slice's fragments take.
+template <int D, int FW, bool NS>
+struct FreqSlice<float, D, FW, NS> {
+  static constexpr int FT = FW / 16;
+  static constexpr int PR = NS ? 2 * FT : FT;
+  static constexpr int KD = D / 32;
+  static constexpr int NSPLIT = 1;
+  static constexpr int NFRAG = PR * KD;   // Frag<float> units of the prepared rows
+  static_assert(NFRAG * WAVE * 8 == (NS ? 2 : 1) * FW * D, "prepared rows fill the fragment block");
+  const float* a;
+  const float* b;
+
+  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
+    a = W1 + (size_t)f0 * D;
+    b = NS ? W2 + (size_t)f0 * D : nullptr;
+  }
+  __device__ __forceinline__ void store_frags(Frag<float>* out) const {
+    float* o = reinterpret_cast<float*>(out);
+    const int l = threadIdx.x % WAVE;
+    for (int i = l; i < FW * D; i += WAVE) {
+      o[i] = a[i];
+      if (NS) o[FW * D + i] = b[i];
+    }
+  }
+  __device__ __forceinline__ void load_frags(const Frag<float>* in) {
+    a = reinterpret_cast<const float*>(in);
+    b = NS ? a + FW * D : nullptr;
+  }
+};
+
 // A-operand fragments of W'^T (rows = input dimension d, k = projection rows of
 // this wave, paired tiles) in radians, in the operand type.  Used for
 // dX = dP W'.  Projection row tile pr < FT is W'1 (or W), pr >= FT is W'2.
@@ -351,35 +397,6 @@ __global__ __launch_bounds__(WAVE) void k_prep_freqs2(const float* W1, const flo
 
 
 
-// Projection of one 16-token tile onto a wave's frequency slice, plus the
-// squared row norm.  X points at the token rows of this (b,h) slice; rows at
-// or beyond n_valid read as zero.  p[pr] receives the P^T tile (revolutions).
-template <class T, int D, int FW, bool NS>
-__device__ __forceinline__ void project_tile(const FreqSlice<T, D, FW, NS>& fs,
-                                             const typename Io<T>::type* __restrict__ X,
-                                             int tok0, int n_valid,
-                                             f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR], float& ssq) {
-  typedef FreqSlice<T, D, FW, NS> FS;
-  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const int tok = tok0 + r;
-  const bool ok = tok < n_valid;
-#pragma unroll
-  for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
-  float s = 0.f;
-#pragma unroll
-  for (int ks = 0; ks < FS::KD; ++ks) {
-    Frag<T> x;
-    load8(x, X + (size_t)tok * D + ks * 32 + 8 * g, ok);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) { const float v = x.get(j); s += v * v; }
-#pragma unroll
-    for (int pr = 0; pr < FS::PR; ++pr)
-#pragma unroll
-      for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], fs.w[sp][pr][ks], x);
-  }
-  ssq = group_sum(s);
-}
-
 // Trigonometric values of a projection in revolutions: cos(2 pi p), sin(2 pi p).
 // v_sin_f32 / v_cos_f32 take revolutions and reduce the argument themselves:
 // measured on gfx950 over |p| <= 200 their absolute error is 1.25e-7, lower
@@ -389,12 +406,24 @@ __device__ __forceinline__ void sincos_rev(float p, float& s, float& c) {
   c = __builtin_amdgcn_cosf(p);
 }
 __device__ __forceinline__ float cos_rev(float p) { return __builtin_amdgcn_cosf(p); }
+// fp32 path: a float64 phase in revolutions.  p - rint(p) is exact in float64
+// and lies in [-1/2, 1/2]; the angle 2 pi r is then at most pi in size, and
+// sine and cosine are taken in float64 (OCML) and rounded once to fp32.
+constexpr double TWO_PI_D = 6.283185307179586;
+__device__ __forceinline__ void sincos_rev(double p, float& s, float& c) {
+  const double t = (p - rint(p)) * TWO_PI_D;
+  double sd, cd;
+  sincos(t, &sd, &cd);
+  s = (float)sd;
+  c = (float)cd;
+}
+__device__ __forceinline__ float cos_rev(double p) { return (float)cos((p - rint(p)) * TWO_PI_D); }
 
 // Feature epilogue for one frequency tile ft of one 16-token tile:
 // scale = s * e(x) (0 for rows that are not valid).  Returns the operand
 // fragment [cos-type features 4g..4g+3 | sin-type features 4g..4g+3].
-template <class T, int FT, bool NS>
-__device__ __forceinline__ Frag<T> features(const f32x4 (&p)[NS ? 2 * FT : FT], int ft, float scale) {
+template <class T, int FT, bool NS, class P>
+__device__ __forceinline__ Frag<T> features(const P (&p)[NS ? 2 * FT : FT], int ft, float scale) {
   Frag<T> f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -411,5 +440,17 @@ __device__ __forceinline__ Frag<T> features(const f32x4 (&p)[NS ? 2 * FT : FT], 
 __device__ __forceinline__ float row_scale(float ssq, float inv_c, float s_const, bool ok) {
   return ok ? s_const * __expf(ssq * inv_c) : 0.0f;
 }
+// fp32 path: the squared norm and 1/exp(tau) in float64, one rounding at the end.
+__device__ __forceinline__ float row_scale(double ssq, double inv_c, float s_const, bool ok) {
+  return ok ? (float)((double)s_const * exp(ssq * inv_c)) : 0.0f;
+}
+// 1 / exp(tau) in the precision of the path's norm factor.
+template <class T> struct InvC {
+  __device__ static __forceinline__ float of(float tau) { return __expf(-tau); }
+};
+template <> struct InvC<float> {
+  __device__ static __forceinline__ double of(float tau) { return exp(-(double)tau); }
+};
+template <class T> __device__ __forceinline__ auto inv_c_of(float tau) { return InvC<T>::of(tau); }
 
 }  // namespace flex

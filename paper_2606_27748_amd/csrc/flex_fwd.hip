@@ -52,7 +52,7 @@ void k_fwd_state(FwdArgs a) {
     sv.fetch(V, c0 * CHUNK, a.N);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
-  const float inv_c = __expf(-a.tau[h]);
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
 
   f32x4 S[SH::FC][SH::DVT1];
 #pragma unroll
@@ -72,7 +72,7 @@ void k_fwd_state(FwdArgs a) {
     const int tok0 = c * CHUNK;
     if (!KEEP_FS) fs.load_frags(wproj);
     __syncthreads();
-    sk.store(XK, SCK, [&](int t, float ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
+    sk.store(XK, SCK, [&](int t, auto ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV);
     {
       const int t1 = c + 1 < c1 ? tok0 + CHUNK : tok0;   // the last chunk refetches itself (unused)
@@ -154,20 +154,30 @@ __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1
 // ADD: add this frequency group's numerator and denominator to the sums the
 // earlier groups stored; the old sums are loaded at the start of each chunk,
 // so their latency overlaps the chunk's work.
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG, bool ADD>
+// CH: tokens per chunk of the causal sweep (16, 32 or 64; the intra-chunk
+// term covers j <= i within a chunk, earlier tokens enter through the carried
+// state).  Token contractions run in 32-token MFMA k-steps; a 16-token chunk
+// pads its k-step with zero rows (staged once, never written).
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG, bool ADD, int CH>
 __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
-  typedef Shape<T, D, FW, NW, NS> SH;
+  typedef Shape<T, D, FW, NW, NS, CH> SH;
   typedef typename Io<T>::type IO;
-  typedef RowStage<IO, D, SH::NT> StX;
-  typedef RowStage<IO, SH::DV, SH::NT> StV;
-  constexpr int XV_N = CAUSAL ? StV::LDS_ELEMS : 8;
+  typedef RowStage<IO, D, SH::NT, CH> StX;
+  typedef RowStage<IO, SH::DV, SH::NT, CH> StV;
+  constexpr int TT = CH / 16;                  // token tiles per chunk
+  constexpr int KT = (CH + 31) / 32;           // 32-token k-steps per chunk
+  constexpr int ROWS = KT * 32;                // token rows of the k-step operands
+  static_assert(CH == 16 || CH == 32 || CH == 64, "chunk of 16, 32 or 64 tokens");
+  static_assert(CAUSAL || CH == CHUNK, "the non-causal sweep uses 64-token chunks");
+  constexpr int XV_N = CAUSAL ? ROWS * StV::LD : 8;
   constexpr int LDP = SH::FC * 16 + 4;     // [token][feature] rows of a wave's phi(K) block
-  constexpr int PT_N = CAUSAL ? CHUNK * LDP : 8;
+  constexpr int PT_N = CAUSAL ? ROWS * LDP : 8;
   constexpr int C4 = SH::DV / 4;                                // float4 columns of a row
   constexpr int NIT = (QG * 16 * C4 + SH::NT - 1) / SH::NT;    // readout items per thread and round
+  static_assert(TT % QG == 0, "whole reduction rounds per chunk");
   __shared__ __attribute__((aligned(16))) IO XQ[StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XK[CAUSAL ? StX::LDS_ELEMS : 8];
-  __shared__ float SSQ[CHUNK], SSK[CHUNK];
+  __shared__ typename StX::Ssq SSQ[CH], SSK[CH];
   __shared__ __attribute__((aligned(16))) IO XV[XV_N];   // [token][value col]
   __shared__ __attribute__((aligned(16))) T PT[NW][PT_N];
   __shared__ __attribute__((aligned(16))) float RED[NW][QG * 16][SH::RPAD];
@@ -177,8 +187,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   const WgCoord wc = wg_coord(a.sweep_groups, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int nch = (a.N + CH - 1) / CH;
   const int c0 = seg * a.sweep_cps;
-  const int c1 = min(c0 + a.sweep_cps, a.nchunks);
+  const int c1 = min(c0 + a.sweep_cps, nch);
   const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
   const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
   const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
@@ -188,11 +199,17 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   StX sq, sk;
   StV sv;
   if (c0 < c1) {
-    sq.fetch(Q, c0 * CHUNK, a.N);
-    if (CAUSAL) sk.fetch(K, c0 * CHUNK, a.N);
-    if (CAUSAL) sv.fetch(V, c0 * CHUNK, a.N);
+    sq.fetch(Q, c0 * CH, a.N);
+    if (CAUSAL) sk.fetch(K, c0 * CH, a.N);
+    if (CAUSAL) sv.fetch(V, c0 * CH, a.N);
   }
-  const float inv_c = __expf(-a.tau[h]);
+  if (CAUSAL && CH < ROWS) {
+    // zero k-step padding rows of V and of this wave's phi(K) block (both
+    // zero, so no product with uninitialised LDS enters a sum)
+    for (int i = threadIdx.x; i < (ROWS - CH) * StV::LD; i += SH::NT) XV[CH * StV::LD + i] = IO(0);
+    for (int i = l; i < (ROWS - CH) * LDP; i += WAVE) PT[w][CH * LDP + i] = T(0.0f);
+  }
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
 
   // carry-in state (exclusive prefix for causal, total for non-causal)
   f32x4 S[SH::FC][SH::DVT1];
@@ -218,7 +235,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   }
 
   for (int c = c0; c < c1; ++c) {
-    const int tok0 = c * CHUNK;
+    const int tok0 = c * CH;
     __syncthreads();
     sq.store(XQ, SSQ);
     if (CAUSAL) sk.store(XK, SSK);
@@ -226,7 +243,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     __syncthreads();
     // next chunk's rows
     {
-      const int t1 = c + 1 < c1 ? tok0 + CHUNK : tok0;   // the last chunk refetches itself (unused)
+      const int t1 = c + 1 < c1 ? tok0 + CH : tok0;   // the last chunk refetches itself (unused)
       sq.fetch(Q, t1, a.N);
       if (CAUSAL) sk.fetch(K, t1, a.N);
       if (CAUSAL) sv.fetch(V, t1, a.N);
@@ -252,8 +269,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     Frag<T> pk[CAUSAL ? SH::FT : 1][TT];
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
-      f32x4 p[SH::PR];
-      float ssq;
+      ProjT<T> p[SH::PR];
+      typename StX::Ssq ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
@@ -279,7 +296,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     }
 
     // intra-chunk kernel matrix, transposed: rows = key tokens, cols = query tokens
-    Frag<T> ap[CAUSAL ? SH::KT : 1][TT];
+    Frag<T> ap[CAUSAL ? KT : 1][TT];
     if (CAUSAL) {
 #pragma unroll
       for (int tq = 0; tq < TT; ++tq) {
@@ -298,16 +315,16 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
           }
         }
 #pragma unroll
-        for (int ks = 0; ks < SH::KT; ++ks) ap[ks][tq] = pair_tiles<T>(at[2 * ks], at[2 * ks + 1]);
+        for (int ks = 0; ks < KT; ++ks) ap[ks][tq] = pair_tiles<T>(at[2 * ks], 2 * ks + 1 < TT ? at[(2 * ks + 1) % TT] : zero4());
       }
     }
 
-    Frag<T> vf[CAUSAL ? SH::DVT : 1][SH::KT];
+    Frag<T> vf[CAUSAL ? SH::DVT : 1][KT];
     if (CAUSAL) {
 #pragma unroll
       for (int dt = 0; dt < SH::DVT; ++dt)
 #pragma unroll
-        for (int ks = 0; ks < SH::KT; ++ks) vf[dt][ks] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
+        for (int ks = 0; ks < KT; ++ks) vf[dt][ks] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
     }
 
     // readout partials, reduced across waves in groups of QG query tiles
@@ -322,7 +339,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
           f32x4 acc = zero4();
           if (CAUSAL) {
 #pragma unroll
-            for (int ks = 0; ks < SH::KT; ++ks)
+            for (int ks = 0; ks < KT; ++ks)
               if (32 * ks <= 16 * tq + 15) mma(acc, dt < SH::DVT ? vf[dt][ks] : ones, ap[ks][tq]);
           }
 #pragma unroll
@@ -333,7 +350,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       if (CAUSAL && q0 + QG >= TT) {
         // state update S' += phi(K)^T [V | 1] with this wave's transposed phi(K)
 #pragma unroll
-        for (int ks = 0; ks < SH::KT; ++ks)
+        for (int ks = 0; ks < KT; ++ks)
 #pragma unroll
           for (int fc = 0; fc < SH::FC; ++fc) {
             const Frag<T> pkt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16);
@@ -417,7 +434,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
   constexpr int LDF = F + VEC;                 // row stride of the staged features
   constexpr int NVO = CHUNK * F / VEC;         // output vectors per chunk
   __shared__ __attribute__((aligned(16))) IO XL[StX::LDS_ELEMS];
-  __shared__ float SSQ[CHUNK];
+  __shared__ typename StX::Ssq SSQ[CHUNK];
   __shared__ __attribute__((aligned(16))) IO PH[CHUNK * LDF];
   const int bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
@@ -429,7 +446,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
   if (c0 < c1) sx.fetch(X, c0 * CHUNK, a.N);
   FreqSlice<T, D, FW, NS> fs;
   fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
-  const float inv_c = __expf(-a.tau[h]);
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
     __syncthreads();   // the previous chunk's reads of XL and PH are done
@@ -438,8 +455,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
     __syncthreads();
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
-      f32x4 p[SH::PR];
-      float ssq;
+      ProjT<T> p[SH::PR];
+      typename StX::Ssq ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XL, SSQ, tt, p, ssq);
       // the values are produced in fp32 and rounded once to the io dtype
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
@@ -502,12 +519,35 @@ hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st
 // ---------------------------------------------------------------------------
 // Host-side dispatch.
 // ---------------------------------------------------------------------------
+// Causal sweep launch for one chunk length CH (token tiles per cross-wave
+// reduction round: fewer rounds where LDS allows).
+template <class T, int D, int FW, int NW, bool NS, bool ADD, int CH>
+static void launch_causal_sweep(const FwdArgs& a, dim3 grid, hipStream_t st) {
+  typedef Shape<T, D, FW, NW, NS, CH> SH;
+  constexpr int TTc = CH / 16;
+  constexpr int QG0 = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TTc);
+  constexpr int QG = QG0 < TTc ? QG0 : TTc;
+  k_fwd_sweep<T, D, FW, NW, NS, true, QG, ADD, CH><<<grid, SH::NT, 0, st>>>(a);
+}
+
+template <class T, int D, int FW, int NW, bool NS, bool ADD>
+static void launch_sweep(const FwdArgs& a, bool causal, dim3 grid, hipStream_t st) {
+  typedef Shape<T, D, FW, NW, NS> SH;
+  if (!causal) {
+    // one token tile per round: the non-causal sweep then fits several workgroups per CU
+    k_fwd_sweep<T, D, FW, NW, NS, false, 1, ADD, CHUNK><<<grid, SH::NT, 0, st>>>(a);
+  } else if (a.sweep_chunk == 16) {
+    launch_causal_sweep<T, D, FW, NW, NS, ADD, 16>(a, grid, st);
+  } else if (a.sweep_chunk == 32) {
+    launch_causal_sweep<T, D, FW, NW, NS, ADD, 32>(a, grid, st);
+  } else {
+    launch_causal_sweep<T, D, FW, NW, NS, ADD, 64>(a, grid, st);
+  }
+}
+
 template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
-  // token tiles per cross-wave reduction round: fewer rounds where LDS allows;
-  // one for the non-causal sweep, which then fits several workgroups per CU
-  constexpr int QG = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TT);
   const dim3 grid(a.sweep_groups * a.BH);
   const dim3 pgrid(a.segments * a.sub * a.BH);
   // prepared fragments serve the state pre-pass at d > 64, which reloads them
@@ -521,17 +561,10 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   timing_mark(KC_FWD_SWEEP, st, true);
   // only the frequency-group shape (d = 128) adds to an earlier group's sums
   constexpr bool GROUPED = D == 128;
-  if (GROUPED && a.acc == 2) {
-    if (causal)
-      k_fwd_sweep<T, D, FW, NW, NS, true, QG, GROUPED><<<grid, SH::NT, 0, st>>>(a);
-    else
-      k_fwd_sweep<T, D, FW, NW, NS, false, 1, GROUPED><<<grid, SH::NT, 0, st>>>(a);
-  } else {
-    if (causal)
-      k_fwd_sweep<T, D, FW, NW, NS, true, QG, false><<<grid, SH::NT, 0, st>>>(a);
-    else
-      k_fwd_sweep<T, D, FW, NW, NS, false, 1, false><<<grid, SH::NT, 0, st>>>(a);
-  }
+  if (GROUPED && a.acc == 2)
+    launch_sweep<T, D, FW, NW, NS, GROUPED>(a, causal, grid, st);
+  else
+    launch_sweep<T, D, FW, NW, NS, false>(a, causal, grid, st);
   timing_mark(KC_FWD_SWEEP, st, false);
   return hipGetLastError();
 }

@@ -33,6 +33,8 @@ struct FwdArgs {
   int sub;            // state pre-pass workgroups per segment (chunks_per_seg % sub == 0)
   int sweep_groups;   // sweep workgroups per (b,h): the segments (causal) or chunk groups (non-causal)
   int sweep_cps;      // chunks per sweep workgroup
+  int sweep_chunk;    // tokens per chunk of the causal sweep: 16, 32 or 64 (the
+                      // pre-pass, the segments and the non-causal sweep use 64)
   float s_const;      // sigma/sqrt(m) or sigma/(2 sqrt(m))
   // Frequency groups: W1/W2 point at this group's rows, w_stride is the
   // element stride between heads.  acc = 0 writes O (and den) directly; 1 and

@@ -56,28 +56,36 @@ struct RowStage {
       }
     }
   }
+  // Squared norms are summed in fp32 for bf16 rows and in float64 for fp32
+  // rows (the fp32 path's norm factor is formed in float64).
+  typedef typename SsqType<IO>::type Ssq;
   // store, plus the squared norm of every row into ssq[ROWS] (the VPR vectors
   // of a row sit in VPR consecutive lanes: summed with lane shuffles)
-  __device__ __forceinline__ void store(IO* lds, float* ssq) const {
-    store(lds, ssq, [](int, float s) { return s; });
+  __device__ __forceinline__ void store(IO* lds, Ssq* ssq) const {
+    store(lds, ssq, [](int, Ssq s) { return s; });
   }
   // store, plus f(row, squared norm of the row) into out[ROWS]
-  template <class F>
-  __device__ __forceinline__ void store(IO* lds, float* out, F f) const {
+  template <class OUT, class F>
+  __device__ __forceinline__ void store(IO* lds, OUT* out, F f) const {
     static_assert(NT % VPR == 0 && VPR <= WAVE, "a row's vectors must share a wave");
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int v = threadIdx.x + i * NT;
-      float s = 0.f;
+      Ssq s = 0;
       if (v < NV) {
         const int t = v / VPR, c = v % VPR;
         const uint4 x = vec(i);
         *reinterpret_cast<uint4*>(lds + t * LD + c * VEC) = x;
         const IO* e = reinterpret_cast<const IO*>(&x);
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) { const float y = io_to_float(e[j]); s += y * y; }
+        for (int j = 0; j < VEC; ++j) { const Ssq y = io_to_float(e[j]); s += y * y; }
       }
-      s = lane_sum<VPR>(s);
+      if constexpr (sizeof(Ssq) == 4) {
+        s = lane_sum<VPR>(s);
+      } else {
+#pragma unroll
+        for (int o = 1; o < VPR; o <<= 1) s += __shfl_xor(s, o);
+      }
       if (v < NV && v % VPR == 0) out[v / VPR] = f(v / VPR, s);
     }
   }
@@ -109,26 +117,80 @@ __device__ __forceinline__ void lds_row8(Frag<float>& f, const float* row, int c
   f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
 }
 
+// fp32 path: one projection tile in float64 on the vector ALU.  Lane (r, g)
+// forms tile element i of projection row tile pr as the dot product of token
+// row xr(i) with frequency row fr(i) of its matrix pair; W'1 = (w1 + w2)/2 and
+// W'2 = (w1 - w2)/2 are exact in float64.  ROWS_AS_TOKENS = false: the tile
+// holds frequencies 4g+i (rows) x token r (cols), as the MFMA tile of
+// project_tile_lds; true: tokens 4g+i x frequency r, as project_rows_lds.
+template <int D, int FW, bool NS, int LD, bool ROWS_AS_TOKENS>
+__device__ __forceinline__ void project_f64(const FreqSlice<float, D, FW, NS>& fs, const float* X, int tt,
+                                            f64x4 (&p)[FreqSlice<float, D, FW, NS>::PR]) {
+  typedef FreqSlice<float, D, FW, NS> FS;
+  constexpr double INV_2PI_D = 0.15915494309189535;
+  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+#pragma unroll
+  for (int ft = 0; ft < FS::FT; ++ft)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tok = ROWS_AS_TOKENS ? tt * 16 + 4 * g + i : tt * 16 + r;
+      const int fr = ROWS_AS_TOKENS ? ft * 16 + r : ft * 16 + 4 * g + i;
+      const float* xr = X + tok * LD;
+      const float* wa = fs.a + (size_t)fr * D;
+      const float* wb = NS ? fs.b + (size_t)fr * D : nullptr;
+      double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+      for (int k = 0; k < D; k += 4) {
+        const float4 x4 = *reinterpret_cast<const float4*>(xr + k);
+        const float4 a4 = *reinterpret_cast<const float4*>(wa + k);
+        const double xv[4] = {x4.x, x4.y, x4.z, x4.w};
+        const double av[4] = {a4.x, a4.y, a4.z, a4.w};
+        if (NS) {
+          const float4 b4 = *reinterpret_cast<const float4*>(wb + k);
+          const double bv[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            s1 = fma(xv[j], av[j] + bv[j], s1);
+            s2 = fma(xv[j], av[j] - bv[j], s2);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) s1 = fma(xv[j], av[j], s1);
+        }
+      }
+      if (NS) {
+        p[ft][i] = s1 * (0.5 * INV_2PI_D);
+        p[FS::FT + ft][i] = s2 * (0.5 * INV_2PI_D);
+      } else {
+        p[ft][i] = s1 * INV_2PI_D;
+      }
+    }
+}
+
 // Projection of one 16-token tile (rows staged in LDS, row stride LD) onto a
 // wave's frequency slice, plus the squared row norm (summed over lane groups).
-template <class T, int D, int FW, bool NS, int LD>
+template <class T, int D, int FW, bool NS, int LD, class S>
 __device__ __forceinline__ void project_tile_lds(const FreqSlice<T, D, FW, NS>& fs,
-                                                 const typename Io<T>::type* X, const float* ssq_rows,
-                                                 int tt, f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR],
-                                                 float& ssq) {
+                                                 const typename Io<T>::type* X, const S* ssq_rows,
+                                                 int tt, ProjT<T> (&p)[FreqSlice<T, D, FW, NS>::PR],
+                                                 S& ssq) {
   typedef FreqSlice<T, D, FW, NS> FS;
   const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const typename Io<T>::type* row = X + (tt * 16 + r) * LD;
+  if constexpr (!IsBf16<T>::value) {
+    project_f64<D, FW, NS, LD, false>(fs, X, tt, p);
+  } else {
+    const typename Io<T>::type* row = X + (tt * 16 + r) * LD;
 #pragma unroll
-  for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
+    for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
 #pragma unroll
-  for (int ks = 0; ks < FS::KD; ++ks) {
-    Frag<T> x;
-    lds_row8(x, row, ks * 32 + 8 * g);
+    for (int ks = 0; ks < FS::KD; ++ks) {
+      Frag<T> x;
+      lds_row8(x, row, ks * 32 + 8 * g);
 #pragma unroll
-    for (int pr = 0; pr < FS::PR; ++pr)
+      for (int pr = 0; pr < FS::PR; ++pr)
 #pragma unroll
-      for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], fs.w[sp][pr][ks], x);
+        for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], fs.w[sp][pr][ks], x);
+    }
   }
   ssq = ssq_rows[tt * 16 + r];
 }
@@ -206,20 +268,24 @@ __device__ __forceinline__ Frag<T> pair_tiles(const f32x4& a, const f32x4& b) {
 template <class T, int D, int FW, bool NS, int LD>
 __device__ __forceinline__ void project_rows_lds(const FreqSlice<T, D, FW, NS>& fs,
                                                  const typename Io<T>::type* X, int tt,
-                                                 f32x4 (&p)[FreqSlice<T, D, FW, NS>::PR]) {
+                                                 ProjT<T> (&p)[FreqSlice<T, D, FW, NS>::PR]) {
   typedef FreqSlice<T, D, FW, NS> FS;
-  const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const typename Io<T>::type* row = X + (tt * 16 + r) * LD;
+  if constexpr (!IsBf16<T>::value) {
+    project_f64<D, FW, NS, LD, true>(fs, X, tt, p);
+  } else {
+    const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+    const typename Io<T>::type* row = X + (tt * 16 + r) * LD;
 #pragma unroll
-  for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
+    for (int pr = 0; pr < FS::PR; ++pr) p[pr] = zero4();
 #pragma unroll
-  for (int ks = 0; ks < FS::KD; ++ks) {
-    Frag<T> x;
-    lds_row8(x, row, ks * 32 + 8 * g);
+    for (int ks = 0; ks < FS::KD; ++ks) {
+      Frag<T> x;
+      lds_row8(x, row, ks * 32 + 8 * g);
 #pragma unroll
-    for (int pr = 0; pr < FS::PR; ++pr)
+      for (int pr = 0; pr < FS::PR; ++pr)
 #pragma unroll
-      for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], x, fs.w[sp][pr][ks]);
+        for (int sp = 0; sp < FS::NSPLIT; ++sp) mma(p[pr], x, fs.w[sp][pr][ks]);
+    }
   }
 }
 
@@ -240,7 +306,7 @@ __device__ __forceinline__ void feature_frags_rows(const FreqSlice<T, D, FW, NS>
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) {
     const int tt = 2 * ks + hh;
-    f32x4 p[FS::PR];
+    ProjT<T> p[FS::PR];
     project_rows_lds<T, D, FW, NS, LD>(fs, X, tt, p);
     const float4 s4 = *reinterpret_cast<const float4*>(sc + tt * 16 + 4 * g);
     const float sv[4] = {s4.x, s4.y, s4.z, s4.w};

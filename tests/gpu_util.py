@@ -23,7 +23,7 @@ def to_f64(t):
     return t.detach().to(torch.float64).cpu().numpy()
 
 
-def desc_of(wl, segments=0, sigma=1.0):
+def desc_of(wl, segments=0, sigma=1.0, chunk=0):
     import paper_2606_27748_amd as F
     return F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, wl.causal, wl.io,
-                       sigma=sigma, segments=segments)
+                       sigma=sigma, segments=segments, chunk=chunk)

@@ -45,8 +45,8 @@ TOL = {"f32": 1e-4, "bf16": 2e-2}
 KAPPA_MAX = {"f32": 1e3, "bf16": 20.0}
 # Gradients of a kept row depend on every other kept row (through the states),
 # so their error is an average of c u kappa_i over kept rows; kappa_max is set
-# so that u kappa_max stays well below the tolerance (fp32: 6e-8 * 100).
-KAPPA_MAX_GRAD = {"f32": 100.0, "bf16": 20.0}
+# so that u kappa_max stays well below the tolerance (fp32: 6e-8 * 1e3).
+KAPPA_MAX_GRAD = {"f32": 1e3, "bf16": 20.0}
 UNIT = {"f32": 2.0 ** -24, "bf16": 2.0 ** -9}
 
 

@@ -84,7 +84,10 @@ def test_awd_workspace_size():
     ("B", 0, F.FLEX_ERR_INVALID_ARG), ("N", -1, F.FLEX_ERR_INVALID_ARG),
     ("variant", 2, F.FLEX_ERR_INVALID_ARG), ("causal", 3, F.FLEX_ERR_INVALID_ARG),
     ("io_dtype", 5, F.FLEX_ERR_INVALID_ARG), ("sigma", 0.0, F.FLEX_ERR_INVALID_ARG),
-    ("sigma", float("nan"), F.FLEX_ERR_INVALID_ARG), ("chunk", 32, F.FLEX_ERR_UNSUPPORTED),
+    ("sigma", float("nan"), F.FLEX_ERR_INVALID_ARG), ("chunk", 48, F.FLEX_ERR_UNSUPPORTED),
+    ("chunk", 128, F.FLEX_ERR_UNSUPPORTED), ("chunk", 8, F.FLEX_ERR_UNSUPPORTED),
+    ("chunk", -16, F.FLEX_ERR_INVALID_ARG), ("chunk", 16, F.FLEX_OK), ("chunk", 32, F.FLEX_OK),
+    ("chunk", 64, F.FLEX_OK),
     ("d", 48, F.FLEX_ERR_UNSUPPORTED), ("m", 96, F.FLEX_ERR_UNSUPPORTED),
     ("dv", 32, F.FLEX_ERR_UNSUPPORTED), ("grad_dtype", 1, F.FLEX_ERR_UNSUPPORTED),
 ])
@@ -92,6 +95,18 @@ def test_descriptor_validation(field, value, status):
     d = F.make_desc(1, 2, 100, 64, 128, "nonstationary", True, "bf16")
     setattr(d, field, value)
     assert _ws(d)[0] == status
+
+
+@pytest.mark.parametrize("field,value", [("dv", 0), ("dv", 48), ("causal", 7), ("chunk", 48),
+                                         ("segments", -1), ("grad_dtype", 9)])
+def test_feature_map_ignores_attention_fields(field, value):
+    """The feature map has no values, mask, chunks, segments or gradients: it
+    accepts any value of those descriptor fields (its workspace is empty)."""
+    d = F.make_desc(1, 2, 100, 64, 128, "nonstationary", True, "bf16")
+    setattr(d, field, value)
+    assert _ws(d, F.FLEX_PASS_FEATURE_MAP) == (F.FLEX_OK, 0)
+    d.d = 48   # the shape itself is still checked
+    assert _ws(d, F.FLEX_PASS_FEATURE_MAP)[0] == F.FLEX_ERR_UNSUPPORTED
 
 
 def test_fp32_large_shapes_unsupported():

@@ -13,7 +13,7 @@ import pytest
 import oracle as orc
 import workloads as W
 from tests.gpu_util import to_device, to_f64, desc_of
-from tests.parity import check_forward, abs_scales, TOL
+from tests.parity import check_forward, abs_scales, TOL, UNIT
 
 pytestmark = pytest.mark.gpu
 
@@ -55,7 +55,9 @@ def test_feature_map(F, io, d, m, variant):
     s = 1 / math.sqrt(m) if variant == "stationary" else 1 / (2 * math.sqrt(m))
     scale = s * orc.norm_factor(x.f64("Q"), x.tau)[..., None]
     err = np.max(np.abs(got - ref) / scale)
-    tol = 1e-5 if io == "f32" else 2.0 ** -8
+    # fp32: phase and norm factor in float64, features rounded to fp32 about
+    # twice (a few units of 2^-24); bf16: one rounding of the stored value
+    tol = 1e-6 if io == "f32" else 2.0 ** -8
     assert err <= tol, err
 
 
@@ -122,6 +124,34 @@ def test_forward_edge_lengths(F, N, causal):
         np.testing.assert_allclose(to_f64(O)[:, :, 0], x.f64("V")[:, :, 0], rtol=2 ** -8, atol=1e-6)
 
 
+@pytest.mark.parametrize("io,d,m", SHAPES)
+@pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
+def test_forward_chunk_invariance(F, io, d, m, variant):
+    """Chunk lengths C = 16, 32, 64 of the causal sweep (tril inside a chunk,
+    the running state across chunks) give the same attention: each matches the
+    oracle, and any two differ by no more than the rounding of the features
+    they contract in a different order.  N = 203 with 3 segments leaves ragged
+    last chunks and segment boundaries inside every chunk length's grid."""
+    wl, x = small(io, d, m, variant, True, B=1, H=2, N=203, seed=19)
+    t = to_device(x)
+    O_ref, den_ref, kap, sc = oracle_fwd(x, wl)
+    outs = {}
+    for C in (16, 32, 64):
+        O, den = F.flex_linattn_fwd(desc_of(wl, segments=3, chunk=C), t["Q"], t["K"], t["V"],
+                                    t["W1"], t["W2"], t["tau"])
+        outs[C] = (to_f64(O), to_f64(den))
+        check_forward(io, outs[C][0], outs[C][1], O_ref, den_ref, kap, sc)
+    # den: the same sums grouped differently (intra-chunk products rounded to
+    # the feature type, or the carried state rounded to it).  Either rounding
+    # moves a row by at most u/2 of sum_j sum_f |phi(Q_i)_f phi(K_j)_f| (T1a's
+    # scale); fp32 adds the accumulation order over up to 203 terms.
+    den_abs = sc[1]
+    bound = (4 if io == "bf16" else 64) * UNIT[io]
+    for a, b in ((16, 32), (16, 64), (32, 64)):
+        diff = np.abs(outs[a][1] - outs[b][1]) / den_abs
+        assert np.max(diff) <= bound, (a, b, np.max(diff))
+
+
 def test_forward_deterministic_and_den_optional(F):
     import torch
     wl, x = small("bf16", 64, 128, "nonstationary", True, N=300)
@@ -164,6 +194,8 @@ def test_forward_full_size_sampled(F, name):
     O, den = F.flex_linattn_fwd(desc_of(wl), t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"])
     O = to_f64(O)
     den = to_f64(den)
+    # every (b,h) slice: two random rows and one boundary row (chunk, segment
+    # or sequence end), so a mapping error confined to some slices is seen
     rng = np.random.default_rng(5)
     idx = [0, 1, 63, 64, 65, wl.N // 2, wl.N - 65, wl.N - 1]
     rows = []
@@ -171,7 +203,7 @@ def test_forward_full_size_sampled(F, name):
         for h in range(wl.H):
             for i in list(rng.integers(0, wl.N, 2)) + ([idx[(b * wl.H + h) % len(idx)]]):
                 rows.append((b, h, int(i)))
-    rows = np.array(rows[:48])
+    rows = np.array(rows)
     Q, K, V = x.f64("Q"), x.f64("K"), x.f64("V")
     O_ref, den_ref = orc.linattn_fwd_rows(Q, K, V, x.W1, x.W2, x.tau, wl.variant, wl.causal, rows)
     # conditioning of the sampled rows
