@@ -122,6 +122,59 @@ def dtau_scale(x, wl, aux):
     return t.sum(axis=(0, 2))
 
 
+ROW_TOL = {"f32": 5e-4, "bf16": 0.1}
+
+
+def dv_row_scale(pq, pk, dO, den, kappa, causal):
+    """Scale of the rounding error of each dV row (dV = A^T dO, Eq.(linear att)):
+    s_j = sum_i sum_f |phi(Q_i)_f| |phi(K_j)_f| (1 + kappa_i) |dO_i| / |den_i|
+    over i >= j (causal) or all i.  Rounding the features to precision u moves
+    a_ij by at most ~u sum_f |phi_if phi_jf| and den_i by ~u kappa_i |den_i|,
+    so |delta dV_j| <~ u s_j.  Formed as |phi(K_j)| . (suffix) sum_i w_i |phi(Q_i)|,
+    O(N d') per slice.  Rows i whose dO is zero contribute nothing."""
+    nrm = np.linalg.norm(dO, axis=-1)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        w = np.where(nrm > 0, (1.0 + kappa) * nrm / np.abs(den), 0.0)
+    t = w[..., None] * np.abs(pq)
+    if causal:
+        acc = np.flip(np.cumsum(np.flip(t, -2), axis=-2), -2)
+    else:
+        acc = np.broadcast_to(t.sum(-2, keepdims=True), t.shape)
+    return (np.abs(pk) * acc).sum(-1)
+
+
+def check_grad_rows(io, got: dict, ref: dict, names=("dQ", "dK", "dV"), dv_scale=None, n_terms=1):
+    """Row-wise checks of [..., N, d] gradients, which a Frobenius norm over the
+    whole tensor would not see for a single wrong row:
+
+    * every row's error relative to max(|row|, RMS row norm) <= ROW_TOL
+      (5 tol; a wrong row scores about 1).  Meant for slices of tens of rows
+      or more: at N = 1, 2 the exact gradients of some rows vanish and every
+      row may be rounding noise (those lengths have their own checks);
+    * with dv_scale (dv_row_scale), |delta dV_j| <= (4 u + 4 u32 sqrt(n_terms)) s_j,
+      u the feature precision and u32 the fp32 accumulation over n_terms rows."""
+    stats = {}
+    ok = True
+    for n in names:
+        g = np.asarray(got[n], np.float64)
+        r = np.asarray(ref[n], np.float64)
+        nr = np.linalg.norm(r, axis=-1)
+        rms = float(np.sqrt(np.mean(nr * nr)))
+        rr = np.linalg.norm(g - r, axis=-1) / np.maximum(nr, rms if rms > 0 else 1.0)
+        stats[n + "_row_max"] = float(rr.max())
+        ok = ok and stats[n + "_row_max"] <= ROW_TOL[io]
+    if dv_scale is not None:
+        e = np.linalg.norm(np.asarray(got["dV"], np.float64) - ref["dV"], axis=-1)
+        bound = (4 * UNIT[io] + 4 * 2.0 ** -24 * np.sqrt(n_terms)) * dv_scale
+        with np.errstate(divide="ignore", invalid="ignore"):
+            q = np.where(bound > 0, e / bound, np.where(e > 0, np.inf, 0.0))
+        stats["dV_row_bound"] = float(q.max())
+        ok = ok and stats["dV_row_bound"] <= 1.0
+    _log("grad_rows", stats)
+    assert ok, stats
+    return stats
+
+
 def check_grads(io, got: dict, ref: dict, names, scales=None):
     """T3.  For names listed in `scales` the error is measured relative to the
     given magnitude of the summed terms instead of the value (dtau is a sum

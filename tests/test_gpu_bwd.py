@@ -12,7 +12,7 @@ import pytest
 import oracle as orc
 import workloads as W
 from tests.gpu_util import to_device, to_f64, desc_of
-from tests.parity import check_grads, dtau_scale, KAPPA_MAX_GRAD as KAPPA_MAX, TOL
+from tests.parity import check_grads, check_grad_rows, dv_row_scale, dtau_scale, KAPPA_MAX_GRAD as KAPPA_MAX, TOL
 
 pytestmark = pytest.mark.gpu
 
@@ -29,11 +29,23 @@ def F():
 
 
 def masked_inputs(wl, x):
-    """Zero dO on rows with kappa > kappa_max (stored precision kept)."""
+    """Zero dO on rows with kappa > kappa_max (stored precision kept); returns
+    the condition numbers."""
     kap = orc.conditioning(x.f64("Q"), x.f64("K"), x.W1, x.W2, x.tau, wl.variant, wl.causal)
     keep = kap <= KAPPA_MAX[wl.io]
     x.dO = x.dO * keep[..., None].astype(x.dO.dtype)
-    return keep
+    return kap
+
+
+def check_rows(wl, x, got, ref, kap):
+    """Row-wise gradient checks (tests/parity.py check_grad_rows), for slices
+    of at least 32 rows."""
+    if wl.N < 32:
+        return None
+    pq = orc.feature_map(x.f64("Q"), x.W1, x.W2, x.tau, wl.variant)
+    pk = orc.feature_map(x.f64("K"), x.W1, x.W2, x.tau, wl.variant)
+    sc = dv_row_scale(pq, pk, x.f64("dO"), ref["den"], kap, wl.causal)
+    return check_grad_rows(wl.io, got, ref, dv_scale=sc, n_terms=wl.N)
 
 
 def gpu_fwd_bwd(F, wl, x, segments=0, reuse=False):
@@ -67,10 +79,11 @@ def names_of(wl):
 def test_backward_small(F, io, d, m, variant, causal, reuse):
     wl = W.Workload("small", 2, 2, 200, d, m, variant, causal, io, True, 21)
     x = W.generate(wl)
-    masked_inputs(wl, x)
+    kap = masked_inputs(wl, x)
     got = gpu_fwd_bwd(F, wl, x, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads(io, got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
 
 
 @pytest.mark.parametrize("reuse", [False, True])
@@ -79,10 +92,11 @@ def test_backward_small(F, io, d, m, variant, causal, reuse):
 def test_backward_segments(F, segments, causal, reuse):
     wl = W.Workload("seg", 1, 2, 330, 64, 128, "nonstationary", causal, "bf16", True, 23)
     x = W.generate(wl)
-    masked_inputs(wl, x)
+    kap = masked_inputs(wl, x)
     got = gpu_fwd_bwd(F, wl, x, segments=segments, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
 
 
 @pytest.mark.parametrize("reuse", [False, True])
@@ -91,10 +105,11 @@ def test_backward_many_partials(F, reuse):
     reduce takes them in two batches, the second one partly past the list."""
     wl = W.Workload("partials", 3, 2, 500, 64, 64, "nonstationary", True, "bf16", True, 33)
     x = W.generate(wl)
-    masked_inputs(wl, x)
+    kap = masked_inputs(wl, x)
     got = gpu_fwd_bwd(F, wl, x, segments=7, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
 
 
 @pytest.mark.parametrize("reuse", [False, True])
@@ -105,10 +120,11 @@ def test_backward_edge_lengths(F, N, reuse):
     forward's segments."""
     wl = W.Workload("edge", 1, 2, N, 64, 64, "nonstationary", True, "bf16", True, 25)
     x = W.generate(wl)
-    masked_inputs(wl, x)
+    kap = masked_inputs(wl, x)
     got = gpu_fwd_bwd(F, wl, x, segments=3 if N > 1000 else 0, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
 
 
 def test_backward_reuse_matches_recompute(F):
@@ -178,29 +194,48 @@ def _slice_bwd_oracle(wl, x, b, h):
 
 @pytest.mark.parametrize("name", ["nonstationary_causal_train", "train_at_scale_d128", "headline_causal_train_d64"])
 def test_backward_full_size_sampled(F, name):
-    """Full configured size, default launch configuration.  For one head, every
-    slice's dQ, dK, dV rows and the head's dW1, dW2, dtau (sums over its B
-    slices) are compared with the oracle run on those slices."""
+    """Full configured size, default launch configuration.  For two heads (the
+    first and the last), every slice's dQ, dK, dV rows and the head's dW1, dW2,
+    dtau (sums over its B slices) are compared with the oracle run on those
+    slices: Frobenius norms (T3) and row by row (check_grad_rows)."""
     wl = W.WORKLOADS[name]
     x = W.generate(wl)
-    h = wl.H - 1
+    heads = [0, wl.H - 1]
     Q, K = x.f64("Q"), x.f64("K")
-    keep = np.ones((wl.B, wl.H, wl.N), bool)
-    W2h = None if x.W2 is None else x.W2[h:h + 1]
-    for b in range(wl.B):
-        kap = orc.conditioning(Q[b:b + 1, h:h + 1], K[b:b + 1, h:h + 1], x.W1[h:h + 1], W2h,
-                               x.tau[h:h + 1], wl.variant, wl.causal)[0, 0]
-        keep[b, h] = kap <= KAPPA_MAX[wl.io]
+    keep = np.zeros((wl.B, wl.H, wl.N), bool)
+    kaps = {}
+    for h in heads:
+        W2h = None if x.W2 is None else x.W2[h:h + 1]
+        for b in range(wl.B):
+            kap = orc.conditioning(Q[b:b + 1, h:h + 1], K[b:b + 1, h:h + 1], x.W1[h:h + 1], W2h,
+                                   x.tau[h:h + 1], wl.variant, wl.causal)[0, 0]
+            kaps[b, h] = kap
+            keep[b, h] = kap <= KAPPA_MAX[wl.io]
+    # heads that are not checked keep their full dO (their gradients are not compared)
+    others = np.ones(wl.H, bool)
+    others[heads] = False
+    keep[:, others] = True
     x.dO = x.dO * keep[..., None].astype(x.dO.dtype)
-    got = gpu_fwd_bwd(F, wl, x, reuse=True)
-    refs = [_slice_bwd_oracle(wl, x, b, h) for b in range(wl.B)]
-    ref = {}
-    for n in ("dQ", "dK", "dV"):
-        ref[n] = np.concatenate([r[n] for r in refs], axis=0)
-        got[n] = got[n][:, h:h + 1]
-    for n in ("dW1", "dW2", "dtau"):
-        if refs[0][n] is None:
-            continue
-        ref[n] = sum(r[n] for r in refs)
-        got[n] = got[n][h:h + 1]
-    check_grads(wl.io, got, ref, names_of(wl), {"dtau": np.array([sum(r["tau_scale"] for r in refs)])})
+    got_all = gpu_fwd_bwd(F, wl, x, reuse=True)
+    dO = x.f64("dO")
+    for h in heads:
+        refs = [_slice_bwd_oracle(wl, x, b, h) for b in range(wl.B)]
+        ref, got = {}, {}
+        for n in ("dQ", "dK", "dV"):
+            ref[n] = np.concatenate([r[n] for r in refs], axis=0)
+            got[n] = got_all[n][:, h:h + 1]
+        for n in ("dW1", "dW2", "dtau"):
+            if refs[0][n] is None:
+                continue
+            ref[n] = sum(r[n] for r in refs)
+            got[n] = got_all[n][h:h + 1]
+        check_grads(wl.io, got, ref, names_of(wl), {"dtau": np.array([sum(r["tau_scale"] for r in refs)])})
+        # row-wise, slice by slice
+        W2h = None if x.W2 is None else x.W2[h:h + 1]
+        for b, r in enumerate(refs):
+            sl = (slice(b, b + 1), slice(h, h + 1))
+            pq = orc.feature_map(Q[sl], x.W1[h:h + 1], W2h, x.tau[h:h + 1], wl.variant)
+            pk = orc.feature_map(K[sl], x.W1[h:h + 1], W2h, x.tau[h:h + 1], wl.variant)
+            sc = dv_row_scale(pq, pk, dO[sl], r["den"], kaps[b, h][None, None], wl.causal)
+            check_grad_rows(wl.io, {n: got[n][b:b + 1] for n in ("dQ", "dK", "dV")}, r,
+                            dv_scale=sc, n_terms=wl.N)
