@@ -36,32 +36,120 @@ KERNEL_FILES = {"fwd_state": "flex_fwd.hip", "fwd_sweep": "flex_fwd.hip", "scan"
                 "awd_wgrad": "flex_awd.hip"}
 
 
+# transcendental VALU rate: 256 CUs x 4 SIMDs x 16 lanes per clock at quarter
+# rate x 2.4 GHz
+PEAK_TRANS_PER_S = 256 * 4 * 16 / 4 * 2.4e9
+
+
+def _trans_per_row(wl, with_psi=False):
+    """Transcendentals of one feature-map evaluation of one row: sin and cos of
+    every frequency (stationary), plus cos P2 (nonstationary; plus sin P2 where
+    the backward needs dphi/dP2), plus one exp for the norm factor."""
+    if wl.variant == "nonstationary":
+        return (4 if with_psi else 3) * wl.m + 1
+    return 2 * wl.m + 1
+
+
 def kernel_work(wl, kernel):
-    """Algorithmic bytes and flops of one launch of a kernel class for a workload:
-    the inputs it must read and the outputs it must write once, and the
-    contractions of the method it performs (no recomputation, intra-chunk
-    masking overhead, state hand-off or padding counted)."""
+    """Algorithmic (bytes, flops, transcendentals) of one launch of a kernel
+    class for a workload: the inputs it must read and the outputs it must write
+    once, the contractions of the method it performs, and the feature maps it
+    must evaluate (no recomputation, intra-chunk masking overhead, state
+    hand-off or padding counted)."""
     T = wl.B * wl.H * wl.N                        # (b,h,token) rows
     bio = 2 if wl.io == "bf16" else 4
     d, dv, dp = wl.d, wl.dv, 2 * wl.m
     meff = 2 * wl.m if wl.variant == "nonstationary" else wl.m
     proj = 2 * d * meff                           # one row onto all frequencies
     state = 2 * dp * (dv + 1)                     # one row into / out of the state
+    tr, trp = _trans_per_row(wl), _trans_per_row(wl, True)
     if kernel == "fwd_state":
-        return T * 2 * d * bio, T * (proj + state)
+        return T * 2 * d * bio, T * (proj + state), T * tr
     if kernel == "fwd_sweep":
         if not wl.causal:   # reads Q, writes O and den; phi(Q) and the readout
-            return T * (2 * d * bio + 4), T * (proj + state)
-        return T * (4 * d * bio + 4), T * (2 * proj + 2 * state)
+            return T * (2 * d * bio + 4), T * (proj + state), T * tr
+        return T * (4 * d * bio + 4), T * (2 * proj + 2 * state), T * 2 * tr
     if kernel == "bwd_prepass":
-        return T * (5 * d * bio + 4 + 8), T * (2 * proj + 2 * state)
+        return T * (5 * d * bio + 4 + 8), T * (2 * proj + 2 * state), T * 2 * tr
     if kernel == "bwd_dq":
         # reads Q, K, V, dO, 1/den and delta; writes dQ; dphi(Q) = S'G, dQ = dP W', dW' += dP^T Q
-        return T * (4 * d * bio + 8 + 4 * d), T * (state + 2 * proj)
+        return T * (4 * d * bio + 8 + 4 * d), T * (state + 2 * proj), T * trp
     if kernel == "bwd_dkv":
         # reads Q, K, V, dO, 1/den and delta; writes dK, dV; dphi(K), dV, dK, dW' and R'
-        return T * (4 * d * bio + 8 + 8 * d), T * (3 * state + 2 * proj)
-    return 0, 0
+        return T * (4 * d * bio + 8 + 8 * d), T * (3 * state + 2 * proj), T * trp
+    return 0, 0, 0
+
+
+def step_work(wl, backward):
+    """Algorithmic (bytes, flops, transcendentals) of one step: each input read
+    and each output written once, the method's contractions (forward:
+    projections of Q and K and the state / readout contractions; backward: the
+    four state contractions and the chain rule's two products per projection),
+    and each row's feature map once per pass (twice with the backward)."""
+    BH, N, d, dv, m = wl.B * wl.H, wl.N, wl.d, wl.dv, wl.m
+    bio = 2 if wl.io == "bf16" else 4
+    nmat = 2 if wl.variant == "nonstationary" else 1
+    meff = nmat * m
+    dp = 2 * m
+    wbytes = nmat * wl.H * m * d * 4
+    b = BH * (3 * N * d * bio + N * dv * bio) + wbytes
+    f = BH * (4 * N * d * meff + 4 * N * dp * (dv + 1))
+    t = BH * 2 * N * _trans_per_row(wl)
+    if backward:
+        b += BH * (4 * N * d * bio + N * dv * bio + 4 * N + 3 * N * d * 4) + 2 * wbytes + BH * 4 * N
+        f += BH * (8 * N * dp * (dv + 1) + 8 * N * meff * d)
+        t += BH * 2 * N * _trans_per_row(wl)
+    return b, f, t
+
+
+def roofs_of(wl, work):
+    """Roof times (s) of (bytes, flops, transcendentals) on MI355X: HBM 8 TB/s,
+    dense MFMA at the io dtype's peak, transcendentals at the quarter-rate
+    VALU's 9.8e12/s."""
+    b, f, t = work
+    peak_f = (PEAK_BF16_TFLOPS if wl.io == "bf16" else PEAK_FP32_TFLOPS) * 1e12
+    return {"hbm": b / (PEAK_HBM_GBS * 1e9), "mfma": f / peak_f, "trans": t / PEAK_TRANS_PER_S}
+
+
+def roofline_entry(wl, work, seconds):
+    """Position of `work` done in `seconds` against its binding roof (the
+    largest of the three roof times)."""
+    b, f, t = work
+    roofs = roofs_of(wl, work)
+    bound = max(roofs, key=roofs.get)
+    if bound == "hbm":
+        e = {"bound": "hbm", "achieved": b / seconds / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    elif bound == "mfma":
+        e = {"bound": "mfma", "achieved": f / seconds / 1e12,
+             "peak": PEAK_BF16_TFLOPS if wl.io == "bf16" else PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        e = {"bound": "alu", "achieved": t / seconds / 1e12, "peak": PEAK_TRANS_PER_S / 1e12,
+             "unit": "Ttranscendental/s"}
+    e["frac"] = e["achieved"] / e["peak"]
+    e["roof_us"] = {k: round(v * 1e6, 2) for k, v in roofs.items()}
+    e["frac_per_roof"] = {k: round(v / seconds, 4) for k, v in roofs.items()}
+    return e
+
+
+def copy_bandwidth_gbs(nbytes=1 << 30, reps=10):
+    """Read + write bandwidth of a plain device copy of nbytes (the practical
+    HBM ceiling), timed with events on the current stream."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * nbytes / (e0.elapsed_time(e1) / reps * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbs
 
 
 def source_hash(kernel):
@@ -87,10 +175,36 @@ def traffic_from_profiles(workload, kernel):
     return rec.get("hbm_bytes_per_launch")
 
 
+def host_facts():
+    """The host the CPU baseline ran on: logical CPUs, CPU model, NumPy and its
+    BLAS, and the BLAS thread pools (threadpoolctl)."""
+    import numpy as np
+    facts = {"os_cpu_count": os.cpu_count(), "numpy": np.__version__}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    facts["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        facts["affinity_cpus"] = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        facts["blas"] = [{"api": i.get("internal_api"), "version": i.get("version"),
+                          "threads": i.get("num_threads")} for i in threadpool_info()]
+    except Exception as e:   # noqa: BLE001 (the facts are informative only)
+        facts["blas"] = f"unavailable: {e}"
+    return facts
+
+
 def cpu_baseline(wl, slices, seed_offset=0):
     """Time the float64 oracle (forward + backward) on `slices` (b,h) slices of
-    the workload at full sequence length; scale to the whole batch."""
-    import numpy as np
+    the workload at full sequence length; scale to the whole batch.  `cores`
+    is the threads the run kept busy on average (CPU time over wall time)."""
     import oracle
     import workloads as W
     sub = wl.scaled(B=1, H=slices)
@@ -102,8 +216,10 @@ def cpu_baseline(wl, slices, seed_offset=0):
     per_step = (t1 - t0) * (wl.B * wl.H) / slices
     return {"value": wl.B * wl.N / per_step, "unit": "tokens/s",
             "cores": max(1, int(round((c1 - c0) / (t1 - t0)))), "kind": "oracle",
+            "cpu_s_per_wall_s": round((c1 - c0) / (t1 - t0), 2),
             "sample": f"{slices} of {wl.B * wl.H} (b,h) slices at N={wl.N}, forward+backward in "
-                      f"float64 ({t1 - t0:.1f} s), scaled by {wl.B * wl.H}/{slices}"}
+                      f"float64 ({t1 - t0:.1f} s), scaled by {wl.B * wl.H}/{slices}",
+            "host": host_facts()}
 
 
 FLUSH_BYTES = 512 << 20   # twice the 256 MB last-level cache
@@ -213,24 +329,35 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
     tokens = wl.B * wl.N
     value = tokens / (ms_step * 1e-3)
 
+    # the same loop with no timing events, for comparison (outside the contract's region)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step_noev = (time.perf_counter() - t2) * 1e3 / steps
+
     # the class's time per step (several launches when the shape runs as
     # frequency groups) against its algorithmic work per step
     per_step = max(k_n // steps, 1)
     avg_s = (k_ms / steps) * 1e-3
     kwl = wl if backward == wl.backward else wl.scaled(backward=False)
-    kbytes, kflops = kernel_work(kwl, dominant)
-    ridge = (PEAK_BF16_TFLOPS * 1e12) / (PEAK_HBM_GBS * 1e9)
-    if kbytes and kflops / kbytes >= ridge:
-        roof = {"bound": "mfma", "achieved": kflops / avg_s / 1e12,
-                "peak": PEAK_BF16_TFLOPS if wl.io == "bf16" else PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": kbytes / avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof = roofline_entry(wl, kernel_work(kwl, dominant), avg_s)
     roof["traffic"] = traffic_from_profiles(wl.name, dominant)
     roof["kernel"] = dominant
     roof["kernel_ms"] = avg_s * 1e3
     roof["launches_per_step"] = per_step
     roof["kernel_share"] = {k: round(v / sum(share.values()), 4) for k, v in share.items()}
+    copy_gbs = copy_bandwidth_gbs()
+    if roof["bound"] == "hbm":
+        roof["copy_gbs"] = copy_gbs
+        roof["frac_vs_copy"] = roof["achieved"] / copy_gbs
+    # the whole step against its own binding roof
+    step_roof = roofline_entry(wl, step_work(wl, backward), ms_step * 1e-3)
+    step_roof["copy_gbs"] = copy_gbs
+    if step_roof["bound"] == "hbm":
+        step_roof["frac_vs_copy"] = step_roof["achieved"] / copy_gbs
+    roof["step"] = step_roof
 
     out = {"metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": steps,
            "warmup": warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
@@ -240,7 +367,13 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
                       "pass": "fwd+bwd" if backward else "fwd", "parallelism": "single-gpu"},
            "roofline": roof}
     out["step_timing"] = {"warm": step_stats(step, 20, False), "cold": step_stats(step, 20, True),
-                          "flush_bytes": FLUSH_BYTES}
+                          "flush_bytes": FLUSH_BYTES, "ms_per_step_no_events": ms_step_noev,
+                          "note": "value and ms_per_step: the contract's K back-to-back steps, warm "
+                                  "(a step's inputs, outputs and workspaces stay in the 256 MB "
+                                  "last-level cache where they fit); cold: single steps with a "
+                                  "512 MiB buffer written before each, so no input is cached"}
+    cold = out["step_timing"]["cold"]["median_ms"]
+    out["value_cold"] = tokens / (cold * 1e-3)
     if wl.backward and not backward:
         out["config"]["note"] = "backward not built for this shape; forward only"
     if want_cpu:
@@ -290,9 +423,6 @@ def run_sweep(steps, warmup):
 
 
 AWD_CLASSES = ("feature_map", "awd_fwd", "awd_bwd_k", "awd_wgrad")
-# transcendental VALU rate: 256 CUs x 4 SIMDs x 16 lanes per clock at quarter
-# rate x 2.4 GHz
-PEAK_TRANS_PER_S = 256 * 4 * 16 / 4 * 2.4e9
 
 
 def awd_kernel_work(wl, kernel):
