@@ -131,6 +131,34 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K,
                          const float* tau, void* O, float* den,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* Bytes of the static device scratch that serves flex_linattn_fwd_noalloc
+ * as its workspace (one array per GPU). */
+#define FLEX_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* flex_linattn_fwd for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments and results as flex_linattn_fwd (bitwise), without the
+ * workspace: the library keeps the forward's workspace in a file-scope device
+ * array of FLEX_NOALLOC_SCRATCH_BYTES on each GPU it runs on, held until the
+ * process ends.  The call allocates and frees nothing (no hipMalloc, no
+ * allocating library routine); its first call on a device looks up that
+ * device's array.  The caller still owns Q, K, V, W1, W2, tau, O and den.
+ *   - A descriptor whose forward workspace (flex_workspace_size with
+ *     FLEX_PASS_FWD) exceeds FLEX_NOALLOC_SCRATCH_BYTES returns
+ *     FLEX_ERR_WORKSPACE with no device work (e.g. d = 128, m = 256 at
+ *     B = 2, H = 16, N = 8192).
+ *   - `stream` must belong to the current device (hipGetDevice); the array of
+ *     that device is used.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents (the forward overwrites all of it that it reads): calls
+ *     whose executions overlap on one GPU (several streams, several threads)
+ *     race and give wrong results.  Issue them on one stream.
+ *   - The backward cannot reuse this forward's segment states: pass
+ *     fwd_ws = NULL to flex_linattn_bwd. */
+int32_t flex_linattn_fwd_noalloc(const flex_desc* desc, const void* Q, const void* K,
+                                 const void* V, const float* W1, const float* W2,
+                                 const float* tau, void* O, float* den, void* stream);
+
 /* Backward of flex_linattn_fwd for an upstream gradient dO (the paper gives no
  * backward; it is the derivative of the forward above).
  *   Q, K, V, W1, W2, tau  the forward inputs

@@ -18,7 +18,8 @@ FLEX_F32, FLEX_BF16 = 0, 1
 FLEX_STATIONARY, FLEX_NONSTATIONARY = 0, 1
 FLEX_PASS_FEATURE_MAP, FLEX_PASS_FWD, FLEX_PASS_BWD, FLEX_PASS_AWD = 0, 1, 2, 3
 EXPORTS = ("flex_abi_version", "flex_status_string", "flex_workspace_size",
-           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_bwd", "flex_decode_step",
+           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_fwd_noalloc", "flex_linattn_bwd",
+           "flex_decode_step",
            "flex_awd_loss", "flex_timing_enable", "flex_timing_read")
 KERNELS = {"none": 0, "fwd_state": 1, "fwd_sweep": 2, "scan": 3, "bwd_prepass": 4,
            "bwd_dq": 5, "bwd_dkv": 6, "bwd_reduce": 7, "feature_map": 8, "decode_step": 9,
@@ -71,6 +72,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flex_feature_map.argtypes = [D, P, P, P, P, P, P, S, P]
     lib.flex_linattn_fwd.restype = I
     lib.flex_linattn_fwd.argtypes = [D, P, P, P, P, P, P, P, P, P, S, P]
+    lib.flex_linattn_fwd_noalloc.restype = I
+    lib.flex_linattn_fwd_noalloc.argtypes = [D, P, P, P, P, P, P, P, P, P]
     lib.flex_linattn_bwd.restype = I
     lib.flex_linattn_bwd.argtypes = [D] + [P] * 15 + [P, S] + [P, S, P]
     lib.flex_decode_step.restype = I
@@ -152,6 +155,16 @@ def flex_linattn_fwd(desc: flex_desc, Q, K, V, W1, W2, tau, O=None, den=None, ws
                                  _ptr(W2), _ptr(tau), _ptr(O), _ptr(den), _ptr(ws),
                                  ws.numel(), _stream())
     _check(st, "flex_linattn_fwd")
+    return O, den
+
+
+def flex_linattn_fwd_noalloc(desc: flex_desc, Q, K, V, W1, W2, tau, O, den=None):
+    """Forward linear attention with the library's static scratch as its
+    workspace: O (and den, if given) are caller-allocated, nothing else is.
+    Returns (O, den)."""
+    st = load().flex_linattn_fwd_noalloc(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(V), _ptr(W1),
+                                         _ptr(W2), _ptr(tau), _ptr(O), _ptr(den), _stream())
+    _check(st, "flex_linattn_fwd_noalloc")
     return O, den
 
 

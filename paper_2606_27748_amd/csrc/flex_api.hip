@@ -284,6 +284,103 @@ void timing_mark(int kernel_class, hipStream_t st, bool begin) {
 
 }  // namespace flex
 
+// Workspace of flex_linattn_fwd_noalloc: a file-scope device array.  Each GPU
+// the library runs on holds its own copy at its own address until the process
+// ends.  In host code `scratch` names a host-side stand-in, not device memory,
+// so it is never passed to a kernel: its device address is looked up once per
+// device (hipGetSymbolAddress, with that device current) and kept in a table.
+static __device__ __align__(256) unsigned char scratch[FLEX_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// Validation of the forward's arguments (everything but the workspace).
+int32_t check_fwd_args(const flex_desc* desc, const void* Q, const void* K, const void* V,
+                       const float* W1, const float* W2, const float* tau, const void* O,
+                       const float* den) {
+  const int32_t st = check_desc(desc);
+  if (st != FLEX_OK) return st;
+  if (!Q || !K || !V || !W1 || !tau || !O) return FLEX_ERR_INVALID_ARG;
+  if ((desc->variant == FLEX_NONSTATIONARY) != (W2 != nullptr)) return FLEX_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(W1) || (W2 && !aligned16(W2)) ||
+      !aligned16(O) || (den && !aligned16(den)))
+    return FLEX_ERR_INVALID_ARG;
+  return FLEX_OK;
+}
+
+// The forward on validated arguments with a workspace of at least
+// ws_bytes_of(desc, FLEX_PASS_FWD) bytes at `base`.
+int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void* V, const float* W1,
+                const float* W2, const float* tau, void* O, float* den, char* base, hipStream_t stream) {
+  FwdArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den;
+  const Groups G = groups_of(desc);
+  const KernelShape ks = attn_shape(desc);
+  const size_t sb = fwd_group_state_bytes(desc);
+  a.wfrag = base + G.n * sb;
+  if (G.n > 1) {
+    char* acc = base + G.n * sb + align256(wfrag_bytes(ks, desc->H));
+    a.acc_num = reinterpret_cast<float*>(acc);
+    a.acc_den = reinterpret_cast<float*>(acc + align256((size_t)desc->B * desc->H * desc->N * desc->dv * sizeof(float)));
+  }
+  const int P0 = pick_segments(desc);
+  a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
+  a.nchunks = nchunks_of(desc);
+  a.segments = P0;
+  a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
+  a.sub = fwd_sub_of(desc, P0);
+  if (desc->causal) {
+    // the sweep's chunks of chunk_of(desc) tokens: a segment spans the same
+    // tokens as its 64-token pre-pass chunks
+    a.sweep_chunk = chunk_of(desc);
+    a.sweep_groups = a.segments;
+    a.sweep_cps = a.chunks_per_seg * (kChunk / a.sweep_chunk);
+  } else {
+    a.sweep_chunk = kChunk;
+    a.sweep_cps = a.nchunks < kSweepChunks ? a.nchunks : kSweepChunks;
+    a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
+  }
+  a.s_const = s_const_of(desc);
+  a.w_stride = desc->m * desc->d;
+  for (int g = 0; g < G.n; ++g) {
+    const size_t woff = (size_t)g * G.m * desc->d;   // this group's frequency rows
+    a.W1 = W1 + woff;
+    a.W2 = W2 ? W2 + woff : nullptr;
+    a.state = reinterpret_cast<float*>(base + g * sb);
+    a.acc = G.n == 1 ? 0 : (g == 0 ? 1 : 2);
+    const hipError_t e = launch_fwd(a, ks, false, stream);
+    if (e != hipSuccess) return FLEX_ERR_HIP;
+  }
+  if (G.n > 1 && launch_fwd_finish(a, ks.bf16, desc->dv, stream) != hipSuccess) return FLEX_ERR_HIP;
+  return FLEX_OK;
+}
+
+constexpr int kMaxDevices = 64;
+struct ScratchTable {
+  std::mutex mu;
+  void* ptr[kMaxDevices] = {};
+};
+ScratchTable& scratch_table() {
+  static ScratchTable t;
+  return t;
+}
+
+int32_t scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FLEX_ERR_HIP;
+  ScratchTable& t = scratch_table();
+  std::lock_guard<std::mutex> lk(t.mu);
+  if (!t.ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FLEX_ERR_HIP;
+    t.ptr[dev] = p;
+  }
+  *out = t.ptr[dev];
+  return FLEX_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int32_t flex_abi_version(void) { return FLEX_ABI_VERSION; }
@@ -443,59 +540,25 @@ int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1, 
 int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, const void* V,
                          const float* W1, const float* W2, const float* tau, void* O, float* den,
                          void* ws, size_t ws_bytes, void* stream) {
-  const int32_t st = check_desc(desc);
+  const int32_t st = check_fwd_args(desc, Q, K, V, W1, W2, tau, O, den);
   if (st != FLEX_OK) return st;
-  if (!Q || !K || !V || !W1 || !tau || !O) return FLEX_ERR_INVALID_ARG;
-  if ((desc->variant == FLEX_NONSTATIONARY) != (W2 != nullptr)) return FLEX_ERR_INVALID_ARG;
-  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(W1) || (W2 && !aligned16(W2)) ||
-      !aligned16(O) || (den && !aligned16(den)))
-    return FLEX_ERR_INVALID_ARG;
   const size_t need = ws_bytes_of(desc, FLEX_PASS_FWD);
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
-  FwdArgs a;
-  memset(&a, 0, sizeof(a));
-  a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den;
-  const Groups G = groups_of(desc);
-  const KernelShape ks = attn_shape(desc);
-  const size_t sb = fwd_group_state_bytes(desc);
-  char* base = static_cast<char*>(ws);
-  a.wfrag = base + G.n * sb;
-  if (G.n > 1) {
-    char* acc = base + G.n * sb + align256(wfrag_bytes(ks, desc->H));
-    a.acc_num = reinterpret_cast<float*>(acc);
-    a.acc_den = reinterpret_cast<float*>(acc + align256((size_t)desc->B * desc->H * desc->N * desc->dv * sizeof(float)));
-  }
-  const int P0 = pick_segments(desc);
-  a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
-  a.nchunks = nchunks_of(desc);
-  a.segments = P0;
-  a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
-  a.sub = fwd_sub_of(desc, P0);
-  if (desc->causal) {
-    // the sweep's chunks of chunk_of(desc) tokens: a segment spans the same
-    // tokens as its 64-token pre-pass chunks
-    a.sweep_chunk = chunk_of(desc);
-    a.sweep_groups = a.segments;
-    a.sweep_cps = a.chunks_per_seg * (kChunk / a.sweep_chunk);
-  } else {
-    a.sweep_chunk = kChunk;
-    a.sweep_cps = a.nchunks < kSweepChunks ? a.nchunks : kSweepChunks;
-    a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
-  }
-  a.s_const = s_const_of(desc);
-  a.w_stride = desc->m * desc->d;
-  for (int g = 0; g < G.n; ++g) {
-    const size_t woff = (size_t)g * G.m * desc->d;   // this group's frequency rows
-    a.W1 = W1 + woff;
-    a.W2 = W2 ? W2 + woff : nullptr;
-    a.state = reinterpret_cast<float*>(base + g * sb);
-    a.acc = G.n == 1 ? 0 : (g == 0 ? 1 : 2);
-    const hipError_t e = launch_fwd(a, ks, false, (hipStream_t)stream);
-    if (e != hipSuccess) return FLEX_ERR_HIP;
-  }
-  if (G.n > 1 && launch_fwd_finish(a, ks.bf16, desc->dv, (hipStream_t)stream) != hipSuccess)
-    return FLEX_ERR_HIP;
-  return FLEX_OK;
+  return run_fwd(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream);
+}
+
+int32_t flex_linattn_fwd_noalloc(const flex_desc* desc, const void* Q, const void* K, const void* V,
+                                 const float* W1, const float* W2, const float* tau, void* O,
+                                 float* den, void* stream) {
+  const int32_t st = check_fwd_args(desc, Q, K, V, W1, W2, tau, O, den);
+  if (st != FLEX_OK) return st;
+  if (ws_bytes_of(desc, FLEX_PASS_FWD) > (size_t)FLEX_NOALLOC_SCRATCH_BYTES) return FLEX_ERR_WORKSPACE;
+  void* ws = nullptr;
+  const int32_t sst = scratch_of_current_device(&ws);
+  if (sst != FLEX_OK) return sst;
+  // the forward writes every workspace byte it reads (segment states, their
+  // scan, fragments, group sums), so the scratch needs no clearing
+  return run_fwd(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream);
 }
 
 int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, const void* V,

@@ -145,6 +145,13 @@ def test_entry_points_reject_bad_arguments():
     assert lib.flex_linattn_bwd(ctypes.byref(dn), *args, *nofwd, P, 16, None) == F.FLEX_ERR_WORKSPACE
     # a forward workspace smaller than the forward needs
     assert lib.flex_linattn_bwd(ctypes.byref(dn), *args, P, 16, P, big, None) == F.FLEX_ERR_WORKSPACE
+    # the forward without a workspace: the same argument checks, and a forward
+    # workspace beyond the static scratch is refused before any device work
+    assert lib.flex_linattn_fwd_noalloc(None, P, P, P, P, P, P, P, P, None) == F.FLEX_ERR_INVALID_ARG
+    assert lib.flex_linattn_fwd_noalloc(ctypes.byref(dn), P, P, P, P, None, P, P, P, None) == 1
+    assert lib.flex_linattn_fwd_noalloc(ctypes.byref(ds), P, P, P, P, P, P, P, P, None) == 1
+    d5 = F.make_desc(2, 16, 8192, 128, 256, "nonstationary", True, "bf16")
+    assert lib.flex_linattn_fwd_noalloc(ctypes.byref(d5), P, P, P, P, P, P, P, P, None) == 3
     # feature map
     assert lib.flex_feature_map(ctypes.byref(dn), None, P, P, P, P, None, 0, None) == 1
     assert lib.flex_feature_map(ctypes.byref(ds), P, P, P, P, P, None, 0, None) == 1
