@@ -131,6 +131,23 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K,
                          const float* tau, void* O, float* den,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* Causal prefill for autoregressive generation (the language model of
+ * Sec. 4.2): flex_linattn_fwd on a causal prefix of N tokens (same O and den,
+ * bitwise), which also writes the state of the whole prefix,
+ *     S' = sum_{j<N} phi(K_j) [V_j ; 1]^T   (Eq.(linear att)),
+ * in the layout of flex_decode_step.  Decode steps started from it continue
+ * the sequence: after t steps with tokens N .. N+t-1, the step's output equals
+ * row N+t-1 of flex_linattn_fwd's causal output on all N+t tokens.
+ *   state  fp32, B*H*2m*(dv+1) floats, overwritten: per (b,h) slice S [2m][dv]
+ *          row-major, then z [2m], feature rows in [cos | sin] order.
+ *   ws     flex_workspace_size(desc, FLEX_PASS_FWD) bytes, as for the forward.
+ * desc->causal must be 1 (FLEX_ERR_UNSUPPORTED otherwise); a NULL or
+ * misaligned state returns FLEX_ERR_INVALID_ARG.  Shapes as flex_linattn_fwd. */
+int32_t flex_linattn_prefill(const flex_desc* desc, const void* Q, const void* K,
+                             const void* V, const float* W1, const float* W2,
+                             const float* tau, void* O, float* den, float* state,
+                             void* ws, size_t ws_bytes, void* stream);
+
 /* Bytes of the static device scratch that serves flex_linattn_fwd_noalloc
  * as its workspace (one array per GPU). */
 #define FLEX_NOALLOC_SCRATCH_BYTES (32u << 20)

@@ -4,7 +4,7 @@ The computation lives in the HIP library ``libflexattn.so`` (C ABI in
 include/flex.h); this package is its thin Python binding.
 """
 from ._lib import (FlexError, flex_desc, make_desc, workspace_size, flex_feature_map,  # noqa: F401
-                   flex_linattn_fwd, flex_linattn_fwd_noalloc, flex_linattn_bwd, flex_decode_step,
+                   flex_linattn_fwd, flex_linattn_prefill, flex_linattn_fwd_noalloc, flex_linattn_bwd, flex_decode_step,
                    flex_awd_loss, decode_state,
                    decode_state_views, load, status_string,
                    FLEX_OK, FLEX_ERR_INVALID_ARG, FLEX_ERR_UNSUPPORTED, FLEX_ERR_WORKSPACE,

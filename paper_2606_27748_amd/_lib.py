@@ -18,7 +18,8 @@ FLEX_F32, FLEX_BF16 = 0, 1
 FLEX_STATIONARY, FLEX_NONSTATIONARY = 0, 1
 FLEX_PASS_FEATURE_MAP, FLEX_PASS_FWD, FLEX_PASS_BWD, FLEX_PASS_AWD = 0, 1, 2, 3
 EXPORTS = ("flex_abi_version", "flex_status_string", "flex_workspace_size",
-           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_fwd_noalloc", "flex_linattn_bwd",
+           "flex_feature_map", "flex_linattn_fwd", "flex_linattn_prefill", "flex_linattn_fwd_noalloc",
+           "flex_linattn_bwd",
            "flex_decode_step",
            "flex_awd_loss", "flex_timing_enable", "flex_timing_read")
 KERNELS = {"none": 0, "fwd_state": 1, "fwd_sweep": 2, "scan": 3, "bwd_prepass": 4,
@@ -72,6 +73,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.flex_feature_map.argtypes = [D, P, P, P, P, P, P, S, P]
     lib.flex_linattn_fwd.restype = I
     lib.flex_linattn_fwd.argtypes = [D, P, P, P, P, P, P, P, P, P, S, P]
+    lib.flex_linattn_prefill.restype = I
+    lib.flex_linattn_prefill.argtypes = [D, P, P, P, P, P, P, P, P, P, P, S, P]
     lib.flex_linattn_fwd_noalloc.restype = I
     lib.flex_linattn_fwd_noalloc.argtypes = [D, P, P, P, P, P, P, P, P, P]
     lib.flex_linattn_bwd.restype = I
@@ -156,6 +159,28 @@ def flex_linattn_fwd(desc: flex_desc, Q, K, V, W1, W2, tau, O=None, den=None, ws
                                  ws.numel(), _stream())
     _check(st, "flex_linattn_fwd")
     return O, den
+
+
+def flex_linattn_prefill(desc: flex_desc, Q, K, V, W1, W2, tau, state=None, O=None, den=None,
+                         ws=None, want_den=True):
+    """Causal forward that also writes the prefix's state in the decode layout
+    (decode_state).  Returns (O, den, state)."""
+    import torch
+    dev = Q.device
+    if O is None:
+        O = torch.empty(desc.B, desc.H, desc.N, desc.dv, dtype=Q.dtype, device=dev)
+    if den is None and want_den:
+        den = torch.empty(desc.B, desc.H, desc.N, dtype=torch.float32, device=dev)
+    if state is None:
+        state = torch.empty(desc.B, desc.H, 2 * desc.m * (desc.dv + 1), dtype=torch.float32, device=dev)
+    if state.numel() != desc.B * desc.H * 2 * desc.m * (desc.dv + 1) or state.dtype != torch.float32:
+        raise FlexError(FLEX_ERR_INVALID_ARG, "flex_linattn_prefill: state must hold B*H*2m*(dv+1) fp32")
+    ws = _workspace(desc, FLEX_PASS_FWD, ws, dev)
+    st = load().flex_linattn_prefill(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(V), _ptr(W1),
+                                     _ptr(W2), _ptr(tau), _ptr(O), _ptr(den), _ptr(state), _ptr(ws),
+                                     ws.numel(), _stream())
+    _check(st, "flex_linattn_prefill")
+    return O, den, state
 
 
 def flex_linattn_fwd_noalloc(desc: flex_desc, Q, K, V, W1, W2, tau, O, den=None):

@@ -310,10 +310,13 @@ int32_t check_fwd_args(const flex_desc* desc, const void* Q, const void* K, cons
 // The forward on validated arguments with a workspace of at least
 // ws_bytes_of(desc, FLEX_PASS_FWD) bytes at `base`.
 int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void* V, const float* W1,
-                const float* W2, const float* tau, void* O, float* den, char* base, hipStream_t stream) {
+                const float* W2, const float* tau, void* O, float* den, char* base, hipStream_t stream,
+                float* state_out = nullptr) {
   FwdArgs a;
   memset(&a, 0, sizeof(a));
   a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den;
+  a.state_out = state_out;
+  a.state_m = desc->m;
   const Groups G = groups_of(desc);
   const KernelShape ks = attn_shape(desc);
   const size_t sb = fwd_group_state_bytes(desc);
@@ -347,6 +350,7 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
     a.W1 = W1 + woff;
     a.W2 = W2 ? W2 + woff : nullptr;
     a.state = reinterpret_cast<float*>(base + g * sb);
+    a.state_f0 = g * G.m;
     a.acc = G.n == 1 ? 0 : (g == 0 ? 1 : 2);
     const hipError_t e = launch_fwd(a, ks, false, stream);
     if (e != hipSuccess) return FLEX_ERR_HIP;
@@ -545,6 +549,18 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
   const size_t need = ws_bytes_of(desc, FLEX_PASS_FWD);
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
   return run_fwd(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream);
+}
+
+int32_t flex_linattn_prefill(const flex_desc* desc, const void* Q, const void* K, const void* V,
+                             const float* W1, const float* W2, const float* tau, void* O, float* den,
+                             float* state, void* ws, size_t ws_bytes, void* stream) {
+  const int32_t st = check_fwd_args(desc, Q, K, V, W1, W2, tau, O, den);
+  if (st != FLEX_OK) return st;
+  if (desc->causal != 1) return FLEX_ERR_UNSUPPORTED;
+  if (!state || !aligned16(state)) return FLEX_ERR_INVALID_ARG;
+  const size_t need = ws_bytes_of(desc, FLEX_PASS_FWD);
+  if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
+  return run_fwd(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream, state);
 }
 
 int32_t flex_linattn_fwd_noalloc(const flex_desc* desc, const void* Q, const void* K, const void* V,

@@ -400,6 +400,26 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       }
     }
   }
+  if (CAUSAL && a.state_out && seg == a.sweep_groups - 1) {
+    // causal prefill: the last segment ends with the state of the whole
+    // sequence (an empty trailing segment holds it as its carry-in).  Tile
+    // (fc, dt) has rows = features 4g+i of feature tile fc (fc = 2ft: cos of
+    // frequency tile ft, 2ft+1: its sin) and cols = value columns; the
+    // normaliser tile holds z in column 0.
+    const size_t F2 = 2 * (size_t)a.state_m;
+    float* so = a.state_out + (size_t)bh * F2 * (SH::DV + 1);
+    float* zo = so + F2 * SH::DV;
+#pragma unroll
+    for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int f = a.state_f0 + w * FW + (fc / 2) * 16 + 4 * g + i;
+        const size_t row = (fc % 2) ? (size_t)a.state_m + f : (size_t)f;
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt) so[row * SH::DV + dt * 16 + r] = S[fc][dt][i];
+        if (r == 0) zo[row] = S[fc][SH::DVT][i];
+      }
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -47,6 +47,11 @@ struct FwdArgs {
   // feature map of a second input in the same launch (grid.z = 2): X = K,
   // Phi = O2; nullptr K maps Q only
   void* O2;
+  // causal prefill: the final state sum_j phi(K_j) [V_j ; 1]^T of every slice in
+  // the decode layout (per slice S [2m][dv] row-major, then z [2m]); state_f0 is
+  // the first frequency of this launch's group, state_m the total m.  NULL: none.
+  float* state_out;
+  int state_f0, state_m;
 };
 
 struct BwdArgs {

@@ -152,6 +152,11 @@ def test_entry_points_reject_bad_arguments():
     assert lib.flex_linattn_fwd_noalloc(ctypes.byref(ds), P, P, P, P, P, P, P, P, None) == 1
     d5 = F.make_desc(2, 16, 8192, 128, 256, "nonstationary", True, "bf16")
     assert lib.flex_linattn_fwd_noalloc(ctypes.byref(d5), P, P, P, P, P, P, P, P, None) == 3
+    # prefill: causal only, state required, workspace checked
+    nc = F.make_desc(1, 2, 100, 64, 128, "nonstationary", False, "bf16")
+    assert lib.flex_linattn_prefill(ctypes.byref(nc), P, P, P, P, P, P, P, P, P, P, big, None) == 2
+    assert lib.flex_linattn_prefill(ctypes.byref(dn), P, P, P, P, P, P, P, P, None, P, big, None) == 1
+    assert lib.flex_linattn_prefill(ctypes.byref(dn), P, P, P, P, P, P, P, P, P, P, 16, None) == 3
     # feature map
     assert lib.flex_feature_map(ctypes.byref(dn), None, P, P, P, P, None, 0, None) == 1
     assert lib.flex_feature_map(ctypes.byref(ds), P, P, P, P, P, None, 0, None) == 1

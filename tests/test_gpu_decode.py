@@ -8,7 +8,7 @@ import pytest
 import oracle as orc
 import workloads as W
 from tests.gpu_util import to_device, to_f64
-from tests.parity import check_forward
+from tests.parity import check_forward, UNIT
 
 pytestmark = pytest.mark.gpu
 
@@ -96,3 +96,68 @@ def test_decode_state_layout(F):
     ref_S = pk[..., :, None] * x.f64("V")[:, :, 0][..., None, :]
     assert np.linalg.norm(S - ref_S) <= 1e-5 * np.linalg.norm(ref_S)
     assert np.linalg.norm(z - pk) <= 1e-5 * np.linalg.norm(pk)
+
+
+PREFILL_CASES = [("bf16", 64, 128, "nonstationary", 0), ("bf16", 64, 128, "nonstationary", 16),
+                 ("bf16", 32, 64, "stationary", 32), ("f32", 32, 64, "stationary", 0),
+                 ("f32", 32, 64, "nonstationary", 16), ("bf16", 128, 256, "nonstationary", 0)]
+
+
+@pytest.mark.parametrize("io,d,m,variant,chunk", PREFILL_CASES)
+def test_prefill_then_decode(F, io, d, m, variant, chunk):
+    """Prefill a causal prefix of N0 = 300 tokens (3 segments), then decode 6
+    more tokens from the prefill's state.  The prefill's O and den are bitwise
+    those of flex_linattn_fwd; its state is sum_j phi(K_j) [V_j ; 1]^T over the
+    prefix (within the rounding of the features it sums); the decode outputs
+    are rows N0 .. N0+5 of the oracle's causal attention over all 306 tokens."""
+    import torch
+    N0, steps = 300, 6
+    wl = W.Workload("prefill", 2, 3, N0 + steps, d, m, variant, True, io, False, 43)
+    x = W.generate(wl)
+    t = to_device(x)
+    pre = {k: t[k][:, :, :N0].contiguous() for k in ("Q", "K", "V")}
+    dp = F.make_desc(wl.B, wl.H, N0, d, m, variant, True, io, segments=3, chunk=chunk)
+    O_p, den_p, state = F.flex_linattn_prefill(dp, pre["Q"], pre["K"], pre["V"], t["W1"], t["W2"],
+                                               t["tau"])
+    O_f, den_f = F.flex_linattn_fwd(dp, pre["Q"], pre["K"], pre["V"], t["W1"], t["W2"], t["tau"])
+    torch.cuda.synchronize()
+    assert torch.equal(O_p.view(torch.int16) if io == "bf16" else O_p,
+                       O_f.view(torch.int16) if io == "bf16" else O_f)
+    assert torch.equal(den_p, den_f)
+    # the prefill state against the oracle's prefix sum, relative to the
+    # magnitude of the summed terms (features rounded to the io precision,
+    # fp32 accumulation over N0 terms)
+    Q, K, V = x.f64("Q"), x.f64("K"), x.f64("V")
+    pk = orc.feature_map(K[:, :, :N0], x.W1, x.W2, x.tau, variant)
+    Vp = np.concatenate([V[:, :, :N0], np.ones(V[:, :, :N0].shape[:-1] + (1,))], axis=-1)
+    ref_S = np.einsum("bhnf,bhnv->bhfv", pk, Vp)
+    abs_S = np.einsum("bhnf,bhnv->bhfv", np.abs(pk), np.abs(Vp))
+    S, z = F.decode_state_views(dp, state)
+    got_S = np.concatenate([to_f64(S), to_f64(z)[..., None]], axis=-1)
+    bound = (4 * UNIT[io] + 4 * 2.0 ** -24 * np.sqrt(N0)) * np.linalg.norm(abs_S)
+    assert np.linalg.norm(got_S - ref_S) <= bound, (np.linalg.norm(got_S - ref_S), bound)
+    # decode the next tokens from the prefill's state
+    dd = F.make_desc(wl.B, wl.H, 1, d, m, variant, True, io)
+    outs, dens = [], []
+    for i in range(N0, N0 + steps):
+        o, den = F.flex_decode_step(dd, t["Q"][:, :, i].contiguous(), t["K"][:, :, i].contiguous(),
+                                    t["V"][:, :, i].contiguous(), t["W1"], t["W2"], t["tau"], state)
+        outs.append(o)
+        dens.append(den)
+    O = torch.stack(outs, dim=2)
+    den = torch.stack(dens, dim=2)
+    torch.cuda.synchronize()
+    ref_O, ref_den = orc.linattn_fwd(Q, K, V, x.W1, x.W2, x.tau, variant, True)
+    kap = orc.conditioning(Q, K, x.W1, x.W2, x.tau, variant, True)
+    check_forward(io, to_f64(O), to_f64(den), ref_O[:, :, N0:], ref_den[:, :, N0:], kap[:, :, N0:])
+
+
+def test_prefill_rejects_non_causal_and_missing_state(F):
+    import torch
+    d = F.make_desc(1, 2, 64, 64, 64, "stationary", False, "bf16")
+    x = torch.zeros(1, 2, 64, 64, dtype=torch.bfloat16, device="cuda")
+    W1 = torch.zeros(2, 64, 64, device="cuda")
+    tau = torch.zeros(2, device="cuda")
+    with pytest.raises(F.FlexError) as e:
+        F.flex_linattn_prefill(d, x, x, x, W1, None, tau)
+    assert e.value.status == F.FLEX_ERR_UNSUPPORTED
