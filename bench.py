@@ -172,7 +172,9 @@ def traffic_from_profiles(workload, kernel):
         rec = json.load(f)
     if rec.get("source_hash") != source_hash(kernel):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    # the class's counted bytes per step (one launch per step, or the frequency
+    # groups' launches together), like `achieved`
+    return rec.get("hbm_bytes_per_step", rec.get("hbm_bytes_per_launch"))
 
 
 def host_facts():

@@ -339,8 +339,12 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
     a.sweep_groups = a.segments;
     a.sweep_cps = a.chunks_per_seg * (kChunk / a.sweep_chunk);
   } else {
+    // chunks per non-causal sweep workgroup: up to kSweepChunks, fewer when
+    // that leaves the CUs short of workgroups (small B*H*N)
+    const long long per_cu = ((long long)a.nchunks * a.BH + kCUs - 1) / kCUs;
     a.sweep_chunk = kChunk;
-    a.sweep_cps = a.nchunks < kSweepChunks ? a.nchunks : kSweepChunks;
+    a.sweep_cps = (int)(per_cu < 1 ? 1 : (per_cu > kSweepChunks ? kSweepChunks : per_cu));
+    if (a.sweep_cps > a.nchunks) a.sweep_cps = a.nchunks;
     a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
   }
   a.s_const = s_const_of(desc);

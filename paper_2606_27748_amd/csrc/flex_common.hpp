@@ -243,38 +243,77 @@ struct FreqSlice {
   }
 };
 
-// fp32 path: the wave's frequency rows themselves (no operand fragments).  The
-// projection is formed in float64 on the vector ALU from these rows (W'1, W'2
-// exactly as (w1 +- w2)/2 in float64), so no frequency is rounded before it
-// multiplies x.  The rows of matrix 1 start at `a`, those of matrix 2 at `b`,
-// both with row stride D.  A prepared block holds the same rows as plain
-// floats, [matrix][FW][D], in the space the generic slice's fragments take.
+// fp32 path: float64 operands of the projection on the FP64 matrix cores
+// (v_mfma_f64_16x16x4f64: A[m][k] and B[k][n] one element per lane, lane l
+// supplying index l%16 at k = l/16; D holds rows l/16 + 4i, i = 0..3, of
+// column l%16).  The frequencies W'/(2 pi) are formed in float64 from the fp32
+// rows (W'1 = (w1 + w2)/2 and W'2 = (w1 - w2)/2 exactly), so the projection
+// reaches float64 accuracy before the phase is reduced.  Two operand layouts:
+//   wt: A operand of the frequency-row tile P^T = W' X^T; lane row rho holds
+//       frequency 4 (rho % 4) + rho / 4, so that accumulator slot i of lane
+//       group g is frequency 4g + i as in the bf16 tiles;
+//   wr: B operand of the token-row tile P = X W'^T; lane row rho holds
+//       frequency rho (the token rows are permuted on the X side instead).
+// A prepared block holds wt then wr per lane, in the space NFRAG reserves.
+__device__ __forceinline__ int f64_tile_row(int rho) { return 4 * (rho % 4) + rho / 4; }
+
 template <int D, int FW, bool NS>
 struct FreqSlice<float, D, FW, NS> {
   static constexpr int FT = FW / 16;
   static constexpr int PR = NS ? 2 * FT : FT;
   static constexpr int KD = D / 32;
   static constexpr int NSPLIT = 1;
-  static constexpr int NFRAG = PR * KD;   // Frag<float> units of the prepared rows
-  static_assert(NFRAG * WAVE * 8 == (NS ? 2 : 1) * FW * D, "prepared rows fill the fragment block");
-  const float* a;
-  const float* b;
+  static constexpr int KS = D / 4;                 // f64 MFMA k-steps over d
+  static constexpr int NFRAG = 2 * PR * KS / 4;    // Frag<float> units (32 bytes per lane)
+  static_assert((2 * PR * KS) % 4 == 0, "whole fragment units");
+  double wt[PR][KS];
+  double wr[PR][KS];
 
   __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
-    a = W1 + (size_t)f0 * D;
-    b = NS ? W2 + (size_t)f0 * D : nullptr;
-  }
-  __device__ __forceinline__ void store_frags(Frag<float>* out) const {
-    float* o = reinterpret_cast<float*>(out);
-    const int l = threadIdx.x % WAVE;
-    for (int i = l; i < FW * D; i += WAVE) {
-      o[i] = a[i];
-      if (NS) o[FW * D + i] = b[i];
+    constexpr double INV_2PI_D = 0.15915494309189535;
+    const int l = threadIdx.x % WAVE, rho = l % 16, g = l / 16;
+#pragma unroll
+    for (int pr = 0; pr < PR; ++pr) {
+      const int ft = pr % FT;
+      const bool second = pr >= FT;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int k = 4 * ks + g;
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+          const int f = f0 + ft * 16 + (v == 0 ? f64_tile_row(rho) : rho);
+          double w = W1[(size_t)f * D + k];
+          if (NS) {
+            const double w2 = W2[(size_t)f * D + k];
+            w = second ? 0.5 * (w - w2) : 0.5 * (w + w2);
+          }
+          w *= INV_2PI_D;
+          if (v == 0) wt[pr][ks] = w; else wr[pr][ks] = w;
+        }
+      }
     }
   }
+  __device__ __forceinline__ void store_frags(Frag<float>* out) const {
+    double* o = reinterpret_cast<double*>(out);
+    const int l = threadIdx.x % WAVE;
+#pragma unroll
+    for (int pr = 0; pr < PR; ++pr)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        o[(pr * KS + ks) * WAVE + l] = wt[pr][ks];
+        o[((PR + pr) * KS + ks) * WAVE + l] = wr[pr][ks];
+      }
+  }
   __device__ __forceinline__ void load_frags(const Frag<float>* in) {
-    a = reinterpret_cast<const float*>(in);
-    b = NS ? a + FW * D : nullptr;
+    const double* o = reinterpret_cast<const double*>(in);
+    const int l = threadIdx.x % WAVE;
+#pragma unroll
+    for (int pr = 0; pr < PR; ++pr)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        wt[pr][ks] = o[(pr * KS + ks) * WAVE + l];
+        wr[pr][ks] = o[((PR + pr) * KS + ks) * WAVE + l];
+      }
   }
 };
 
@@ -406,18 +445,25 @@ __device__ __forceinline__ void sincos_rev(float p, float& s, float& c) {
   c = __builtin_amdgcn_cosf(p);
 }
 __device__ __forceinline__ float cos_rev(float p) { return __builtin_amdgcn_cosf(p); }
-// fp32 path: a float64 phase in revolutions.  p - rint(p) is exact in float64
-// and lies in [-1/2, 1/2]; the angle 2 pi r is then at most pi in size, and
-// sine and cosine are taken in float64 (OCML) and rounded once to fp32.
-constexpr double TWO_PI_D = 6.283185307179586;
+// fp32 path: a float64 phase in revolutions.  r = p - rint(p) is exact in
+// float64 and lies in [-1/2, 1/2].  It is split as r = rh + rl with rh its
+// fp32 rounding (|rl| <= 2^-26); sine and cosine of rh come from v_sin_f32 /
+// v_cos_f32 and the remainder enters to first order:
+// sin 2pi(rh + rl) = sin 2pi rh + 2pi rl cos 2pi rh + O(rl^2).
 __device__ __forceinline__ void sincos_rev(double p, float& s, float& c) {
-  const double t = (p - rint(p)) * TWO_PI_D;
-  double sd, cd;
-  sincos(t, &sd, &cd);
-  s = (float)sd;
-  c = (float)cd;
+  const double r = p - rint(p);
+  const float rh = (float)r;
+  const float a = 6.2831853f * (float)(r - (double)rh);
+  const float s0 = __builtin_amdgcn_sinf(rh), c0 = __builtin_amdgcn_cosf(rh);
+  s = fmaf(a, c0, s0);
+  c = fmaf(-a, s0, c0);
 }
-__device__ __forceinline__ float cos_rev(double p) { return (float)cos((p - rint(p)) * TWO_PI_D); }
+__device__ __forceinline__ float cos_rev(double p) {
+  const double r = p - rint(p);
+  const float rh = (float)r;
+  const float a = 6.2831853f * (float)(r - (double)rh);
+  return fmaf(-a, __builtin_amdgcn_sinf(rh), __builtin_amdgcn_cosf(rh));
+}
 
 // Feature epilogue for one frequency tile ft of one 16-token tile:
 // scale = s * e(x) (0 for rows that are not valid).  Returns the operand

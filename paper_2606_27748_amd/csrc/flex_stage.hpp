@@ -117,54 +117,27 @@ __device__ __forceinline__ void lds_row8(Frag<float>& f, const float* row, int c
   f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
 }
 
-// fp32 path: one projection tile in float64 on the vector ALU.  Lane (r, g)
-// forms tile element i of projection row tile pr as the dot product of token
-// row xr(i) with frequency row fr(i) of its matrix pair; W'1 = (w1 + w2)/2 and
-// W'2 = (w1 - w2)/2 are exact in float64.  ROWS_AS_TOKENS = false: the tile
-// holds frequencies 4g+i (rows) x token r (cols), as the MFMA tile of
-// project_tile_lds; true: tokens 4g+i x frequency r, as project_rows_lds.
+// fp32 path: one projection tile on the FP64 matrix cores (operand layouts in
+// FreqSlice<float>).  ROWS_AS_TOKENS = false: the tile holds frequencies 4g+i
+// (rows) x token r (cols), as the bf16 tile of project_tile_lds; true: tokens
+// 4g+i x frequency r, as project_rows_lds (the X rows are then permuted so
+// that accumulator slot i of lane group g is token 4g + i).
 template <int D, int FW, bool NS, int LD, bool ROWS_AS_TOKENS>
 __device__ __forceinline__ void project_f64(const FreqSlice<float, D, FW, NS>& fs, const float* X, int tt,
                                             f64x4 (&p)[FreqSlice<float, D, FW, NS>::PR]) {
   typedef FreqSlice<float, D, FW, NS> FS;
-  constexpr double INV_2PI_D = 0.15915494309189535;
   const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const float* xr = X + (tt * 16 + (ROWS_AS_TOKENS ? f64_tile_row(r) : r)) * LD;
 #pragma unroll
-  for (int ft = 0; ft < FS::FT; ++ft)
+  for (int pr = 0; pr < FS::PR; ++pr) p[pr] = f64x4{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int tok = ROWS_AS_TOKENS ? tt * 16 + 4 * g + i : tt * 16 + r;
-      const int fr = ROWS_AS_TOKENS ? ft * 16 + r : ft * 16 + 4 * g + i;
-      const float* xr = X + tok * LD;
-      const float* wa = fs.a + (size_t)fr * D;
-      const float* wb = NS ? fs.b + (size_t)fr * D : nullptr;
-      double s1 = 0.0, s2 = 0.0;
+  for (int ks = 0; ks < FS::KS; ++ks) {
+    const double x = xr[4 * ks + g];
 #pragma unroll
-      for (int k = 0; k < D; k += 4) {
-        const float4 x4 = *reinterpret_cast<const float4*>(xr + k);
-        const float4 a4 = *reinterpret_cast<const float4*>(wa + k);
-        const double xv[4] = {x4.x, x4.y, x4.z, x4.w};
-        const double av[4] = {a4.x, a4.y, a4.z, a4.w};
-        if (NS) {
-          const float4 b4 = *reinterpret_cast<const float4*>(wb + k);
-          const double bv[4] = {b4.x, b4.y, b4.z, b4.w};
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            s1 = fma(xv[j], av[j] + bv[j], s1);
-            s2 = fma(xv[j], av[j] - bv[j], s2);
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) s1 = fma(xv[j], av[j], s1);
-        }
-      }
-      if (NS) {
-        p[ft][i] = s1 * (0.5 * INV_2PI_D);
-        p[FS::FT + ft][i] = s2 * (0.5 * INV_2PI_D);
-      } else {
-        p[ft][i] = s1 * INV_2PI_D;
-      }
-    }
+    for (int pr = 0; pr < FS::PR; ++pr)
+      p[pr] = ROWS_AS_TOKENS ? __builtin_amdgcn_mfma_f64_16x16x4f64(x, fs.wr[pr][ks], p[pr], 0, 0, 0)
+                             : __builtin_amdgcn_mfma_f64_16x16x4f64(fs.wt[pr][ks], x, p[pr], 0, 0, 0);
+  }
 }
 
 // Projection of one 16-token tile (rows staged in LDS, row stride LD) onto a
