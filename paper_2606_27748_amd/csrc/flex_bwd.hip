@@ -186,9 +186,16 @@ __device__ __forceinline__ void dump_dw(float* out, const float* dwl, int f0) {
 // ---------------------------------------------------------------------------
 // WITH_S: also the key-side states S' (not needed when the forward's segment
 // states are passed in).
+// The pre-pass forms sums over a segment and per-token scalars only, so at
+// d <= 64 it walks the segment in 64-token chunks (a backward segment is a
+// whole number of them: it spans the forward's 64-token chunks), not the
+// sweeps' 32; at d = 128 the double-buffered staging of 64 rows would not fit
+// in LDS.
 template <class T, int D, int FW, int NW, bool NS, bool WITH_S>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
-  typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
+  constexpr int PCH = D <= 64 ? CHUNK : BWD_CHUNK;
+  typedef Shape<T, D, FW, NW, NS, PCH> SH;
+  static_assert(PCH % BWD_CHUNK == 0 && CHUNK % PCH == 0, "pre-pass chunks hold whole sweep chunks");
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, SH::NT, SH::CH> StX;
   typedef RowStage<IO, SH::DV, SH::NT, SH::CH> StV;
@@ -207,8 +214,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
-  const int c0 = seg * a.chunks_per_seg;
-  const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
+  const int cps = a.chunks_per_seg / (PCH / BWD_CHUNK);   // pre-pass chunks per segment
+  const int c0 = seg * cps;
+  const int c1 = min(c0 + cps, (a.N + SH::CH - 1) / SH::CH);
   const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
   const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
   const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
