@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define FLEX_ABI_VERSION 4
+#define FLEX_ABI_VERSION 5
 
 typedef enum {
   FLEX_OK = 0,
