@@ -113,15 +113,35 @@ int nchunks_of(const flex_desc* d) { return (d->N + kChunk - 1) / kChunk; }
 // Chunks per workgroup of the non-causal sweep (its chunks are independent).
 constexpr int kSweepChunks = 8;
 
-// Forward state pre-pass workgroups per segment: two (each half a segment)
-// for 4-wave workgroups when that still leaves fewer than two workgroups per
-// CU, so that two of them share a CU (8-wave workgroups already give each SIMD
-// two waves).
+// Segments whose local state the forward pre-pass forms: a causal forward
+// reads only exclusive prefixes, so the last segment's own state is never used.
+int pre_segs_of(const flex_desc* d, int P) { return d->causal ? P - 1 : P; }
+
+// Forward state pre-pass workgroups per segment (sub-segments): 1, 2, 4 or 8,
+// dividing the segment's chunks.  More sub-segments shorten the pre-pass's
+// critical path when its workgroups underfill the CUs (one 8-wave or two
+// 4-wave workgroups per CU at a time) but write and scan more states; the
+// cost is the rounds of chunks (about a third of a sweep chunk each, scaled
+// by MFMA work like pick_segments) plus that state traffic at 5 TB/s.
 int fwd_sub_of(const flex_desc* d, int P) {
   const int nc = nchunks_of(d);
   const int cps = (nc + P - 1) / P;
-  const long long wgs = (long long)d->B * d->H * P;
-  return (fwd_state_waves(attn_shape(d)) == 4 && cps % 2 == 0 && wgs < 2LL * kCUs) ? 2 : 1;
+  const long long used = pre_segs_of(d, P);
+  if (used <= 0) return 1;
+  const KernelShape ks = attn_shape(d);
+  const long long cap = (long long)kCUs * (fwd_state_waves(ks) == 4 ? 2 : 1);
+  const double m_eff = ks.nonstationary ? 2.0 * ks.m : ks.m;
+  const double t_pre = 2.2e-6 * (2.0 * ks.d * m_eff + 4.0 * ks.m * (d->dv + 1)) / 66048.0;
+  const double state_bytes = (double)fwd_state_floats(ks) * sizeof(float);
+  int best = 1;
+  double best_t = 1e30;
+  for (int sub = 1; sub <= 8; sub *= 2) {
+    if (cps % sub != 0) break;
+    const long long wgs = (long long)d->B * d->H * used * sub;
+    const double t = (double)((wgs + cap - 1) / cap) * (cps / sub) * t_pre + 2.0 * wgs * state_bytes / 5.0e12;
+    if (t < best_t - 1e-12) { best_t = t; best = sub; }
+  }
+  return best;
 }
 
 // Segments per (b,h): enough workgroups to cover the 256 CUs in whole rounds
@@ -332,6 +352,7 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
   a.segments = P0;
   a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
   a.sub = fwd_sub_of(desc, P0);
+  a.pre_segs = pre_segs_of(desc, P0);
   if (desc->causal) {
     // the sweep's chunks of chunk_of(desc) tokens: a segment spans the same
     // tokens as its 64-token pre-pass chunks

@@ -161,6 +161,17 @@ __device__ __forceinline__ void dw_accumulate(float* dwl, const f32x4 (&acc)[SH:
     }
 }
 
+// One projection-row tile pr of the partial: acc[dt] added to its LDS tiles.
+template <class SH, int D>
+__device__ __forceinline__ void dw_accumulate_row(float* dwl, int pr, const f32x4 (&acc)[D / 16]) {
+  const int l = threadIdx.x % WAVE;
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    f32x4* p = reinterpret_cast<f32x4*>(dwl + ((pr * (D / 16) + dt) * WAVE + l) * 4);
+    *p += acc[dt];
+  }
+}
+
 // Write a wave's frequency-gradient partial tiles DW[pr][dt] (rows = projection
 // rows, cols = d) into the canonical layout [matrix][m][d].
 template <class SH, int D, int FW, bool NS>
@@ -608,24 +619,23 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     }
     // frequency gradient partial: dW'[rows][d] += dP^T Q
     {
-      f32x4 dw[SH::PR][DT];
+      // one 32-token k-step per chunk: each projection-row tile's product is
+      // complete after its MFMAs and goes to LDS before the next one is formed
+      static_assert(SH::KT == 1, "one token k-step per chunk");
+      Frag<T> xq[DT];
 #pragma unroll
-      for (int pr = 0; pr < SH::PR; ++pr)
+      for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XQ), StX::LD, 4 * g, 16 + 4 * g, dt * 16);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) dw[pr][dt] = zero4();
+      for (int pr = 0; pr < SH::PR; ++pr) {
+        const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 4 * g, 16 + 4 * g, pr * 16);
+        f32x4 dw[DT];
 #pragma unroll
-      for (int ks = 0; ks < SH::KT; ++ks) {
-        Frag<T> xq[DT];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) xq[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XQ), StX::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
-#pragma unroll
-        for (int pr = 0; pr < SH::PR; ++pr) {
-          const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, pr * 16);
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) mma(dw[pr][dt], dpt, xq[dt]);
+        for (int dt = 0; dt < DT; ++dt) {
+          dw[dt] = zero4();
+          mma(dw[dt], dpt, xq[dt]);
         }
+        dw_accumulate_row<SH, D>(DWL[w], pr, dw);
       }
-      dw_accumulate<SH, D>(DWL[w], dw);
     }
   }
   const size_t nmat = NS ? 2 : 1;
@@ -732,7 +742,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         for (int sp = 0; sp < WTS::NSPLIT; ++sp) wf[ww][ks][sp] = wd[((sp * DT + dt) * WTS::KP + ks) * WAVE + l];
     }
   };
-  if (DT <= NW) load_wf(w % DT);
+  // held for the whole sweep with up to 4 waves; 8-wave workgroups (two
+  // waves per SIMD, 256 registers) load them per chunk
+  constexpr bool HOLD_WF = DT <= NW && NW <= 4;
+  if (HOLD_WF) load_wf(w % DT);
   for (int c = c1 - 1; c >= c0; --c) {
     // This chunk's staging buffers.  Double-buffered, they need no barrier
     // before they are written: the chunk that last read them (two back) is
@@ -966,7 +979,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     // dt = w mod DT (+ NW, ...) and, when there are fewer d tiles than waves,
     // the token tiles tt = w / DT (+ NW / DT, ...).  The dX fragments of its
     // first d tile are loaded before the barrier, so their latency overlaps it.
-    if (DT > NW) load_wf(w % DT);
+    if (!HOLD_WF) load_wf(w % DT);
     // dP of this wave as [token][projection row] in its LDS block (its own reads
     // of phi(Q)/den there are done: one wave's LDS accesses complete in order),
     // and this lane's share of g per token
@@ -1028,24 +1041,23 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       }
     }
     {
-      f32x4 dw[SH::PR][DT];
+      // one 32-token k-step per chunk: each projection-row tile's product is
+      // complete after its MFMAs and goes to LDS before the next one is formed
+      static_assert(SH::KT == 1, "one token k-step per chunk");
+      Frag<T> xk[DT];
 #pragma unroll
-      for (int pr = 0; pr < SH::PR; ++pr)
+      for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XK), StX::LD, 4 * g, 16 + 4 * g, dt * 16);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) dw[pr][dt] = zero4();
+      for (int pr = 0; pr < SH::PR; ++pr) {
+        const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 4 * g, 16 + 4 * g, pr * 16);
+        f32x4 dw[DT];
 #pragma unroll
-      for (int ks = 0; ks < SH::KT; ++ks) {
-        Frag<T> xk[DT];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) xk[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XK), StX::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
-#pragma unroll
-        for (int pr = 0; pr < SH::PR; ++pr) {
-          const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, pr * 16);
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) mma(dw[pr][dt], dpt, xk[dt]);
+        for (int dt = 0; dt < DT; ++dt) {
+          dw[dt] = zero4();
+          mma(dw[dt], dpt, xk[dt]);
         }
+        dw_accumulate_row<SH, D>(DWL[w], pr, dw);
       }
-      dw_accumulate<SH, D>(DWL[w], dw);
     }
   }
   const size_t nmat = NS ? 2 : 1;
@@ -1161,7 +1173,8 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
     k_bwd_prepass<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
   timing_mark(KC_BWD_PREPASS, st, false);
   const hipError_t e =
-      launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st);
+      launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st,
+                        a.segments);
   if (e != hipSuccess) return e;
   timing_mark(KC_BWD_DQ, st, true);
   // only the frequency-group shape (d = 128) adds into an earlier group's outputs

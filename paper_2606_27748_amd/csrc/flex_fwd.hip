@@ -36,7 +36,7 @@ void k_fwd_state(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) float SCK[CHUNK];   // staged: per-token scale s e(k)
   __shared__ __attribute__((aligned(16))) IO XV[StV::LDS_ELEMS];   // [token][value col]
 
-  const WgCoord wc = wg_coord(a.segments * a.sub, a.H, a.BH);   // seg: sub-segment
+  const WgCoord wc = wg_coord(a.pre_segs * a.sub, a.H, a.BH);   // seg: sub-segment
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE;
   const int cps = a.chunks_per_seg / a.sub;
@@ -110,7 +110,7 @@ void k_fwd_state(FwdArgs a) {
 // state: [BH][P][E] fp32.  Fixed summation order.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1, int P, int sub, int E,
-                                                    int causal, int reverse0) {
+                                                    int causal, int reverse0, int nread0) {
   // one thread per 4 consecutive elements (E is a multiple of 256)
   const int e4 = blockIdx.x * 256 + threadIdx.x;
   if (4 * e4 >= E) return;
@@ -120,6 +120,7 @@ __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1
   const int reverse = blockIdx.z == 0 ? reverse0 : 1 - reverse0;
   float4* s = reinterpret_cast<float4*>((blockIdx.z == 0 ? state0 : state1) + (size_t)blockIdx.y * n * E) + e4;
   const size_t E4 = E / 4;
+  const int nread = blockIdx.z == 0 ? nread0 : n;   // slots holding local states (scan order)
   constexpr int BATCH = 16;  // independent loads in flight per thread
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int k0 = 0; k0 < n; k0 += BATCH) {
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1
     for (int j = 0; j < BATCH; ++j) {
       const int k = k0 + j;
       const int p = reverse ? n - 1 - k : k;
-      v[j] = k < n ? s[(size_t)p * E4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      v[j] = k < nread ? s[(size_t)p * E4] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (causal) {
 #pragma unroll
@@ -569,14 +570,15 @@ template <class T, int D, int FW, int NW, bool NS>
 static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   const dim3 grid(a.sweep_groups * a.BH);
-  const dim3 pgrid(a.segments * a.sub * a.BH);
+  const dim3 pgrid(a.pre_segs * a.sub * a.BH);
   // prepared fragments serve the state pre-pass at d > 64, which reloads them
   // per chunk; the other forward kernels build theirs from W once
   if (D > 64) k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
   timing_mark(KC_FWD_STATE, st, true);
-  k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
+  if (pgrid.x > 0) k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_STATE, st, false);
-  const hipError_t e = launch_state_scan(a.state, nullptr, a.BH, a.segments, a.sub, SH::STATE, causal, st);
+  const hipError_t e =
+      launch_state_scan(a.state, nullptr, a.BH, a.segments, a.sub, SH::STATE, causal, st, a.pre_segs * a.sub);
   if (e != hipSuccess) return e;
   timing_mark(KC_FWD_SWEEP, st, true);
   // only the frequency-group shape (d = 128) adds to an earlier group's sums
@@ -634,14 +636,14 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool fmap, hipStr
 }
 
 hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
-                             hipStream_t st) {
+                             hipStream_t st, int nread) {
   if (E % 4 != 0) return hipErrorInvalidValue;   // the scan moves 4 floats per thread
   dim3 sgrid((E / 4 + 255) / 256, BH, (state && state_rev) ? 2 : 1);
   timing_mark(KC_SCAN, st, true);
   if (state)
-    k_state_scan<<<sgrid, 256, 0, st>>>(state, state_rev, P, sub, E, causal ? 1 : 0, 0);
+    k_state_scan<<<sgrid, 256, 0, st>>>(state, state_rev, P, sub, E, causal ? 1 : 0, 0, nread);
   else
-    k_state_scan<<<sgrid, 256, 0, st>>>(state_rev, nullptr, P, sub, E, causal ? 1 : 0, 1);
+    k_state_scan<<<sgrid, 256, 0, st>>>(state_rev, nullptr, P, sub, E, causal ? 1 : 0, 1, P * sub);
   timing_mark(KC_SCAN, st, false);
   return hipGetLastError();
 }

@@ -31,6 +31,8 @@ struct FwdArgs {
   int BH, H, N;
   int nchunks, segments, chunks_per_seg;
   int sub;            // state pre-pass workgroups per segment (chunks_per_seg % sub == 0)
+  int pre_segs;       // segments whose local state the pre-pass forms: all (non-causal),
+                      // all but the last (causal: only exclusive prefixes are read)
   int sweep_groups;   // sweep workgroups per (b,h): the segments (causal) or chunk groups (non-causal)
   int sweep_cps;      // chunks per sweep workgroup
   int sweep_chunk;    // tokens per chunk of the causal sweep: 16, 32 or 64 (the
@@ -159,8 +161,10 @@ int fwd_state_waves(const KernelShape& ks);
 // state_rev (or NULL): [BH][P][E] (sub must then be 1), scanned in the same
 // launch in reverse: the exclusive suffix (causal) into slot p, or the total
 // into slot 0.
+// nread: slots of `state` that hold local states (the rest are taken as zero
+// and never read); state_rev is read in full.
 hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int sub, int E, bool causal,
-                             hipStream_t st);
+                             hipStream_t st, int nread);
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);
 // O = acc_num / acc_den (io dtype), den = acc_den, after the last frequency group.
 hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st);
