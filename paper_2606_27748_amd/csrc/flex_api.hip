@@ -112,6 +112,13 @@ int nchunks_of(const flex_desc* d) { return (d->N + kChunk - 1) / kChunk; }
 
 // Chunks per workgroup of the non-causal sweep (its chunks are independent).
 constexpr int kSweepChunks = 8;
+// The bf16 stationary shapes with m = 64 read out with the tokens split
+// across waves (k_fwd_readout): a workgroup holds the whole total state, so it
+// takes up to 64 chunks, about one round of two workgroups per CU.
+constexpr int kReadoutChunks = 64;
+bool readout_split(const flex_desc* d) {
+  return !d->causal && d->io_dtype == FLEX_BF16 && d->variant == FLEX_STATIONARY && d->m == 64 && d->d <= 64;
+}
 
 // Segments whose local state the forward pre-pass forms: a causal forward
 // reads only exclusive prefixes, so the last segment's own state is never used.
@@ -360,11 +367,14 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
     a.sweep_groups = a.segments;
     a.sweep_cps = a.chunks_per_seg * (kChunk / a.sweep_chunk);
   } else {
-    // chunks per non-causal sweep workgroup: up to kSweepChunks, fewer when
-    // that leaves the CUs short of workgroups (small B*H*N)
-    const long long per_cu = ((long long)a.nchunks * a.BH + kCUs - 1) / kCUs;
+    // chunks per non-causal sweep workgroup: up to kSweepChunks (or
+    // kReadoutChunks), fewer when that leaves the CUs short of workgroups
+    // (one, or for the token-split readout two, resident per CU)
+    const int per_wg = readout_split(desc) ? 2 : 1;
+    const int cap = readout_split(desc) ? kReadoutChunks : kSweepChunks;
+    const long long per_cu = ((long long)a.nchunks * a.BH + per_wg * kCUs - 1) / (per_wg * kCUs);
     a.sweep_chunk = kChunk;
-    a.sweep_cps = (int)(per_cu < 1 ? 1 : (per_cu > kSweepChunks ? kSweepChunks : per_cu));
+    a.sweep_cps = (int)(per_cu < 1 ? 1 : (per_cu > cap ? cap : per_cu));
     if (a.sweep_cps > a.nchunks) a.sweep_cps = a.nchunks;
     a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
   }

@@ -423,12 +423,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   }
 }
 
-// ---------------------------------------------------------------------------
-// Standalone feature map: Phi [B,H,N,2m], [cos | sin] blocks.  A workgroup
-// walks a.chunks_per_seg consecutive chunks of one (b,h) slice with its
-// frequency fragments built once; each lane writes its four consecutive
-// features of a block as one vector store.
-// ---------------------------------------------------------------------------
+// Four consecutive values of one row as one vector store in the io dtype.
 template <class IO>
 __device__ __forceinline__ void store4(IO* p, const float (&v)[4]);
 template <>
@@ -442,6 +437,104 @@ __device__ __forceinline__ void store4<float>(float* p, const float (&v)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
+// ---------------------------------------------------------------------------
+// Non-causal readout with the tokens split across waves (bf16, m_eff <= 64).
+// Every chunk reads the same total state, so each of the four waves takes one
+// 16-token tile of a 64-token chunk over all 2m features: the total state is
+// held by every wave as bf16 operand fragments (rows = value columns, k = the
+// 32 features of one frequency tile, [cos | sin] as the feature fragments),
+// and each wave projects its tokens onto all m frequencies.  No partial sums
+// cross waves, so the only barrier per chunk is the staging one.
+// ---------------------------------------------------------------------------
+template <class T, int D, int M, bool NS>
+__global__ __launch_bounds__(4 * WAVE) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_fwd_readout(FwdArgs a) {
+  constexpr int NWR = 4;                        // waves: one 16-token tile each
+  constexpr int FT = M / 16;                    // frequency tiles (all of them)
+  constexpr int DVT = D / 16, DVT1 = DVT + 1;
+  typedef FreqSlice<T, D, M, NS> FS;
+  typedef Shape<T, D, 16, M / 16, NS> SS;       // the state pre-pass's split: 16 frequencies per wave
+  typedef typename Io<T>::type IO;
+  typedef RowStage<IO, D, NWR * WAVE> StX;
+  static_assert(CHUNK == 16 * NWR, "one token tile per wave");
+  __shared__ __attribute__((aligned(16))) IO XQ2[2][StX::LDS_ELEMS];
+  __shared__ typename StX::Ssq SSQ2[2][CHUNK];
+
+  const WgCoord wc = wg_coord(a.sweep_groups, a.H, a.BH);
+  const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
+  const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int c0 = seg * a.sweep_cps;
+  const int c1 = min(c0 + a.sweep_cps, a.nchunks);
+  const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
+  IO* O = static_cast<IO*>(a.O) + (size_t)bh * a.N * D;
+  float* den = a.den ? a.den + (size_t)bh * a.N : nullptr;
+
+  StX sq;
+  if (c0 < c1) sq.fetch(Q, c0 * CHUNK, a.N);
+  const auto inv_c = inv_c_of<T>(a.tau[h]);
+  // total state (slot 0 of this slice after the scan): pre-pass wave ft holds
+  // frequency tile ft, its tile fc = 0 the cos features and fc = 1 the sin ones
+  Frag<T> sf[DVT1][FT];
+  {
+    const float* in = a.state + (size_t)bh * a.segments * a.sub * SS::STATE;
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+      for (int dt = 0; dt < DVT1; ++dt) {
+        const float* blk = in + (size_t)ft * SS::WAVE_STATE;
+        const f32x4 cs = *reinterpret_cast<const f32x4*>(blk + ((0 * DVT1 + dt) * WAVE + l) * 4);
+        const f32x4 sn = *reinterpret_cast<const f32x4*>(blk + ((1 * DVT1 + dt) * WAVE + l) * 4);
+        sf[dt][ft] = pair_tiles<T>(cs, sn);
+      }
+  }
+  FS fs;
+  fs.load(a.W1 + (size_t)h * a.w_stride, NS ? a.W2 + (size_t)h * a.w_stride : nullptr, 0);
+
+  for (int c = c0; c < c1; ++c) {
+    // double-buffered staging: the chunk that last read this buffer (two back)
+    // is separated from this store by the previous chunk's barrier
+    const int par = (c - c0) & 1;
+    IO* XQ = XQ2[par];
+    typename StX::Ssq* SSQ = SSQ2[par];
+    const int tok0 = c * CHUNK;
+    sq.store(XQ, SSQ);
+    sq.fetch(Q, c + 1 < c1 ? tok0 + CHUNK : tok0, a.N);   // the last chunk refetches itself (unused)
+    __syncthreads();
+    ProjT<T> p[FS::PR];
+    typename StX::Ssq ssq;
+    project_tile_lds<T, D, M, NS, StX::LD>(fs, XQ, SSQ, w, p, ssq);
+    const int tok = tok0 + w * 16 + r;
+    const float sc = row_scale(ssq, inv_c, a.s_const, tok < a.N);
+    f32x4 acc[DVT1];
+#pragma unroll
+    for (int dt = 0; dt < DVT1; ++dt) acc[dt] = zero4();
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) {
+      const Frag<T> pq = features<T, FT, NS>(p, ft, sc);
+#pragma unroll
+      for (int dt = 0; dt < DVT1; ++dt) mma(acc[dt], sf[dt][ft], pq);
+    }
+    // acc[dt]: rows = value columns dt*16 + 4g + i, column = token r; the
+    // normaliser tile holds den in its row 0 (lane r of lane group 0)
+    const float dn = __shfl(acc[DVT][0], r);
+    const float inv = __builtin_amdgcn_rcpf(dn);   // den = 0 gives inf/NaN as num/0 does
+    if (tok < a.N) {
+#pragma unroll
+      for (int dt = 0; dt < DVT; ++dt) {
+        const float v[4] = {acc[dt][0] * inv, acc[dt][1] * inv, acc[dt][2] * inv, acc[dt][3] * inv};
+        store4<IO>(O + (size_t)tok * D + dt * 16 + 4 * g, v);
+      }
+      if (den && g == 0) den[tok] = dn;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Standalone feature map: Phi [B,H,N,2m], [cos | sin] blocks.  A workgroup
+// walks a.chunks_per_seg consecutive chunks of one (b,h) slice with its
+// frequency fragments built once; each lane writes its four consecutive
+// features of a block as one vector store.
+// ---------------------------------------------------------------------------
 // The chunk's X rows are staged through LDS (prefetched a chunk ahead), every
 // wave projects them for its frequency slice, and the features are gathered
 // as [token][feature] rows in LDS, then written out as whole 16-byte vectors.
@@ -551,9 +644,22 @@ static void launch_causal_sweep(const FwdArgs& a, dim3 grid, hipStream_t st) {
   k_fwd_sweep<T, D, FW, NW, NS, true, QG, ADD, CH><<<grid, SH::NT, 0, st>>>(a);
 }
 
+// The token-split readout serves bf16 shapes whose projection onto all m
+// frequencies fits one wave's registers (m_eff <= 64, state split 4 x 16).
+template <class T, int D, int FW, int NW, bool NS>
+struct ReadoutSplit {
+  static constexpr bool value = IsBf16<T>::value && !NS && FW * NW == 64 && FW == 16 && D <= 64;
+};
+
 template <class T, int D, int FW, int NW, bool NS, bool ADD>
 static void launch_sweep(const FwdArgs& a, bool causal, dim3 grid, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
+  if constexpr (!ADD && ReadoutSplit<T, D, FW, NW, NS>::value) {
+    if (!causal) {
+      k_fwd_readout<T, D, FW * NW, NS><<<grid, 4 * WAVE, 0, st>>>(a);
+      return;
+    }
+  }
   if (!causal) {
     // one token tile per round: the non-causal sweep then fits several workgroups per CU
     k_fwd_sweep<T, D, FW, NW, NS, false, 1, ADD, CHUNK><<<grid, SH::NT, 0, st>>>(a);
