@@ -147,29 +147,20 @@ __device__ __forceinline__ float feature_grad(const Frag<T>& phi, const Frag<T>&
 }
 
 // The per-wave frequency-gradient partial dW'[rows][d] lives in LDS in
-// register-dump order (tile, lane, 4 floats): each chunk's MFMA tiles are added
-// with one 16-byte read and write per lane and tile.
-template <class SH, int D>
-__device__ __forceinline__ void dw_accumulate(float* dwl, const f32x4 (&acc)[SH::PR][D / 16]) {
+// register-dump order (tile, lane, 4 floats).  Each chunk's product for
+// projection-row tile pr is formed with the LDS tiles as the MFMA's
+// accumulator input (one 16-byte read and write per lane and tile), so the
+// sum takes no vector ALU work.
+template <int D, class T>
+__device__ __forceinline__ void dw_mma_row(float* dwl, int pr, const Frag<T>& dpt, const Frag<T> (&x)[D / 16]) {
   const int l = threadIdx.x % WAVE;
+  f32x4 c[D / 16];
 #pragma unroll
-  for (int pr = 0; pr < SH::PR; ++pr)
+  for (int dt = 0; dt < D / 16; ++dt) c[dt] = *reinterpret_cast<const f32x4*>(dwl + ((pr * (D / 16) + dt) * WAVE + l) * 4);
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
-      f32x4* p = reinterpret_cast<f32x4*>(dwl + ((pr * (D / 16) + dt) * WAVE + l) * 4);
-      *p += acc[pr][dt];
-    }
-}
-
-// One projection-row tile pr of the partial: acc[dt] added to its LDS tiles.
-template <class SH, int D>
-__device__ __forceinline__ void dw_accumulate_row(float* dwl, int pr, const f32x4 (&acc)[D / 16]) {
-  const int l = threadIdx.x % WAVE;
+  for (int dt = 0; dt < D / 16; ++dt) mma(c[dt], dpt, x[dt]);
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    f32x4* p = reinterpret_cast<f32x4*>(dwl + ((pr * (D / 16) + dt) * WAVE + l) * 4);
-    *p += acc[dt];
-  }
+  for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<f32x4*>(dwl + ((pr * (D / 16) + dt) * WAVE + l) * 4) = c[dt];
 }
 
 // Write a wave's frequency-gradient partial tiles DW[pr][dt] (rows = projection
@@ -619,8 +610,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     }
     // frequency gradient partial: dW'[rows][d] += dP^T Q
     {
-      // one 32-token k-step per chunk: each projection-row tile's product is
-      // complete after its MFMAs and goes to LDS before the next one is formed
+      // one 32-token k-step per chunk, added to the LDS partial one
+      // projection-row tile at a time
       static_assert(SH::KT == 1, "one token k-step per chunk");
       Frag<T> xq[DT];
 #pragma unroll
@@ -628,13 +619,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 #pragma unroll
       for (int pr = 0; pr < SH::PR; ++pr) {
         const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 4 * g, 16 + 4 * g, pr * 16);
-        f32x4 dw[DT];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          dw[dt] = zero4();
-          mma(dw[dt], dpt, xq[dt]);
-        }
-        dw_accumulate_row<SH, D>(DWL[w], pr, dw);
+        dw_mma_row<D, T>(DWL[w], pr, dpt, xq);
       }
     }
   }
@@ -858,13 +843,53 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         }
       }
     }
-    // bf16 copy of R' as [feature][value col] for dV (read back transposed)
+    // dphi(K)^T[feature][key] = phi(Q)^T M + R'^T-rows x [V | 1].  R' is
+    // converted to operand fragments once per chunk and feature tile; the same
+    // fragments, stored as [feature][value col], are the bf16 copy of R' that
+    // the dV product reads back transposed.
+    f32x4 dph[SH::FC][SH::TT];
+    {
+      Frag<T> vf[SH::TT][KG];
 #pragma unroll
-    for (int dt = 0; dt < SH::DVT; ++dt)
+      for (int tk = 0; tk < SH::TT; ++tk)
 #pragma unroll
-      for (int fc = 0; fc < SH::FC; ++fc)
-        store_tile_nm<T>(RLw, RLP, fc * 16, dt * 16, RT[dt][fc]);
-
+        for (int kd = 0; kd < KG; ++kd) {
+          if (32 * kd < SH::DV) {
+            vf[tk][kd] = lds_tok_frag<T>(reinterpret_cast<const T*>(XV) + (tk * 16 + r) * StV::LD, kd);
+          } else {
+            Frag<T> f;
+            f.zero();
+            if (g == 0) { f.set(0, 1.0f); f.set(1, 1.0f); }
+            vf[tk][kd] = f;
+          }
+        }
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) {
+        Frag<T> rp[KG];
+#pragma unroll
+        for (int kd = 0; kd < KG; ++kd) {
+          rp[kd] = pair_tiles<T>(RT[2 * kd][fc], 2 * kd + 1 < SH::DVT1 ? RT[2 * kd + 1][fc] : zero4());
+          if (2 * kd + 1 < SH::DVT) {
+            store_frag_nm<T>(RLw, RLP, fc * 16, (2 * kd) * 16, (2 * kd + 1) * 16, rp[kd]);
+          } else if (2 * kd < SH::DVT) {
+            store_tile_nm<T>(RLw, RLP, fc * 16, (2 * kd) * 16, RT[2 * kd][fc]);
+          }
+        }
+#pragma unroll
+        for (int tk = 0; tk < SH::TT; ++tk) {
+          f32x4 acc = zero4();
+          if (CAUSAL) {
+#pragma unroll
+            for (int ks = 0; ks < SH::KT; ++ks)
+              if (32 * ks + 31 >= 16 * tk)
+                mma(acc, lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16), mp[ks][tk]);
+          }
+#pragma unroll
+          for (int kd = 0; kd < KG; ++kd) mma(acc, rp[kd], vf[tk][kd]);
+          dph[fc][tk] = acc;
+        }
+      }
+    }
     // dV^T partial[value col][key] = dO^T A/den (intra) + R'[:dv]^T-rows x phi(K)
     f32x4 dvp[SH::DVT][SH::TT];
 #pragma unroll
@@ -907,39 +932,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
           s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
         }
         if (tok < a.N) *reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4) = s;
-      }
-    }
-    // dphi(K)^T[feature][key] = phi(Q)^T M + R'^T-rows x [V | 1]
-    f32x4 dph[SH::FC][SH::TT];
-#pragma unroll
-    for (int tk = 0; tk < SH::TT; ++tk) {
-      Frag<T> vf[KG];
-#pragma unroll
-      for (int kd = 0; kd < KG; ++kd) {
-        if (32 * kd < SH::DV) {
-          vf[kd] = lds_tok_frag<T>(reinterpret_cast<const T*>(XV) + (tk * 16 + r) * StV::LD, kd);
-        } else {
-          Frag<T> f;
-          f.zero();
-          if (g == 0) { f.set(0, 1.0f); f.set(1, 1.0f); }
-          vf[kd] = f;
-        }
-      }
-#pragma unroll
-      for (int fc = 0; fc < SH::FC; ++fc) {
-        f32x4 acc = zero4();
-        if (CAUSAL) {
-#pragma unroll
-          for (int ks = 0; ks < SH::KT; ++ks)
-            if (32 * ks + 31 >= 16 * tk)
-              mma(acc, lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16), mp[ks][tk]);
-        }
-#pragma unroll
-        for (int kd = 0; kd < KG; ++kd) {
-          const Frag<T> rp = pair_tiles<T>(RT[2 * kd][fc], 2 * kd + 1 < SH::DVT1 ? RT[2 * kd + 1][fc] : zero4());
-          mma(acc, rp, vf[kd]);
-        }
-        dph[fc][tk] = acc;
       }
     }
     // R'^T += [dO | -delta]^T-rows x phi(Q)/den  (after every use of R'_{>c})
@@ -1041,8 +1033,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       }
     }
     {
-      // one 32-token k-step per chunk: each projection-row tile's product is
-      // complete after its MFMAs and goes to LDS before the next one is formed
+      // one 32-token k-step per chunk, added to the LDS partial one
+      // projection-row tile at a time
       static_assert(SH::KT == 1, "one token k-step per chunk");
       Frag<T> xk[DT];
 #pragma unroll
@@ -1050,13 +1042,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
       for (int pr = 0; pr < SH::PR; ++pr) {
         const Frag<T> dpt = lds_tr_frag<T>(PT[w], LDP, 4 * g, 16 + 4 * g, pr * 16);
-        f32x4 dw[DT];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          dw[dt] = zero4();
-          mma(dw[dt], dpt, xk[dt]);
-        }
-        dw_accumulate_row<SH, D>(DWL[w], pr, dw);
+        dw_mma_row<D, T>(DWL[w], pr, dpt, xk);
       }
     }
   }
