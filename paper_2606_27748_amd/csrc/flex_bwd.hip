@@ -908,16 +908,20 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
               phk[ft][tk]);
         dvp[dt][tk] = acc;
       }
-    // dV: reduce the per-wave partials
-#pragma unroll
-    for (int q0 = 0; q0 < SH::TT; q0 += QG) {
-      if (q0 > 0) __syncthreads();   // the previous round's reads of every slot are done
+    // dV: reduce the per-wave partials.  With one reduction round per chunk the
+    // partials are written now and reduced after the dP barrier below, which
+    // orders these writes before every wave's reads (the slots are written
+    // again only after the next chunk's staging barrier); with several rounds
+    // each round has barriers of its own.
+    constexpr bool DEFER_DV = QG == SH::TT;
+    auto dv_write = [&](int q0) {
 #pragma unroll
       for (int qq = 0; qq < QG; ++qq)
 #pragma unroll
         for (int dt = 0; dt < SH::DVT; ++dt)
           *reinterpret_cast<f32x4*>(&RED(w)[qq * 16 + r][dt * 16 + 4 * g]) = dvp[dt][q0 + qq];
-      __syncthreads();
+    };
+    auto dv_reduce = [&](int q0) {
 #pragma unroll
       for (int k = 0; k < NIT; ++k) {
         const int it = threadIdx.x + k * SH::NT;
@@ -932,6 +936,17 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
           s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
         }
         if (tok < a.N) *reinterpret_cast<float4*>(dV + (size_t)tok * SH::DV + 4 * c4) = s;
+      }
+    };
+    if (DEFER_DV) {
+      dv_write(0);
+    } else {
+#pragma unroll
+      for (int q0 = 0; q0 < SH::TT; q0 += QG) {
+        if (q0 > 0) __syncthreads();   // the previous round's reads of every slot are done
+        dv_write(q0);
+        __syncthreads();
+        dv_reduce(q0);
       }
     }
     // R'^T += [dO | -delta]^T-rows x phi(Q)/den  (after every use of R'_{>c})
@@ -982,6 +997,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
     for (int tt = 0; tt < SH::TT; ++tt) GP[tt * 16 + r][w][g] = gp[tt];
     __syncthreads();   // every wave's dP block and g shares complete
+    if (DEFER_DV) dv_reduce(0);
 #pragma unroll
     for (int kd = 0; kd < NDK; ++kd) {
       const int dt = w % DT + kd * NW;

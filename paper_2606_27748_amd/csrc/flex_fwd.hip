@@ -237,7 +237,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
 
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CH;
-    __syncthreads();
+    // no barrier before the staging stores: every read of the staging buffers
+    // (projections, value fragments) precedes the previous chunk's last
+    // readout barrier
     sq.store(XQ, SSQ);
     if (CAUSAL) sk.store(XK, SSK);
     if (CAUSAL) sv.store(XV);
