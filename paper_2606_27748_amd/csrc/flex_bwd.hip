@@ -659,17 +659,23 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int RED_W = QG * 16 * RP * 4;
   constexpr int RL_W = SH::FC * 16 * RLP * (int)sizeof(T);
   constexpr int SLOT = RED_W > RL_W ? RED_W : RL_W;
-  // staging is double-buffered by chunk parity where LDS allows (d <= 64)
+  // Staging is double-buffered by chunk parity where LDS allows (d <= 64).
+  // There the next chunk is staged before this chunk's dP barrier, which then
+  // also orders those stores before the next chunk's reads, so a chunk needs
+  // no staging barrier of its own.  K rows and norms are read after the dP
+  // barrier too (dK, dW', dtau), so they take three buffers.
   constexpr int NBUF = D <= 64 ? 2 : 1;
+  constexpr bool EARLY = NBUF == 2;
+  constexpr int NKB = EARLY ? 3 : 1;
   __shared__ __attribute__((aligned(16))) IO XQ2[NBUF][StX::LDS_ELEMS];
-  __shared__ __attribute__((aligned(16))) IO XK2[NBUF][StX::LDS_ELEMS];
+  __shared__ __attribute__((aligned(16))) IO XK2[NKB][StX::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XV2[NBUF][StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) IO XDO2[NBUF][StV::LDS_ELEMS];
   __shared__ __attribute__((aligned(16))) T PT[NW][SH::CH * LDP];   // phi(Q)/den, then dP: [token][row]
   __shared__ __attribute__((aligned(16))) char REDRL[NW * SLOT];
   __shared__ __attribute__((aligned(16))) float DWL[NW][SH::PR * DT * WAVE * 4];
   __shared__ float GS2[NBUF][SH::CH][2];
-  __shared__ typename StX::Ssq SSQ2[NBUF][SH::CH], SSK2[NBUF][SH::CH];
+  __shared__ typename StX::Ssq SSQ2[NBUF][SH::CH], SSK2[NKB][SH::CH];
   __shared__ float TRED[SH::NT];
   __shared__ __attribute__((aligned(16))) float GP[SH::CH][NW][4];   // per-lane-group shares of g
   typedef float RedRow[QG * 16][RP];
@@ -731,18 +737,37 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   // waves per SIMD, 256 registers) load them per chunk
   constexpr bool HOLD_WF = DT <= NW && NW <= 4;
   if (HOLD_WF) load_wf(w % DT);
+  // Store the prefetched rows into the buffers of sweep step i and prefetch
+  // chunk cn - 1 (chunk cn itself again when cn is the last one: the prefetch
+  // is issued on every step, from an in-range chunk).
+  auto stage = [&](int i, int cn) {
+    const int par = NBUF == 2 ? i & 1 : 0, kp = i % NKB;
+    sq.store(XQ2[par], SSQ2[par]); sk.store(XK2[kp], SSK2[kp]); sv.store(XV2[par]); sdo.store(XDO2[par]);
+    if (threadIdx.x < SH::CH) {
+      GS2[par][threadIdx.x][0] = gs_ok ? gs_next.x : 0.f;
+      GS2[par][threadIdx.x][1] = gs_ok ? gs_next.y : 0.f;
+    }
+    const int t1 = (cn - 1 >= c0 ? cn - 1 : cn) * SH::CH;
+    sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
+    gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
+  };
+  if (EARLY) {
+    if (c0 < c1) stage(0, c1 - 1);
+    __syncthreads();
+  }
   for (int c = c1 - 1; c >= c0; --c) {
-    // This chunk's staging buffers.  Double-buffered, they need no barrier
-    // before they are written: the chunk that last read them (two back) is
-    // separated from this point by the previous chunk's barriers.
-    const int par = NBUF == 2 ? (c1 - 1 - c) & 1 : 0;
+    // This chunk's staging buffers.  Double-buffered, no store into them
+    // needs a barrier of its own: the chunk that last read them (two back;
+    // three back for K) is separated from the store by a dP barrier.
+    const int step = c1 - 1 - c;
+    const int par = NBUF == 2 ? step & 1 : 0, kp = step % NKB;
     IO* XQ = XQ2[par];
-    IO* XK = XK2[par];
+    IO* XK = XK2[kp];
     IO* XV = XV2[par];
     IO* XDO = XDO2[par];
     float (*GS)[2] = GS2[par];
     typename StX::Ssq* SSQ = SSQ2[par];
-    typename StX::Ssq* SSK = SSK2[par];
+    typename StX::Ssq* SSK = SSK2[kp];
     const int tok0 = c * SH::CH;
     // this chunk's projection fragments: in flight across the staging barrier
     FreqSlice<T, D, FW, NS> fs;
@@ -770,15 +795,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
             old_v[q][k] = *reinterpret_cast<const float4*>(dV + (size_t)tok * SH::DV + 4 * (it % C4));
         }
     }
-    if (NBUF == 1) __syncthreads();   // single buffer: the previous chunk's reads are done
-    sq.store(XQ, SSQ); sk.store(XK, SSK); sv.store(XV); sdo.store(XDO);
-    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
-    {
-      const int t1 = c - 1 >= c0 ? tok0 - SH::CH : tok0;   // the last chunk refetches itself (unused)
-      sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-      gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
+    if (!EARLY) {
+      if (NBUF == 1) __syncthreads();   // single buffer: the previous chunk's reads are done
+      stage(step, c);
+      __syncthreads();
     }
-    __syncthreads();
 
     // phi(Q)/den as [token][feature] in the wave's LDS block: read back as it is
     // for the intra-chunk kernel matrix, transposed for the token sums (the
@@ -987,6 +1008,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     // the token tiles tt = w / DT (+ NW / DT, ...).  The dX fragments of its
     // first d tile are loaded before the barrier, so their latency overlaps it.
     if (!HOLD_WF) load_wf(w % DT);
+    // the next chunk's rows (the last step stages its own rows again, unused)
+    if (EARLY) stage(step + 1, c - 1 >= c0 ? c - 1 : c);
     // dP of this wave as [token][projection row] in its LDS block (its own reads
     // of phi(Q)/den there are done: one wave's LDS accesses complete in order),
     // and this lane's share of g per token
