@@ -689,12 +689,19 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
       launch_state_scan(a.state, nullptr, a.BH, a.segments, a.sub, SH::STATE, causal, st, a.pre_segs * a.sub);
   if (e != hipSuccess) return e;
   timing_mark(KC_FWD_SWEEP, st, true);
+  // At d = 64, m = 128 the sweep runs 4 waves of 32 frequencies (one wave per
+  // SIMD; the readout's cross-wave reduction then covers a whole 64-token
+  // chunk in one round), the state pre-pass 8 waves of 16.  Both keep the
+  // states in the same layout: feature tile 2f + (0: cos, 1: sin) of
+  // frequency tile f, whatever wave holds it.
+  constexpr int FWS = (D == 64 && FW * NW == 128) ? 32 : FW;
+  constexpr int NWS = FW * NW / FWS;
   // only the frequency-group shape (d = 128) adds to an earlier group's sums
   constexpr bool GROUPED = D == 128;
   if (GROUPED && a.acc == 2)
-    launch_sweep<T, D, FW, NW, NS, GROUPED>(a, causal, grid, st);
+    launch_sweep<T, D, FWS, NWS, NS, GROUPED>(a, causal, grid, st);
   else
-    launch_sweep<T, D, FW, NW, NS, false>(a, causal, grid, st);
+    launch_sweep<T, D, FWS, NWS, NS, false>(a, causal, grid, st);
   timing_mark(KC_FWD_SWEEP, st, false);
   return hipGetLastError();
 }
