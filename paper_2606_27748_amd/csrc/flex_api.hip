@@ -151,6 +151,15 @@ int fwd_sub_of(const flex_desc* d, int P) {
   return best;
 }
 
+// Whether the causal sweeps (the forward's and the backward's dQ sweep) sum
+// their carry-in from the segments' local states themselves, with no scan
+// launch: when a workgroup reads at most kFoldMax local states.  The sum runs
+// in the scan's order, so both ways give the same bits.
+constexpr int kFoldMax = 4;
+int fwd_fold_of(const flex_desc* d, int P) {
+  return d->causal && (long long)pre_segs_of(d, P) * fwd_sub_of(d, P) <= kFoldMax ? 1 : 0;
+}
+
 // Segments per (b,h): enough workgroups to cover the 256 CUs in whole rounds
 // while keeping the per-segment state traffic small.  Costs are in units of
 // one sweep chunk: the sweep's rounds of chunks (a pre-pass adds about a third
@@ -359,6 +368,7 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
   a.segments = P0;
   a.chunks_per_seg = (a.nchunks + a.segments - 1) / a.segments;
   a.sub = fwd_sub_of(desc, P0);
+  a.fold = fwd_fold_of(desc, P0);
   a.pre_segs = pre_segs_of(desc, P0);
   if (desc->causal) {
     // the sweep's chunks of chunk_of(desc) tokens: a segment spans the same
@@ -646,7 +656,10 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
     const int fcps = (nchunks_of(desc) + a.segments - 1) / a.segments;   // forward chunks per segment
     a.chunks_per_seg = fcps * (kChunk / BWD_CHUNK);
   }
-  if (fwd_ws) a.fsub = fwd_sub_of(desc, a.segments);
+  if (fwd_ws) {
+    a.fsub = fwd_sub_of(desc, a.segments);
+    a.ffold = fwd_fold_of(desc, a.segments);
+  }
   a.s_const = s_const_of(desc);
   const size_t bh = (size_t)a.BH, P = (size_t)a.segments;
   char* base = static_cast<char*>(ws);

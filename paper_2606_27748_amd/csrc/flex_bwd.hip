@@ -397,7 +397,22 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   const auto inv_c = inv_c_of<T>(a.tau[h]);
 
   f32x4 ST[SH::DVT1][SH::FC];
-  if (a.fstate) {
+  if (a.fstate && CAUSAL && a.ffold) {
+    // the forward ran no scan: the exclusive prefix of its local states, summed
+    // in the scan's order (the same sum the forward sweep formed)
+    const float* blk = a.fstate + (size_t)bh * a.segments * a.fsub * SH::STATE;
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) ST[dt][fc] = zero4();
+    for (int k = 0; k < seg * a.fsub; ++k) {
+      const float* in = blk + (size_t)k * SH::STATE;
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc) ST[dt][fc] += fwd_state_tile_t<SH>(in, w, dt, fc);
+    }
+  } else if (a.fstate) {
     const float* in = a.fstate + ((size_t)bh * a.segments * a.fsub + (CAUSAL ? seg * a.fsub : 0)) * SH::STATE;
 #pragma unroll
     for (int dt = 0; dt < SH::DVT1; ++dt)

@@ -215,13 +215,29 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   // carry-in state (exclusive prefix for causal, total for non-causal)
   f32x4 S[SH::FC][SH::DVT1];
   {
-    const float* in = a.state + ((size_t)bh * a.segments * a.sub + (CAUSAL ? seg * a.sub : 0)) * SH::STATE +
-                      (size_t)w * SH::WAVE_STATE;
+    const float* blk = a.state + (size_t)bh * a.segments * a.sub * SH::STATE + (size_t)w * SH::WAVE_STATE;
+    if (CAUSAL && a.fold) {
+      // the exclusive prefix of the local states, summed in the scan's order
 #pragma unroll
-    for (int fc = 0; fc < SH::FC; ++fc)
+      for (int fc = 0; fc < SH::FC; ++fc)
 #pragma unroll
-      for (int dt = 0; dt < SH::DVT1; ++dt)
-        S[fc][dt] = *reinterpret_cast<const f32x4*>(in + ((fc * SH::DVT1 + dt) * WAVE + l) * 4);
+        for (int dt = 0; dt < SH::DVT1; ++dt) S[fc][dt] = zero4();
+      for (int k = 0; k < seg * a.sub; ++k) {
+        const float* in = blk + (size_t)k * SH::STATE;
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+          for (int dt = 0; dt < SH::DVT1; ++dt)
+            S[fc][dt] += *reinterpret_cast<const f32x4*>(in + ((fc * SH::DVT1 + dt) * WAVE + l) * 4);
+      }
+    } else {
+      const float* in = blk + (size_t)(CAUSAL ? seg * a.sub : 0) * SH::STATE;
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc)
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT1; ++dt)
+          S[fc][dt] = *reinterpret_cast<const f32x4*>(in + ((fc * SH::DVT1 + dt) * WAVE + l) * 4);
+    }
   }
   const Frag<T> ones = ones_col0<T>();
   // projection fragments, held for the whole sweep: built from W by each wave
@@ -685,9 +701,11 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   timing_mark(KC_FWD_STATE, st, true);
   if (pgrid.x > 0) k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
   timing_mark(KC_FWD_STATE, st, false);
-  const hipError_t e =
-      launch_state_scan(a.state, nullptr, a.BH, a.segments, a.sub, SH::STATE, causal, st, a.pre_segs * a.sub);
-  if (e != hipSuccess) return e;
+  if (!a.fold) {
+    const hipError_t e =
+        launch_state_scan(a.state, nullptr, a.BH, a.segments, a.sub, SH::STATE, causal, st, a.pre_segs * a.sub);
+    if (e != hipSuccess) return e;
+  }
   timing_mark(KC_FWD_SWEEP, st, true);
   // At d = 64, m = 128 the sweep runs 4 waves of 32 frequencies (one wave per
   // SIMD; the readout's cross-wave reduction then covers a whole 64-token

@@ -33,6 +33,10 @@ struct FwdArgs {
   int sub;            // state pre-pass workgroups per segment (chunks_per_seg % sub == 0)
   int pre_segs;       // segments whose local state the pre-pass forms: all (non-causal),
                       // all but the last (causal: only exclusive prefixes are read)
+  int fold;           // causal: 1 = no scan launch, each sweep workgroup sums its carry-in
+                      // from the local states of the segments before its own (in the
+                      // scan's order); 0 = the scan writes the carry-ins over each
+                      // segment's first slot
   int sweep_groups;   // sweep workgroups per (b,h): the segments (causal) or chunk groups (non-causal)
   int sweep_cps;      // chunks per sweep workgroup
   int sweep_chunk;    // tokens per chunk of the causal sweep: 16, 32 or 64 (the
@@ -79,8 +83,11 @@ struct BwdArgs {
   float* dtaupart;    // [BH][segments] partial dtau
   void* wfrag;        // per-head frequency fragments (prepared by k_prep_freqs)
   void* wfrag_kv;     // fragments of the dK/dV sweep (== wfrag when its split is the same)
-  const float* fstate; // forward segment states after its scan ([BH][segments*fsub][state]) or NULL
+  const float* fstate; // forward segment states ([BH][segments*fsub][state]) or NULL
   int fsub;           // forward pre-pass workgroups per segment
+  int ffold;          // 1: fstate holds the local states (the forward ran no scan) and
+                      // the dQ sweep sums its carry-in from them; 0: the carry-in of
+                      // segment p is in slot p*fsub
   int BH, B, H, N;
   int nchunks, segments, chunks_per_seg;
   float s_const;
