@@ -230,10 +230,19 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   StX sq, sk;
   StV sv, sdo, so;
   float dn_next = 0.f;
+  // FUSED: every thread stages one vector of one row of Q, dO and O alike
+  // (same vectors per row, one vector per thread), so the row sums dO . O and
+  // ||q||^2 come out of the staging registers with lane sums, and the
+  // per-token scalars need no barrier of their own.  Each thread then loads
+  // den of its own row; otherwise thread t < CH loads that of row t.
+  constexpr bool FUSED = StX::VPR == StV::VPR && StX::NV == SH::NT && StV::NV == SH::NT;
+  auto den_row = [&](int t0) {
+    return den[min(t0 + (int)(FUSED ? threadIdx.x / StV::VPR : threadIdx.x % SH::CH), a.N - 1)];
+  };
   if (c0 < c1) {
     sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
     sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N); so.fetch(Ob, c0 * SH::CH, a.N);
-    dn_next = den[min(c0 * SH::CH + (int)(threadIdx.x % SH::CH), a.N - 1)];   // rows past N unused
+    dn_next = den_row(c0 * SH::CH);   // rows past N unused
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const auto inv_c = inv_c_of<T>(a.tau[h]);
@@ -269,24 +278,51 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     float* SCQ = SCQ2[par];
     const int tok0 = c * SH::CH;
     if (!KEEP_FS) fs.load_frags(wproj);
-    sq.store(XQ, SSQ); sdo.store(XDO); so.store(XO);
+    if constexpr (FUSED) {
+      // per-token 1/den and delta = dO . O of this thread's row (rows past N
+      // are zero vectors: delta 0)
+      const int t = threadIdx.x / StV::VPR;
+      const bool ok = tok0 + t < a.N;
+      const float inv = ok ? 1.0f / dn_next : 0.f;
+      float dsum = 0.f;
+      {
+        const uint4 x = sdo.vec(0), y = so.vec(0);
+        const IO* ex = reinterpret_cast<const IO*>(&x);
+        const IO* ey = reinterpret_cast<const IO*>(&y);
+#pragma unroll
+        for (int j = 0; j < StV::VEC; ++j) dsum += io_to_float(ex[j]) * io_to_float(ey[j]);
+      }
+      dsum = lane_sum<StV::VPR>(dsum);
+      sq.store(XQ, SCQ, [&](int, auto ssq) { return row_scale(ssq, inv_c, a.s_const, ok) * inv; });
+      sdo.store(XDO);
+      if (threadIdx.x % StV::VPR == 0) {
+        GS[t][0] = inv;
+        GS[t][1] = ok ? dsum : 0.f;
+        if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = dsum; }
+      }
+    } else {
+      sq.store(XQ, SSQ); sdo.store(XDO); so.store(XO);
+      if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
+    }
     if (WITH_S) {
-      sk.store(XK, SSK);
+      if constexpr (FUSED)
+        sk.store(XK, SCK, [&](int t, auto ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
+      else
+        sk.store(XK, SSK);
       sv.store(XV);
     } else {   // K and V only warm the caches for the sweeps that follow
       sk.touch();
       sv.touch();
     }
-    if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
     {
       const int t1 = c + 1 < c1 ? tok0 + SH::CH : tok0;   // the last chunk refetches itself (unused)
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N);
       sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N); so.fetch(Ob, t1, a.N);
-      dn_next = den[min(t1 + (int)(threadIdx.x % SH::CH), a.N - 1)];
+      dn_next = den_row(t1);
     }
     __syncthreads();
-    // per-token 1/den and delta = dO . O
-    {
+    // per-token 1/den and delta = dO . O (FUSED: done above)
+    if constexpr (!FUSED) {
       const int t = threadIdx.x / TPT, part = threadIdx.x % TPT;
       float s = 0.f;
       for (int cidx = part; cidx < SH::DV; cidx += TPT)
@@ -301,8 +337,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
         SCQ[t] = row_scale(SSQ[t], inv_c, a.s_const, ok) * inv;
         if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = s; }
       }
+      __syncthreads();
     }
-    __syncthreads();
     // both feature maps enter only the token sums: token-row features, no
     // transpose; the key side and the query side one after the other
 #pragma unroll
