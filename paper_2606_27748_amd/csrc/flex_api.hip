@@ -156,6 +156,7 @@ int fwd_sub_of(const flex_desc* d, int P) {
 // launch: when a workgroup reads at most kFoldMax local states.  The sum runs
 // in the scan's order, so both ways give the same bits.
 constexpr int kFoldMax = 4;
+constexpr int kRFoldMax = 8;   // R' suffixes: native-layout reads, cheaper to sum
 int fwd_fold_of(const flex_desc* d, int P) {
   return d->causal && (long long)pre_segs_of(d, P) * fwd_sub_of(d, P) <= kFoldMax ? 1 : 0;
 }
@@ -659,6 +660,9 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   if (fwd_ws) {
     a.fsub = fwd_sub_of(desc, a.segments);
     a.ffold = fwd_fold_of(desc, a.segments);
+    // with the forward's key-side states the scan would handle R' alone: the
+    // dK/dV sweep sums its suffix itself when it reads at most kRFoldMax states
+    a.rfold = desc->causal && a.segments - 1 <= kRFoldMax ? 1 : 0;
   }
   a.s_const = s_const_of(desc);
   const size_t bh = (size_t)a.BH, P = (size_t)a.segments;

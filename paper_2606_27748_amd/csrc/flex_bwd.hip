@@ -759,7 +759,22 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   const auto inv_c = inv_c_of<T>(a.tau[h]);
 
   f32x4 RT[SH::DVT1][SH::FC];
-  {
+  if (CAUSAL && a.rfold) {
+    // the suffix of the later segments' local states, summed in the scan's
+    // order (last segment first)
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) RT[dt][fc] = zero4();
+    for (int q = a.segments - 1; q > seg; --q) {
+      const float* in = a.rstate + ((size_t)bh * a.segments + q) * SH::STATE;
+#pragma unroll
+      for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc)
+          RT[dt][fc] += *reinterpret_cast<const f32x4*>(in + state_off<SH>(w, dt, fc, l));
+    }
+  } else {
     const float* in = a.rstate + ((size_t)bh * a.segments + (CAUSAL ? seg : 0)) * SH::STATE;
 #pragma unroll
     for (int dt = 0; dt < SH::DVT1; ++dt)
@@ -1248,10 +1263,12 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   else
     k_bwd_prepass<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
   timing_mark(KC_BWD_PREPASS, st, false);
-  const hipError_t e =
-      launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st,
-                        a.segments);
-  if (e != hipSuccess) return e;
+  if (!(causal && a.rfold)) {
+    const hipError_t e =
+        launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st,
+                          a.segments);
+    if (e != hipSuccess) return e;
+  }
   timing_mark(KC_BWD_DQ, st, true);
   // only the frequency-group shape (d = 128) adds into an earlier group's outputs
   constexpr bool GROUPED = D == 128;

@@ -88,6 +88,9 @@ struct BwdArgs {
   int ffold;          // 1: fstate holds the local states (the forward ran no scan) and
                       // the dQ sweep sums its carry-in from them; 0: the carry-in of
                       // segment p is in slot p*fsub
+  int rfold;          // causal with fstate: 1 = no scan launch, the dK/dV sweep sums its
+                      // R' carry-in from the local states of the later segments (in the
+                      // scan's order); 0 = the scan writes the suffixes over them
   int BH, B, H, N;
   int nchunks, segments, chunks_per_seg;
   float s_const;
