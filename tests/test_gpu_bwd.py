@@ -100,6 +100,19 @@ def test_backward_segments(F, segments, causal, reuse):
 
 
 @pytest.mark.parametrize("reuse", [False, True])
+def test_backward_many_segments(F, reuse):
+    """12 segments: the carry-ins of both states come from the scans (up to a
+    few segments the sweeps sum them from the local states themselves)."""
+    wl = W.Workload("manyseg", 1, 2, 900, 64, 128, "nonstationary", True, "bf16", True, 37)
+    x = W.generate(wl)
+    kap = masked_inputs(wl, x)
+    got = gpu_fwd_bwd(F, wl, x, segments=12, reuse=reuse)
+    ref, sc = oracle_bwd(wl, x)
+    check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
+
+
+@pytest.mark.parametrize("reuse", [False, True])
 def test_backward_many_partials(F, reuse):
     """B = 3 and 7 segments give 42 frequency-gradient partials per head: the
     reduce takes them in two batches, the second one partly past the list."""
