@@ -384,7 +384,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // ACC: add dQ to the values an earlier frequency group stored (loaded at the
 // start of each chunk, ahead of the next chunk's prefetch).
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC>
+// WR: this sweep also does the pre-pass's query-side work (used when the
+// forward's key-side states are passed in, so no pre-pass runs): the per-token
+// 1/den and delta = dO . O, from the staging registers, written for the dK/dV
+// sweep, and the segment-local R'^T = sum [dO | -delta]^T-rows x phi(Q)/den.
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC, bool WR>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
@@ -416,17 +420,31 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   const IO* K = static_cast<const IO*>(a.K) + (size_t)bh * a.N * D;
   const IO* V = static_cast<const IO*>(a.V) + (size_t)bh * a.N * SH::DV;
   const IO* dO = static_cast<const IO*>(a.dO) + (size_t)bh * a.N * SH::DV;
-  const float* gst = a.gstats + (size_t)bh * a.N * 2;
+  float* gst = a.gstats + (size_t)bh * a.N * 2;
   float* dQ = a.dQ + (size_t)bh * a.N * D;
+  // WR: thread v stages vector v % VPR of row v / VPR of Q, dO and O alike
+  static_assert(!WR || (StX::VPR == StV::VPR && StX::NV == StV::NV && StV::NV <= SH::NT),
+                "one row vector per thread in the same layout for Q, dO and O");
+  const IO* Ob = static_cast<const IO*>(a.O) + (size_t)bh * a.N * SH::DV;
+  const float* den = a.den + (size_t)bh * a.N;
+  auto den_row = [&](int t0) {   // rows past N (and threads past the rows) unused
+    return den[min(t0 + (int)(threadIdx.x / StV::VPR), a.N - 1)];
+  };
 
   StX sq, sk;
-  StV sv, sdo;
+  StV sv, sdo, so;
   float2 gs_next = make_float2(0.f, 0.f);
   bool gs_ok = false;
+  float dn_next = 0.f;
   if (c0 < c1) {
     sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
     sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N);
-    gs_next = load_gs(gst, c0 * SH::CH, a.N, SH::CH, gs_ok);
+    if (WR) {
+      so.fetch(Ob, c0 * SH::CH, a.N);
+      dn_next = den_row(c0 * SH::CH);
+    } else {
+      gs_next = load_gs(gst, c0 * SH::CH, a.N, SH::CH, gs_ok);
+    }
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const Frag<T>* wdx = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, w);
@@ -465,10 +483,16 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   for (int i = l; i < SH::PR * DT * WAVE; i += WAVE)
     *reinterpret_cast<f32x4*>(&DWL[w][i * 4]) = zero4();
   const Frag<T> ones = ones_col01<T>();
+  f32x4 RT[WR ? SH::DVT1 : 1][WR ? SH::FC : 1];
+#pragma unroll
+  for (int dt = 0; dt < (WR ? SH::DVT1 : 1); ++dt)
+#pragma unroll
+    for (int fc = 0; fc < (WR ? SH::FC : 1); ++fc) RT[dt][fc] = zero4();
 
-  // projection fragments: held for the whole sweep at d <= 64, else reloaded
-  // per chunk ahead of the staging barriers
-  constexpr bool KEEP_FS = D <= 64;
+  // projection fragments: held for the whole sweep at d <= 64 (without the
+  // query-side states, which take those registers), else reloaded per chunk
+  // ahead of the staging barriers
+  constexpr bool KEEP_FS = D <= 64 && !WR;
   FreqSlice<T, D, FW, NS> fs;
   if (KEEP_FS) fs.load_frags(wproj);
   for (int c = c0; c < c1; ++c) {
@@ -499,11 +523,38 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     sq.store(XQ, SSQ);
     sk.store(XK, SCK, [&](int t, auto ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV); sdo.store(XDO);
-    if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
+    if constexpr (WR) {
+      // 1/den and delta of this thread's row (rows past N: zero vectors, delta 0)
+      const int t = threadIdx.x / StV::VPR;
+      const bool mine = (int)threadIdx.x < StV::NV;
+      const bool ok = mine && tok0 + t < a.N;
+      float dsum = 0.f;
+      {
+        const uint4 x = sdo.vec(0), y = so.vec(0);
+        const IO* ex = reinterpret_cast<const IO*>(&x);
+        const IO* ey = reinterpret_cast<const IO*>(&y);
+#pragma unroll
+        for (int j = 0; j < StV::VEC; ++j) dsum += io_to_float(ex[j]) * io_to_float(ey[j]);
+      }
+      dsum = lane_sum<StV::VPR>(dsum);
+      if (mine && threadIdx.x % StV::VPR == 0) {
+        const float inv = ok ? 1.0f / dn_next : 0.f;
+        GS[t][0] = inv;
+        GS[t][1] = ok ? dsum : 0.f;
+        if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = dsum; }
+      }
+    } else {
+      if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
+    }
     {
       const int t1 = c + 1 < c1 ? tok0 + SH::CH : tok0;   // the last chunk refetches itself (unused)
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
-      gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
+      if (WR) {
+        so.fetch(Ob, t1, a.N);
+        dn_next = den_row(t1);
+      } else {
+        gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
+      }
     }
     __syncthreads();
 
@@ -512,16 +563,41 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     Frag<T> pk[SH::KT][SH::FC];
 #pragma unroll
     for (int ks = 0; ks < SH::KT; ++ks) feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk[ks]);
-    // phi(Q) and its P2-derivative fragments
+    // phi(Q)/den and its P2-derivative fragments (the 1/den of dphi(Q) is
+    // carried by these: their products with dphi(Q) in the chain rule are the
+    // same)
     Frag<T> phq[SH::FT][SH::TT], psq[SH::FT][SH::TT];
 #pragma unroll
     for (int tt = 0; tt < SH::TT; ++tt) {
       ProjT<T> p[SH::PR];
       typename StX::Ssq ssq;
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
-      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
+      const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
 #pragma unroll
       for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phq[ft][tt], psq[ft][tt]);
+    }
+    if constexpr (WR) {
+      // R'^T += [dO | -delta]^T-rows x phi(Q)/den, with phi(Q)/den as [token]
+      // [feature] in this wave's LDS block (read transposed; the block takes
+      // this wave's dP later, after these reads)
+#pragma unroll
+      for (int tt = 0; tt < SH::TT; ++tt)
+#pragma unroll
+        for (int ft = 0; ft < SH::FT; ++ft)
+          store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16, phq[ft][tt]);
+#pragma unroll
+      for (int ks = 0; ks < SH::KT; ++ks) {
+        Frag<T> gt[SH::DVT1];
+#pragma unroll
+        for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XDO), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
+        gt[SH::DVT] = delta_rows<T>(GS, ks);
+#pragma unroll
+        for (int fc = 0; fc < SH::FC; ++fc) {
+          const Frag<T> pq = lds_tr_frag<T>(PT[w], LDP, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, fc * 16);
+#pragma unroll
+          for (int dt = 0; dt < SH::DVT1; ++dt) mma(RT[dt][fc], gt[dt], pq);
+        }
+      }
     }
     // intra-chunk M^T[j][i] = dO_i . V_j - delta_i for j <= i (1/den_i applied later)
     Frag<T> mt[CAUSAL ? SH::KT : 1][SH::TT];
@@ -552,7 +628,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
         for (int ks = 0; ks < SH::KT; ++ks) mt[ks][tq] = pair_tiles<T>(m[2 * ks], m[2 * ks + 1]);
       }
     }
-    // dphi(Q)^T[feature][query] = (phi(K)^T M^T + S'^T-rows x [dO | -delta]) / den
+    // den * dphi(Q)^T[feature][query] = phi(K)^T M^T + S'^T-rows x [dO | -delta]
     f32x4 dph[SH::FC][SH::TT];
 #pragma unroll
     for (int tq = 0; tq < SH::TT; ++tq) {
@@ -570,7 +646,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
           gf[kd] = f;
         }
       }
-      const float inv = GS[tq * 16 + r][0];
 #pragma unroll
       for (int fc = 0; fc < SH::FC; ++fc) {
         f32x4 acc = zero4();
@@ -585,8 +660,6 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
           const Frag<T> sp = pair_tiles<T>(ST[2 * kd][fc], 2 * kd + 1 < SH::DVT1 ? ST[2 * kd + 1][fc] : z);
           mma(acc, sp, gf[kd]);
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] *= inv;
         dph[fc][tq] = acc;
       }
     }
@@ -677,6 +750,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   const size_t nmat = NS ? 2 : 1;
   float* out = a.dwpart + (((size_t)0 * a.BH + bh) * a.segments + seg) * nmat * SH::M * D;
   dump_dw<SH, D, FW, NS>(out, DWL[w], w * FW);
+  if constexpr (WR) {
+    float* ro = a.rstate + ((size_t)bh * a.segments + seg) * SH::STATE;
+#pragma unroll
+    for (int dt = 0; dt < SH::DVT1; ++dt)
+#pragma unroll
+      for (int fc = 0; fc < SH::FC; ++fc) *reinterpret_cast<f32x4*>(ro + state_off<SH>(w, dt, fc, l)) = RT[dt][fc];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1257,16 +1337,24 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
         a.W1, a.W2, a.wfrag, a.wfrag_kv, a.w_stride);
   else
     k_prep_freqs<T, D, FWA, NWA, NS><<<dim3(a.H, NWA, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
-  timing_mark(KC_BWD_PREPASS, st, true);
-  if (a.fstate)
-    k_bwd_prepass<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
-  else
-    k_bwd_prepass<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
-  timing_mark(KC_BWD_PREPASS, st, false);
-  if (!(causal && a.rfold)) {
-    const hipError_t e =
-        launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st,
-                          a.segments);
+  // With the forward's key-side states passed in (d <= 64), the dQ sweep does
+  // the pre-pass's query-side work itself and no pre-pass runs; the R' local
+  // states it leaves feed the scan, or the dK/dV sweep's own suffix sum.
+  constexpr bool CAN_WR = D <= 64;
+  const bool wr = CAN_WR && a.fstate != nullptr;
+  auto scan_r = [&]() -> hipError_t {
+    if (causal && a.rfold) return hipSuccess;
+    return launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st,
+                             a.segments);
+  };
+  if (!wr) {
+    timing_mark(KC_BWD_PREPASS, st, true);
+    if (a.fstate)
+      k_bwd_prepass<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
+    else
+      k_bwd_prepass<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
+    timing_mark(KC_BWD_PREPASS, st, false);
+    const hipError_t e = scan_r();
     if (e != hipSuccess) return e;
   }
   timing_mark(KC_BWD_DQ, st, true);
@@ -1274,16 +1362,27 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   constexpr bool GROUPED = D == 128;
   if (GROUPED && a.acc) {
     if (causal)
-      k_bwd_dq<T, D, FWA, NWA, NS, true, GROUPED><<<grid, SA::NT, 0, st>>>(a);
+      k_bwd_dq<T, D, FWA, NWA, NS, true, GROUPED, false><<<grid, SA::NT, 0, st>>>(a);
     else
-      k_bwd_dq<T, D, FWA, NWA, NS, false, GROUPED><<<grid, SA::NT, 0, st>>>(a);
+      k_bwd_dq<T, D, FWA, NWA, NS, false, GROUPED, false><<<grid, SA::NT, 0, st>>>(a);
+  } else if (wr) {
+    if constexpr (CAN_WR) {
+      if (causal)
+        k_bwd_dq<T, D, FWA, NWA, NS, true, false, true><<<grid, SA::NT, 0, st>>>(a);
+      else
+        k_bwd_dq<T, D, FWA, NWA, NS, false, false, true><<<grid, SA::NT, 0, st>>>(a);
+    }
   } else {
     if (causal)
-      k_bwd_dq<T, D, FWA, NWA, NS, true, false><<<grid, SA::NT, 0, st>>>(a);
+      k_bwd_dq<T, D, FWA, NWA, NS, true, false, false><<<grid, SA::NT, 0, st>>>(a);
     else
-      k_bwd_dq<T, D, FWA, NWA, NS, false, false><<<grid, SA::NT, 0, st>>>(a);
+      k_bwd_dq<T, D, FWA, NWA, NS, false, false, false><<<grid, SA::NT, 0, st>>>(a);
   }
   timing_mark(KC_BWD_DQ, st, false);
+  if (wr) {
+    const hipError_t e = scan_r();
+    if (e != hipSuccess) return e;
+  }
   timing_mark(KC_BWD_DKV, st, true);
   if (GROUPED && a.acc) {
     if (causal)
