@@ -410,6 +410,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ float GS2[NBUF][SH::CH][2];
   __shared__ typename StX::Ssq SSQ2[NBUF][SH::CH];
   __shared__ __attribute__((aligned(16))) float SCK2[NBUF][SH::CH];   // per-token key scale s e(k)
+  // dX fragments of every wave's projection rows, copied to LDS once per
+  // workgroup where it has room (d <= 64): the dQ tiles read them there
+  // instead of from the L2 cache every chunk
+  constexpr int NDX = FragBlock<T, D, FW, NS>::NT_ * WAVE;   // fragments per wave
+  constexpr bool DX_LDS = D <= 64;
+  __shared__ Frag<T> DXL[DX_LDS ? NW : 1][DX_LDS ? NDX : 1];
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
@@ -482,6 +488,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   }
   for (int i = l; i < SH::PR * DT * WAVE; i += WAVE)
     *reinterpret_cast<f32x4*>(&DWL[w][i * 4]) = zero4();
+  if constexpr (DX_LDS) {   // ordered before the first dQ tile by the first staging barrier
+    for (int i = threadIdx.x; i < NW * NDX; i += SH::NT)
+      DXL[i / NDX][i % NDX] = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, i / NDX)[i % NDX];
+  }
   const Frag<T> ones = ones_col01<T>();
   f32x4 RT[WR ? SH::DVT1 : 1][WR ? SH::FC : 1];
 #pragma unroll
@@ -708,7 +718,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       const int dt = ot % DT, tt = ot / DT;
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) {
-        const Frag<T>* wd = FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, ww);
+        const Frag<T>* wd = DX_LDS ? DXL[ww] : FragBlock<T, D, FW, NS>::dx(a.wfrag, h, NW, ww);
 #pragma unroll
         for (int ks = 0; ks < WTS::KP; ++ks) {
           Frag<T> b = load_frag_nm<T>(PT[ww], LDP, tt * 16, (2 * ks) * 16, (2 * ks + 1) * 16);
