@@ -907,7 +907,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
     gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
   };
+  // Projection fragments, reloaded per chunk (held for the whole sweep they
+  // would not fit the registers).
+  FreqSlice<T, D, FW, NS> fs;
   if (EARLY) {
+    fs.load_frags(wproj);
     if (c0 < c1) stage(0, c1 - 1);
     __syncthreads();
   }
@@ -925,9 +929,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     typename StX::Ssq* SSQ = SSQ2[par];
     typename StX::Ssq* SSK = SSK2[kp];
     const int tok0 = c * SH::CH;
-    // this chunk's projection fragments: in flight across the staging barrier
-    FreqSlice<T, D, FW, NS> fs;
-    fs.load_frags(wproj);
+    // this chunk's projection fragments (with early staging, issued at the
+    // end of the previous chunk, before its dW' products)
+    if (!EARLY) fs.load_frags(wproj);
     // an earlier group's dK and dV of this chunk (rows past N read row N-1, unused)
     f32x4 old_k[ACC ? NDK : 1][ACC ? NTK : 1];
     float4 old_v[ACC ? SH::TT / QG : 1][ACC ? NIT : 1];
@@ -1227,6 +1231,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
         }
       }
     }
+    if (EARLY) fs.load_frags(wproj);   // the next chunk's (the last step's are unused)
     {
       // one 32-token k-step per chunk, added to the LDS partial one
       // projection-row tile at a time
