@@ -802,9 +802,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   constexpr int SLOT = RED_W > RL_W ? RED_W : RL_W;
   // Staging is double-buffered by chunk parity where LDS allows (d <= 64).
   // There the next chunk is staged before this chunk's dP barrier, which then
-  // also orders those stores before the next chunk's reads, so a chunk needs
-  // no staging barrier of its own.  K rows and norms are read after the dP
-  // barrier too (dK, dW', dtau), so they take three buffers.
+  // also orders those stores before the next chunk's reads.  K rows and norms
+  // are read after the dP barrier too (dK, dW', dtau), so they take three
+  // buffers.
   constexpr int NBUF = D <= 64 ? 2 : 1;
   constexpr bool EARLY = NBUF == 2;
   constexpr int NKB = EARLY ? 3 : 1;
@@ -932,6 +932,11 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
     // this chunk's projection fragments (with early staging, issued at the
     // end of the previous chunk, before its dW' products)
     if (!EARLY) fs.load_frags(wproj);
+    // With early staging this is the chunk's one barrier besides the dP
+    // barrier: after it, every wave has finished the previous chunk's reads
+    // of the other waves' LDS blocks (dP, dV partials, g shares), which this
+    // chunk writes again before its dP barrier.
+    if (EARLY) __syncthreads();
     // an earlier group's dK and dV of this chunk (rows past N read row N-1, unused)
     f32x4 old_k[ACC ? NDK : 1][ACC ? NTK : 1];
     float4 old_v[ACC ? SH::TT / QG : 1][ACC ? NIT : 1];
