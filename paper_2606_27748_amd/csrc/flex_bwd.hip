@@ -411,10 +411,10 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   __shared__ typename StX::Ssq SSQ2[NBUF][SH::CH];
   __shared__ __attribute__((aligned(16))) float SCK2[NBUF][SH::CH];   // per-token key scale s e(k)
   // dX fragments of every wave's projection rows, copied to LDS once per
-  // workgroup where it has room (d <= 64): the dQ tiles read them there
-  // instead of from the L2 cache every chunk
+  // workgroup: the dQ tiles read them there instead of from the L2 cache
+  // every chunk
   constexpr int NDX = FragBlock<T, D, FW, NS>::NT_ * WAVE;   // fragments per wave
-  constexpr bool DX_LDS = D <= 64;
+  constexpr bool DX_LDS = true;
   __shared__ Frag<T> DXL[DX_LDS ? NW : 1][DX_LDS ? NDX : 1];
 
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
