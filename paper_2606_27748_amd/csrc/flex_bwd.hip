@@ -182,6 +182,17 @@ __device__ __forceinline__ void dump_dw(float* out, const float* dwl, int f0) {
     }
 }
 
+// The query side's partial is handed to the dK/dV sweep in tile-major order
+// [matrix][frequency tile][d tile][lane][4], which does not depend on how a
+// kernel's waves split the frequencies: the dK/dV sweep starts its own
+// partial from it, so one partial per workgroup position holds both sides.
+template <class SH, int D>
+__device__ __forceinline__ size_t dw_tile_off(int w, int pr, int dt, int l) {
+  constexpr int NFT = SH::M / 16;   // frequency tiles of one matrix
+  const int mat = pr / SH::FT, ft = pr % SH::FT;
+  return ((((size_t)mat * NFT + w * SH::FT + ft) * (D / 16) + dt) * WAVE + l) * 4;
+}
+
 // ---------------------------------------------------------------------------
 // Pre-pass: segment-local S'^T = sum [V;1]^T-rows x phi(K) and
 // R'^T = sum [dO;-delta]^T-rows x phi(Q)/den; per-token 1/den and delta.
@@ -759,7 +770,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   }
   const size_t nmat = NS ? 2 : 1;
   float* out = a.dwpart + (((size_t)0 * a.BH + bh) * a.segments + seg) * nmat * SH::M * D;
-  dump_dw<SH, D, FW, NS>(out, DWL[w], w * FW);
+#pragma unroll
+  for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      *reinterpret_cast<f32x4*>(out + dw_tile_off<SH, D>(w, pr, dt, l)) =
+          *reinterpret_cast<const f32x4*>(&DWL[w][((pr * DT + dt) * WAVE + l) * 4]);
   if constexpr (WR) {
     float* ro = a.rstate + ((size_t)bh * a.segments + seg) * SH::STATE;
 #pragma unroll
@@ -872,8 +888,18 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       for (int fc = 0; fc < SH::FC; ++fc)
         RT[dt][fc] = *reinterpret_cast<const f32x4*>(in + state_off<SH>(w, dt, fc, l));
   }
-  for (int i = l; i < SH::PR * DT * WAVE; i += WAVE)
-    *reinterpret_cast<f32x4*>(&DWL[w][i * 4]) = zero4();
+  {
+    // this wave's dW' partial starts from the query side's (dQ sweep) partial
+    // of this workgroup position
+    const size_t nmat = NS ? 2 : 1;
+    const float* qpart = a.dwpart + (((size_t)0 * a.BH + bh) * a.segments + seg) * nmat * SH::M * D;
+#pragma unroll
+    for (int pr = 0; pr < SH::PR; ++pr)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<f32x4*>(&DWL[w][((pr * DT + dt) * WAVE + l) * 4]) =
+            *reinterpret_cast<const f32x4*>(qpart + dw_tile_off<SH, D>(w, pr, dt, l));
+  }
   float dtau_acc = 0.f;
 
   // dX fragments of this wave's d tile: held for the whole sweep when every
@@ -1266,13 +1292,15 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 
 // ---------------------------------------------------------------------------
 // Fixed-order reduction of the frequency-gradient and dtau partials.
-// dwpart: [2][B*H][P][nmat][m][d].  dW'1, dW'2 -> dW1 = (dW'1+dW'2)/2,
+// dwpart: [2][B*H][P][nmat][m][d]; the key side's blocks hold the sums of
+// both sides in [matrix][m][d] order.  dW'1, dW'2 -> dW1 = (dW'1+dW'2)/2,
 // dW2 = (dW'1-dW'2)/2 because W'1 = (W1+W2)/2 and W'2 = (W1-W2)/2.
 // ---------------------------------------------------------------------------
 template <int NMAT>
 __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int md4) {
   // 256 elements (f, k) of one head per workgroup, 4 consecutive per thread;
-  // the 4 waves split the list of partials (side, b, segment) round-robin and
+  // the 4 waves split the list of partials (b, segment; each already the sum
+  // of the query and key sides) round-robin and
   // issue a batch of loads of every matrix before summing it (a partial past
   // the list reads the last one, added as zero), then the 4 wave sums are
   // combined in a fixed order.
@@ -1281,7 +1309,7 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int md4) {
   const int e4 = blockIdx.x * 64 + (threadIdx.x % 64);
   const int q = threadIdx.x / 64;
   const int h = blockIdx.y;
-  const int count = 2 * a.B * a.segments;
+  const int count = a.B * a.segments;
   const float4* src = reinterpret_cast<const float4*>(a.dwpart);
   float4 acc[NMAT];
 #pragma unroll
@@ -1292,9 +1320,8 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int md4) {
 #pragma unroll
       for (int u = 0; u < BATCH; ++u) {
         const int j = min(i0 + 4 * u, count - 1);
-        const int side = j / (a.B * a.segments), rem = j % (a.B * a.segments);
-        const int b = rem / a.segments, p = rem % a.segments;
-        const size_t blk = ((size_t)side * a.BH + (size_t)b * a.H + h) * a.segments + p;
+        const int b = j / a.segments, p = j % a.segments;
+        const size_t blk = ((size_t)1 * a.BH + (size_t)b * a.H + h) * a.segments + p;
 #pragma unroll
         for (int mat = 0; mat < NMAT; ++mat) v[u][mat] = src[(blk * NMAT + mat) * md4 + e4];
       }

@@ -79,7 +79,9 @@ struct BwdArgs {
   float* sstate;      // [BH][segments][state floats]: key-side prefix states
   float* rstate;      // [BH][segments][state floats]: query-side suffix states
   float* gstats;      // [BH][N][2]: 1/den_i and delta_i = dO_i . O_i
-  float* dwpart;      // [2 sides][BH][segments][rows][d] frequency-gradient partials
+  float* dwpart;      // [2 sides][BH][segments][rows][d] frequency-gradient partials: the
+                      // query side's in tile-major order (the dK/dV sweep starts from
+                      // it), the key side's holding both sides' sums in [matrix][m][d]
   float* dtaupart;    // [BH][segments] partial dtau
   void* wfrag;        // per-head frequency fragments (prepared by k_prep_freqs)
   void* wfrag_kv;     // fragments of the dK/dV sweep (== wfrag when its split is the same)
