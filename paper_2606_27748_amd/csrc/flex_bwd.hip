@@ -206,7 +206,9 @@ __device__ __forceinline__ size_t dw_tile_off(int w, int pr, int dt, int l) {
 // in LDS.
 template <class T, int D, int FW, int NW, bool NS, bool WITH_S>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
-  constexpr int PCH = D <= 64 ? CHUNK : BWD_CHUNK;
+  // 64-token chunks where the staging fits: at d <= 64, and at d = 128 on the
+  // query-side-only pass (K and V are not staged there)
+  constexpr int PCH = (D <= 64 || !WITH_S) ? CHUNK : BWD_CHUNK;
   typedef Shape<T, D, FW, NW, NS, PCH> SH;
   static_assert(PCH % BWD_CHUNK == 0 && CHUNK % PCH == 0, "pre-pass chunks hold whole sweep chunks");
   typedef typename Io<T>::type IO;
@@ -240,20 +242,27 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 
   StX sq, sk;
   StV sv, sdo, so;
-  float dn_next = 0.f;
-  // FUSED: every thread stages one vector of one row of Q, dO and O alike
-  // (same vectors per row, one vector per thread), so the row sums dO . O and
-  // ||q||^2 come out of the staging registers with lane sums, and the
-  // per-token scalars need no barrier of their own.  Each thread then loads
-  // den of its own row; otherwise thread t < CH loads that of row t.
-  constexpr bool FUSED = StX::VPR == StV::VPR && StX::NV == SH::NT && StV::NV == SH::NT;
-  auto den_row = [&](int t0) {
-    return den[min(t0 + (int)(FUSED ? threadIdx.x / StV::VPR : threadIdx.x % SH::CH), a.N - 1)];
+  // FUSED: every thread stages the same PER vectors of Q, dO and O (same
+  // vectors per row, all threads busy), so the row sums dO . O and ||q||^2
+  // come out of the staging registers with lane sums, and the per-token
+  // scalars need no barrier of their own.  Each thread then loads den of its
+  // own rows; otherwise thread t < CH loads that of row t.
+  constexpr bool FUSED = StX::VPR == StV::VPR && StX::NV == StV::NV && StV::NV % SH::NT == 0;
+  constexpr int FPER = FUSED ? StV::PER : 1;
+  float dn_next[FPER];
+#pragma unroll
+  for (int i = 0; i < FPER; ++i) dn_next[i] = 0.f;
+  auto den_rows = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < FPER; ++i) {
+      const int t = FUSED ? (int)(threadIdx.x + i * SH::NT) / StV::VPR : (int)(threadIdx.x % SH::CH);
+      dn_next[i] = den[min(t0 + t, a.N - 1)];   // rows past N unused
+    }
   };
   if (c0 < c1) {
     sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
     sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N); so.fetch(Ob, c0 * SH::CH, a.N);
-    dn_next = den_row(c0 * SH::CH);   // rows past N unused
+    den_rows(c0 * SH::CH);
   }
   const Frag<T>* wproj = FragBlock<T, D, FW, NS>::proj(a.wfrag, h, NW, w);
   const auto inv_c = inv_c_of<T>(a.tau[h]);
@@ -290,30 +299,33 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
     const int tok0 = c * SH::CH;
     if (!KEEP_FS) fs.load_frags(wproj);
     if constexpr (FUSED) {
-      // per-token 1/den and delta = dO . O of this thread's row (rows past N
+      // per-token 1/den and delta = dO . O of this thread's rows (rows past N
       // are zero vectors: delta 0)
-      const int t = threadIdx.x / StV::VPR;
-      const bool ok = tok0 + t < a.N;
-      const float inv = ok ? 1.0f / dn_next : 0.f;
-      float dsum = 0.f;
-      {
-        const uint4 x = sdo.vec(0), y = so.vec(0);
+      float inv[FPER];
+      bool ok[FPER];
+#pragma unroll
+      for (int i = 0; i < FPER; ++i) {
+        const int t = (int)(threadIdx.x + i * SH::NT) / StV::VPR;
+        ok[i] = tok0 + t < a.N;
+        inv[i] = ok[i] ? 1.0f / dn_next[i] : 0.f;
+        float dsum = 0.f;
+        const uint4 x = sdo.vec(i), y = so.vec(i);
         const IO* ex = reinterpret_cast<const IO*>(&x);
         const IO* ey = reinterpret_cast<const IO*>(&y);
 #pragma unroll
         for (int j = 0; j < StV::VEC; ++j) dsum += io_to_float(ex[j]) * io_to_float(ey[j]);
+        dsum = lane_sum<StV::VPR>(dsum);
+        if (threadIdx.x % StV::VPR == 0) {
+          GS[t][0] = inv[i];
+          GS[t][1] = ok[i] ? dsum : 0.f;
+          if (ok[i]) { gst[(size_t)(tok0 + t) * 2] = inv[i]; gst[(size_t)(tok0 + t) * 2 + 1] = dsum; }
+        }
       }
-      dsum = lane_sum<StV::VPR>(dsum);
-      sq.store(XQ, SCQ, [&](int, auto ssq) { return row_scale(ssq, inv_c, a.s_const, ok) * inv; });
+      sq.store_idx(XQ, SCQ, [&](int i, int, auto ssq) { return row_scale(ssq, inv_c, a.s_const, ok[i]) * inv[i]; });
       sdo.store(XDO);
-      if (threadIdx.x % StV::VPR == 0) {
-        GS[t][0] = inv;
-        GS[t][1] = ok ? dsum : 0.f;
-        if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = dsum; }
-      }
     } else {
       sq.store(XQ, SSQ); sdo.store(XDO); so.store(XO);
-      if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next;
+      if (threadIdx.x < SH::CH) DEN[threadIdx.x] = dn_next[0];
     }
     if (WITH_S) {
       if constexpr (FUSED)
@@ -329,7 +341,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
       const int t1 = c + 1 < c1 ? tok0 + SH::CH : tok0;   // the last chunk refetches itself (unused)
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N);
       sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N); so.fetch(Ob, t1, a.N);
-      dn_next = den_row(t1);
+      den_rows(t1);
     }
     __syncthreads();
     // per-token 1/den and delta = dO . O (FUSED: done above)

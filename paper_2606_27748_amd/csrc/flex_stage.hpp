@@ -67,6 +67,11 @@ struct RowStage {
   // store, plus f(row, squared norm of the row) into out[ROWS]
   template <class OUT, class F>
   __device__ __forceinline__ void store(IO* lds, OUT* out, F f) const {
+    store_idx(lds, out, [&](int, int t, Ssq s) { return f(t, s); });
+  }
+  // as store, with f also given the index i < PER of the thread's vector
+  template <class OUT, class F>
+  __device__ __forceinline__ void store_idx(IO* lds, OUT* out, F f) const {
     static_assert(NT % VPR == 0 && VPR <= WAVE, "a row's vectors must share a wave");
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
@@ -86,7 +91,7 @@ struct RowStage {
 #pragma unroll
         for (int o = 1; o < VPR; o <<= 1) s += __shfl_xor(s, o);
       }
-      if (v < NV && v % VPR == 0) out[v / VPR] = f(v / VPR, s);
+      if (v < NV && v % VPR == 0) out[v / VPR] = f(i, v / VPR, s);
     }
   }
   // transposed store: ldsT[col][token] with row stride LDT (operand type T)
