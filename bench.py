@@ -30,7 +30,7 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_TFLOPS = 157.3
 KERNEL_FILES = {"fwd_state": "flex_fwd.hip", "fwd_sweep": "flex_fwd.hip", "scan": "flex_fwd.hip",
-                "bwd_prepass": "flex_bwd.hip", "bwd_dq": "flex_bwd.hip", "bwd_dkv": "flex_bwd.hip",
+                "bwd_prepass": "flex_bwd.hip", "bwd_dq": "flex_bwd_dq.hip", "bwd_dkv": "flex_bwd.hip",
                 "bwd_reduce": "flex_bwd.hip", "decode_step": "flex_decode.hip",
                 "awd_fwd": "flex_awd.hip", "awd_bwd_k": "flex_awd.hip",
                 "awd_wgrad": "flex_awd.hip"}
@@ -158,11 +158,14 @@ def copy_bandwidth_gbs(nbytes=1 << 30, reps=10):
 
 
 def source_hash(kernel):
-    path = os.path.join(ROOT, "paper_2606_27748_amd", "csrc", KERNEL_FILES.get(kernel, "flex_fwd.hip"))
+    src = os.path.join(ROOT, "paper_2606_27748_amd", "csrc")
+    name = KERNEL_FILES.get(kernel, "flex_fwd.hip")
+    files = [name, "flex_common.hpp", "flex_stage.hpp"]
+    if name.startswith("flex_bwd"):
+        files.append("flex_bwd_common.hpp")
     h = hashlib.sha256()
-    for p in (path, os.path.join(ROOT, "paper_2606_27748_amd", "csrc", "flex_common.hpp"),
-              os.path.join(ROOT, "paper_2606_27748_amd", "csrc", "flex_stage.hpp")):
-        with open(p, "rb") as f:
+    for p in files:
+        with open(os.path.join(src, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 

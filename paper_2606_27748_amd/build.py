@@ -11,16 +11,18 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libflexattn.so")
-SOURCES = ["flex_api.hip", "flex_fwd.hip", "flex_bwd.hip", "flex_decode.hip", "flex_awd.hip"]
+SOURCES = ["flex_api.hip", "flex_fwd.hip", "flex_bwd.hip", "flex_bwd_dq.hip", "flex_decode.hip", "flex_awd.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # never emit packed fp32 arithmetic (v_pk_fma/mul/add_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # MFMA results that feed VALU code are placed in VGPRs (fewer AGPR copies)
-    # "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"),
 ]
+# Per-source additions: the dQ sweep places MFMA results in VGPRs (its results
+# mostly feed vector code; fewer accumulator-register copies).  Measured slower
+# for the other kernels.
+FILE_FLAGS = {"flex_bwd_dq.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _run(cmd):
@@ -38,7 +40,7 @@ def build(verbose: bool = False) -> str:
     for s in SOURCES:
         o = os.path.join(BUILD, s.replace(".hip", ".o"))
         objs.append(o)
-        cmds.append([HIPCC] + FLAGS + ["-c", os.path.join(CSRC, s), "-o", o])
+        cmds.append([HIPCC] + FLAGS + FILE_FLAGS.get(s, []) + ["-c", os.path.join(CSRC, s), "-o", o])
     with cf.ThreadPoolExecutor(max_workers=min(len(cmds), 4)) as ex:
         for err in ex.map(_run, cmds):
             if verbose and err.strip():

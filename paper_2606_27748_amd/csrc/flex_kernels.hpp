@@ -181,5 +181,9 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_
 // O = acc_num / acc_den (io dtype), den = acc_den, after the last frequency group.
 hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);
+// The dQ sweep of one shape (flex_bwd_dq.hip): grouped_acc adds into an
+// earlier frequency group's dQ; wr also does the pre-pass's query-side work.
+template <class T, int D, int FW, int NW, bool NS>
+hipError_t launch_bwd_dq(const BwdArgs& a, bool causal, bool grouped_acc, bool wr, hipStream_t st);
 
 }  // namespace flex
