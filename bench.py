@@ -72,13 +72,10 @@ def kernel_work(wl, kernel):
     if kernel == "bwd_prepass":
         return T * (5 * d * bio + 4 + 8), T * (2 * proj + 2 * state), T * 2 * tr
     if kernel == "bwd_dq":
-        if d <= 64:
-            # with the forward's states (as the bench runs it) the sweep also does
-            # the pre-pass's query-side work: reads Q, K, V, dO, O and den; writes
-            # dQ, 1/den and delta; adds the R' local state to its contractions
-            return T * (5 * d * bio + 4 + 8 + 4 * d), T * (2 * state + 2 * proj), T * trp
-        # reads Q, K, V, dO, 1/den and delta; writes dQ; dphi(Q) = S'G, dQ = dP W', dW' += dP^T Q
-        return T * (4 * d * bio + 8 + 4 * d), T * (state + 2 * proj), T * trp
+        # with the forward's states (as the bench runs it) the sweep also does
+        # the pre-pass's query-side work: reads Q, K, V, dO, O and den; writes
+        # dQ, 1/den and delta; adds the R' local state to its contractions
+        return T * (5 * d * bio + 4 + 8 + 4 * d), T * (2 * state + 2 * proj), T * trp
     if kernel == "bwd_dkv":
         # reads Q, K, V, dO, 1/den and delta; writes dK, dV; dphi(K), dV, dK, dW' and R'
         return T * (4 * d * bio + 8 + 8 * d), T * (3 * state + 2 * proj), T * trp

@@ -832,11 +832,10 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
         a.W1, a.W2, a.wfrag, a.wfrag_kv, a.w_stride);
   else
     k_prep_freqs<T, D, FWA, NWA, NS><<<dim3(a.H, NWA, 2), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
-  // With the forward's key-side states passed in (d <= 64), the dQ sweep does
-  // the pre-pass's query-side work itself and no pre-pass runs; the R' local
+  // With the forward's key-side states passed in, the dQ sweep does the
+  // pre-pass's query-side work itself and no pre-pass runs; the R' local
   // states it leaves feed the scan, or the dK/dV sweep's own suffix sum.
-  constexpr bool CAN_WR = D <= 64;
-  const bool wr = CAN_WR && a.fstate != nullptr;
+  const bool wr = a.fstate != nullptr;
   auto scan_r = [&]() -> hipError_t {
     if (causal && a.rfold) return hipSuccess;
     return launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st,

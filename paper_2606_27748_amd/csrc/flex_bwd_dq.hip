@@ -55,26 +55,32 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   const IO* dO = static_cast<const IO*>(a.dO) + (size_t)bh * a.N * SH::DV;
   float* gst = a.gstats + (size_t)bh * a.N * 2;
   float* dQ = a.dQ + (size_t)bh * a.N * D;
-  // WR: thread v stages vector v % VPR of row v / VPR of Q, dO and O alike
-  static_assert(!WR || (StX::VPR == StV::VPR && StX::NV == StV::NV && StV::NV <= SH::NT),
-                "one row vector per thread in the same layout for Q, dO and O");
+  // WR: thread v stages vectors v + i NT (i < PER) of Q, dO and O alike, so
+  // the row sums dO . O come out of its staging registers
+  static_assert(!WR || (StX::VPR == StV::VPR && StX::NV == StV::NV && (StV::NV <= SH::NT || StV::NV % SH::NT == 0)),
+                "the same row vectors per thread for Q, dO and O");
+  constexpr int WPER = WR ? StV::PER : 1;
   const IO* Ob = static_cast<const IO*>(a.O) + (size_t)bh * a.N * SH::DV;
   const float* den = a.den + (size_t)bh * a.N;
-  auto den_row = [&](int t0) {   // rows past N (and threads past the rows) unused
-    return den[min(t0 + (int)(threadIdx.x / StV::VPR), a.N - 1)];
+  float dn_next[WPER];
+#pragma unroll
+  for (int i = 0; i < WPER; ++i) dn_next[i] = 0.f;
+  auto den_rows = [&](int t0) {   // rows past N (and threads past the rows) unused
+#pragma unroll
+    for (int i = 0; i < WPER; ++i)
+      dn_next[i] = den[min(t0 + (int)(threadIdx.x + i * SH::NT) / StV::VPR, a.N - 1)];
   };
 
   StX sq, sk;
   StV sv, sdo, so;
   float2 gs_next = make_float2(0.f, 0.f);
   bool gs_ok = false;
-  float dn_next = 0.f;
   if (c0 < c1) {
     sq.fetch(Q, c0 * SH::CH, a.N); sk.fetch(K, c0 * SH::CH, a.N);
     sv.fetch(V, c0 * SH::CH, a.N); sdo.fetch(dO, c0 * SH::CH, a.N);
     if (WR) {
       so.fetch(Ob, c0 * SH::CH, a.N);
-      dn_next = den_row(c0 * SH::CH);
+      den_rows(c0 * SH::CH);
     } else {
       gs_next = load_gs(gst, c0 * SH::CH, a.N, SH::CH, gs_ok);
     }
@@ -161,24 +167,25 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     sk.store(XK, SCK, [&](int t, auto ssq) { return row_scale(ssq, inv_c, a.s_const, tok0 + t < a.N); });
     sv.store(XV); sdo.store(XDO);
     if constexpr (WR) {
-      // 1/den and delta of this thread's row (rows past N: zero vectors, delta 0)
-      const int t = threadIdx.x / StV::VPR;
-      const bool mine = (int)threadIdx.x < StV::NV;
-      const bool ok = mine && tok0 + t < a.N;
-      float dsum = 0.f;
-      {
-        const uint4 x = sdo.vec(0), y = so.vec(0);
+      // 1/den and delta of this thread's rows (rows past N: zero vectors, delta 0)
+#pragma unroll
+      for (int i = 0; i < WPER; ++i) {
+        const int v = threadIdx.x + i * SH::NT, t = v / StV::VPR;
+        const bool mine = v < StV::NV;
+        const bool ok = mine && tok0 + t < a.N;
+        float dsum = 0.f;
+        const uint4 x = sdo.vec(i), y = so.vec(i);
         const IO* ex = reinterpret_cast<const IO*>(&x);
         const IO* ey = reinterpret_cast<const IO*>(&y);
 #pragma unroll
         for (int j = 0; j < StV::VEC; ++j) dsum += io_to_float(ex[j]) * io_to_float(ey[j]);
-      }
-      dsum = lane_sum<StV::VPR>(dsum);
-      if (mine && threadIdx.x % StV::VPR == 0) {
-        const float inv = ok ? 1.0f / dn_next : 0.f;
-        GS[t][0] = inv;
-        GS[t][1] = ok ? dsum : 0.f;
-        if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = dsum; }
+        dsum = lane_sum<StV::VPR>(dsum);
+        if (mine && v % StV::VPR == 0) {
+          const float inv = ok ? 1.0f / dn_next[i] : 0.f;
+          GS[t][0] = inv;
+          GS[t][1] = ok ? dsum : 0.f;
+          if (ok) { gst[(size_t)(tok0 + t) * 2] = inv; gst[(size_t)(tok0 + t) * 2 + 1] = dsum; }
+        }
       }
     } else {
       if (threadIdx.x < SH::CH) { GS[threadIdx.x][0] = gs_ok ? gs_next.x : 0.f; GS[threadIdx.x][1] = gs_ok ? gs_next.y : 0.f; }
@@ -188,7 +195,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       sq.fetch(Q, t1, a.N); sk.fetch(K, t1, a.N); sv.fetch(V, t1, a.N); sdo.fetch(dO, t1, a.N);
       if (WR) {
         so.fetch(Ob, t1, a.N);
-        dn_next = den_row(t1);
+        den_rows(t1);
       } else {
         gs_next = load_gs(gst, t1, a.N, SH::CH, gs_ok);
       }
@@ -403,33 +410,30 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 
 // Launch of the dQ sweep for one shape: grouped_acc adds into an earlier
 // frequency group's dQ (d = 128); wr does the pre-pass's query-side work
-// (d <= 64, with the forward's key-side states).
+// (with the forward's key-side states).
+template <class T, int D, int FW, int NW, bool NS, bool ACC>
+static void launch_dq_acc(const BwdArgs& a, bool causal, bool wr, const dim3& grid, int nt, hipStream_t st) {
+  if (wr) {
+    if (causal) k_bwd_dq<T, D, FW, NW, NS, true, ACC, true><<<grid, nt, 0, st>>>(a);
+    else k_bwd_dq<T, D, FW, NW, NS, false, ACC, true><<<grid, nt, 0, st>>>(a);
+  } else {
+    if (causal) k_bwd_dq<T, D, FW, NW, NS, true, ACC, false><<<grid, nt, 0, st>>>(a);
+    else k_bwd_dq<T, D, FW, NW, NS, false, ACC, false><<<grid, nt, 0, st>>>(a);
+  }
+}
+
 template <class T, int D, int FW, int NW, bool NS>
 hipError_t launch_bwd_dq(const BwdArgs& a, bool causal, bool grouped_acc, bool wr, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SA;
   const dim3 grid(a.segments * a.BH);
   constexpr bool GROUPED = D == 128;
-  constexpr bool CAN_WR = D <= 64;
-  if (GROUPED && grouped_acc) {
-    if (causal)
-      k_bwd_dq<T, D, FW, NW, NS, true, GROUPED, false><<<grid, SA::NT, 0, st>>>(a);
-    else
-      k_bwd_dq<T, D, FW, NW, NS, false, GROUPED, false><<<grid, SA::NT, 0, st>>>(a);
-  } else if (wr) {
-    if constexpr (CAN_WR) {
-      if (causal)
-        k_bwd_dq<T, D, FW, NW, NS, true, false, true><<<grid, SA::NT, 0, st>>>(a);
-      else
-        k_bwd_dq<T, D, FW, NW, NS, false, false, true><<<grid, SA::NT, 0, st>>>(a);
-    } else {
-      return hipErrorInvalidValue;
+  if constexpr (GROUPED) {
+    if (grouped_acc) {
+      launch_dq_acc<T, D, FW, NW, NS, true>(a, causal, wr, grid, SA::NT, st);
+      return hipGetLastError();
     }
-  } else {
-    if (causal)
-      k_bwd_dq<T, D, FW, NW, NS, true, false, false><<<grid, SA::NT, 0, st>>>(a);
-    else
-      k_bwd_dq<T, D, FW, NW, NS, false, false, false><<<grid, SA::NT, 0, st>>>(a);
   }
+  launch_dq_acc<T, D, FW, NW, NS, false>(a, causal, wr, grid, SA::NT, st);
   return hipGetLastError();
 }
 
