@@ -126,8 +126,8 @@ int pre_segs_of(const flex_desc* d, int P) { return d->causal ? P - 1 : P; }
 
 // Forward state pre-pass workgroups per segment (sub-segments): 1, 2, 4 or 8,
 // dividing the segment's chunks.  More sub-segments shorten the pre-pass's
-// critical path when its workgroups underfill the CUs (one 8-wave or two
-// 4-wave workgroups per CU at a time) but write and scan more states; the
+// critical path when its workgroups underfill the CUs (fwd_state_wgs_per_cu
+// workgroups per CU at a time) but write and scan more states; the
 // cost is the rounds of chunks (about a third of a sweep chunk each, scaled
 // by MFMA work like pick_segments) plus that state traffic at 5 TB/s.
 int fwd_sub_of(const flex_desc* d, int P) {
@@ -136,7 +136,7 @@ int fwd_sub_of(const flex_desc* d, int P) {
   const long long used = pre_segs_of(d, P);
   if (used <= 0) return 1;
   const KernelShape ks = attn_shape(d);
-  const long long cap = (long long)kCUs * (fwd_state_waves(ks) == 4 ? 2 : 1);
+  const long long cap = (long long)kCUs * fwd_state_wgs_per_cu(ks);
   const double m_eff = ks.nonstationary ? 2.0 * ks.m : ks.m;
   const double t_pre = 2.2e-6 * (2.0 * ks.d * m_eff + 4.0 * ks.m * (d->dv + 1)) / 66048.0;
   const double state_bytes = (double)fwd_state_floats(ks) * sizeof(float);

@@ -26,7 +26,7 @@ namespace flex {
 // Segment-local state: S'_seg = sum over the segment's tokens of phi(K)[V;1]^T.
 // ---------------------------------------------------------------------------
 template <class T, int D, int FW, int NW, bool NS>
-__global__ __launch_bounds__(NW * WAVE) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 2 : 1, 2)))
+__global__ __launch_bounds__(NW * WAVE) __attribute__((amdgpu_waves_per_eu(state_waves_per_eu(D, NS), state_waves_per_eu(D, NS))))
 void k_fwd_state(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
@@ -801,6 +801,14 @@ size_t wfrag_bytes(const KernelShape& ks, int H) {
 
 // Waves per workgroup of the forward attention kernels of a shape.
 int fwd_state_waves(const KernelShape& ks) { return (ks.bf16 && ks.d == 64 && ks.m == 128) ? 8 : 4; }
+
+// Workgroups of the forward state pre-pass that run on one CU at a time, from
+// the waves per SIMD its launch attributes fix.
+int fwd_state_wgs_per_cu(const KernelShape& ks) {
+  const int per_simd = state_waves_per_eu(ks.d, ks.nonstationary);
+  const int wg_per_simd = fwd_state_waves(ks) / 4;
+  return per_simd >= wg_per_simd ? per_simd / wg_per_simd : 1;
+}
 
 size_t fwd_state_floats(const KernelShape& ks) {
   const int fw = (ks.m == 64) ? 16 : 32;

@@ -167,6 +167,11 @@ size_t bwd_dw_floats(const KernelShape& ks);
 size_t wfrag_bytes(const KernelShape& ks, int H);
 bool bwd_split_differs(const KernelShape& ks);
 int fwd_state_waves(const KernelShape& ks);
+// Waves per SIMD of the forward state pre-pass (its launch attribute): two,
+// except at d = 128 nonstationary, whose wave holds more than half a SIMD's
+// registers.
+constexpr int state_waves_per_eu(int d, bool ns) { return (d <= 64 || !ns) ? 2 : 1; }
+int fwd_state_wgs_per_cu(const KernelShape& ks);
 
 // state (or NULL): [BH][P*sub][E]; writes the exclusive prefix (causal) into
 // slot p*sub of every segment p, or the total (non-causal) into slot 0.
