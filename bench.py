@@ -417,8 +417,9 @@ def run_sweep(steps, warmup):
     for N in (1024, 2048, 4096, 8192, 16384, 32768):
         for bwd in (False, True):
             cases.append(("N", base.scaled(name=f"sweep_N{N}_{'fwdbwd' if bwd else 'fwd'}", N=N, backward=bwd)))
-    for m, variant in ((64, "nonstationary"), (128, "nonstationary"), (64, "stationary"), (128, "stationary")):
-        cases.append(("m", base.scaled(name=f"sweep_m{m}_{variant[:4]}", m=m, variant=variant)))
+    for variant in ("nonstationary", "stationary"):
+        for m in (64, 128, 192, 256):
+            cases.append(("m", base.scaled(name=f"sweep_m{m}_{variant[:4]}", m=m, variant=variant)))
     for axis, wl in cases:
         rec = measure(wl, steps, warmup, False, 0)
         tensors, ws = device_bytes(wl)

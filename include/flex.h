@@ -40,13 +40,14 @@
  *     kernel launch returns FLEX_ERR_HIP.  No C++ exception crosses the ABI.
  *   - Results are deterministic (bitwise identical from run to run).
  *   - Supported shapes: N >= 1 (a ragged last chunk is masked); d = dv in
- *     {32, 64, 128}; m in {64, 128, 256} with the combinations
- *     (d, m) = (32, 64), (64, 64), (64, 128), (128, 256) with io_dtype FLEX_BF16,
- *     and (32, 64) with FLEX_F32; chunk in {0, 16, 32, 64}.  Others return
- *     FLEX_ERR_UNSUPPORTED.
- *     Every supported shape has the forward and the backward.  (128, 256) runs
- *     as four groups of 64 frequencies whose sums are combined in a fixed
- *     order; its forward workspace holds an fp32 numerator/denominator buffer.
+ *     {32, 64, 128} with io_dtype FLEX_BF16 and d = dv = 32 with FLEX_F32;
+ *     m a multiple of 64 up to 256; chunk in {0, 16, 32, 64}.  Others return
+ *     FLEX_ERR_UNSUPPORTED.  Every supported shape has the forward and the
+ *     backward.  (d, m) = (32, 64), (64, 64), (64, 128) (bf16) and (128, 64)
+ *     run as one pass; every other shape runs as groups of 64 frequencies whose
+ *     sums are combined in a fixed order (its forward workspace holds an fp32
+ *     numerator/denominator buffer).  flex_feature_map takes (d, m) = (32, 64),
+ *     (64, 64), (64, 128), (128, 256) with FLEX_BF16 and (32, 64) with FLEX_F32.
  *   - io_dtype FLEX_F32 computes every contraction in fp32 (MFMA f32);
  *     FLEX_BF16 reads bf16 inputs, projects with a two-term bf16 split of the
  *     frequencies and contracts bf16 features with fp32 accumulation (the
@@ -63,7 +64,7 @@
 extern "C" {
 #endif
 
-#define FLEX_ABI_VERSION 5
+#define FLEX_ABI_VERSION 6
 
 typedef enum {
   FLEX_OK = 0,

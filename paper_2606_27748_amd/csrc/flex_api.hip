@@ -22,14 +22,23 @@ constexpr int kCUs = 256;
 bool chunk_supported(int c) { return c == 0 || c == 16 || c == 32 || c == 64; }
 int chunk_of(const flex_desc* d) { return d->chunk == 0 ? kChunk : d->chunk; }
 
+// Attention shapes: d = dv in {32, 64, 128} for bf16 (32 for fp32), m a
+// multiple of 64 up to 256.  Shapes that no single kernel covers run as
+// frequency groups of 64 (groups_of).
 bool shape_supported(const flex_desc* d) {
   if (d->dv != d->d) return false;
   if (d->grad_dtype != FLEX_F32) return false;
   if (!chunk_supported(d->chunk)) return false;
+  if (d->m % 64 != 0 || d->m > 256) return false;
+  if (d->io_dtype == FLEX_BF16) return d->d == 32 || d->d == 64 || d->d == 128;
+  return d->d == 32;
+}
+
+// Shapes of the standalone feature map (one kernel each).
+bool fmap_shape_supported(const flex_desc* d) {
   const bool bf = d->io_dtype == FLEX_BF16;
   if (d->d == 32 && d->m == 64) return true;
-  if (d->d == 64 && d->m == 64) return bf;
-  if (d->d == 64 && d->m == 128) return bf;
+  if (d->d == 64 && (d->m == 64 || d->m == 128)) return bf;
   if (d->d == 128 && d->m == 256) return bf;
   return false;
 }
@@ -69,7 +78,9 @@ int32_t check_fmap_desc(const flex_desc* d) {
   c.chunk = 0;
   c.segments = 0;
   c.grad_dtype = FLEX_F32;
-  return check_desc(&c);
+  const int32_t st = check_desc_fields(&c);
+  if (st != FLEX_OK) return st;
+  return fmap_shape_supported(&c) ? FLEX_OK : FLEX_ERR_UNSUPPORTED;
 }
 
 // Shapes of the decode step (one generic kernel): d = dv, a multiple of 4 up to
@@ -88,17 +99,20 @@ KernelShape kshape(const flex_desc* d) {
   return k;
 }
 
-// Frequency groups of the attention kernels: the (d = 128, m = 256) shape runs
-// as four groups of 64 frequencies (per-workgroup state and frequency-gradient
-// partials of one group fit registers and LDS); the groups' contributions to
-// the numerator, denominator and the Q/K/V/tau gradients are summed in launch
-// order, the frequency gradients of a group are its own rows.
+// Frequency groups of the attention kernels.  The kernels cover (d, m) =
+// (32, 64), (64, 64), (64, 128) (bf16) and (128, 64) in one launch per pass;
+// every other shape runs as groups of 64 frequencies (at d = 128, m = 256 the
+// per-workgroup state and frequency-gradient partials of one group fit
+// registers and LDS, all 256 frequencies would not).  The groups'
+// contributions to the numerator, denominator and the Q/K/V/tau gradients are
+// summed in launch order; the frequency gradients of a group are its own rows.
 struct Groups {
   int n, m;
 };
 Groups groups_of(const flex_desc* d) {
-  if (d->d == 128 && d->m == 256) return Groups{4, 64};
-  return Groups{1, d->m};
+  if (d->m == 64) return Groups{1, 64};
+  if (d->d == 64 && d->m == 128 && d->io_dtype == FLEX_BF16) return Groups{1, 128};
+  return Groups{d->m / 64, 64};
 }
 
 // Kernel shape of the attention passes (one frequency group).

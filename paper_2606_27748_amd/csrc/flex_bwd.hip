@@ -852,8 +852,8 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
     if (e != hipSuccess) return e;
   }
   timing_mark(KC_BWD_DQ, st, true);
-  // only the frequency-group shape (d = 128) adds into an earlier group's outputs
-  constexpr bool GROUPED = D == 128;
+  // the 64-frequency group shape adds into an earlier group's outputs
+  constexpr bool GROUPED = SA::M == 64;
   {
     const hipError_t e = launch_bwd_dq<T, D, FWA, NWA, NS>(a, causal, GROUPED && a.acc, wr, st);
     if (e != hipSuccess) return e;

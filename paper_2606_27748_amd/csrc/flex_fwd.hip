@@ -673,7 +673,7 @@ template <class T, int D, int FW, int NW, bool NS, bool ADD>
 static void launch_sweep(const FwdArgs& a, bool causal, dim3 grid, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   if constexpr (!ADD && ReadoutSplit<T, D, FW, NW, NS>::value) {
-    if (!causal) {
+    if (!causal && a.acc == 0) {   // it writes O itself, not a group's sums
       k_fwd_readout<T, D, FW * NW, NS><<<grid, 4 * WAVE, 0, st>>>(a);
       return;
     }
@@ -714,8 +714,8 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   // frequency tile f, whatever wave holds it.
   constexpr int FWS = (D == 64 && FW * NW == 128) ? 32 : FW;
   constexpr int NWS = FW * NW / FWS;
-  // only the frequency-group shape (d = 128) adds to an earlier group's sums
-  constexpr bool GROUPED = D == 128;
+  // the 64-frequency group shape adds to an earlier group's sums
+  constexpr bool GROUPED = FW * NW == 64;
   if (GROUPED && a.acc == 2)
     launch_sweep<T, D, FWS, NWS, NS, GROUPED>(a, causal, grid, st);
   else

@@ -31,7 +31,7 @@ def test_exports_match_header():
     assert set(names) == set(F.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.flex_abi_version() == 5
+    assert lib.flex_abi_version() == 6
 
 
 def test_status_strings():
@@ -63,6 +63,22 @@ def test_workspace_size():
     # an unsupported shape is reported for both passes
     d6 = F.make_desc(2, 16, 8192, 96, 128, "nonstationary", True, "bf16")
     assert _ws(d6)[0] == F.FLEX_ERR_UNSUPPORTED and _ws(d6, F.FLEX_PASS_BWD)[0] == F.FLEX_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("io,d,m,ok", [
+    ("bf16", 32, 128, True), ("bf16", 32, 256, True), ("bf16", 64, 192, True), ("bf16", 64, 256, True),
+    ("bf16", 128, 64, True), ("bf16", 128, 192, True), ("f32", 32, 256, True),
+    ("bf16", 64, 320, False), ("bf16", 64, 96, False), ("bf16", 64, 16, False), ("f32", 64, 64, False),
+])
+def test_attention_shape_set(io, d, m, ok):
+    """The attention passes take d in {32, 64, 128} (fp32: 32) and m a multiple
+    of 64 up to 256 (frequency groups of 64 where no one kernel covers the
+    shape); the standalone feature map keeps its own kernels' shapes."""
+    want = F.FLEX_OK if ok else F.FLEX_ERR_UNSUPPORTED
+    dd = F.make_desc(1, 2, 100, d, m, "nonstationary", True, io)
+    assert _ws(dd)[0] == want and _ws(dd, F.FLEX_PASS_BWD)[0] == want
+    fm = (d, m) in ((32, 64), (64, 64), (64, 128), (128, 256)) and (io == "bf16" or (d, m) == (32, 64))
+    assert _ws(dd, F.FLEX_PASS_FEATURE_MAP)[0] == (F.FLEX_OK if fm else F.FLEX_ERR_UNSUPPORTED)
 
 
 def test_awd_workspace_size():

@@ -16,7 +16,9 @@ from tests.parity import check_grads, check_grad_rows, dv_row_scale, dtau_scale,
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256)]
+SHAPES = [("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256),
+          # frequency groups of 64 at the other shapes
+          ("f32", 32, 128), ("bf16", 32, 192), ("bf16", 64, 256), ("bf16", 128, 64), ("bf16", 128, 128)]
 
 
 @pytest.fixture(scope="module")

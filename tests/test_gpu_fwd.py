@@ -20,6 +20,8 @@ pytestmark = pytest.mark.gpu
 SHAPES = [  # (io, d, m)
     ("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256),
 ]
+# attention shapes that run as frequency groups of 64 (besides d = 128, m = 256)
+GROUP_SHAPES = [("f32", 32, 128), ("bf16", 32, 192), ("bf16", 64, 256), ("bf16", 128, 64), ("bf16", 128, 128)]
 
 
 @pytest.fixture(scope="module")
@@ -76,7 +78,7 @@ def test_feature_map_several_chunks_per_workgroup(F, variant):
     assert np.max(np.abs(got - ref) / scale) <= 2.0 ** -8
 
 
-@pytest.mark.parametrize("io,d,m", SHAPES)
+@pytest.mark.parametrize("io,d,m", SHAPES + GROUP_SHAPES)
 @pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
 @pytest.mark.parametrize("causal", [False, True])
 def test_forward_small(F, io, d, m, variant, causal):
