@@ -101,17 +101,17 @@ KernelShape kshape(const flex_desc* d) {
 
 // Frequency groups of the attention kernels.  The kernels cover (d, m) =
 // (32, 64), (64, 64), (64, 128) (bf16) and (128, 64) in one launch per pass;
-// every other shape runs as groups of 64 frequencies (at d = 128, m = 256 the
-// per-workgroup state and frequency-gradient partials of one group fit
-// registers and LDS, all 256 frequencies would not).  The groups'
-// contributions to the numerator, denominator and the Q/K/V/tau gradients are
-// summed in launch order; the frequency gradients of a group are its own rows.
+// every other shape runs as groups of 128 frequencies (bf16 d = 64, m a
+// multiple of 128) or of 64 (at d = 128, m = 256 the per-workgroup state and
+// frequency-gradient partials of one group fit registers and LDS, all 256
+// frequencies would not).  The groups' contributions to the numerator,
+// denominator and the Q/K/V/tau gradients are summed in launch order; the
+// frequency gradients of a group are its own rows.
 struct Groups {
   int n, m;
 };
 Groups groups_of(const flex_desc* d) {
-  if (d->m == 64) return Groups{1, 64};
-  if (d->d == 64 && d->m == 128 && d->io_dtype == FLEX_BF16) return Groups{1, 128};
+  if (d->d == 64 && d->m % 128 == 0 && d->io_dtype == FLEX_BF16) return Groups{d->m / 128, 128};
   return Groups{d->m / 64, 64};
 }
 

@@ -852,10 +852,9 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
     if (e != hipSuccess) return e;
   }
   timing_mark(KC_BWD_DQ, st, true);
-  // the 64-frequency group shape adds into an earlier group's outputs
-  constexpr bool GROUPED = SA::M == 64;
+  // a later frequency group adds into the earlier groups' outputs
   {
-    const hipError_t e = launch_bwd_dq<T, D, FWA, NWA, NS>(a, causal, GROUPED && a.acc, wr, st);
+    const hipError_t e = launch_bwd_dq<T, D, FWA, NWA, NS>(a, causal, a.acc != 0, wr, st);
     if (e != hipSuccess) return e;
   }
   timing_mark(KC_BWD_DQ, st, false);
@@ -864,11 +863,11 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
     if (e != hipSuccess) return e;
   }
   timing_mark(KC_BWD_DKV, st, true);
-  if (GROUPED && a.acc) {
+  if (a.acc) {
     if (causal)
-      k_bwd_dkv<T, D, FWB, NWB, NS, true, GROUPED><<<grid, SB::NT, 0, st>>>(a);
+      k_bwd_dkv<T, D, FWB, NWB, NS, true, true><<<grid, SB::NT, 0, st>>>(a);
     else
-      k_bwd_dkv<T, D, FWB, NWB, NS, false, GROUPED><<<grid, SB::NT, 0, st>>>(a);
+      k_bwd_dkv<T, D, FWB, NWB, NS, false, true><<<grid, SB::NT, 0, st>>>(a);
   } else {
     if (causal)
       k_bwd_dkv<T, D, FWB, NWB, NS, true, false><<<grid, SB::NT, 0, st>>>(a);

@@ -409,7 +409,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 }
 
 // Launch of the dQ sweep for one shape: grouped_acc adds into an earlier
-// frequency group's dQ (64-frequency groups); wr does the pre-pass's query-side work
+// frequency group's dQ; wr does the pre-pass's query-side work
 // (with the forward's key-side states).
 template <class T, int D, int FW, int NW, bool NS, bool ACC>
 static void launch_dq_acc(const BwdArgs& a, bool causal, bool wr, const dim3& grid, int nt, hipStream_t st) {
@@ -426,14 +426,10 @@ template <class T, int D, int FW, int NW, bool NS>
 hipError_t launch_bwd_dq(const BwdArgs& a, bool causal, bool grouped_acc, bool wr, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SA;
   const dim3 grid(a.segments * a.BH);
-  constexpr bool GROUPED = FW * NW == 64;   // the 64-frequency group shape
-  if constexpr (GROUPED) {
-    if (grouped_acc) {
-      launch_dq_acc<T, D, FW, NW, NS, true>(a, causal, wr, grid, SA::NT, st);
-      return hipGetLastError();
-    }
-  }
-  launch_dq_acc<T, D, FW, NW, NS, false>(a, causal, wr, grid, SA::NT, st);
+  if (grouped_acc)
+    launch_dq_acc<T, D, FW, NW, NS, true>(a, causal, wr, grid, SA::NT, st);
+  else
+    launch_dq_acc<T, D, FW, NW, NS, false>(a, causal, wr, grid, SA::NT, st);
   return hipGetLastError();
 }
 

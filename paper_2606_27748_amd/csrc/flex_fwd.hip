@@ -714,10 +714,9 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   // frequency tile f, whatever wave holds it.
   constexpr int FWS = (D == 64 && FW * NW == 128) ? 32 : FW;
   constexpr int NWS = FW * NW / FWS;
-  // the 64-frequency group shape adds to an earlier group's sums
-  constexpr bool GROUPED = FW * NW == 64;
-  if (GROUPED && a.acc == 2)
-    launch_sweep<T, D, FWS, NWS, NS, GROUPED>(a, causal, grid, st);
+  // a later frequency group adds to the earlier groups' sums
+  if (a.acc == 2)
+    launch_sweep<T, D, FWS, NWS, NS, true>(a, causal, grid, st);
   else
     launch_sweep<T, D, FWS, NWS, NS, false>(a, causal, grid, st);
   timing_mark(KC_FWD_SWEEP, st, false);
