@@ -193,7 +193,7 @@ int pick_segments(const flex_desc* d) {
   const double state_bytes = (double)fwd_state_floats(ks) * sizeof(float);
   int best = 1;
   double best_cost = 1e30;
-  for (int p = 1; p <= nc && p <= 64; ++p) {
+  for (int p = 1; p <= nc && p <= kCUs; ++p) {
     const int cps = (nc + p - 1) / p;
     const int used = (nc + cps - 1) / cps;  // segments that hold chunks
     if (used != p) continue;

@@ -115,6 +115,20 @@ def test_backward_many_segments(F, reuse):
 
 
 @pytest.mark.parametrize("reuse", [False, True])
+def test_backward_128_segments(F, reuse):
+    """128 segments of one 64-token chunk each (small B*H, long N takes up to
+    one segment per CU): scans over 128 states, 128 frequency-gradient
+    partials per head."""
+    wl = W.Workload("seg128", 1, 1, 128 * 64 - 17, 32, 64, "nonstationary", True, "bf16", True, 41)
+    x = W.generate(wl)
+    kap = masked_inputs(wl, x)
+    got = gpu_fwd_bwd(F, wl, x, segments=128, reuse=reuse)
+    ref, sc = oracle_bwd(wl, x)
+    check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
+
+
+@pytest.mark.parametrize("reuse", [False, True])
 def test_backward_many_partials(F, reuse):
     """B = 3 and 7 segments give 42 frequency-gradient partials per head: the
     reduce takes them in two batches, the second one partly past the list."""
