@@ -24,7 +24,7 @@ int chunk_of(const flex_desc* d) { return d->chunk == 0 ? kChunk : d->chunk; }
 
 // Attention shapes: d = dv in {32, 64, 128} for bf16 (32 for fp32), m a
 // multiple of 64 up to 256.  Shapes that no single kernel covers run as
-// frequency groups of 64 (groups_of).
+// frequency groups (groups_of).
 bool shape_supported(const flex_desc* d) {
   if (d->dv != d->d) return false;
   if (d->grad_dtype != FLEX_F32) return false;
