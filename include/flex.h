@@ -41,13 +41,17 @@
  *   - Results are deterministic (bitwise identical from run to run).
  *   - Supported shapes: N >= 1 (a ragged last chunk is masked); d = dv in
  *     {32, 64, 128} with io_dtype FLEX_BF16 and d = dv = 32 with FLEX_F32;
- *     m a multiple of 64 up to 256; chunk in {0, 16, 32, 64}.  Others return
+ *     m a multiple of 16 up to 256; chunk in {0, 16, 32, 64}.  Others return
  *     FLEX_ERR_UNSUPPORTED.  Every supported shape has the forward and the
  *     backward.  (d, m) = (32, 64), (64, 64), (64, 128) (bf16) and (128, 64)
- *     run as one pass; every other shape runs as groups of 64 frequencies whose
- *     sums are combined in a fixed order (its forward workspace holds an fp32
- *     numerator/denominator buffer).  flex_feature_map takes (d, m) = (32, 64),
- *     (64, 64), (64, 128), (128, 256) with FLEX_BF16 and (32, 64) with FLEX_F32.
+ *     run as one pass; every other shape runs as frequency groups (of 128 at
+ *     bf16 d = 64 when 128 divides m, else of 64, the first one zero-padded
+ *     when 64 does not divide m) whose sums are combined in a fixed order (the
+ *     forward workspace then holds an fp32 numerator/denominator buffer).
+ *     With FLEX_BF16 and m < 48 the gradients' relative error can exceed 2e-2:
+ *     rounding the features to bf16 alone costs 1.5-2.3% at m = 16.
+ *     flex_feature_map takes (d, m) = (32, 64), (64, 64), (64, 128),
+ *     (128, 256) with FLEX_BF16 and (32, 64) with FLEX_F32.
  *   - io_dtype FLEX_F32 computes every contraction in fp32 (MFMA f32);
  *     FLEX_BF16 reads bf16 inputs, projects with a two-term bf16 split of the
  *     frequencies and contracts bf16 features with fp32 accumulation (the

@@ -16,6 +16,8 @@ namespace {
 constexpr int kChunk = 64;
 constexpr int kCUs = 256;
 
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
 // Chunk lengths of the causal forward sweep.  The segment split, the state
 // pre-pass and the non-causal sweep work in 64-token chunks whatever the
 // chunk; the backward in 32-token chunks.
@@ -23,13 +25,13 @@ bool chunk_supported(int c) { return c == 0 || c == 16 || c == 32 || c == 64; }
 int chunk_of(const flex_desc* d) { return d->chunk == 0 ? kChunk : d->chunk; }
 
 // Attention shapes: d = dv in {32, 64, 128} for bf16 (32 for fp32), m a
-// multiple of 64 up to 256.  Shapes that no single kernel covers run as
+// multiple of 16 up to 256.  Shapes that no single kernel covers run as
 // frequency groups (groups_of).
 bool shape_supported(const flex_desc* d) {
   if (d->dv != d->d) return false;
   if (d->grad_dtype != FLEX_F32) return false;
   if (!chunk_supported(d->chunk)) return false;
-  if (d->m % 64 != 0 || d->m > 256) return false;
+  if (d->m % 16 != 0 || d->m > 256) return false;
   if (d->io_dtype == FLEX_BF16) return d->d == 32 || d->d == 64 || d->d == 128;
   return d->d == 32;
 }
@@ -104,15 +106,68 @@ KernelShape kshape(const flex_desc* d) {
 // every other shape runs as groups of 128 frequencies (bf16 d = 64, m a
 // multiple of 128) or of 64 (at d = 128, m = 256 the per-workgroup state and
 // frequency-gradient partials of one group fit registers and LDS, all 256
-// frequencies would not).  The groups' contributions to the numerator,
-// denominator and the Q/K/V/tau gradients are summed in launch order; the
-// frequency gradients of a group are its own rows.
+// frequencies would not).  When 64 does not divide m, the first group holds
+// the first `last` frequencies and zero rows after them, whose features the
+// kernels mask to zero (it runs first, so only write variants need masking).
+// The groups' contributions to the numerator, denominator and the Q/K/V/tau
+// gradients are summed in launch order; the frequency gradients of a group
+// are its own rows.
 struct Groups {
-  int n, m;
+  int n, m, last;
 };
 Groups groups_of(const flex_desc* d) {
-  if (d->d == 64 && d->m % 128 == 0 && d->io_dtype == FLEX_BF16) return Groups{d->m / 128, 128};
-  return Groups{d->m / 64, 64};
+  if (d->d == 64 && d->m % 128 == 0 && d->io_dtype == FLEX_BF16) return Groups{d->m / 128, 128, 128};
+  const int n = (d->m + 63) / 64;
+  return Groups{n, 64, d->m - 64 * (n - 1)};
+}
+
+// First frequency row of group g (the padded group, if any, is group 0).
+int group_off(const Groups& G, int g) { return g == 0 ? 0 : G.last + (g - 1) * G.m; }
+
+// Padded frequency rows of a first group that 64 does not fill: [H][group][d]
+// per matrix, at the end of the forward and backward workspaces.
+size_t pad_bytes(const flex_desc* d) {
+  const Groups G = groups_of(d);
+  if (G.last == G.m) return 0;
+  const size_t nmat = d->variant == FLEX_NONSTATIONARY ? 2 : 1;
+  return nmat * align256((size_t)d->H * G.m * d->d * sizeof(float));
+}
+
+// The padded rows' place in a workspace that ends at `end`.
+struct PadRows {
+  float* w1;
+  float* w2;
+};
+PadRows pad_rows_of(const flex_desc* d, char* end) {
+  const size_t pb = pad_bytes(d);
+  if (pb == 0) return PadRows{nullptr, nullptr};
+  char* p = end - pb;
+  const size_t one = align256((size_t)d->H * groups_of(d).m * d->d * sizeof(float));
+  return PadRows{reinterpret_cast<float*>(p),
+                 d->variant == FLEX_NONSTATIONARY ? reinterpret_cast<float*>(p + one) : nullptr};
+}
+
+// Frequency rows of group g: the caller's rows of W1/W2 (head stride m d),
+// or for a padded group a zero-padded copy of them (head stride group width
+// x d), written on the stream first.  fvalid: the group's rows that are
+// frequencies.  False if the copy's launch fails.
+bool group_rows(const flex_desc* d, const Groups& G, const PadRows& pr, int g, const float* W1, const float* W2,
+                hipStream_t st, const float** w1, const float** w2, int* stride, int* fvalid) {
+  const size_t woff = (size_t)group_off(G, g) * d->d;
+  const bool padded = g == 0 && G.last < G.m;
+  *fvalid = g == 0 ? G.last : G.m;
+  if (!padded) {
+    *w1 = W1 + woff;
+    *w2 = W2 ? W2 + woff : nullptr;
+    *stride = d->m * d->d;
+    return true;
+  }
+  if (launch_pad_rows(W1 + woff, pr.w1, d->H, G.last, G.m, d->d, d->m * d->d, st) != hipSuccess) return false;
+  if (W2 && launch_pad_rows(W2 + woff, pr.w2, d->H, G.last, G.m, d->d, d->m * d->d, st) != hipSuccess) return false;
+  *w1 = pr.w1;
+  *w2 = W2 ? pr.w2 : nullptr;
+  *stride = G.m * d->d;
+  return true;
 }
 
 // Kernel shape of the attention passes (one frequency group).
@@ -212,7 +267,6 @@ float s_const_of(const flex_desc* d) {
   return (float)s;
 }
 
-size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Forward workspace: the segment states of every frequency group, one block of
 // prepared fragments (reused group after group) and, with several groups, the
@@ -234,13 +288,13 @@ size_t ws_bytes_of(const flex_desc* d, int pass) {
   const size_t P = (size_t)pick_segments(d);
   if (pass == FLEX_PASS_FEATURE_MAP) return 0;
   const size_t wf = align256(wfrag_bytes(ks, d->H));
-  if (pass == FLEX_PASS_FWD) return groups_of(d).n * fwd_group_state_bytes(d) + wf + fwd_acc_bytes(d);
+  if (pass == FLEX_PASS_FWD) return groups_of(d).n * fwd_group_state_bytes(d) + wf + fwd_acc_bytes(d) + pad_bytes(d);
   // backward: key-side and query-side states, per-token scalars, frequency-gradient
   // and dtau partials
   return 2 * align256(bh * P * bwd_state_floats(ks) * sizeof(float)) +
          align256(bh * (size_t)d->N * 2 * sizeof(float)) +
          align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float)) +
-         (bwd_split_differs(ks) ? 2 : 1) * wf;
+         (bwd_split_differs(ks) ? 2 : 1) * wf + pad_bytes(d);
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -404,13 +458,11 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
     a.sweep_groups = (a.nchunks + a.sweep_cps - 1) / a.sweep_cps;
   }
   a.s_const = s_const_of(desc);
-  a.w_stride = desc->m * desc->d;
+  const PadRows pr = pad_rows_of(desc, base + ws_bytes_of(desc, FLEX_PASS_FWD));
   for (int g = 0; g < G.n; ++g) {
-    const size_t woff = (size_t)g * G.m * desc->d;   // this group's frequency rows
-    a.W1 = W1 + woff;
-    a.W2 = W2 ? W2 + woff : nullptr;
+    if (!group_rows(desc, G, pr, g, W1, W2, stream, &a.W1, &a.W2, &a.w_stride, &a.fvalid)) return FLEX_ERR_HIP;
     a.state = reinterpret_cast<float*>(base + g * sb);
-    a.state_f0 = g * G.m;
+    a.state_f0 = group_off(G, g);
     a.acc = G.n == 1 ? 0 : (g == 0 ? 1 : 2);
     const hipError_t e = launch_fwd(a, ks, false, stream);
     if (e != hipSuccess) return FLEX_ERR_HIP;
@@ -690,11 +742,12 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
   a.wfrag = base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
   a.wfrag_kv = bwd_split_differs(ks) ? static_cast<char*>(a.wfrag) + align256(wfrag_bytes(ks, desc->H)) : a.wfrag;
-  a.w_stride = desc->m * desc->d;
+  a.dw_stride = desc->m * desc->d;
+  const PadRows pr = pad_rows_of(desc, base + ws_bytes_of(desc, FLEX_PASS_BWD));
   for (int g = 0; g < G.n; ++g) {
-    const size_t woff = (size_t)g * G.m * desc->d;   // this group's frequency rows
-    a.W1 = W1 + woff;
-    a.W2 = W2 ? W2 + woff : nullptr;
+    if (!group_rows(desc, G, pr, g, W1, W2, (hipStream_t)stream, &a.W1, &a.W2, &a.w_stride, &a.fvalid))
+      return FLEX_ERR_HIP;
+    const size_t woff = (size_t)group_off(G, g) * desc->d;   // this group's frequency rows
     a.dW1 = dW1 + woff;
     a.dW2 = dW2 ? dW2 + woff : nullptr;
     a.acc = g > 0;

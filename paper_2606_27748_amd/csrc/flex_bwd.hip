@@ -35,7 +35,7 @@ namespace flex {
 // whole number of them: it spans the forward's 64-token chunks), not the
 // sweeps' 32; at d = 128 the double-buffered staging of 64 rows would not fit
 // in LDS.
-template <class T, int D, int FW, int NW, bool NS, bool WITH_S>
+template <class T, int D, int FW, int NW, bool NS, bool WITH_S, bool MASK = false>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   // 64-token chunks where the staging fits: at d <= 64, and at d = 128 on the
   // query-side-only pass (K and V are not staged there)
@@ -60,6 +60,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int fv = slice_valid<MASK, FW>(a.fvalid, w);
   const int cps = a.chunks_per_seg / (PCH / BWD_CHUNK);   // pre-pass chunks per segment
   const int c0 = seg * cps;
   const int c1 = min(c0 + cps, (a.N + SH::CH - 1) / SH::CH);
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 #pragma unroll
         for (int dt = 0; dt < SH::DVT; ++dt) vt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
         vt[SH::DVT] = ones;
-        feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk);
+        feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk, fv);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc)
 #pragma unroll
@@ -214,7 +215,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 #pragma unroll
         for (int dt = 0; dt < SH::DVT; ++dt) gt[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XDO), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
         gt[SH::DVT] = delta_rows<T>(GS, ks);
-        feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XQ, SCQ, ks, pq);
+        feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XQ, SCQ, ks, pq, fv);
 #pragma unroll
         for (int fc = 0; fc < SH::FC; ++fc)
 #pragma unroll
@@ -239,7 +240,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_prepass(BwdArgs a) {
 // ACC: add dK and dV to the values an earlier frequency group stored.  The
 // old values are loaded at the start of each chunk, ahead of the next chunk's
 // prefetch, so waiting for them never waits for that prefetch.
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC>
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC, bool MASK = false>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
@@ -289,6 +290,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int fv = slice_valid<MASK, FW>(a.fvalid, w);
   const int c0 = seg * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
   const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
@@ -453,7 +455,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft)
           store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16,
-                           features<T, SH::FT, NS>(p, ft, sc));
+                           features<T, SH::FT, NS>(p, ft, sc, fv));
       }
     }
     // phi(K) and its P2-derivative fragments
@@ -465,7 +467,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phk[ft][tt], psk[ft][tt]);
+      for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phk[ft][tt], psk[ft][tt], fv);
     }
     // intra-chunk M[i][j] = dO_i . V_j - delta_i and A[i][j] = phi(Q_i)/den_i . phi(K_j), i >= j
     Frag<T> mp[CAUSAL ? SH::KT : 1][SH::TT], ap[CAUSAL ? SH::KT : 1][SH::TT];
@@ -745,7 +747,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dkv(BwdArgs a) {
 // dW2 = (dW'1-dW'2)/2 because W'1 = (W1+W2)/2 and W'2 = (W1-W2)/2.
 // ---------------------------------------------------------------------------
 template <int NMAT>
-__global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int md4) {
+__global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int md4, int d) {
   // 256 elements (f, k) of one head per workgroup, 4 consecutive per thread;
   // the 4 waves split the list of partials (b, segment; each already the sum
   // of the query and key sides) round-robin and
@@ -796,9 +798,11 @@ __global__ __launch_bounds__(256) void k_bwd_reduce(BwdArgs a, int md4) {
       x[mat] = make_float4((p0.x + p1.x) + (p2.x + p3.x), (p0.y + p1.y) + (p2.y + p3.y),
                            (p0.z + p1.z) + (p2.z + p3.z), (p0.w + p1.w) + (p2.w + p3.w));
     }
-    float4* o1 = reinterpret_cast<float4*>(a.dW1 + (size_t)h * a.w_stride) + e4;
-    if (NMAT == 2) {
-      float4* o2 = reinterpret_cast<float4*>(a.dW2 + (size_t)h * a.w_stride) + e4;
+    float4* o1 = reinterpret_cast<float4*>(a.dW1 + (size_t)h * a.dw_stride) + e4;
+    if (4 * e4 / d >= a.fvalid) {
+      // a padding row of a last frequency group: no output row
+    } else if (NMAT == 2) {
+      float4* o2 = reinterpret_cast<float4*>(a.dW2 + (size_t)h * a.dw_stride) + e4;
       const float4 u = x[0], w = x[NMAT - 1];
       *o1 = make_float4(0.5f * (u.x + w.x), 0.5f * (u.y + w.y), 0.5f * (u.z + w.z), 0.5f * (u.w + w.w));
       *o2 = make_float4(0.5f * (u.x - w.x), 0.5f * (u.y - w.y), 0.5f * (u.z - w.z), 0.5f * (u.w - w.w));
@@ -836,6 +840,11 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   // pre-pass's query-side work itself and no pre-pass runs; the R' local
   // states it leaves feed the scan, or the dK/dV sweep's own suffix sum.
   const bool wr = a.fstate != nullptr;
+  // a padded frequency group (only the 64-frequency shape has one, and it runs
+  // first, so it never adds) takes the masking kernel variants
+  const bool masked = a.fvalid < SA::M;
+  constexpr bool CAN_MASK = SA::M == 64;
+  if (masked && (!CAN_MASK || a.acc)) return hipErrorInvalidValue;
   auto scan_r = [&]() -> hipError_t {
     if (causal && a.rfold) return hipSuccess;
     return launch_state_scan(a.fstate ? nullptr : a.sstate, a.rstate, a.BH, a.segments, 1, SA::STATE, causal, st,
@@ -843,10 +852,16 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   };
   if (!wr) {
     timing_mark(KC_BWD_PREPASS, st, true);
-    if (a.fstate)
-      k_bwd_prepass<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
-    else
-      k_bwd_prepass<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
+    if constexpr (CAN_MASK) {
+      if (masked) {
+        if (a.fstate) k_bwd_prepass<T, D, FWA, NWA, NS, false, true><<<grid, SA::NT, 0, st>>>(a);
+        else k_bwd_prepass<T, D, FWA, NWA, NS, true, true><<<grid, SA::NT, 0, st>>>(a);
+      }
+    }
+    if (!masked) {
+      if (a.fstate) k_bwd_prepass<T, D, FWA, NWA, NS, false><<<grid, SA::NT, 0, st>>>(a);
+      else k_bwd_prepass<T, D, FWA, NWA, NS, true><<<grid, SA::NT, 0, st>>>(a);
+    }
     timing_mark(KC_BWD_PREPASS, st, false);
     const hipError_t e = scan_r();
     if (e != hipSuccess) return e;
@@ -854,7 +869,7 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   timing_mark(KC_BWD_DQ, st, true);
   // a later frequency group adds into the earlier groups' outputs
   {
-    const hipError_t e = launch_bwd_dq<T, D, FWA, NWA, NS>(a, causal, a.acc != 0, wr, st);
+    const hipError_t e = launch_bwd_dq<T, D, FWA, NWA, NS>(a, causal, a.acc != 0, wr, masked, st);
     if (e != hipSuccess) return e;
   }
   timing_mark(KC_BWD_DQ, st, false);
@@ -868,6 +883,13 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
       k_bwd_dkv<T, D, FWB, NWB, NS, true, true><<<grid, SB::NT, 0, st>>>(a);
     else
       k_bwd_dkv<T, D, FWB, NWB, NS, false, true><<<grid, SB::NT, 0, st>>>(a);
+  } else if (masked) {
+    if constexpr (CAN_MASK) {
+      if (causal)
+        k_bwd_dkv<T, D, FWB, NWB, NS, true, false, true><<<grid, SB::NT, 0, st>>>(a);
+      else
+        k_bwd_dkv<T, D, FWB, NWB, NS, false, false, true><<<grid, SB::NT, 0, st>>>(a);
+    }
   } else {
     if (causal)
       k_bwd_dkv<T, D, FWB, NWB, NS, true, false><<<grid, SB::NT, 0, st>>>(a);
@@ -879,7 +901,7 @@ static hipError_t run_bwd_t(const BwdArgs& a, bool causal, hipStream_t st) {
   constexpr int MD4 = SA::M * D / 4;
   dim3 rgrid((MD4 + 63) / 64, a.H);
   timing_mark(KC_BWD_REDUCE, st, true);
-  k_bwd_reduce<NS ? 2 : 1><<<rgrid, 256, 0, st>>>(a, MD4);
+  k_bwd_reduce<NS ? 2 : 1><<<rgrid, 256, 0, st>>>(a, MD4, D);
   timing_mark(KC_BWD_REDUCE, st, false);
   return hipGetLastError();
 }

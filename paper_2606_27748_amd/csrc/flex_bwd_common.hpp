@@ -11,9 +11,10 @@ namespace flex {
 
 // Feature fragment (as in the forward) plus, for the nonstationary variant,
 // the fragment of d phi / d P2 up to sign: slots [s e sin P2 cos P1 | s e sin P2 sin P1].
+// fv: as in features (slice frequencies >= fv give zero fragments).
 template <class T, int FT, bool NS, class P>
 __device__ __forceinline__ void features_psi(const P (&p)[NS ? 2 * FT : FT], int ft, float scale,
-                                             Frag<T>& phi, Frag<T>& psi) {
+                                             Frag<T>& phi, Frag<T>& psi, int fv = FT * 16) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     float s1, c1;
@@ -30,6 +31,10 @@ __device__ __forceinline__ void features_psi(const P (&p)[NS ? 2 * FT : FT], int
       phi.set(i, c1 * scale);
       phi.set(4 + i, s1 * scale);
     }
+  }
+  if (fv < FT * 16) {
+    mask_features(phi, ft, fv);
+    if (NS) mask_features(psi, ft, fv);
   }
 }
 

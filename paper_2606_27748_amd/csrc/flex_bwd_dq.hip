@@ -15,7 +15,7 @@ namespace flex {
 // forward's key-side states are passed in, so no pre-pass runs): the per-token
 // 1/den and delta = dO . O, from the staging registers, written for the dK/dV
 // sweep, and the segment-local R'^T = sum [dO | -delta]^T-rows x phi(Q)/den.
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC, bool WR>
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, bool ACC, bool WR, bool MASK = false>
 __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SH;
   typedef typename Io<T>::type IO;
@@ -47,6 +47,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
   const WgCoord wc = wg_coord(a.segments, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int fv = slice_valid<MASK, FW>(a.fvalid, w);
   const int c0 = seg * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
   const IO* Q = static_cast<const IO*>(a.Q) + (size_t)bh * a.N * D;
@@ -206,7 +207,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
     // tokens: token-row fragments (k = tokens), no transpose
     Frag<T> pk[SH::KT][SH::FC];
 #pragma unroll
-    for (int ks = 0; ks < SH::KT; ++ks) feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk[ks]);
+    for (int ks = 0; ks < SH::KT; ++ks) feature_frags_rows<T, D, FW, NS, StX::LD>(fs, XK, SCK, ks, pk[ks], fv);
     // phi(Q)/den and its P2-derivative fragments (the 1/den of dphi(Q) is
     // carried by these: their products with dphi(Q) in the chain rule are the
     // same)
@@ -218,7 +219,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       const float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N) * GS[tt * 16 + r][0];
 #pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phq[ft][tt], psq[ft][tt]);
+      for (int ft = 0; ft < SH::FT; ++ft) features_psi<T, SH::FT, NS>(p, ft, sc, phq[ft][tt], psq[ft][tt], fv);
     }
     if constexpr (WR) {
       // R'^T += [dO | -delta]^T-rows x phi(Q)/den, with phi(Q)/den as [token]
@@ -411,31 +412,40 @@ __global__ __launch_bounds__(NW * WAVE) void k_bwd_dq(BwdArgs a) {
 // Launch of the dQ sweep for one shape: grouped_acc adds into an earlier
 // frequency group's dQ; wr does the pre-pass's query-side work
 // (with the forward's key-side states).
-template <class T, int D, int FW, int NW, bool NS, bool ACC>
+template <class T, int D, int FW, int NW, bool NS, bool ACC, bool MASK>
 static void launch_dq_acc(const BwdArgs& a, bool causal, bool wr, const dim3& grid, int nt, hipStream_t st) {
   if (wr) {
-    if (causal) k_bwd_dq<T, D, FW, NW, NS, true, ACC, true><<<grid, nt, 0, st>>>(a);
-    else k_bwd_dq<T, D, FW, NW, NS, false, ACC, true><<<grid, nt, 0, st>>>(a);
+    if (causal) k_bwd_dq<T, D, FW, NW, NS, true, ACC, true, MASK><<<grid, nt, 0, st>>>(a);
+    else k_bwd_dq<T, D, FW, NW, NS, false, ACC, true, MASK><<<grid, nt, 0, st>>>(a);
   } else {
-    if (causal) k_bwd_dq<T, D, FW, NW, NS, true, ACC, false><<<grid, nt, 0, st>>>(a);
-    else k_bwd_dq<T, D, FW, NW, NS, false, ACC, false><<<grid, nt, 0, st>>>(a);
+    if (causal) k_bwd_dq<T, D, FW, NW, NS, true, ACC, false, MASK><<<grid, nt, 0, st>>>(a);
+    else k_bwd_dq<T, D, FW, NW, NS, false, ACC, false, MASK><<<grid, nt, 0, st>>>(a);
   }
 }
 
 template <class T, int D, int FW, int NW, bool NS>
-hipError_t launch_bwd_dq(const BwdArgs& a, bool causal, bool grouped_acc, bool wr, hipStream_t st) {
+hipError_t launch_bwd_dq(const BwdArgs& a, bool causal, bool grouped_acc, bool wr, bool masked, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS, BWD_CHUNK> SA;
   const dim3 grid(a.segments * a.BH);
+  if (masked) {   // a padded group: the 64-frequency shape, never adding
+    if constexpr (FW * NW == 64) {
+      if (!grouped_acc) {
+        launch_dq_acc<T, D, FW, NW, NS, false, true>(a, causal, wr, grid, SA::NT, st);
+        return hipGetLastError();
+      }
+    }
+    return hipErrorInvalidValue;
+  }
   if (grouped_acc)
-    launch_dq_acc<T, D, FW, NW, NS, true>(a, causal, wr, grid, SA::NT, st);
+    launch_dq_acc<T, D, FW, NW, NS, true, false>(a, causal, wr, grid, SA::NT, st);
   else
-    launch_dq_acc<T, D, FW, NW, NS, false>(a, causal, wr, grid, SA::NT, st);
+    launch_dq_acc<T, D, FW, NW, NS, false, false>(a, causal, wr, grid, SA::NT, st);
   return hipGetLastError();
 }
 
 #define FLEX_DQ_SHAPE(T, D, FW, NW)                                                                  \
-  template hipError_t launch_bwd_dq<T, D, FW, NW, true>(const BwdArgs&, bool, bool, bool, hipStream_t); \
-  template hipError_t launch_bwd_dq<T, D, FW, NW, false>(const BwdArgs&, bool, bool, bool, hipStream_t);
+  template hipError_t launch_bwd_dq<T, D, FW, NW, true>(const BwdArgs&, bool, bool, bool, bool, hipStream_t); \
+  template hipError_t launch_bwd_dq<T, D, FW, NW, false>(const BwdArgs&, bool, bool, bool, bool, hipStream_t);
 FLEX_DQ_SHAPE(__bf16, 32, 16, 4)
 FLEX_DQ_SHAPE(__bf16, 64, 16, 4)
 FLEX_DQ_SHAPE(__bf16, 64, 16, 8)

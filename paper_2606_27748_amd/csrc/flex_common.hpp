@@ -465,11 +465,37 @@ __device__ __forceinline__ float cos_rev(double p) {
   return fmaf(-a, __builtin_amdgcn_sinf(rh), __builtin_amdgcn_cosf(rh));
 }
 
+// Frequencies of wave w's slice (FW frequencies from w FW) that exist when
+// the launch's group holds fvalid of its frequencies: the kernel variants
+// compiled for a padded group (MASK) mask the rest; the others keep every
+// feature, decided at compile time.
+template <bool MASK, int FW>
+__device__ __forceinline__ int slice_valid(int fvalid, int w) {
+  if constexpr (!MASK) return FW;
+  else return __builtin_amdgcn_readfirstlane(fvalid - w * FW);
+}
+
+// Zero the slots of an operand fragment of frequency tile ft (slots i and
+// 4 + i: slice frequency ft*16 + 4g + i) whose frequency is not below fv.
+template <class T>
+__device__ __forceinline__ void mask_features(Frag<T>& f, int ft, int fv) {
+  const int g = (threadIdx.x % WAVE) / 16;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (ft * 16 + 4 * g + i >= fv) { f.set(i, 0.0f); f.set(4 + i, 0.0f); }
+}
+
 // Feature epilogue for one frequency tile ft of one 16-token tile:
 // scale = s * e(x) (0 for rows that are not valid).  Returns the operand
 // fragment [cos-type features 4g..4g+3 | sin-type features 4g..4g+3].
+// fv: frequencies of the wave's slice that exist (the last frequency group of
+// an m that is not a multiple of the group width pads its slice with zero
+// rows of W, whose features must vanish, not be cos 0 = 1): the features of
+// slice frequencies ft*16 + 4g + i >= fv are zero.  The default keeps them all
+// and compiles to the unmasked code.
 template <class T, int FT, bool NS, class P>
-__device__ __forceinline__ Frag<T> features(const P (&p)[NS ? 2 * FT : FT], int ft, float scale) {
+__device__ __forceinline__ Frag<T> features(const P (&p)[NS ? 2 * FT : FT], int ft, float scale,
+                                            int fv = FT * 16) {
   Frag<T> f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -479,6 +505,7 @@ __device__ __forceinline__ Frag<T> features(const P (&p)[NS ? 2 * FT : FT], int 
     f.set(i, c1 * sc);
     f.set(4 + i, s1 * sc);
   }
+  if (fv < FT * 16) mask_features(f, ft, fv);
   return f;
 }
 

@@ -25,7 +25,9 @@ namespace flex {
 // ---------------------------------------------------------------------------
 // Segment-local state: S'_seg = sum over the segment's tokens of phi(K)[V;1]^T.
 // ---------------------------------------------------------------------------
-template <class T, int D, int FW, int NW, bool NS>
+// MASK: the variant for a padded frequency group (features of its padding
+// rows masked to zero), as in the sweeps.
+template <class T, int D, int FW, int NW, bool NS, bool MASK = false>
 __global__ __launch_bounds__(NW * WAVE) __attribute__((amdgpu_waves_per_eu(state_waves_per_eu(D, NS), state_waves_per_eu(D, NS))))
 void k_fwd_state(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
@@ -39,6 +41,7 @@ void k_fwd_state(FwdArgs a) {
   const WgCoord wc = wg_coord(a.pre_segs * a.sub, a.H, a.BH);   // seg: sub-segment
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE;
+  const int fv = slice_valid<MASK, FW>(a.fvalid, w);
   const int cps = a.chunks_per_seg / a.sub;
   const int c0 = seg * cps;
   const int c1 = min(c0 + cps, a.nchunks);
@@ -84,7 +87,7 @@ void k_fwd_state(FwdArgs a) {
 #pragma unroll
     for (int ks = 0; ks < SH::KT; ++ks) {
       Frag<T> pk[SH::FC];
-      feature_frags_rows<T, D, FW, NS, StK::LD>(fs, XK, SCK, ks, pk);
+      feature_frags_rows<T, D, FW, NS, StK::LD>(fs, XK, SCK, ks, pk, fv);
       Frag<T> vf[SH::DVT];
 #pragma unroll
       for (int dt = 0; dt < SH::DVT; ++dt) vf[dt] = lds_tr_frag<T>(reinterpret_cast<const T*>(XV), StV::LD, 32 * ks + 4 * g, 32 * ks + 16 + 4 * g, dt * 16);
@@ -159,7 +162,7 @@ __global__ __launch_bounds__(256) void k_state_scan(float* state0, float* state1
 // term covers j <= i within a chunk, earlier tokens enter through the carried
 // state).  Token contractions run in 32-token MFMA k-steps; a 16-token chunk
 // pads its k-step with zero rows (staged once, never written).
-template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG, bool ADD, int CH>
+template <class T, int D, int FW, int NW, bool NS, bool CAUSAL, int QG, bool ADD, int CH, bool MASK = false>
 __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS, CH> SH;
   typedef typename Io<T>::type IO;
@@ -188,6 +191,7 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
   const WgCoord wc = wg_coord(a.sweep_groups, a.H, a.BH);
   const int seg = wc.seg, bh = wc.bh, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  const int fv = slice_valid<MASK, FW>(a.fvalid, w);
   const int nch = (a.N + CH - 1) / CH;
   const int c0 = seg * a.sweep_cps;
   const int c1 = min(c0 + a.sweep_cps, nch);
@@ -293,13 +297,13 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
       project_tile_lds<T, D, FW, NS, StX::LD>(fs, XQ, SSQ, tt, p, ssq);
       float sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
-      for (int ft = 0; ft < SH::FT; ++ft) pq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
+      for (int ft = 0; ft < SH::FT; ++ft) pq[ft][tt] = features<T, SH::FT, NS>(p, ft, sc, fv);
       if (CAUSAL) {
         project_tile_lds<T, D, FW, NS, StX::LD>(fs, XK, SSK, tt, p, ssq);
         sc = row_scale(ssq, inv_c, a.s_const, tok0 + tt * 16 + r < a.N);
 #pragma unroll
         for (int ft = 0; ft < SH::FT; ++ft) {
-          pk[ft][tt] = features<T, SH::FT, NS>(p, ft, sc);
+          pk[ft][tt] = features<T, SH::FT, NS>(p, ft, sc, fv);
           store_frag_nm<T>(PT[w], LDP, tt * 16, (2 * ft) * 16, (2 * ft + 1) * 16, pk[ft][tt]);
         }
       }
@@ -432,7 +436,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     for (int fc = 0; fc < SH::FC; ++fc)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int f = a.state_f0 + w * FW + (fc / 2) * 16 + 4 * g + i;
+        const int fl = w * FW + (fc / 2) * 16 + 4 * g + i;   // row within the group
+        if (fl >= a.fvalid) continue;   // a padding row of a padded group
+        const int f = a.state_f0 + fl;
         const size_t row = (fc % 2) ? (size_t)a.state_m + f : (size_t)f;
 #pragma unroll
         for (int dt = 0; dt < SH::DVT; ++dt) so[row * SH::DV + dt * 16 + r] = S[fc][dt][i];
@@ -464,7 +470,7 @@ __device__ __forceinline__ void store4<float>(float* p, const float (&v)[4]) {
 // and each wave projects its tokens onto all m frequencies.  No partial sums
 // cross waves, so the only barrier per chunk is the staging one.
 // ---------------------------------------------------------------------------
-template <class T, int D, int M, bool NS>
+template <class T, int D, int M, bool NS, bool MASK = false>
 __global__ __launch_bounds__(4 * WAVE) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_fwd_readout(FwdArgs a) {
   constexpr int NWR = 4;                        // waves: one 16-token tile each
@@ -528,7 +534,7 @@ void k_fwd_readout(FwdArgs a) {
     for (int dt = 0; dt < DVT1; ++dt) acc[dt] = zero4();
 #pragma unroll
     for (int ft = 0; ft < FT; ++ft) {
-      const Frag<T> pq = features<T, FT, NS>(p, ft, sc);
+      const Frag<T> pq = features<T, FT, NS>(p, ft, sc, MASK ? a.fvalid : M);
 #pragma unroll
       for (int dt = 0; dt < DVT1; ++dt) mma(acc[dt], sf[dt][ft], pq);
     }
@@ -638,6 +644,29 @@ __global__ __launch_bounds__(256) void k_fwd_finish(FwdArgs a, int dv) {
   if (a.den && c4 == 0) a.den[row] = dn;
 }
 
+// ---------------------------------------------------------------------------
+// Frequency rows of a padded last group: dst[h][rows][d] holds the group's
+// rows_valid rows of W, then zero rows (their features are masked to zero).
+// One thread per 4 elements.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_pad_rows(const float* src, float* dst, int rows_valid, int rows, int d,
+                                                  int src_stride) {
+  const int h = blockIdx.y;
+  const int i4 = blockIdx.x * 256 + threadIdx.x;
+  if (4 * i4 >= rows * d) return;
+  const int row = 4 * i4 / d;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (row < rows_valid) v = *reinterpret_cast<const float4*>(src + (size_t)h * src_stride + 4 * i4);
+  *reinterpret_cast<float4*>(dst + ((size_t)h * rows) * d + 4 * i4) = v;
+}
+
+hipError_t launch_pad_rows(const float* src, float* dst, int H, int rows_valid, int rows, int d, int src_stride,
+                           hipStream_t st) {
+  if (d % 4 != 0) return hipErrorInvalidValue;
+  k_pad_rows<<<dim3((rows * d / 4 + 255) / 256, H), 256, 0, st>>>(src, dst, rows_valid, rows, d, src_stride);
+  return hipGetLastError();
+}
+
 hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st) {
   const size_t n = (size_t)a.BH * a.N * (dv / 4);
   const dim3 grid((unsigned)((n + 255) / 256));
@@ -653,13 +682,13 @@ hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st
 // ---------------------------------------------------------------------------
 // Causal sweep launch for one chunk length CH (token tiles per cross-wave
 // reduction round: fewer rounds where LDS allows).
-template <class T, int D, int FW, int NW, bool NS, bool ADD, int CH>
+template <class T, int D, int FW, int NW, bool NS, bool ADD, int CH, bool MASK>
 static void launch_causal_sweep(const FwdArgs& a, dim3 grid, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS, CH> SH;
   constexpr int TTc = CH / 16;
   constexpr int QG0 = (SH::DV >= 128) ? 1 : (NW >= 8 ? 2 : TTc);
   constexpr int QG = QG0 < TTc ? QG0 : TTc;
-  k_fwd_sweep<T, D, FW, NW, NS, true, QG, ADD, CH><<<grid, SH::NT, 0, st>>>(a);
+  k_fwd_sweep<T, D, FW, NW, NS, true, QG, ADD, CH, MASK><<<grid, SH::NT, 0, st>>>(a);
 }
 
 // The token-split readout serves bf16 shapes whose projection onto all m
@@ -669,24 +698,24 @@ struct ReadoutSplit {
   static constexpr bool value = IsBf16<T>::value && !NS && FW * NW == 64 && FW == 16 && D <= 64;
 };
 
-template <class T, int D, int FW, int NW, bool NS, bool ADD>
+template <class T, int D, int FW, int NW, bool NS, bool ADD, bool MASK>
 static void launch_sweep(const FwdArgs& a, bool causal, dim3 grid, hipStream_t st) {
   typedef Shape<T, D, FW, NW, NS> SH;
   if constexpr (!ADD && ReadoutSplit<T, D, FW, NW, NS>::value) {
     if (!causal && a.acc == 0) {   // it writes O itself, not a group's sums
-      k_fwd_readout<T, D, FW * NW, NS><<<grid, 4 * WAVE, 0, st>>>(a);
+      k_fwd_readout<T, D, FW * NW, NS, MASK><<<grid, 4 * WAVE, 0, st>>>(a);
       return;
     }
   }
   if (!causal) {
     // one token tile per round: the non-causal sweep then fits several workgroups per CU
-    k_fwd_sweep<T, D, FW, NW, NS, false, 1, ADD, CHUNK><<<grid, SH::NT, 0, st>>>(a);
+    k_fwd_sweep<T, D, FW, NW, NS, false, 1, ADD, CHUNK, MASK><<<grid, SH::NT, 0, st>>>(a);
   } else if (a.sweep_chunk == 16) {
-    launch_causal_sweep<T, D, FW, NW, NS, ADD, 16>(a, grid, st);
+    launch_causal_sweep<T, D, FW, NW, NS, ADD, 16, MASK>(a, grid, st);
   } else if (a.sweep_chunk == 32) {
-    launch_causal_sweep<T, D, FW, NW, NS, ADD, 32>(a, grid, st);
+    launch_causal_sweep<T, D, FW, NW, NS, ADD, 32, MASK>(a, grid, st);
   } else {
-    launch_causal_sweep<T, D, FW, NW, NS, ADD, 64>(a, grid, st);
+    launch_causal_sweep<T, D, FW, NW, NS, ADD, 64, MASK>(a, grid, st);
   }
 }
 
@@ -699,7 +728,19 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   // per chunk; the other forward kernels build theirs from W once
   if (D > 64) k_prep_freqs<T, D, FW, NW, NS><<<dim3(a.H, NW, 1), WAVE, 0, st>>>(a.W1, a.W2, a.wfrag, a.w_stride);
   timing_mark(KC_FWD_STATE, st, true);
-  if (pgrid.x > 0) k_fwd_state<T, D, FW, NW, NS><<<pgrid, SH::NT, 0, st>>>(a);
+  // a padded frequency group (only the 64-frequency shape has one, and it
+  // runs first, so it never adds) takes the masking kernel variants
+  const bool masked = a.fvalid < FW * NW;
+  constexpr bool CAN_MASK = FW * NW == 64;
+  if (masked && (!CAN_MASK || a.acc == 2)) return hipErrorInvalidValue;
+  if (pgrid.x > 0) {
+    if constexpr (CAN_MASK) {
+      if (masked) k_fwd_state<T, D, FW, NW, NS, true><<<pgrid, SH::NT, 0, st>>>(a);
+      else k_fwd_state<T, D, FW, NW, NS, false><<<pgrid, SH::NT, 0, st>>>(a);
+    } else {
+      k_fwd_state<T, D, FW, NW, NS, false><<<pgrid, SH::NT, 0, st>>>(a);
+    }
+  }
   timing_mark(KC_FWD_STATE, st, false);
   if (!a.fold) {
     const hipError_t e =
@@ -715,10 +756,13 @@ static hipError_t run_fwd_t(const FwdArgs& a, bool causal, hipStream_t st) {
   constexpr int FWS = (D == 64 && FW * NW == 128) ? 32 : FW;
   constexpr int NWS = FW * NW / FWS;
   // a later frequency group adds to the earlier groups' sums
-  if (a.acc == 2)
-    launch_sweep<T, D, FWS, NWS, NS, true>(a, causal, grid, st);
-  else
-    launch_sweep<T, D, FWS, NWS, NS, false>(a, causal, grid, st);
+  if (a.acc == 2) {
+    launch_sweep<T, D, FWS, NWS, NS, true, false>(a, causal, grid, st);
+  } else if (masked) {
+    if constexpr (CAN_MASK) launch_sweep<T, D, FWS, NWS, NS, false, true>(a, causal, grid, st);
+  } else {
+    launch_sweep<T, D, FWS, NWS, NS, false, false>(a, causal, grid, st);
+  }
   timing_mark(KC_FWD_SWEEP, st, false);
   return hipGetLastError();
 }

@@ -46,8 +46,11 @@ struct FwdArgs {
   // element stride between heads.  acc = 0 writes O (and den) directly; 1 and
   // 2 write / add the group's numerator and denominator into acc_num
   // [BH][N][dv] and acc_den [BH][N] (fp32), which k_fwd_finish divides.
+  // fvalid: rows of this group that are frequencies (the rest of the group's
+  // rows are zero padding whose features the kernels mask to zero).
   int w_stride;
   int acc;
+  int fvalid;
   float* acc_num;
   float* acc_den;
   // feature map of a second input in the same launch (grid.z = 2): X = K,
@@ -98,9 +101,13 @@ struct BwdArgs {
   float s_const;
   // Frequency groups: W1/W2 and dW1/dW2 point at this group's rows, w_stride
   // is the element stride between heads; acc = 1 adds dQ, dK, dV and dtau to
-  // the outputs (a later group), 0 writes them.
+  // the outputs (a later group), 0 writes them.  fvalid: as in FwdArgs; the
+  // reduce writes dW1/dW2 rows below it only, dw_stride elements apart per
+  // head (W1/W2 of a padded group are a copy with a stride of their own).
   int w_stride;
   int acc;
+  int fvalid;
+  int dw_stride;
 };
 
 // Event bracketing of one kernel class (see flex_timing_enable); no-ops unless
@@ -185,10 +192,15 @@ hipError_t launch_state_scan(float* state, float* state_rev, int BH, int P, int 
 hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_only, hipStream_t st);
 // O = acc_num / acc_den (io dtype), den = acc_den, after the last frequency group.
 hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st);
+// dst[h][rows][d] = the first rows_valid rows of src[h] (src_stride elements
+// apart per head), zero after them: the frequency rows of a padded last group.
+hipError_t launch_pad_rows(const float* src, float* dst, int H, int rows_valid, int rows, int d, int src_stride,
+                           hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);
 // The dQ sweep of one shape (flex_bwd_dq.hip): grouped_acc adds into an
-// earlier frequency group's dQ; wr also does the pre-pass's query-side work.
+// earlier frequency group's dQ; wr also does the pre-pass's query-side work;
+// masked takes the variant for a padded frequency group.
 template <class T, int D, int FW, int NW, bool NS>
-hipError_t launch_bwd_dq(const BwdArgs& a, bool causal, bool grouped_acc, bool wr, hipStream_t st);
+hipError_t launch_bwd_dq(const BwdArgs& a, bool causal, bool grouped_acc, bool wr, bool masked, hipStream_t st);
 
 }  // namespace flex

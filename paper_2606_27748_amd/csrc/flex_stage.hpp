@@ -272,11 +272,12 @@ __device__ __forceinline__ void project_rows_lds(const FreqSlice<T, D, FW, NS>& 
 // (sin-type) have cols = the feature (lane % 16) and k = tokens in the order
 // of pair_tiles / lds_tok_frag.  sc[t] is the per-token scale (0 for tokens
 // past the end).  Used where a feature map only enters contractions over
-// tokens (state sums), which then need no transpose through LDS.
+// tokens (state sums), which then need no transpose through LDS.  fv: as in
+// features (slice frequencies ft*16 + lane%16 >= fv give zero features).
 template <class T, int D, int FW, bool NS, int LD>
 __device__ __forceinline__ void feature_frags_rows(const FreqSlice<T, D, FW, NS>& fs,
                                                    const typename Io<T>::type* X, const float* sc,
-                                                   int ks, Frag<T> (&out)[2 * (FW / 16)]) {
+                                                   int ks, Frag<T> (&out)[2 * (FW / 16)], int fv = FW) {
   typedef FreqSlice<T, D, FW, NS> FS;
   constexpr int FT = FW / 16;
   const int g = (threadIdx.x % WAVE) / 16;
@@ -303,6 +304,11 @@ __device__ __forceinline__ void feature_frags_rows(const FreqSlice<T, D, FW, NS>
   for (int ft = 0; ft < FT; ++ft) {
     out[2 * ft] = pair_tiles<T>(fc[0][ft], fc[1][ft]);
     out[2 * ft + 1] = pair_tiles<T>(fsn[0][ft], fsn[1][ft]);
+  }
+  if (fv < FW) {   // this lane's frequency is slice frequency ft*16 + lane % 16
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft)
+      if (ft * 16 + (int)(threadIdx.x % 16) >= fv) { out[2 * ft].zero(); out[2 * ft + 1].zero(); }
   }
 }
 

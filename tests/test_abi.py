@@ -68,17 +68,29 @@ def test_workspace_size():
 @pytest.mark.parametrize("io,d,m,ok", [
     ("bf16", 32, 128, True), ("bf16", 32, 256, True), ("bf16", 64, 192, True), ("bf16", 64, 256, True),
     ("bf16", 128, 64, True), ("bf16", 128, 192, True), ("f32", 32, 256, True),
-    ("bf16", 64, 320, False), ("bf16", 64, 96, False), ("bf16", 64, 16, False), ("f32", 64, 64, False),
+    ("bf16", 64, 96, True), ("bf16", 64, 16, True), ("bf16", 128, 208, True), ("f32", 32, 48, True),
+    ("bf16", 64, 320, False), ("bf16", 64, 40, False), ("bf16", 64, 0, False), ("f32", 64, 64, False),
 ])
 def test_attention_shape_set(io, d, m, ok):
     """The attention passes take d in {32, 64, 128} (fp32: 32) and m a multiple
-    of 64 up to 256 (frequency groups of 64 where no one kernel covers the
-    shape); the standalone feature map keeps its own kernels' shapes."""
-    want = F.FLEX_OK if ok else F.FLEX_ERR_UNSUPPORTED
+    of 16 up to 256 (frequency groups where no one kernel covers the shape, the
+    last one padded); the standalone feature map keeps its own kernels' shapes."""
+    want = F.FLEX_OK if ok else (F.FLEX_ERR_INVALID_ARG if m <= 0 else F.FLEX_ERR_UNSUPPORTED)
     dd = F.make_desc(1, 2, 100, d, m, "nonstationary", True, io)
     assert _ws(dd)[0] == want and _ws(dd, F.FLEX_PASS_BWD)[0] == want
     fm = (d, m) in ((32, 64), (64, 64), (64, 128), (128, 256)) and (io == "bf16" or (d, m) == (32, 64))
-    assert _ws(dd, F.FLEX_PASS_FEATURE_MAP)[0] == (F.FLEX_OK if fm else F.FLEX_ERR_UNSUPPORTED)
+    if m > 0:
+        assert _ws(dd, F.FLEX_PASS_FEATURE_MAP)[0] == (F.FLEX_OK if fm else F.FLEX_ERR_UNSUPPORTED)
+
+
+def test_padded_group_workspace():
+    """A last frequency group that 64 does not fill adds its zero-padded rows
+    of W1 and W2 to both workspaces."""
+    full = F.make_desc(1, 4, 1000, 64, 64, "nonstationary", True, "bf16")
+    part = F.make_desc(1, 4, 1000, 64, 48, "nonstationary", True, "bf16")
+    pad = 2 * 4 * 64 * 64 * 4
+    for p in (F.FLEX_PASS_FWD, F.FLEX_PASS_BWD):
+        assert _ws(part, p)[1] == _ws(full, p)[1] + pad
 
 
 def test_awd_workspace_size():
@@ -104,7 +116,7 @@ def test_awd_workspace_size():
     ("chunk", 128, F.FLEX_ERR_UNSUPPORTED), ("chunk", 8, F.FLEX_ERR_UNSUPPORTED),
     ("chunk", -16, F.FLEX_ERR_INVALID_ARG), ("chunk", 16, F.FLEX_OK), ("chunk", 32, F.FLEX_OK),
     ("chunk", 64, F.FLEX_OK),
-    ("d", 48, F.FLEX_ERR_UNSUPPORTED), ("m", 96, F.FLEX_ERR_UNSUPPORTED),
+    ("d", 48, F.FLEX_ERR_UNSUPPORTED), ("m", 100, F.FLEX_ERR_UNSUPPORTED), ("m", 96, F.FLEX_OK),
     ("dv", 32, F.FLEX_ERR_UNSUPPORTED), ("grad_dtype", 1, F.FLEX_ERR_UNSUPPORTED),
 ])
 def test_descriptor_validation(field, value, status):

@@ -17,8 +17,11 @@ from tests.parity import check_grads, check_grad_rows, dv_row_scale, dtau_scale,
 pytestmark = pytest.mark.gpu
 
 SHAPES = [("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256),
-          # frequency groups of 64 at the other shapes
-          ("f32", 32, 128), ("bf16", 32, 192), ("bf16", 64, 256), ("bf16", 128, 64), ("bf16", 128, 128)]
+          # frequency groups at the other shapes, some with a padded last group
+          # (bf16 from m = 48: below that, rounding the features to bf16 alone
+          # puts the gradients at the 2e-2 bar)
+          ("f32", 32, 128), ("bf16", 32, 192), ("bf16", 64, 256), ("bf16", 128, 64), ("bf16", 128, 128),
+          ("f32", 32, 16), ("bf16", 64, 48), ("bf16", 128, 80), ("f32", 32, 96)]
 
 
 @pytest.fixture(scope="module")

@@ -21,7 +21,9 @@ SHAPES = [  # (io, d, m)
     ("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256),
 ]
 # attention shapes that run as frequency groups of 64 (besides d = 128, m = 256)
-GROUP_SHAPES = [("f32", 32, 128), ("bf16", 32, 192), ("bf16", 64, 256), ("bf16", 128, 64), ("bf16", 128, 128)]
+GROUP_SHAPES = [("f32", 32, 128), ("bf16", 32, 192), ("bf16", 64, 256), ("bf16", 128, 64), ("bf16", 128, 128),
+                # a last group that 64 does not fill (zero-padded rows, masked features)
+                ("bf16", 32, 16), ("bf16", 64, 48), ("bf16", 128, 80), ("f32", 32, 96)]
 
 
 @pytest.fixture(scope="module")
