@@ -50,8 +50,8 @@
  *     forward workspace then holds an fp32 numerator/denominator buffer).
  *     With FLEX_BF16 and m < 48 the gradients' relative error can exceed 2e-2:
  *     rounding the features to bf16 alone costs 1.5-2.3% at m = 16.
- *     flex_feature_map takes (d, m) = (32, 64), (64, 64), (64, 128),
- *     (128, 256) with FLEX_BF16 and (32, 64) with FLEX_F32.
+ *     flex_feature_map takes the same d and m (it runs in slices of 64, 128
+ *     or 256 frequencies by d, the last one partly filled).
  *   - io_dtype FLEX_F32 computes every contraction in fp32 (MFMA f32);
  *     FLEX_BF16 reads bf16 inputs, projects with a two-term bf16 split of the
  *     frequencies and contracts bf16 features with fp32 accumulation (the

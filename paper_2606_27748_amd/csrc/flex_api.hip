@@ -36,13 +36,18 @@ bool shape_supported(const flex_desc* d) {
   return d->d == 32;
 }
 
-// Shapes of the standalone feature map (one kernel each).
+// Shapes of the standalone feature map: the attention's d and m (it ignores
+// dv).  It runs in slices of the frequency count of its kernel for d
+// (fmap_slice_m), the last one partly filled when that does not divide m.
 bool fmap_shape_supported(const flex_desc* d) {
-  const bool bf = d->io_dtype == FLEX_BF16;
-  if (d->d == 32 && d->m == 64) return true;
-  if (d->d == 64 && (d->m == 64 || d->m == 128)) return bf;
-  if (d->d == 128 && d->m == 256) return bf;
-  return false;
+  if (d->m % 16 != 0 || d->m > 256) return false;
+  if (d->io_dtype == FLEX_BF16) return d->d == 32 || d->d == 64 || d->d == 128;
+  return d->d == 32;
+}
+int fmap_slice_m(const flex_desc* d) {
+  if (d->d == 128) return 256;
+  if (d->d == 64) return d->m <= 64 ? 64 : 128;
+  return 64;
 }
 
 // 0 = ok, else a flex_status: the descriptor's fields, without the shape list
@@ -537,6 +542,8 @@ int32_t flex_awd_loss(const flex_desc* desc, const void* Q, const void* K, const
   f.nchunks = nchunks_of(desc); f.segments = 1; f.chunks_per_seg = fmap_chunks_per_wg(desc); f.sub = 1;
   f.sweep_groups = 1; f.sweep_cps = f.nchunks;
   f.s_const = s_const_of(desc);
+  f.w_stride = desc->m * desc->d;
+  f.fvalid = desc->m; f.state_m = desc->m; f.state_f0 = 0;   // all frequencies in one launch
   const KernelShape ks = kshape(desc);
   f.Q = Q; f.O = base + L.phq;   // both matrices in one launch
   f.K = K; f.O2 = base + L.phk;
@@ -644,13 +651,25 @@ int32_t flex_feature_map(const flex_desc* desc, const void* X, const float* W1, 
     return FLEX_ERR_INVALID_ARG;
   FwdArgs a;
   memset(&a, 0, sizeof(a));
-  a.Q = X; a.W1 = W1; a.W2 = W2; a.tau = tau; a.O = Phi;
+  a.Q = X; a.tau = tau; a.O = Phi;
   a.BH = desc->B * desc->H; a.H = desc->H; a.N = desc->N;
   a.nchunks = nchunks_of(desc); a.segments = 1; a.chunks_per_seg = fmap_chunks_per_wg(desc); a.sub = 1;
   a.sweep_groups = 1; a.sweep_cps = a.nchunks;
   a.s_const = s_const_of(desc);
-  const hipError_t e = launch_fwd(a, kshape(desc), true, (hipStream_t)stream);
-  return e == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
+  a.w_stride = desc->m * desc->d;
+  a.state_m = desc->m;
+  // slices of the kernel's frequency count; a last slice it does not fill reads
+  // only its own rows of W and writes only their columns
+  KernelShape ks = kshape(desc);
+  ks.m = fmap_slice_m(desc);
+  for (int f0 = 0; f0 < desc->m; f0 += ks.m) {
+    a.W1 = W1 + (size_t)f0 * desc->d;
+    a.W2 = W2 ? W2 + (size_t)f0 * desc->d : nullptr;
+    a.state_f0 = f0;
+    a.fvalid = desc->m - f0 < ks.m ? desc->m - f0 : ks.m;
+    if (launch_fwd(a, ks, true, (hipStream_t)stream) != hipSuccess) return FLEX_ERR_HIP;
+  }
+  return FLEX_OK;
 }
 
 int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, const void* V,

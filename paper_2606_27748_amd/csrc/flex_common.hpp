@@ -182,29 +182,37 @@ struct FreqSlice {
   static constexpr int NSPLIT = IsBf16<T>::value ? 2 : 1;
   Frag<T> w[NSPLIT][PR][KD];
 
-  // W1, W2: [m, d] fp32 rows of this head.
-  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
+  // W1, W2: [m, d] fp32 rows of this head.  ROWS: rows f >= rows (when
+  // given) are not read and load as zero frequencies.
+  template <bool ROWS = false>
+  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0, int rows = 0) {
     const int l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
 #pragma unroll
     for (int pr = 0; pr < PR; ++pr) {
       const int f = f0 + (pr % FT) * 16 + r;
       const bool second = pr >= FT;
+      const bool in = !ROWS || f < rows;
+      const int fr = in ? f : 0;
 #pragma unroll
       for (int ks = 0; ks < KD; ++ks) {
         const int c0 = ks * 32 + 8 * g;
-        const float* a = W1 + (size_t)f * D + c0;
+        const float* a = W1 + (size_t)fr * D + c0;
         float x[8];
         float4 a0 = *reinterpret_cast<const float4*>(a);
         float4 a1 = *reinterpret_cast<const float4*>(a + 4);
         x[0] = a0.x; x[1] = a0.y; x[2] = a0.z; x[3] = a0.w;
         x[4] = a1.x; x[5] = a1.y; x[6] = a1.z; x[7] = a1.w;
         if (NS) {
-          const float* b = W2 + (size_t)f * D + c0;
+          const float* b = W2 + (size_t)fr * D + c0;
           float4 b0 = *reinterpret_cast<const float4*>(b);
           float4 b1 = *reinterpret_cast<const float4*>(b + 4);
           float y[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
           for (int j = 0; j < 8; ++j) x[j] = second ? 0.5f * (x[j] - y[j]) : 0.5f * (x[j] + y[j]);
+        }
+        if (!in) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) x[j] = 0.0f;
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -269,7 +277,8 @@ struct FreqSlice<float, D, FW, NS> {
   double wt[PR][KS];
   double wr[PR][KS];
 
-  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0) {
+  template <bool ROWS = false>
+  __device__ void load(const float* __restrict__ W1, const float* __restrict__ W2, int f0, int rows = 0) {
     constexpr double INV_2PI_D = 0.15915494309189535;
     const int l = threadIdx.x % WAVE, rho = l % 16, g = l / 16;
 #pragma unroll
@@ -282,11 +291,14 @@ struct FreqSlice<float, D, FW, NS> {
 #pragma unroll
         for (int v = 0; v < 2; ++v) {
           const int f = f0 + ft * 16 + (v == 0 ? f64_tile_row(rho) : rho);
-          double w = W1[(size_t)f * D + k];
+          const bool in = !ROWS || f < rows;
+          const int fr = in ? f : 0;
+          double w = W1[(size_t)fr * D + k];
           if (NS) {
-            const double w2 = W2[(size_t)f * D + k];
+            const double w2 = W2[(size_t)fr * D + k];
             w = second ? 0.5 * (w - w2) : 0.5 * (w + w2);
           }
+          if (!in) w = 0.0;
           w *= INV_2PI_D;
           if (v == 0) wt[pr][ks] = w; else wr[pr][ks] = w;
         }

@@ -567,23 +567,28 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
   typedef Shape<T, D, FW, NW, NS> SH;
   typedef typename Io<T>::type IO;
   typedef RowStage<IO, D, SH::NT> StX;
-  constexpr int F = 2 * SH::M;                 // features per row
+  constexpr int F = 2 * SH::M;                 // features per staged row
   constexpr int VEC = 16 / (int)sizeof(IO);    // elements per 16-byte vector
   constexpr int LDF = F + VEC;                 // row stride of the staged features
-  constexpr int NVO = CHUNK * F / VEC;         // output vectors per chunk
   __shared__ __attribute__((aligned(16))) IO XL[StX::LDS_ELEMS];
   __shared__ typename StX::Ssq SSQ[CHUNK];
   __shared__ __attribute__((aligned(16))) IO PH[CHUNK * LDF];
   const int bh = blockIdx.y, h = bh % a.H;
   const int w = threadIdx.x / WAVE, l = threadIdx.x % WAVE, r = l % 16, g = l / 16;
+  // this launch covers frequencies [state_f0, state_f0 + fvalid) of state_m
+  // (fvalid <= M, a multiple of 16): their cos and sin columns of rows of
+  // 2 state_m features
+  const int fv = a.fvalid, mo = a.state_m, f0o = a.state_f0;
+  const int vrow = 2 * fv / VEC;               // output vectors per row
+  const int nvo = CHUNK * vrow;
   const IO* X = static_cast<const IO*>(blockIdx.z ? a.K : a.Q) + (size_t)bh * a.N * D;
-  IO* Phi = static_cast<IO*>(blockIdx.z ? a.O2 : a.O) + (size_t)bh * a.N * F;
+  IO* Phi = static_cast<IO*>(blockIdx.z ? a.O2 : a.O) + (size_t)bh * a.N * 2 * mo;
   const int c0 = blockIdx.x * a.chunks_per_seg;
   const int c1 = min(c0 + a.chunks_per_seg, a.nchunks);
   StX sx;
   if (c0 < c1) sx.fetch(X, c0 * CHUNK, a.N);
-  FreqSlice<T, D, FW, NS> fs;
-  fs.load(a.W1 + (size_t)h * SH::M * D, NS ? a.W2 + (size_t)h * SH::M * D : nullptr, w * FW);
+  FreqSlice<T, D, FW, NS> fs;   // frequencies past fvalid load as zero rows (their columns are not written)
+  fs.template load<true>(a.W1 + (size_t)h * a.w_stride, NS ? a.W2 + (size_t)h * a.w_stride : nullptr, w * FW, fv);
   const auto inv_c = inv_c_of<T>(a.tau[h]);
   for (int c = c0; c < c1; ++c) {
     const int tok0 = c * CHUNK;
@@ -610,13 +615,12 @@ __global__ __launch_bounds__(NW * WAVE) void k_feature_map(FwdArgs a) {
       }
     }
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < (NVO + SH::NT - 1) / SH::NT; ++i) {
-      const int v = threadIdx.x + i * SH::NT;
-      const int t = v / (F / VEC), cv = v % (F / VEC);
-      if (v < NVO && tok0 + t < a.N)
-        *reinterpret_cast<uint4*>(Phi + (size_t)(tok0 + t) * F + cv * VEC) =
-            *reinterpret_cast<const uint4*>(PH + t * LDF + cv * VEC);
+    for (int v = threadIdx.x; v < nvo; v += SH::NT) {
+      const int t = v / vrow, j = v % vrow;
+      const int part = j / (fv / VEC), cv = j % (fv / VEC);   // cos block, then sin block
+      if (tok0 + t < a.N)
+        *reinterpret_cast<uint4*>(Phi + (size_t)(tok0 + t) * 2 * mo + part * mo + f0o + cv * VEC) =
+            *reinterpret_cast<const uint4*>(PH + t * LDF + part * SH::M + cv * VEC);
     }
   }
 }

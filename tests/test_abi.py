@@ -72,15 +72,14 @@ def test_workspace_size():
     ("bf16", 64, 320, False), ("bf16", 64, 40, False), ("bf16", 64, 0, False), ("f32", 64, 64, False),
 ])
 def test_attention_shape_set(io, d, m, ok):
-    """The attention passes take d in {32, 64, 128} (fp32: 32) and m a multiple
-    of 16 up to 256 (frequency groups where no one kernel covers the shape, the
-    last one padded); the standalone feature map keeps its own kernels' shapes."""
+    """The attention passes and the standalone feature map take d in
+    {32, 64, 128} (fp32: 32) and m a multiple of 16 up to 256 (frequency groups
+    or slices where no one kernel covers the shape)."""
     want = F.FLEX_OK if ok else (F.FLEX_ERR_INVALID_ARG if m <= 0 else F.FLEX_ERR_UNSUPPORTED)
     dd = F.make_desc(1, 2, 100, d, m, "nonstationary", True, io)
     assert _ws(dd)[0] == want and _ws(dd, F.FLEX_PASS_BWD)[0] == want
-    fm = (d, m) in ((32, 64), (64, 64), (64, 128), (128, 256)) and (io == "bf16" or (d, m) == (32, 64))
     if m > 0:
-        assert _ws(dd, F.FLEX_PASS_FEATURE_MAP)[0] == (F.FLEX_OK if fm else F.FLEX_ERR_UNSUPPORTED)
+        assert _ws(dd, F.FLEX_PASS_FEATURE_MAP)[0] == (F.FLEX_OK if ok else F.FLEX_ERR_UNSUPPORTED)
 
 
 def test_padded_group_workspace():

@@ -47,7 +47,7 @@ def oracle_fwd(x, wl):
     return O, den, kap, abs_scales(x, wl)
 
 
-@pytest.mark.parametrize("io,d,m", SHAPES)
+@pytest.mark.parametrize("io,d,m", SHAPES + GROUP_SHAPES)
 @pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
 def test_feature_map(F, io, d, m, variant):
     wl, x = small(io, d, m, variant, False, N=131)
