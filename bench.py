@@ -344,6 +344,30 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
     torch.cuda.synchronize()
     ms_step_noev = (time.perf_counter() - t2) * 1e3 / steps
 
+    # the step captured once in a HIP graph and replayed K times (outside the
+    # contract's region: the library launches only kernels on the caller's
+    # stream, so the whole step captures)
+    try:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(3):
+            graph.replay()
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        for _ in range(steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        ms_step_graph = (time.perf_counter() - t3) * 1e3 / steps
+    except RuntimeError as e:
+        ms_step_graph = f"capture failed: {e}"
+
     # the class's time per step (several launches when the shape runs as
     # frequency groups) against its algorithmic work per step
     per_step = max(k_n // steps, 1)
@@ -375,6 +399,7 @@ def measure(wl, steps, warmup, want_cpu, cpu_slices, profile_only=False):
            "roofline": roof}
     out["step_timing"] = {"warm": step_stats(step, 20, False), "cold": step_stats(step, 20, True),
                           "flush_bytes": FLUSH_BYTES, "ms_per_step_no_events": ms_step_noev,
+                          "ms_per_step_graph": ms_step_graph,
                           "note": "value and ms_per_step: the contract's K back-to-back steps, warm "
                                   "(a step's inputs, outputs and workspaces stay in the 256 MB "
                                   "last-level cache where they fit); cold: single steps with a "
