@@ -72,9 +72,16 @@ __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 __device__ __forceinline__ void mma(f32x4& c, const Frag<__bf16>& a, const Frag<__bf16>& b) {
   c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, c, 0, 0, 0);
 }
+// One 32-long k-step as eight k=4 MFMAs chained into a fresh accumulator,
+// then one add into c.  Chaining straight into c would round a long-lived
+// accumulator (a carried state) once per 4 tokens instead of once per 32,
+// and over a sequential sweep of a few thousand tokens that rounding grows
+// to the 1e-4 scale in the gradients.
 __device__ __forceinline__ void mma(f32x4& c, const Frag<float>& a, const Frag<float>& b) {
+  f32x4 t = zero4();
 #pragma unroll
-  for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[j], b.v[j], c, 0, 0, 0);
+  for (int j = 0; j < 8; ++j) t = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[j], b.v[j], t, 0, 0, 0);
+  c += t;
 }
 
 template <class T> struct IsBf16 { static constexpr bool value = false; };

@@ -17,7 +17,7 @@ from tests.parity import check_grads, check_grad_rows, dv_row_scale, dtau_scale,
 pytestmark = pytest.mark.gpu
 
 SHAPES = [("f32", 32, 64), ("bf16", 32, 64), ("bf16", 64, 64), ("bf16", 64, 128), ("bf16", 128, 256),
-          # frequency groups at the other shapes, some with a padded last group
+          # frequency groups at the other shapes, some with a padded first group
           # (bf16 from m = 48: below that, rounding the features to bf16 alone
           # puts the gradients at the 2e-2 bar)
           ("f32", 32, 128), ("bf16", 32, 192), ("bf16", 64, 256), ("bf16", 128, 64), ("bf16", 128, 128),
@@ -101,6 +101,21 @@ def test_backward_segments(F, segments, causal, reuse):
     got = gpu_fwd_bwd(F, wl, x, segments=segments, reuse=reuse)
     ref, sc = oracle_bwd(wl, x)
     check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
+
+
+@pytest.mark.parametrize("segments", [1, 2])
+@pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
+def test_backward_f32_long_sweep(F, segments, variant):
+    """fp32, 2048 tokens in one or two sequential sweeps: the carried states
+    take ~1000 MFMA k-steps each, rounded once per 32 tokens.  (With a
+    rounding per 4-token MFMA, dQ reached 1.1e-4 here, over the 1e-4 bar.)"""
+    wl = W.Workload("f32long", 1, 3, 2048, 32, 64, variant, True, "f32", True, 1062)
+    x = W.generate(wl)
+    kap = masked_inputs(wl, x)
+    got = gpu_fwd_bwd(F, wl, x, segments=segments)
+    ref, sc = oracle_bwd(wl, x)
+    check_grads("f32", got, ref, names_of(wl), sc)
     check_rows(wl, x, got, ref, kap)
 
 
