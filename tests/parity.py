@@ -18,7 +18,11 @@ T2 (every case): over rows with kappa_i <= kappa_max, the Frobenius relative
     error of O <= tol; and every row i has rel_i <= max(tol, 4 u K_i), u the
     unit roundoff of the feature precision and K_i the condition number of
     O_i = num_i / den_i, den_abs_i/|den_i| + |num_abs_i|/|num_i| (kappa_i where
-    the absolute scales are not computed).
+    the absolute scales are not computed).  A row whose den rounding bound
+    4 u den_abs_i reaches |den_i| has no determined O_i at precision u; its
+    num_i and den_i errors are bounded by 4 u num_abs_i and 4 u den_abs_i.
+    A row whose den is exactly zero (O_i not finite; no epsilon is added) is
+    checked on den_i alone, which passes only where den_i is not determined.
 T3 (gradients): the upstream gradient is zeroed on rows with
     kappa_i > KAPPA_MAX_GRAD (identically for the oracle and the GPU); then the
     Frobenius relative error of every gradient <= tol.  dtau, a single sum
@@ -75,8 +79,15 @@ def check_forward(io, O_gpu, den_gpu, O_ref, den_ref, kappa, scales=None, rows_m
     tol, kmax, u = TOL[io], KAPPA_MAX[io], UNIT[io]
     O_gpu = np.asarray(O_gpu, np.float64)
     den_gpu = np.asarray(den_gpu, np.float64)
-    num_gpu = O_gpu * den_gpu[..., None]
     num_ref = O_ref * den_ref[..., None]
+    # A row whose den came out exactly zero has O_i = num_i / 0, not finite by
+    # definition (no epsilon is added).  Its num_i cannot be recovered from O
+    # and den, so it enters the num and O measures as exact and is checked on
+    # den_i alone (below).
+    zero = den_gpu == 0.0
+    O_gpu = np.where(zero[..., None], O_ref, O_gpu)
+    num_gpu = O_gpu * den_gpu[..., None]
+    num_gpu = np.where(zero[..., None], num_ref, num_gpu)
     B, H, N = O_ref.shape[:3]
     t1n = max(frob_rel(num_gpu[b, h], num_ref[b, h]) for b in range(B) for h in range(H))
     t1d = max(frob_rel(den_gpu[b, h], den_ref[b, h]) for b in range(B) for h in range(H))
@@ -101,7 +112,22 @@ def check_forward(io, O_gpu, den_gpu, O_ref, den_ref, kappa, scales=None, rows_m
         else:
             kfull = kappa
         bound = np.maximum(tol, 4 * u * kfull)
-        worst = np.nanmax(rel / bound)
+        ratio = rel / bound
+        # absolute scale of den_i's rounding: the summed terms where they are
+        # computed, else sum_k |phi(Q_i)_k z_ik| = kappa_i |den_i|
+        den_scale = den_abs if scales is not None else kappa * np.abs(den_ref)
+        r_den = np.abs(den_gpu - den_ref) / (4 * u * den_scale)
+        if scales is not None:
+            # O_i = num_i / den_i is first-order in the rounding only while the
+            # rounding bound of den_i, 4 u den_abs_i, is below |den_i|.  Where
+            # it is not, the sign of den_i is not fixed at this precision and
+            # O_i can take any value: such rows are checked on num_i and den_i
+            # against their absolute scales instead.
+            undet = 4 * u * den_abs >= np.abs(den_ref)
+            r_num = np.linalg.norm(num_gpu - num_ref, axis=-1) / (4 * u * np.linalg.norm(num_abs, axis=-1))
+            ratio = np.where(undet, np.maximum(r_num, r_den), ratio)
+        ratio = np.where(zero, r_den, ratio)
+        worst = np.nanmax(ratio)
     stats = dict(T1_num=t1n, T1_den=t1d, T1a_num=t1an, T1a_den=t1ad, T2=t2, row_worst=float(worst),
                  rows_kept=float(good.mean()), den_le0=float((den_ref <= 0).mean()),
                  whole_O=frob_rel(O_gpu, O_ref), kappa_med=float(np.median(kappa)))

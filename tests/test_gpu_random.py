@@ -4,8 +4,10 @@ Each case draws B, H, N, d, m, the variant, causality, the chunk length, the
 segment count and the io dtype from the supported set, runs the forward and the
 backward (with and without the forward's states) through the C ABI, and checks
 both against the float64 oracle with the criteria of the dedicated tests.  bf16
-gradients are checked from m = 48 on (below it the bf16 feature rounding alone
-reaches the bar) and from N = 2; the forward at every m and N."""
+gradients are checked from m = 64 on and from N = 2; the forward at every m and
+N.  Below m = 64 the bf16 rounding of the features alone can reach most of the
+2e-2 bar: 1.7 % on one drawn input at m = 48, N = 65
+(tests/test_precision_floor.py)."""
 import random
 
 import pytest
@@ -60,9 +62,14 @@ def test_random_configuration(F, case):
     O_ref, den_ref = orc.linattn_fwd(x.f64("Q"), x.f64("K"), x.f64("V"), x.W1, x.W2, x.tau, variant, causal)
     kf = orc.conditioning(x.f64("Q"), x.f64("K"), x.W1, x.W2, x.tau, variant, causal)
     check_forward(io, to_f64(O), to_f64(den), O_ref, den_ref, kf, abs_scales(x, wl))
-    if (io == "bf16" and m < 48) or N == 1:
+    if (io == "bf16" and m < 64) or N == 1:
         # N = 1: the true dQ, dK, dW, dtau vanish, so relative errors are not
         # defined; test_backward_single_token checks that case
+        return
+    if bool((den == 0).any()):
+        # a den that rounded to exactly zero (possible only where it is not
+        # determined, which the forward check confirmed) makes dO/den
+        # non-finite by definition: no gradient to compare
         return
     ref, sc = oracle_bwd(wl, x)
     for reuse in (False, True):

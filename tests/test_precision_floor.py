@@ -23,12 +23,12 @@ def _bf16(x):
     return ((u + r) & 0xFFFF0000).astype(np.uint32).view(np.float32).astype(np.float64)
 
 
-def _floor(d, m, variant, monkeypatch):
-    wl = W.Workload("small", 2, 2, 200, d, m, variant, False, "bf16", True, 21)
+def _floor(d, m, variant, monkeypatch, shape=(2, 2, 200), causal=False, seed=21):
+    wl = W.Workload("small", *shape, d, m, variant, causal, "bf16", True, seed)
     x = W.generate(wl)
-    kap = orc.conditioning(x.f64("Q"), x.f64("K"), x.W1, x.W2, x.tau, variant, False)
+    kap = orc.conditioning(x.f64("Q"), x.f64("K"), x.W1, x.W2, x.tau, variant, causal)
     x.dO = x.dO * (kap <= KAPPA_MAX["bf16"])[..., None].astype(x.dO.dtype)
-    args = (x.f64("Q"), x.f64("K"), x.f64("V"), x.W1, x.W2, x.tau, x.f64("dO"), variant, False)
+    args = (x.f64("Q"), x.f64("K"), x.f64("V"), x.W1, x.W2, x.tau, x.f64("dO"), variant, causal)
     ref = orc.linattn_bwd(*args)
     exact = orc.feature_map_parts
     with monkeypatch.context() as mp:
@@ -43,3 +43,12 @@ def test_bf16_rounding_floor_against_m(monkeypatch):
     assert few > 1.5e-2          # at m = 16 the floor alone nears the 2e-2 bar
     assert many < 1e-2           # at m = 128 it is well under it
     assert few > 2.5 * many
+
+
+def test_bf16_rounding_floor_m48_short_causal(monkeypatch):
+    """A drawn input at m = 48 (B=1, H=2, N=65, d=64, causal): the feature
+    rounding alone costs 1.7 % of dQ, so the bf16 path's other roundings can
+    take it past the 2e-2 bar (the GPU gives 2.6 %).  The randomized parity
+    test checks bf16 gradients from m = 64."""
+    f = _floor(64, 48, "nonstationary", monkeypatch, shape=(1, 2, 65), causal=True, seed=1173)
+    assert 1.5e-2 < f < 2e-2
