@@ -22,7 +22,7 @@ from tests.parity import check_grads
 pytestmark = pytest.mark.gpu
 
 
-def _cases(n=64, seed=2606):
+def _cases(n=160, seed=2606):
     rnd = random.Random(seed)
     out = []
     for i in range(n):
