@@ -146,6 +146,19 @@ def test_backward_128_segments(F, reuse):
     check_rows(wl, x, got, ref, kap)
 
 
+def test_backward_256_segments(F):
+    """256 segments, the most the heuristic takes (N = 16379: 256 chunks, the
+    last of 59 tokens), with the forward's states: scans over 256 states, R'
+    suffixes from the scan, 256 frequency-gradient partials per head."""
+    wl = W.Workload("seg256", 1, 1, 256 * 64 - 5, 32, 64, "nonstationary", True, "bf16", True, 43)
+    x = W.generate(wl)
+    kap = masked_inputs(wl, x)
+    got = gpu_fwd_bwd(F, wl, x, segments=256, reuse=True)
+    ref, sc = oracle_bwd(wl, x)
+    check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
+
+
 @pytest.mark.parametrize("reuse", [False, True])
 def test_backward_many_partials(F, reuse):
     """B = 3 and 7 segments give 42 frequency-gradient partials per head: the

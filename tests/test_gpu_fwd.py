@@ -187,6 +187,42 @@ FULL_FWD = ["tiny_stationary_noncausal_f32", "lm_stationary_causal", "long_stati
             "nonstationary_causal_train", "train_at_scale_d128", "headline_causal_train_d64"]
 
 
+def _check_sampled_rows(wl, x, O, den, rows, kappa=None, ref=None):
+    """Sampled rows of a GPU forward (O, den as float64 arrays) against the
+    oracle's per-row definition, with the T1/T2 reading of the parity tests.
+    kappa: the oracle's condition numbers of the whole input, and ref: the
+    oracle's (O, den) of the rows, if already computed."""
+    rows = np.array(rows)
+    Q, K, V = x.f64("Q"), x.f64("K"), x.f64("V")
+    O_ref, den_ref = ref if ref is not None else orc.linattn_fwd_rows(Q, K, V, x.W1, x.W2, x.tau, wl.variant,
+                                                                      wl.causal, rows)
+    # conditioning of the sampled rows
+    kap = np.empty(len(rows))
+    for r, (b, h, i) in enumerate(rows):
+        if kappa is not None:
+            kap[r] = kappa[b, h, i]
+            continue
+        sl = slice(None, i + 1) if wl.causal else slice(None)
+        Wb = None if x.W2 is None else x.W2[h:h + 1]
+        pq = orc.feature_map(Q[b:b + 1, h:h + 1, i:i + 1], x.W1[h:h + 1], Wb, x.tau[h:h + 1], wl.variant)
+        pk = orc.feature_map(K[b:b + 1, h:h + 1, sl], x.W1[h:h + 1], Wb, x.tau[h:h + 1], wl.variant)
+        tq = pq[0, 0, 0] * pk[0, 0].sum(0)
+        kap[r] = np.abs(tq).sum() / abs(tq.sum())
+    got_O = O[rows[:, 0], rows[:, 1], rows[:, 2]]
+    got_den = den[rows[:, 0], rows[:, 1], rows[:, 2]]
+    tol = TOL[wl.io]
+    rel_den = np.linalg.norm(got_den - den_ref) / np.linalg.norm(den_ref)
+    num_g = got_O * got_den[:, None]
+    num_r = O_ref * den_ref[:, None]
+    rel_num = np.linalg.norm(num_g - num_r) / np.linalg.norm(num_r)
+    assert rel_den <= tol and rel_num <= tol, (rel_den, rel_num)
+    keep = kap <= (1e3 if wl.io == "f32" else 20.0)
+    if keep.any():
+        rel_O = np.linalg.norm(got_O[keep] - O_ref[keep]) / np.linalg.norm(O_ref[keep])
+        assert rel_O <= tol, rel_O
+    assert np.all(np.isfinite(O[..., 0]) | (den == 0))
+
+
 @pytest.mark.parametrize("name", FULL_FWD)
 def test_forward_full_size_sampled(F, name):
     """Full configured sizes, default launch configuration; rows sampled across
@@ -207,28 +243,33 @@ def test_forward_full_size_sampled(F, name):
         for h in range(wl.H):
             for i in list(rng.integers(0, wl.N, 2)) + ([idx[(b * wl.H + h) % len(idx)]]):
                 rows.append((b, h, int(i)))
-    rows = np.array(rows)
-    Q, K, V = x.f64("Q"), x.f64("K"), x.f64("V")
-    O_ref, den_ref = orc.linattn_fwd_rows(Q, K, V, x.W1, x.W2, x.tau, wl.variant, wl.causal, rows)
-    # conditioning of the sampled rows
-    kap = np.empty(len(rows))
-    for r, (b, h, i) in enumerate(rows):
-        sl = slice(None, i + 1) if wl.causal else slice(None)
-        Wb = None if x.W2 is None else x.W2[h:h + 1]
-        pq = orc.feature_map(Q[b:b + 1, h:h + 1, i:i + 1], x.W1[h:h + 1], Wb, x.tau[h:h + 1], wl.variant)
-        pk = orc.feature_map(K[b:b + 1, h:h + 1, sl], x.W1[h:h + 1], Wb, x.tau[h:h + 1], wl.variant)
-        tq = pq[0, 0, 0] * pk[0, 0].sum(0)
-        kap[r] = np.abs(tq).sum() / abs(tq.sum())
-    got_O = O[rows[:, 0], rows[:, 1], rows[:, 2]]
-    got_den = den[rows[:, 0], rows[:, 1], rows[:, 2]]
-    tol = TOL[wl.io]
-    rel_den = np.linalg.norm(got_den - den_ref) / np.linalg.norm(den_ref)
-    num_g = got_O * got_den[:, None]
-    num_r = O_ref * den_ref[:, None]
-    rel_num = np.linalg.norm(num_g - num_r) / np.linalg.norm(num_r)
-    assert rel_den <= tol and rel_num <= tol, (rel_den, rel_num)
-    keep = kap <= (1e3 if wl.io == "f32" else 20.0)
-    if keep.any():
-        rel_O = np.linalg.norm(got_O[keep] - O_ref[keep]) / np.linalg.norm(O_ref[keep])
-        assert rel_O <= tol, rel_O
-    assert np.all(np.isfinite(O[..., 0]) | (den == 0))
+    _check_sampled_rows(wl, x, O, den, rows)
+
+
+@pytest.fixture(scope="module")
+def long_input():
+    """A long ragged sequence over few heads (B*H = 2, N = 65573: 1025 chunks,
+    the last one of 37 tokens), its sampled rows (chunk and segment boundaries,
+    the sequence end, random positions) and the oracle's values there."""
+    wl = W.Workload("long_few_heads", 1, 2, 65573, 64, 128, "nonstationary", True, "bf16", False, 47)
+    x = W.generate(wl, with_grad=False)
+    kappa = orc.conditioning(x.f64("Q"), x.f64("K"), x.W1, x.W2, x.tau, wl.variant, wl.causal)
+    rng = np.random.default_rng(11)
+    seg = 5 * 64   # tokens per segment at 256 segments
+    idx = [0, 63, 64, seg - 1, seg, 204 * seg - 1, 204 * seg, 8 * 64 - 1, 8 * 64, wl.N - 38, wl.N - 37,
+           wl.N - 1]
+    rows = [(0, h, int(i)) for h in range(wl.H) for i in idx + list(rng.integers(0, wl.N, 3))]
+    ref = orc.linattn_fwd_rows(x.f64("Q"), x.f64("K"), x.f64("V"), x.W1, x.W2, x.tau, wl.variant, wl.causal,
+                               np.array(rows))
+    return wl, x, kappa, rows, ref
+
+
+@pytest.mark.parametrize("segments", [0, 256])
+def test_forward_long_sequence_sampled(F, long_input, segments):
+    """The long input with the heuristic's segment count and with 256 segments
+    of 5 chunks (205 hold chunks, the 51 trailing ones are empty)."""
+    wl, x, kappa, rows, ref = long_input
+    t = to_device(x)
+    O, den = F.flex_linattn_fwd(desc_of(wl, segments=segments), t["Q"], t["K"], t["V"], t["W1"], t["W2"],
+                                t["tau"])
+    _check_sampled_rows(wl, x, to_f64(O), to_f64(den), rows, kappa, ref)
