@@ -39,11 +39,14 @@
  *     too-small workspace returns an error code with no device work.  A failed
  *     kernel launch returns FLEX_ERR_HIP.  No C++ exception crosses the ABI.
  *   - Results are deterministic (bitwise identical from run to run).
- *   - Supported shapes: N >= 1 (a ragged last chunk is masked); d = dv in
- *     {32, 64, 128} with io_dtype FLEX_BF16 and d = dv = 32 with FLEX_F32;
- *     m a multiple of 16 up to 256; chunk in {0, 16, 32, 64}.  Others return
- *     FLEX_ERR_UNSUPPORTED.  Every supported shape has the forward and the
- *     backward.  (d, m) = (32, 64), (64, 64), (64, 128) (bf16) and (128, 64)
+ *   - Supported shapes: N >= 1 (a ragged last chunk is masked); d and dv
+ *     each in {32, 64, 128} with io_dtype FLEX_BF16 and d = dv = 32 with
+ *     FLEX_F32; m a multiple of 16 up to 256; chunk in {0, 16, 32, 64}.
+ *     Others return FLEX_ERR_UNSUPPORTED.  Every supported shape has the
+ *     forward and the backward.  dv != d runs at width max(d, dv) on
+ *     zero-padded copies in the workspace (Q, K and W when dv > d; V, O and dO
+ *     when dv < d), which leave the results unchanged; the prefill takes
+ *     dv = d only.  (d, m) = (32, 64), (64, 64), (64, 128) (bf16) and (128, 64)
  *     run as one pass; every other shape runs as frequency groups (of 128 at
  *     bf16 d = 64 when 128 divides m, else of 64, the first one zero-padded
  *     when 64 does not divide m) whose sums are combined in a fixed order (the
@@ -85,7 +88,7 @@ typedef enum { FLEX_PASS_FEATURE_MAP = 0, FLEX_PASS_FWD = 1, FLEX_PASS_BWD = 2,
 
 typedef struct {
   int32_t B, H, N;      /* batch, heads, sequence length                           */
-  int32_t d, dv;        /* head dimension of Q/K and of V (dv must equal d)         */
+  int32_t d, dv;        /* head dimension of Q/K and of V                          */
   int32_t m;            /* frequencies per matrix (the paper's n); d' = 2m          */
   int32_t variant;      /* flex_variant                                             */
   int32_t causal;       /* 0: all j; 1: j <= i                                      */
@@ -146,8 +149,9 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K,
  *   state  fp32, B*H*2m*(dv+1) floats, overwritten: per (b,h) slice S [2m][dv]
  *          row-major, then z [2m], feature rows in [cos | sin] order.
  *   ws     flex_workspace_size(desc, FLEX_PASS_FWD) bytes, as for the forward.
- * desc->causal must be 1 (FLEX_ERR_UNSUPPORTED otherwise); a NULL or
- * misaligned state returns FLEX_ERR_INVALID_ARG.  Shapes as flex_linattn_fwd. */
+ * desc->causal must be 1 and dv = d (FLEX_ERR_UNSUPPORTED otherwise); a NULL
+ * or misaligned state returns FLEX_ERR_INVALID_ARG.  Shapes as
+ * flex_linattn_fwd otherwise. */
 int32_t flex_linattn_prefill(const flex_desc* desc, const void* Q, const void* K,
                              const void* V, const float* W1, const float* W2,
                              const float* tau, void* O, float* den, float* state,

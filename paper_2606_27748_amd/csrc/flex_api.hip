@@ -24,11 +24,13 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 bool chunk_supported(int c) { return c == 0 || c == 16 || c == 32 || c == 64; }
 int chunk_of(const flex_desc* d) { return d->chunk == 0 ? kChunk : d->chunk; }
 
-// Attention shapes: d = dv in {32, 64, 128} for bf16 (32 for fp32), m a
-// multiple of 16 up to 256.  Shapes that no single kernel covers run as
-// frequency groups (groups_of).
+// Attention shapes: d and dv in {32, 64, 128} for bf16 (d = dv = 32 for fp32),
+// m a multiple of 16 up to 256.  Shapes that no single kernel covers run as
+// frequency groups (groups_of); dv != d runs at the wider of the two on
+// zero-padded operands (padded_desc).
 bool shape_supported(const flex_desc* d) {
-  if (d->dv != d->d) return false;
+  if (d->dv != d->d && (d->io_dtype != FLEX_BF16 || !(d->dv == 32 || d->dv == 64 || d->dv == 128)))
+    return false;
   if (d->grad_dtype != FLEX_F32) return false;
   if (!chunk_supported(d->chunk)) return false;
   if (d->m % 16 != 0 || d->m > 256) return false;
@@ -287,7 +289,59 @@ size_t fwd_acc_bytes(const flex_desc* d) {
   return align256(rows * d->dv * sizeof(float)) + align256(rows * sizeof(float));
 }
 
+// dv != d: the attention runs at width w = max(d, dv) on zero-padded
+// operands.  With dv > d, Q, K and the frequency rows get w - d zero columns:
+// the projections W x and the norms |x|^2 are unchanged, and the padded
+// columns of dQ, dK and dW come out zero and are dropped.  With dv < d, V, O
+// and dO get d - dv zero columns: den, delta and every gradient but the
+// padded columns of dV are unchanged.  The padded copies sit after the
+// padded shape's own workspace.
+flex_desc padded_desc(const flex_desc* d) {
+  flex_desc p = *d;
+  p.d = p.dv = d->d > d->dv ? d->d : d->dv;
+  return p;
+}
+struct ValuePad {
+  size_t q, k, w1, w2, dq, dk, dw1, dw2, v, o, dO, dv, total;
+};
+ValuePad value_pad_of(const flex_desc* d, int pass) {
+  ValuePad L;
+  memset(&L, 0, sizeof(L));
+  if (d->dv == d->d) return L;
+  const size_t rows = (size_t)d->B * d->H * d->N, hm = (size_t)d->H * d->m;
+  const size_t w = d->d > d->dv ? d->d : d->dv;
+  const size_t io = d->io_dtype == FLEX_BF16 ? 2 : 4;
+  const bool ns = d->variant == FLEX_NONSTATIONARY;
+  const bool bwd = pass == FLEX_PASS_BWD;
+  size_t off = 0;
+  if (d->dv > d->d) {
+    L.q = off;  off += align256(rows * w * io);
+    L.k = off;  off += align256(rows * w * io);
+    L.w1 = off; off += align256(hm * w * sizeof(float));
+    if (ns) { L.w2 = off; off += align256(hm * w * sizeof(float)); }
+    if (bwd) {
+      L.dq = off;  off += align256(rows * w * sizeof(float));
+      L.dk = off;  off += align256(rows * w * sizeof(float));
+      L.dw1 = off; off += align256(hm * w * sizeof(float));
+      if (ns) { L.dw2 = off; off += align256(hm * w * sizeof(float)); }
+    }
+  } else {
+    L.v = off; off += align256(rows * w * io);
+    L.o = off; off += align256(rows * w * io);
+    if (bwd) {
+      L.dO = off; off += align256(rows * w * io);
+      L.dv = off; off += align256(rows * w * sizeof(float));
+    }
+  }
+  L.total = off;
+  return L;
+}
+
 size_t ws_bytes_of(const flex_desc* d, int pass) {
+  if (d->dv != d->d && pass != FLEX_PASS_FEATURE_MAP) {
+    const flex_desc pd = padded_desc(d);
+    return ws_bytes_of(&pd, pass) + value_pad_of(d, pass).total;
+  }
   const KernelShape ks = attn_shape(d);
   const size_t bh = (size_t)d->B * d->H;
   const size_t P = (size_t)pick_segments(d);
@@ -476,6 +530,30 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
   return FLEX_OK;
 }
 
+// The forward of a dv != d descriptor: run_fwd at the padded width on
+// zero-padded copies in the workspace (padded_desc).
+int32_t run_fwd_padded(const flex_desc* desc, const void* Q, const void* K, const void* V, const float* W1,
+                       const float* W2, const float* tau, void* O, float* den, char* base, hipStream_t stream) {
+  const flex_desc pd = padded_desc(desc);
+  const ValuePad L = value_pad_of(desc, FLEX_PASS_FWD);
+  char* vp = base + ws_bytes_of(&pd, FLEX_PASS_FWD);
+  const size_t rows = (size_t)desc->B * desc->H * desc->N, hm = (size_t)desc->H * desc->m;
+  const int io = desc->io_dtype == FLEX_BF16 ? 2 : 4, w = pd.d;
+  if (desc->dv > desc->d) {
+    if (launch_copy_cols(Q, desc->d, vp + L.q, w, rows, io, stream) != hipSuccess ||
+        launch_copy_cols(K, desc->d, vp + L.k, w, rows, io, stream) != hipSuccess ||
+        launch_copy_cols(W1, desc->d, vp + L.w1, w, hm, 4, stream) != hipSuccess ||
+        (W2 && launch_copy_cols(W2, desc->d, vp + L.w2, w, hm, 4, stream) != hipSuccess))
+      return FLEX_ERR_HIP;
+    return run_fwd(&pd, vp + L.q, vp + L.k, V, reinterpret_cast<const float*>(vp + L.w1),
+                   W2 ? reinterpret_cast<const float*>(vp + L.w2) : nullptr, tau, O, den, base, stream);
+  }
+  if (launch_copy_cols(V, desc->dv, vp + L.v, w, rows, io, stream) != hipSuccess) return FLEX_ERR_HIP;
+  const int32_t r = run_fwd(&pd, Q, K, vp + L.v, W1, W2, tau, vp + L.o, den, base, stream);
+  if (r != FLEX_OK) return r;
+  return launch_copy_cols(vp + L.o, w, O, desc->dv, rows, io, stream) == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
+}
+
 constexpr int kMaxDevices = 64;
 struct ScratchTable {
   std::mutex mu;
@@ -498,6 +576,103 @@ int32_t scratch_of_current_device(void** out) {
   }
   *out = t.ptr[dev];
   return FLEX_OK;
+}
+
+// The backward on validated arguments with a workspace of at least
+// ws_bytes_of(desc, FLEX_PASS_BWD) bytes at `base`.
+int32_t run_bwd(const flex_desc* desc, const void* Q, const void* K, const void* V, const float* W1,
+                const float* W2, const float* tau, const void* O, const float* den, const void* dO, float* dQ,
+                float* dK, float* dV, float* dW1, float* dW2, float* dtau, const void* fwd_ws, char* base,
+                hipStream_t stream) {
+  const KernelShape ks = attn_shape(desc);
+  const Groups G = groups_of(desc);
+  BwdArgs a;
+  memset(&a, 0, sizeof(a));
+  a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den; a.dO = dO;
+  a.dQ = dQ; a.dK = dK; a.dV = dV;
+  a.dtau = dtau;
+  a.BH = desc->B * desc->H; a.B = desc->B; a.H = desc->H; a.N = desc->N;
+  // the backward sweeps use BWD_CHUNK-token chunks over the forward's segments
+  a.nchunks = (desc->N + BWD_CHUNK - 1) / BWD_CHUNK;
+  a.segments = pick_segments(desc);
+  {
+    const int fcps = (nchunks_of(desc) + a.segments - 1) / a.segments;   // forward chunks per segment
+    a.chunks_per_seg = fcps * (kChunk / BWD_CHUNK);
+  }
+  if (fwd_ws) {
+    a.fsub = fwd_sub_of(desc, a.segments);
+    a.ffold = fwd_fold_of(desc, a.segments);
+    // with the forward's key-side states the scan would handle R' alone: the
+    // dK/dV sweep sums its suffix itself when it reads at most kRFoldMax states
+    a.rfold = desc->causal && a.segments - 1 <= kRFoldMax ? 1 : 0;
+  }
+  a.s_const = s_const_of(desc);
+  const size_t bh = (size_t)a.BH, P = (size_t)a.segments;
+  const size_t sb = align256(bh * P * bwd_state_floats(ks) * sizeof(float));
+  const size_t gb = align256(bh * (size_t)a.N * 2 * sizeof(float));
+  a.sstate = reinterpret_cast<float*>(base);
+  a.rstate = reinterpret_cast<float*>(base + sb);
+  a.gstats = reinterpret_cast<float*>(base + 2 * sb);
+  a.dwpart = reinterpret_cast<float*>(base + 2 * sb + gb);
+  a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
+  a.wfrag = base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
+  a.wfrag_kv = bwd_split_differs(ks) ? static_cast<char*>(a.wfrag) + align256(wfrag_bytes(ks, desc->H)) : a.wfrag;
+  a.dw_stride = desc->m * desc->d;
+  const PadRows pr = pad_rows_of(desc, base + ws_bytes_of(desc, FLEX_PASS_BWD));
+  for (int g = 0; g < G.n; ++g) {
+    if (!group_rows(desc, G, pr, g, W1, W2, stream, &a.W1, &a.W2, &a.w_stride, &a.fvalid))
+      return FLEX_ERR_HIP;
+    const size_t woff = (size_t)group_off(G, g) * desc->d;   // this group's frequency rows
+    a.dW1 = dW1 + woff;
+    a.dW2 = dW2 ? dW2 + woff : nullptr;
+    a.acc = g > 0;
+    if (fwd_ws)
+      a.fstate = reinterpret_cast<const float*>(static_cast<const char*>(fwd_ws) + g * fwd_group_state_bytes(desc));
+    const hipError_t e = launch_bwd(a, ks, stream);
+    if (e != hipSuccess) return FLEX_ERR_HIP;
+  }
+  return FLEX_OK;
+}
+
+// The backward of a dv != d descriptor: run_bwd at the padded width on
+// zero-padded copies in the workspace (padded_desc), then the caller's columns
+// of the padded gradients.
+int32_t run_bwd_padded(const flex_desc* desc, const void* Q, const void* K, const void* V, const float* W1,
+                       const float* W2, const float* tau, const void* O, const float* den, const void* dO,
+                       float* dQ, float* dK, float* dV, float* dW1, float* dW2, float* dtau, const void* fwd_ws,
+                       char* base, hipStream_t stream) {
+  const flex_desc pd = padded_desc(desc);
+  const ValuePad L = value_pad_of(desc, FLEX_PASS_BWD);
+  char* vp = base + ws_bytes_of(&pd, FLEX_PASS_BWD);
+  const size_t rows = (size_t)desc->B * desc->H * desc->N, hm = (size_t)desc->H * desc->m;
+  const int io = desc->io_dtype == FLEX_BF16 ? 2 : 4, w = pd.d, f = (int)sizeof(float);
+  if (desc->dv > desc->d) {
+    if (launch_copy_cols(Q, desc->d, vp + L.q, w, rows, io, stream) != hipSuccess ||
+        launch_copy_cols(K, desc->d, vp + L.k, w, rows, io, stream) != hipSuccess ||
+        launch_copy_cols(W1, desc->d, vp + L.w1, w, hm, f, stream) != hipSuccess ||
+        (W2 && launch_copy_cols(W2, desc->d, vp + L.w2, w, hm, f, stream) != hipSuccess))
+      return FLEX_ERR_HIP;
+    float* dWp2 = W2 ? reinterpret_cast<float*>(vp + L.dw2) : nullptr;
+    const int32_t r = run_bwd(&pd, vp + L.q, vp + L.k, V, reinterpret_cast<const float*>(vp + L.w1),
+                              W2 ? reinterpret_cast<const float*>(vp + L.w2) : nullptr, tau, O, den, dO,
+                              reinterpret_cast<float*>(vp + L.dq), reinterpret_cast<float*>(vp + L.dk), dV,
+                              reinterpret_cast<float*>(vp + L.dw1), dWp2, dtau, fwd_ws, base, stream);
+    if (r != FLEX_OK) return r;
+    if (launch_copy_cols(vp + L.dq, w, dQ, desc->d, rows, f, stream) != hipSuccess ||
+        launch_copy_cols(vp + L.dk, w, dK, desc->d, rows, f, stream) != hipSuccess ||
+        launch_copy_cols(vp + L.dw1, w, dW1, desc->d, hm, f, stream) != hipSuccess ||
+        (W2 && launch_copy_cols(dWp2, w, dW2, desc->d, hm, f, stream) != hipSuccess))
+      return FLEX_ERR_HIP;
+    return FLEX_OK;
+  }
+  if (launch_copy_cols(V, desc->dv, vp + L.v, w, rows, io, stream) != hipSuccess ||
+      launch_copy_cols(O, desc->dv, vp + L.o, w, rows, io, stream) != hipSuccess ||
+      launch_copy_cols(dO, desc->dv, vp + L.dO, w, rows, io, stream) != hipSuccess)
+    return FLEX_ERR_HIP;
+  const int32_t r = run_bwd(&pd, Q, K, vp + L.v, W1, W2, tau, vp + L.o, den, vp + L.dO, dQ, dK,
+                            reinterpret_cast<float*>(vp + L.dv), dW1, dW2, dtau, fwd_ws, base, stream);
+  if (r != FLEX_OK) return r;
+  return launch_copy_cols(vp + L.dv, w, dV, desc->dv, rows, f, stream) == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
 }
 
 }  // namespace
@@ -679,6 +854,8 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K, co
   if (st != FLEX_OK) return st;
   const size_t need = ws_bytes_of(desc, FLEX_PASS_FWD);
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
+  if (desc->dv != desc->d)
+    return run_fwd_padded(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream);
   return run_fwd(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream);
 }
 
@@ -687,7 +864,7 @@ int32_t flex_linattn_prefill(const flex_desc* desc, const void* Q, const void* K
                              float* state, void* ws, size_t ws_bytes, void* stream) {
   const int32_t st = check_fwd_args(desc, Q, K, V, W1, W2, tau, O, den);
   if (st != FLEX_OK) return st;
-  if (desc->causal != 1) return FLEX_ERR_UNSUPPORTED;
+  if (desc->causal != 1 || desc->dv != desc->d) return FLEX_ERR_UNSUPPORTED;
   if (!state || !aligned16(state)) return FLEX_ERR_INVALID_ARG;
   const size_t need = ws_bytes_of(desc, FLEX_PASS_FWD);
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
@@ -704,7 +881,9 @@ int32_t flex_linattn_fwd_noalloc(const flex_desc* desc, const void* Q, const voi
   const int32_t sst = scratch_of_current_device(&ws);
   if (sst != FLEX_OK) return sst;
   // the forward writes every workspace byte it reads (segment states, their
-  // scan, fragments, group sums), so the scratch needs no clearing
+  // scan, fragments, group sums, padded copies), so the scratch needs no clearing
+  if (desc->dv != desc->d)
+    return run_fwd_padded(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream);
   return run_fwd(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream);
 }
 
@@ -727,55 +906,12 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K, co
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
   if (fwd_ws && (fwd_ws_bytes < ws_bytes_of(desc, FLEX_PASS_FWD) || !aligned16(fwd_ws)))
     return FLEX_ERR_WORKSPACE;
-  const KernelShape ks = attn_shape(desc);
-  const Groups G = groups_of(desc);
-  BwdArgs a;
-  memset(&a, 0, sizeof(a));
-  a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den; a.dO = dO;
-  a.dQ = static_cast<float*>(dQ); a.dK = static_cast<float*>(dK); a.dV = static_cast<float*>(dV);
-  a.dtau = dtau;
-  a.BH = desc->B * desc->H; a.B = desc->B; a.H = desc->H; a.N = desc->N;
-  // the backward sweeps use BWD_CHUNK-token chunks over the forward's segments
-  a.nchunks = (desc->N + BWD_CHUNK - 1) / BWD_CHUNK;
-  a.segments = pick_segments(desc);
-  {
-    const int fcps = (nchunks_of(desc) + a.segments - 1) / a.segments;   // forward chunks per segment
-    a.chunks_per_seg = fcps * (kChunk / BWD_CHUNK);
-  }
-  if (fwd_ws) {
-    a.fsub = fwd_sub_of(desc, a.segments);
-    a.ffold = fwd_fold_of(desc, a.segments);
-    // with the forward's key-side states the scan would handle R' alone: the
-    // dK/dV sweep sums its suffix itself when it reads at most kRFoldMax states
-    a.rfold = desc->causal && a.segments - 1 <= kRFoldMax ? 1 : 0;
-  }
-  a.s_const = s_const_of(desc);
-  const size_t bh = (size_t)a.BH, P = (size_t)a.segments;
-  char* base = static_cast<char*>(ws);
-  const size_t sb = align256(bh * P * bwd_state_floats(ks) * sizeof(float));
-  const size_t gb = align256(bh * (size_t)a.N * 2 * sizeof(float));
-  a.sstate = reinterpret_cast<float*>(base);
-  a.rstate = reinterpret_cast<float*>(base + sb);
-  a.gstats = reinterpret_cast<float*>(base + 2 * sb);
-  a.dwpart = reinterpret_cast<float*>(base + 2 * sb + gb);
-  a.dtaupart = reinterpret_cast<float*>(base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)));
-  a.wfrag = base + 2 * sb + gb + align256(bh * P * bwd_dw_floats(ks) * sizeof(float)) + align256(bh * P * sizeof(float));
-  a.wfrag_kv = bwd_split_differs(ks) ? static_cast<char*>(a.wfrag) + align256(wfrag_bytes(ks, desc->H)) : a.wfrag;
-  a.dw_stride = desc->m * desc->d;
-  const PadRows pr = pad_rows_of(desc, base + ws_bytes_of(desc, FLEX_PASS_BWD));
-  for (int g = 0; g < G.n; ++g) {
-    if (!group_rows(desc, G, pr, g, W1, W2, (hipStream_t)stream, &a.W1, &a.W2, &a.w_stride, &a.fvalid))
-      return FLEX_ERR_HIP;
-    const size_t woff = (size_t)group_off(G, g) * desc->d;   // this group's frequency rows
-    a.dW1 = dW1 + woff;
-    a.dW2 = dW2 ? dW2 + woff : nullptr;
-    a.acc = g > 0;
-    if (fwd_ws)
-      a.fstate = reinterpret_cast<const float*>(static_cast<const char*>(fwd_ws) + g * fwd_group_state_bytes(desc));
-    const hipError_t e = launch_bwd(a, ks, (hipStream_t)stream);
-    if (e != hipSuccess) return FLEX_ERR_HIP;
-  }
-  return FLEX_OK;
+  if (desc->dv != desc->d)
+    return run_bwd_padded(desc, Q, K, V, W1, W2, tau, O, den, dO, static_cast<float*>(dQ), static_cast<float*>(dK),
+                          static_cast<float*>(dV), dW1, dW2, dtau, fwd_ws, static_cast<char*>(ws),
+                          (hipStream_t)stream);
+  return run_bwd(desc, Q, K, V, W1, W2, tau, O, den, dO, static_cast<float*>(dQ), static_cast<float*>(dK),
+                 static_cast<float*>(dV), dW1, dW2, dtau, fwd_ws, static_cast<char*>(ws), (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -649,7 +649,7 @@ __global__ __launch_bounds__(256) void k_fwd_finish(FwdArgs a, int dv) {
 }
 
 // ---------------------------------------------------------------------------
-// Frequency rows of a padded last group: dst[h][rows][d] holds the group's
+// Frequency rows of a padded group: dst[h][rows][d] holds the group's
 // rows_valid rows of W, then zero rows (their features are masked to zero).
 // One thread per 4 elements.
 // ---------------------------------------------------------------------------
@@ -668,6 +668,34 @@ hipError_t launch_pad_rows(const float* src, float* dst, int H, int rows_valid, 
                            hipStream_t st) {
   if (d % 4 != 0) return hipErrorInvalidValue;
   k_pad_rows<<<dim3((rows * d / 4 + 255) / 256, H), 256, 0, st>>>(src, dst, rows_valid, rows, d, src_stride);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Column padding and cropping between row-major matrices of two widths, in
+// 16-byte units: dst[r][u] = src[r][u] for u < us, zero for us <= u < ud.
+// One thread per 16-byte unit of dst.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_copy_cols(const uint4* src, int us, uint4* dst, int ud, size_t rows) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * (size_t)ud) return;
+  const size_t r = i / (size_t)ud;
+  const int u = (int)(i - r * (size_t)ud);
+  dst[i] = u < us ? src[r * (size_t)us + u] : make_uint4(0u, 0u, 0u, 0u);
+}
+
+hipError_t launch_copy_cols(const void* src, int cols_src, void* dst, int cols_dst, size_t rows, int elem_bytes,
+                            hipStream_t st) {
+  if (elem_bytes <= 0 || (cols_src * elem_bytes) % 16 != 0 || (cols_dst * elem_bytes) % 16 != 0)
+    return hipErrorInvalidValue;
+  const int us = cols_src * elem_bytes / 16, ud = cols_dst * elem_bytes / 16;
+  const size_t n = rows * (size_t)ud;
+  if (n == 0) return hipSuccess;
+  const size_t blocks = (n + 255) / 256;
+  if (blocks > 0x7fffffffULL) return hipErrorInvalidValue;
+  // a crop reads us units of each source row and copies only the first ud of them
+  k_copy_cols<<<dim3((unsigned)blocks), 256, 0, st>>>(static_cast<const uint4*>(src), us,
+                                                      static_cast<uint4*>(dst), ud, rows);
   return hipGetLastError();
 }
 

@@ -193,9 +193,14 @@ hipError_t launch_fwd(const FwdArgs& a, const KernelShape& ks, bool feature_map_
 // O = acc_num / acc_den (io dtype), den = acc_den, after the last frequency group.
 hipError_t launch_fwd_finish(const FwdArgs& a, bool bf16, int dv, hipStream_t st);
 // dst[h][rows][d] = the first rows_valid rows of src[h] (src_stride elements
-// apart per head), zero after them: the frequency rows of a padded last group.
+// apart per head), zero after them: the frequency rows of a padded group.
 hipError_t launch_pad_rows(const float* src, float* dst, int H, int rows_valid, int rows, int d, int src_stride,
                            hipStream_t st);
+// dst [rows][cols_dst] = src [rows][cols_src] with the columns past cols_src
+// zero (cols_dst > cols_src) or cut off (cols_dst < cols_src); elements of
+// elem_bytes, rows of a whole number of 16-byte units, 16-byte aligned.
+hipError_t launch_copy_cols(const void* src, int cols_src, void* dst, int cols_dst, size_t rows, int elem_bytes,
+                            hipStream_t st);
 hipError_t launch_bwd(const BwdArgs& a, const KernelShape& ks, hipStream_t st);
 // The dQ sweep of one shape (flex_bwd_dq.hip): grouped_acc adds into an
 // earlier frequency group's dQ; wr also does the pre-pass's query-side work;

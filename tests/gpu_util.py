@@ -25,5 +25,5 @@ def to_f64(t):
 
 def desc_of(wl, segments=0, sigma=1.0, chunk=0):
     import paper_2606_27748_amd as F
-    return F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, wl.causal, wl.io,
+    return F.make_desc(wl.B, wl.H, wl.N, wl.d, wl.m, wl.variant, wl.causal, wl.io, dv=wl.dv,
                        sigma=sigma, segments=segments, chunk=chunk)

@@ -116,7 +116,8 @@ def test_awd_workspace_size():
     ("chunk", -16, F.FLEX_ERR_INVALID_ARG), ("chunk", 16, F.FLEX_OK), ("chunk", 32, F.FLEX_OK),
     ("chunk", 64, F.FLEX_OK),
     ("d", 48, F.FLEX_ERR_UNSUPPORTED), ("m", 100, F.FLEX_ERR_UNSUPPORTED), ("m", 96, F.FLEX_OK),
-    ("dv", 32, F.FLEX_ERR_UNSUPPORTED), ("grad_dtype", 1, F.FLEX_ERR_UNSUPPORTED),
+    ("dv", 32, F.FLEX_OK), ("dv", 128, F.FLEX_OK), ("dv", 48, F.FLEX_ERR_UNSUPPORTED),
+    ("dv", 256, F.FLEX_ERR_UNSUPPORTED), ("grad_dtype", 1, F.FLEX_ERR_UNSUPPORTED),
 ])
 def test_descriptor_validation(field, value, status):
     d = F.make_desc(1, 2, 100, 64, 128, "nonstationary", True, "bf16")
@@ -134,6 +135,39 @@ def test_feature_map_ignores_attention_fields(field, value):
     assert _ws(d, F.FLEX_PASS_FEATURE_MAP) == (F.FLEX_OK, 0)
     d.d = 48   # the shape itself is still checked
     assert _ws(d, F.FLEX_PASS_FEATURE_MAP)[0] == F.FLEX_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("d,dv", [(64, 32), (128, 64), (128, 32), (32, 64), (64, 128), (32, 128)])
+def test_value_width_workspace(d, dv):
+    """d_v != d runs at width max(d, d_v) on zero-padded copies: its workspace
+    is the padded shape's plus the copies (Q, K, W and their gradients when
+    d_v > d; V, O, dO and dV when d_v < d)."""
+    for causal in (False, True):
+        for variant in ("stationary", "nonstationary"):
+            desc = F.make_desc(2, 3, 300, d, 128, variant, causal, "bf16", dv=dv)
+            w = max(d, dv)
+            pad = F.make_desc(2, 3, 300, w, 128, variant, causal, "bf16")
+            rows, hm = 2 * 3 * 300, 3 * 128
+            nmat = 2 if variant == "nonstationary" else 1
+            for pas in (F.FLEX_PASS_FWD, F.FLEX_PASS_BWD):
+                st, n = _ws(desc, pas)
+                st0, n0 = _ws(pad, pas)
+                assert st == F.FLEX_OK and st0 == F.FLEX_OK
+                if dv > d:
+                    copies = 2 * rows * w * 2 + nmat * hm * w * 4
+                    if pas == F.FLEX_PASS_BWD:
+                        copies += 2 * rows * w * 4 + nmat * hm * w * 4
+                else:
+                    copies = 2 * rows * w * 2
+                    if pas == F.FLEX_PASS_BWD:
+                        copies += rows * w * 2 + rows * w * 4
+                assert n0 + copies <= n <= n0 + copies + 256 * 8
+
+
+def test_value_width_limits():
+    """fp32 has d = d_v = 32 only, and d_v is one of the head widths."""
+    assert _ws(F.make_desc(1, 1, 64, 32, 64, "stationary", True, "f32", dv=64))[0] == F.FLEX_ERR_UNSUPPORTED
+    assert _ws(F.make_desc(1, 1, 64, 64, 64, "stationary", True, "bf16", dv=48))[0] == F.FLEX_ERR_UNSUPPORTED
 
 
 def test_fp32_large_shapes_unsupported():
@@ -184,6 +218,8 @@ def test_entry_points_reject_bad_arguments():
     assert lib.flex_linattn_prefill(ctypes.byref(nc), P, P, P, P, P, P, P, P, P, P, big, None) == 2
     assert lib.flex_linattn_prefill(ctypes.byref(dn), P, P, P, P, P, P, P, P, None, P, big, None) == 1
     assert lib.flex_linattn_prefill(ctypes.byref(dn), P, P, P, P, P, P, P, P, P, P, 16, None) == 3
+    dvd = F.make_desc(1, 2, 100, 64, 128, "nonstationary", True, "bf16", dv=32)
+    assert lib.flex_linattn_prefill(ctypes.byref(dvd), P, P, P, P, P, P, P, P, P, P, big, None) == 2
     # feature map
     assert lib.flex_feature_map(ctypes.byref(dn), None, P, P, P, P, None, 0, None) == 1
     assert lib.flex_feature_map(ctypes.byref(ds), P, P, P, P, P, None, 0, None) == 1

@@ -91,6 +91,23 @@ def test_backward_small(F, io, d, m, variant, causal, reuse):
     check_rows(wl, x, got, ref, kap)
 
 
+@pytest.mark.parametrize("d,dv", [(64, 32), (128, 64), (128, 32), (32, 64), (64, 128), (32, 128)])
+@pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("reuse", [False, True])
+def test_backward_value_width(F, d, dv, variant, causal, reuse):
+    """d_v != d: the backward at width max(d, d_v) on zero-padded copies."""
+    wl = W.Workload("dv", 2, 2, 150, d, 80, variant, causal, "bf16", True, 63, value_dim=dv)
+    x = W.generate(wl)
+    kap = masked_inputs(wl, x)
+    got = gpu_fwd_bwd(F, wl, x, reuse=reuse)
+    assert got["dQ"].shape == (2, 2, 150, d) and got["dV"].shape == (2, 2, 150, dv)
+    assert got["dW1"].shape == (2, 80, d)
+    ref, sc = oracle_bwd(wl, x)
+    check_grads("bf16", got, ref, names_of(wl), sc)
+    check_rows(wl, x, got, ref, kap)
+
+
 @pytest.mark.parametrize("reuse", [False, True])
 @pytest.mark.parametrize("segments", [1, 2, 3])
 @pytest.mark.parametrize("causal", [False, True])

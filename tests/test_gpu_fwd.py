@@ -91,6 +91,30 @@ def test_forward_small(F, io, d, m, variant, causal):
     check_forward(io, to_f64(O), to_f64(den), O_ref, den_ref, kap, sc)
 
 
+# (d, d_v) with d_v != d: run at width max(d, d_v) on zero-padded copies
+VALUE_WIDTHS = [(64, 32), (128, 64), (128, 32), (32, 64), (64, 128), (32, 128)]
+
+
+@pytest.mark.parametrize("d,dv", VALUE_WIDTHS)
+@pytest.mark.parametrize("variant", ["stationary", "nonstationary"])
+@pytest.mark.parametrize("causal", [False, True])
+def test_forward_value_width(F, d, dv, variant, causal):
+    import torch
+    wl = W.Workload("dv", 2, 2, 150, d, 80, variant, causal, "bf16", False, 61, value_dim=dv)
+    x = W.generate(wl)
+    t = to_device(x)
+    O, den = F.flex_linattn_fwd(desc_of(wl), t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"])
+    assert tuple(O.shape) == (2, 2, 150, dv)
+    O_ref, den_ref, kap, sc = oracle_fwd(x, wl)
+    check_forward("bf16", to_f64(O), to_f64(den), O_ref, den_ref, kap, sc)
+    # the allocation-free entry point takes the same route (its scratch holds
+    # the padded copies at this size): the same bits
+    O2, den2 = torch.empty_like(O), torch.empty_like(den)
+    F.flex_linattn_fwd_noalloc(desc_of(wl), t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"], O2, den2)
+    assert torch.equal(O2.view(torch.int16), O.view(torch.int16))
+    assert torch.equal(den2.view(torch.int32), den.view(torch.int32))
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_forward_many_segments(F, causal):
     """20 segments: the segment scan takes its states in two batches."""

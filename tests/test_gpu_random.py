@@ -1,7 +1,7 @@
 """Parity over randomly drawn valid configurations (a fixed list, seeded).
 
 Each case draws B, H, N, d, m, the variant, causality, the chunk length, the
-segment count and the io dtype from the supported set, runs the forward and the
+segment count, the io dtype and the value width from the supported set, runs the forward and the
 backward (with and without the forward's states) through the C ABI, and checks
 both against the float64 oracle with the criteria of the dedicated tests.  bf16
 gradients are checked from m = 64 on and from N = 2; the forward at every m and
@@ -35,7 +35,8 @@ def _cases(n=160, seed=2606):
         segments = rnd.choice([0, 0, 1, 2, 3, 5])
         variant = rnd.choice(["stationary", "nonstationary"])
         B, H = rnd.choice([1, 2]), rnd.choice([1, 2, 3])
-        out.append((i, io, B, H, N, d, m, variant, causal, chunk, segments))
+        dv = d if io == "f32" else rnd.choice([d, d, 32, 64, 128])
+        out.append((i, io, B, H, N, d, m, variant, causal, chunk, segments, dv))
     return out
 
 
@@ -51,8 +52,8 @@ def F():
 @pytest.mark.parametrize("case", _cases(), ids=lambda c: "-".join(str(v) for v in c))
 def test_random_configuration(F, case):
     import torch
-    i, io, B, H, N, d, m, variant, causal, chunk, segments = case
-    wl = W.Workload(f"rand{i}", B, H, N, d, m, variant, causal, io, True, 1000 + i)
+    i, io, B, H, N, d, m, variant, causal, chunk, segments, dv = case
+    wl = W.Workload(f"rand{i}", B, H, N, d, m, variant, causal, io, True, 1000 + i, value_dim=dv)
     x = W.generate(wl)
     kap = masked_inputs(wl, x)
     t = to_device(x)

@@ -19,13 +19,13 @@ def _rng(seed):
     return np.random.default_rng(seed)
 
 
-def _small_inputs(variant, seed=0, B=2, H=2, N=9, d=5, m=6, scale=0.6):
+def _small_inputs(variant, seed=0, B=2, H=2, N=9, d=5, m=6, scale=0.6, dv=None):
     r = _rng(seed)
     W1 = r.standard_normal((H, m, d))
     W2 = r.standard_normal((H, m, d)) if variant == NS else None
     Q = r.standard_normal((B, H, N, d)) * scale
     K = r.standard_normal((B, H, N, d)) * scale
-    V = r.standard_normal((B, H, N, d))
+    V = r.standard_normal((B, H, N, d if dv is None else dv))
     tau = np.array([math.log(2.0), 0.9])[:H]
     return Q, K, V, W1, W2, tau
 
@@ -156,9 +156,11 @@ def _quadratic(Q, K, V, W1, W2, tau, variant, causal, sigma=1.0):
 
 @pytest.mark.parametrize("variant", [S, NS])
 @pytest.mark.parametrize("causal", [False, True])
-def test_state_form_equals_quadratic(variant, causal):
-    """C1: the state form equals the quadratic form (exactness of Eq.(linear att))."""
-    Q, K, V, W1, W2, tau = _small_inputs(variant, seed=3)
+@pytest.mark.parametrize("dv", [None, 2, 8])
+def test_state_form_equals_quadratic(variant, causal, dv):
+    """C1: the state form equals the quadratic form (exactness of Eq.(linear att)),
+    also with a value width other than d."""
+    Q, K, V, W1, W2, tau = _small_inputs(variant, seed=3, dv=dv)
     O, den = orc.linattn_fwd(Q, K, V, W1, W2, tau, variant, causal)
     Oq, denq, _ = _quadratic(Q, K, V, W1, W2, tau, variant, causal)
     np.testing.assert_allclose(den, denq, rtol=1e-12, atol=1e-12)
@@ -324,10 +326,11 @@ def _loss(Q, K, V, W1, W2, tau, dO, variant, causal):
 
 @pytest.mark.parametrize("variant", [S, NS])
 @pytest.mark.parametrize("causal", [False, True])
-def test_finite_differences(variant, causal):
+@pytest.mark.parametrize("dv", [None, 5])
+def test_finite_differences(variant, causal, dv):
     """C8: every analytic gradient (dQ, dK, dV, dW1, dW2, dtau) matches central
-    finite differences of L = sum(O * dO)."""
-    Q, K, V, W1, W2, tau = _small_inputs(variant, seed=14, B=1, H=2, N=6, d=3, m=4, scale=0.5)
+    finite differences of L = sum(O * dO), also with a value width other than d."""
+    Q, K, V, W1, W2, tau = _small_inputs(variant, seed=14, B=1, H=2, N=6, d=3, m=4, scale=0.5, dv=dv)
     dO = _rng(15).standard_normal(V.shape)
     g = orc.linattn_bwd(Q, K, V, W1, W2, tau, dO, variant, causal, return_aux=True)
     # the query-side norm-factor gradient vanishes identically

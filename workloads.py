@@ -8,8 +8,9 @@ consume exactly the arrays produced here.
 Recipe (stand-in for the paper's LRA / WikiText-103 workloads, which are not
 available here): for workload seed ``s`` a ``numpy.random.default_rng(s)``
 draws, in this order and each standard normal float64 in C order,
-W1 [H,m,d], W2 [H,m,d] (nonstationary only), Q, K, V [B,H,N,d] and dO
-[B,H,N,dv] (workloads with a backward pass).  W is rounded to fp32
+W1 [H,m,d], W2 [H,m,d] (nonstationary only), Q, K [B,H,N,d], V [B,H,N,dv]
+and dO [B,H,N,dv] (workloads with a backward pass; dv = d unless a workload
+sets it).  W is rounded to fp32
 (round-to-nearest-even).  Q, K, V are multiplied by d^-1/4 and rounded to the
 storage dtype (fp32, or bf16 via fp32 with round-to-nearest-even).  dO is
 rounded the same way, without the scale.  tau = ln 2 for every head and
@@ -42,10 +43,11 @@ class Workload:
     backward: bool
     seed: int
     chunk: int = 64
+    value_dim: int = 0  # d_v; 0 means d_v = d
 
     @property
     def dv(self) -> int:
-        return self.d
+        return self.value_dim or self.d
 
     @property
     def dprime(self) -> int:
