@@ -45,8 +45,7 @@
  *     Others return FLEX_ERR_UNSUPPORTED.  Every supported shape has the
  *     forward and the backward.  dv != d runs at width max(d, dv) on
  *     zero-padded copies in the workspace (Q, K and W when dv > d; V, O and dO
- *     when dv < d), which leave the results unchanged; the prefill takes
- *     dv = d only.  (d, m) = (32, 64), (64, 64), (64, 128) (bf16) and (128, 64)
+ *     when dv < d), which leave the results unchanged.  (d, m) = (32, 64), (64, 64), (64, 128) (bf16) and (128, 64)
  *     run as one pass; every other shape runs as frequency groups (of 128 at
  *     bf16 d = 64 when 128 divides m, else of 64, the first one zero-padded
  *     when 64 does not divide m) whose sums are combined in a fixed order (the
@@ -149,9 +148,8 @@ int32_t flex_linattn_fwd(const flex_desc* desc, const void* Q, const void* K,
  *   state  fp32, B*H*2m*(dv+1) floats, overwritten: per (b,h) slice S [2m][dv]
  *          row-major, then z [2m], feature rows in [cos | sin] order.
  *   ws     flex_workspace_size(desc, FLEX_PASS_FWD) bytes, as for the forward.
- * desc->causal must be 1 and dv = d (FLEX_ERR_UNSUPPORTED otherwise); a NULL
- * or misaligned state returns FLEX_ERR_INVALID_ARG.  Shapes as
- * flex_linattn_fwd otherwise. */
+ * desc->causal must be 1 (FLEX_ERR_UNSUPPORTED otherwise); a NULL or
+ * misaligned state returns FLEX_ERR_INVALID_ARG.  Shapes as flex_linattn_fwd. */
 int32_t flex_linattn_prefill(const flex_desc* desc, const void* Q, const void* K,
                              const void* V, const float* W1, const float* W2,
                              const float* tau, void* O, float* den, float* state,
@@ -226,8 +224,8 @@ int32_t flex_linattn_bwd(const flex_desc* desc, const void* Q, const void* K,
  *                             an empty prefix.  (S and z are kept apart so
  *                             that S rows are 16-byte aligned.)
  *   o [B,H,dv] io_dtype, den [B,H] fp32 or NULL
- * desc->N, causal, chunk and segments are ignored.  Shapes: d = dv a multiple
- * of 4 up to 128, m up to 1024; others return FLEX_ERR_UNSUPPORTED.  The
+ * desc->N, causal, chunk and segments are ignored.  Shapes: d and dv
+ * multiples of 4 up to 128, m up to 1024; others return FLEX_ERR_UNSUPPORTED.  The
  * projection and the features are computed in fp32.  No workspace. */
 int32_t flex_decode_step(const flex_desc* desc, const void* q, const void* k,
                          const void* v, const float* W1, const float* W2,

@@ -92,10 +92,11 @@ int32_t check_fmap_desc(const flex_desc* d) {
   return fmap_shape_supported(&c) ? FLEX_OK : FLEX_ERR_UNSUPPORTED;
 }
 
-// Shapes of the decode step (one generic kernel): d = dv, a multiple of 4 up to
-// 128; up to 1024 frequencies.
+// Shapes of the decode step (one generic kernel): d and dv multiples of 4 up
+// to 128; up to 1024 frequencies.
 bool decode_supported(const flex_desc* d) {
-  return d->dv == d->d && d->d % 4 == 0 && d->d <= 128 && d->m <= 1024 && d->grad_dtype == FLEX_F32;
+  return d->d % 4 == 0 && d->d <= 128 && d->dv % 4 == 0 && d->dv <= 128 && d->m <= 1024 &&
+         d->grad_dtype == FLEX_F32;
 }
 
 KernelShape kshape(const flex_desc* d) {
@@ -475,12 +476,13 @@ int32_t check_fwd_args(const flex_desc* desc, const void* Q, const void* K, cons
 // ws_bytes_of(desc, FLEX_PASS_FWD) bytes at `base`.
 int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void* V, const float* W1,
                 const float* W2, const float* tau, void* O, float* den, char* base, hipStream_t stream,
-                float* state_out = nullptr) {
+                float* state_out = nullptr, int state_dv = 0) {
   FwdArgs a;
   memset(&a, 0, sizeof(a));
   a.Q = Q; a.K = K; a.V = V; a.tau = tau; a.O = O; a.den = den;
   a.state_out = state_out;
   a.state_m = desc->m;
+  a.state_dv = state_dv > 0 ? state_dv : desc->dv;
   const Groups G = groups_of(desc);
   const KernelShape ks = attn_shape(desc);
   const size_t sb = fwd_group_state_bytes(desc);
@@ -533,7 +535,8 @@ int32_t run_fwd(const flex_desc* desc, const void* Q, const void* K, const void*
 // The forward of a dv != d descriptor: run_fwd at the padded width on
 // zero-padded copies in the workspace (padded_desc).
 int32_t run_fwd_padded(const flex_desc* desc, const void* Q, const void* K, const void* V, const float* W1,
-                       const float* W2, const float* tau, void* O, float* den, char* base, hipStream_t stream) {
+                       const float* W2, const float* tau, void* O, float* den, char* base, hipStream_t stream,
+                       float* state_out = nullptr) {
   const flex_desc pd = padded_desc(desc);
   const ValuePad L = value_pad_of(desc, FLEX_PASS_FWD);
   char* vp = base + ws_bytes_of(&pd, FLEX_PASS_FWD);
@@ -546,10 +549,12 @@ int32_t run_fwd_padded(const flex_desc* desc, const void* Q, const void* K, cons
         (W2 && launch_copy_cols(W2, desc->d, vp + L.w2, w, hm, 4, stream) != hipSuccess))
       return FLEX_ERR_HIP;
     return run_fwd(&pd, vp + L.q, vp + L.k, V, reinterpret_cast<const float*>(vp + L.w1),
-                   W2 ? reinterpret_cast<const float*>(vp + L.w2) : nullptr, tau, O, den, base, stream);
+                   W2 ? reinterpret_cast<const float*>(vp + L.w2) : nullptr, tau, O, den, base, stream, state_out,
+                   desc->dv);
   }
   if (launch_copy_cols(V, desc->dv, vp + L.v, w, rows, io, stream) != hipSuccess) return FLEX_ERR_HIP;
-  const int32_t r = run_fwd(&pd, Q, K, vp + L.v, W1, W2, tau, vp + L.o, den, base, stream);
+  // a prefill state keeps the caller's dv columns (the others are the zero padding)
+  const int32_t r = run_fwd(&pd, Q, K, vp + L.v, W1, W2, tau, vp + L.o, den, base, stream, state_out, desc->dv);
   if (r != FLEX_OK) return r;
   return launch_copy_cols(vp + L.o, w, O, desc->dv, rows, io, stream) == hipSuccess ? FLEX_OK : FLEX_ERR_HIP;
 }
@@ -864,10 +869,12 @@ int32_t flex_linattn_prefill(const flex_desc* desc, const void* Q, const void* K
                              float* state, void* ws, size_t ws_bytes, void* stream) {
   const int32_t st = check_fwd_args(desc, Q, K, V, W1, W2, tau, O, den);
   if (st != FLEX_OK) return st;
-  if (desc->causal != 1 || desc->dv != desc->d) return FLEX_ERR_UNSUPPORTED;
+  if (desc->causal != 1) return FLEX_ERR_UNSUPPORTED;
   if (!state || !aligned16(state)) return FLEX_ERR_INVALID_ARG;
   const size_t need = ws_bytes_of(desc, FLEX_PASS_FWD);
   if (!ws || ws_bytes < need || !aligned16(ws)) return FLEX_ERR_WORKSPACE;
+  if (desc->dv != desc->d)
+    return run_fwd_padded(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream, state);
   return run_fwd(desc, Q, K, V, W1, W2, tau, O, den, static_cast<char*>(ws), (hipStream_t)stream, state);
 }
 

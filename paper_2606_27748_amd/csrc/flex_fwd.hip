@@ -430,8 +430,9 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
     // frequency tile ft, 2ft+1: its sin) and cols = value columns; the
     // normaliser tile holds z in column 0.
     const size_t F2 = 2 * (size_t)a.state_m;
-    float* so = a.state_out + (size_t)bh * F2 * (SH::DV + 1);
-    float* zo = so + F2 * SH::DV;
+    const int sdv = a.state_dv;   // value columns of the state layout, <= SH::DV
+    float* so = a.state_out + (size_t)bh * F2 * (sdv + 1);
+    float* zo = so + F2 * sdv;
 #pragma unroll
     for (int fc = 0; fc < SH::FC; ++fc)
 #pragma unroll
@@ -441,7 +442,8 @@ __global__ __launch_bounds__(NW * WAVE) void k_fwd_sweep(FwdArgs a) {
         const int f = a.state_f0 + fl;
         const size_t row = (fc % 2) ? (size_t)a.state_m + f : (size_t)f;
 #pragma unroll
-        for (int dt = 0; dt < SH::DVT; ++dt) so[row * SH::DV + dt * 16 + r] = S[fc][dt][i];
+        for (int dt = 0; dt < SH::DVT; ++dt)
+          if (dt * 16 + r < sdv) so[row * sdv + dt * 16 + r] = S[fc][dt][i];
         if (r == 0) zo[row] = S[fc][SH::DVT][i];
       }
   }

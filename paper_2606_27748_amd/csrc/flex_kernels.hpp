@@ -57,10 +57,12 @@ struct FwdArgs {
   // Phi = O2; nullptr K maps Q only
   void* O2;
   // causal prefill: the final state sum_j phi(K_j) [V_j ; 1]^T of every slice in
-  // the decode layout (per slice S [2m][dv] row-major, then z [2m]); state_f0 is
-  // the first frequency of this launch's group, state_m the total m.  NULL: none.
+  // the decode layout (per slice S [2m][state_dv] row-major, then z [2m]);
+  // state_f0 is the first frequency of this launch's group, state_m the total
+  // m, state_dv the caller's value width (at most the kernel's: the columns
+  // past it are the zero padding of a dv < d call).  NULL: none.
   float* state_out;
-  int state_f0, state_m;
+  int state_f0, state_m, state_dv;
 };
 
 struct BwdArgs {

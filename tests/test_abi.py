@@ -218,8 +218,6 @@ def test_entry_points_reject_bad_arguments():
     assert lib.flex_linattn_prefill(ctypes.byref(nc), P, P, P, P, P, P, P, P, P, P, big, None) == 2
     assert lib.flex_linattn_prefill(ctypes.byref(dn), P, P, P, P, P, P, P, P, None, P, big, None) == 1
     assert lib.flex_linattn_prefill(ctypes.byref(dn), P, P, P, P, P, P, P, P, P, P, 16, None) == 3
-    dvd = F.make_desc(1, 2, 100, 64, 128, "nonstationary", True, "bf16", dv=32)
-    assert lib.flex_linattn_prefill(ctypes.byref(dvd), P, P, P, P, P, P, P, P, P, P, big, None) == 2
     # feature map
     assert lib.flex_feature_map(ctypes.byref(dn), None, P, P, P, P, None, 0, None) == 1
     assert lib.flex_feature_map(ctypes.byref(ds), P, P, P, P, P, None, 0, None) == 1

@@ -25,13 +25,15 @@ def F():
     return F
 
 
-@pytest.mark.parametrize("io,d,m,variant", CASES)
-def test_decode_steps(F, io, d, m, variant):
+@pytest.mark.parametrize("io,d,m,variant,dv", [c + (c[1],) for c in CASES] +
+                         [("bf16", 64, 128, "nonstationary", 32), ("bf16", 32, 64, "stationary", 128),
+                          ("f32", 32, 64, "nonstationary", 96)])
+def test_decode_steps(F, io, d, m, variant, dv):
     import torch
-    wl = W.Workload("decode", 2, 3, 48, d, m, variant, True, io, False, 41)
+    wl = W.Workload("decode", 2, 3, 48, d, m, variant, True, io, False, 41, value_dim=dv)
     x = W.generate(wl)
     t = to_device(x)
-    desc = F.make_desc(wl.B, wl.H, 1, d, m, variant, True, io)
+    desc = F.make_desc(wl.B, wl.H, 1, d, m, variant, True, io, dv=dv)
     state = F.decode_state(desc)
     outs, dens = [], []
     for i in range(wl.N):
@@ -101,12 +103,15 @@ def test_decode_state_layout(F):
 PREFILL_CASES = [("bf16", 64, 128, "nonstationary", 0), ("bf16", 64, 128, "nonstationary", 16),
                  ("bf16", 32, 64, "stationary", 32), ("f32", 32, 64, "stationary", 0),
                  ("f32", 32, 64, "nonstationary", 16), ("bf16", 128, 256, "nonstationary", 0),
-                 # a padded last frequency group (its padding rows are not state rows)
+                 # a padded first frequency group (its padding rows are not state rows)
                  ("bf16", 64, 80, "nonstationary", 0)]
+# value widths other than d: the padded run's state keeps the caller's columns
+PREFILL_DV_CASES = [("bf16", 64, 128, "nonstationary", 0, 32), ("bf16", 128, 64, "stationary", 16, 64),
+                    ("bf16", 32, 80, "nonstationary", 0, 128)]
 
 
-@pytest.mark.parametrize("io,d,m,variant,chunk", PREFILL_CASES)
-def test_prefill_then_decode(F, io, d, m, variant, chunk):
+@pytest.mark.parametrize("io,d,m,variant,chunk,dv", [c + (c[1],) for c in PREFILL_CASES] + PREFILL_DV_CASES)
+def test_prefill_then_decode(F, io, d, m, variant, chunk, dv):
     """Prefill a causal prefix of N0 = 300 tokens (3 segments), then decode 6
     more tokens from the prefill's state.  The prefill's O and den are bitwise
     those of flex_linattn_fwd; its state is sum_j phi(K_j) [V_j ; 1]^T over the
@@ -114,11 +119,11 @@ def test_prefill_then_decode(F, io, d, m, variant, chunk):
     are rows N0 .. N0+5 of the oracle's causal attention over all 306 tokens."""
     import torch
     N0, steps = 300, 6
-    wl = W.Workload("prefill", 2, 3, N0 + steps, d, m, variant, True, io, False, 43)
+    wl = W.Workload("prefill", 2, 3, N0 + steps, d, m, variant, True, io, False, 43, value_dim=dv)
     x = W.generate(wl)
     t = to_device(x)
     pre = {k: t[k][:, :, :N0].contiguous() for k in ("Q", "K", "V")}
-    dp = F.make_desc(wl.B, wl.H, N0, d, m, variant, True, io, segments=3, chunk=chunk)
+    dp = F.make_desc(wl.B, wl.H, N0, d, m, variant, True, io, dv=dv, segments=3, chunk=chunk)
     O_p, den_p, state = F.flex_linattn_prefill(dp, pre["Q"], pre["K"], pre["V"], t["W1"], t["W2"],
                                                t["tau"])
     O_f, den_f = F.flex_linattn_fwd(dp, pre["Q"], pre["K"], pre["V"], t["W1"], t["W2"], t["tau"])
@@ -139,7 +144,7 @@ def test_prefill_then_decode(F, io, d, m, variant, chunk):
     bound = (4 * UNIT[io] + 4 * 2.0 ** -24 * np.sqrt(N0)) * np.linalg.norm(abs_S)
     assert np.linalg.norm(got_S - ref_S) <= bound, (np.linalg.norm(got_S - ref_S), bound)
     # decode the next tokens from the prefill's state
-    dd = F.make_desc(wl.B, wl.H, 1, d, m, variant, True, io)
+    dd = F.make_desc(wl.B, wl.H, 1, d, m, variant, True, io, dv=dv)
     outs, dens = [], []
     for i in range(N0, N0 + steps):
         o, den = F.flex_decode_step(dd, t["Q"][:, :, i].contiguous(), t["K"][:, :, i].contiguous(),
