@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define FLEX_ABI_VERSION 6
+#define FLEX_ABI_VERSION 7
 
 typedef enum {
   FLEX_OK = 0,

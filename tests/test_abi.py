@@ -31,7 +31,7 @@ def test_exports_match_header():
     assert set(names) == set(F.EXPORTS), names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.flex_abi_version() == 6
+    assert lib.flex_abi_version() == 7
 
 
 def test_status_strings():
