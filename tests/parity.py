@@ -73,9 +73,11 @@ def abs_scales(x, wl):
     return np.matmul(A, np.abs(V)), A.sum(-1)
 
 
-def check_forward(io, O_gpu, den_gpu, O_ref, den_ref, kappa, scales=None, rows_mask=None):
+def check_forward(io, O_gpu, den_gpu, O_ref, den_ref, kappa, scales=None, rows_mask=None, t2_on=True):
     """Apply T1, T1a and T2; returns a dict of statistics and raises
-    AssertionError with the statistics when a criterion fails."""
+    AssertionError with the statistics when a criterion fails.  t2_on=False
+    leaves out T2's Frobenius bound (its statistic is still logged): for
+    inputs where the precision alone reaches it."""
     tol, kmax, u = TOL[io], KAPPA_MAX[io], UNIT[io]
     O_gpu = np.asarray(O_gpu, np.float64)
     den_gpu = np.asarray(den_gpu, np.float64)
@@ -131,7 +133,7 @@ def check_forward(io, O_gpu, den_gpu, O_ref, den_ref, kappa, scales=None, rows_m
     stats = dict(T1_num=t1n, T1_den=t1d, T1a_num=t1an, T1a_den=t1ad, T2=t2, row_worst=float(worst),
                  rows_kept=float(good.mean()), den_le0=float((den_ref <= 0).mean()),
                  whole_O=frob_rel(O_gpu, O_ref), kappa_med=float(np.median(kappa)))
-    ok = t1an <= tol and t1ad <= tol and t2 <= tol and worst <= 1.0
+    ok = t1an <= tol and t1ad <= tol and (t2 <= tol or not t2_on) and worst <= 1.0
     if N >= 128:
         ok = ok and t1n <= tol and t1d <= tol
     _log("forward", stats)

@@ -10,6 +10,8 @@ N.  Below m = 64 the bf16 rounding of the features alone can reach most of the
 (tests/test_precision_floor.py)."""
 import random
 
+import numpy as np
+
 import pytest
 
 import oracle as orc
@@ -62,7 +64,11 @@ def test_random_configuration(F, case):
     O, den = F.flex_linattn_fwd(desc, t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"], ws=ws_f)
     O_ref, den_ref = orc.linattn_fwd(x.f64("Q"), x.f64("K"), x.f64("V"), x.W1, x.W2, x.tau, variant, causal)
     kf = orc.conditioning(x.f64("Q"), x.f64("K"), x.W1, x.W2, x.tau, variant, causal)
-    check_forward(io, to_f64(O), to_f64(den), O_ref, den_ref, kf, abs_scales(x, wl))
+    # bf16 with few frequencies: rounding the features, the intra-chunk kernel
+    # matrix and the state operand to bf16 alone can reach T2's bar on a short
+    # sequence (2.3 % at m = 16, N = 17; tests/test_precision_floor.py)
+    check_forward(io, to_f64(O), to_f64(den), O_ref, den_ref, kf, abs_scales(x, wl),
+                  t2_on=not (io == "bf16" and m < 48))
     if (io == "bf16" and m < 64) or N == 1:
         # N = 1: the true dQ, dK, dW, dtau vanish, so relative errors are not
         # defined; test_backward_single_token checks that case
@@ -73,9 +79,16 @@ def test_random_configuration(F, case):
         # non-finite by definition: no gradient to compare
         return
     ref, sc = oracle_bwd(wl, x)
+    names = names_of(wl)
+    if causal and not np.any(x.dO[:, :, 1:] != 0):
+        # every row but the first has its dO masked: O_0 = V_0 whatever the
+        # features, so the true dQ, dK, dW and dtau vanish and their relative
+        # errors are not defined (only dV is compared)
+        names = ["dV"]
     for reuse in (False, True):
         g = F.flex_linattn_bwd(desc, t["Q"], t["K"], t["V"], t["W1"], t["W2"], t["tau"], O, den, t["dO"],
                                fwd_ws=ws_f if reuse else None)
         got = {k: (None if v is None else to_f64(v)) for k, v in g.items()}
-        check_grads(io, got, ref, names_of(wl), sc)
-        check_rows(wl, x, got, ref, kap)
+        check_grads(io, got, ref, names, sc)
+        if names != ["dV"]:
+            check_rows(wl, x, got, ref, kap)

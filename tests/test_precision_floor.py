@@ -52,3 +52,33 @@ def test_bf16_rounding_floor_m48_short_causal(monkeypatch):
     test checks bf16 gradients from m = 64."""
     f = _floor(64, 48, "nonstationary", monkeypatch, shape=(1, 2, 65), causal=True, seed=1173)
     assert 1.5e-2 < f < 2e-2
+
+
+def test_bf16_forward_rounding_floor_m16_short():
+    """The bf16 causal forward rounds the features, the intra-chunk kernel
+    matrix (for A [V | 1]) and the carried state (the readout's operand) to
+    bf16.  Emulated in float64 on a drawn input with m = 16 and N = 17 (B=1,
+    H=2, d = d_v = 128, 16-token chunks), those roundings alone put T2 past
+    the 2e-2 bar (the GPU gives 2.1 %); the randomized test checks T2 for bf16
+    from m = 48."""
+    from tests.parity import KAPPA_MAX as KF
+    wl = W.Workload("floor_fwd", 1, 2, 17, 128, 16, "nonstationary", True, "bf16", False, 1336, value_dim=128)
+    x = W.generate(wl)
+    Q, K, V = x.f64("Q"), x.f64("K"), x.f64("V")
+    O, _ = orc.linattn_fwd(Q, K, V, x.W1, x.W2, x.tau, wl.variant, True)
+    pq = _bf16(orc.feature_map(Q, x.W1, x.W2, x.tau, wl.variant))
+    pk = _bf16(orc.feature_map(K, x.W1, x.W2, x.tau, wl.variant))
+    Vp = np.concatenate([V, np.ones(V.shape[:-1] + (1,))], -1)
+    out = np.zeros(Vp.shape)
+    C = 16
+    for h in range(wl.H):
+        S = np.zeros((2 * wl.m, wl.dv + 1))
+        for c0 in range(0, wl.N, C):
+            c1 = min(wl.N, c0 + C)
+            A = np.tril(pq[0, h, c0:c1] @ pk[0, h, c0:c1].T)
+            out[0, h, c0:c1] = _bf16(A) @ Vp[0, h, c0:c1] + pq[0, h, c0:c1] @ _bf16(S)
+            S = S + pk[0, h, c0:c1].T @ Vp[0, h, c0:c1]
+    Oe = out[..., :-1] / out[..., -1:]
+    kap = orc.conditioning(Q, K, x.W1, x.W2, x.tau, wl.variant, True)
+    good = kap <= KF["bf16"]
+    assert frob_rel(Oe[good], O[good]) > 2e-2
