@@ -22,11 +22,12 @@ def F():
     return F
 
 
-# (64, 128): one kernel per pass; (128, 80): two frequency groups, the first padded
-@pytest.mark.parametrize("d,m", [(64, 128), (128, 80)])
-def test_fwd_bwd_graph_replays(F, d, m):
+# (64, 128): one kernel per pass; (128, 80): two frequency groups, the first
+# padded; d_v != d: the zero-padded copies and the cropped results in the graph
+@pytest.mark.parametrize("d,m,dv", [(64, 128, 64), (128, 80, 128), (64, 128, 32), (32, 64, 128)])
+def test_fwd_bwd_graph_replays(F, d, m, dv):
     import torch
-    wl = W.Workload("graph", 2, 3, 700, d, m, "nonstationary", True, "bf16", True, 51)
+    wl = W.Workload("graph", 2, 3, 700, d, m, "nonstationary", True, "bf16", True, 51, value_dim=dv)
     t = to_device(W.generate(wl))
     desc = desc_of(wl)
     dev = t["Q"].device
@@ -36,7 +37,7 @@ def test_fwd_bwd_graph_replays(F, d, m):
     wsb = torch.empty(F.workspace_size(desc, F.FLEX_PASS_BWD), dtype=torch.uint8, device=dev)
     out = dict(O=torch.empty_like(t["V"]), den=torch.empty(B, H, N, dtype=f32, device=dev),
                dQ=torch.empty(B, H, N, d, dtype=f32, device=dev), dK=torch.empty(B, H, N, d, dtype=f32, device=dev),
-               dV=torch.empty(B, H, N, d, dtype=f32, device=dev), dW1=torch.empty(H, m, d, dtype=f32, device=dev),
+               dV=torch.empty(B, H, N, dv, dtype=f32, device=dev), dW1=torch.empty(H, m, d, dtype=f32, device=dev),
                dW2=torch.empty(H, m, d, dtype=f32, device=dev), dtau=torch.empty(H, dtype=f32, device=dev))
 
     def step():
